@@ -1,0 +1,157 @@
+"""Seeded generators for the five workloads.
+
+Every array is a pure function of a key ``(workload, layer, expert, tensor)``
+through ``numpy.random.SeedSequence``, so any expert can be regenerated on its
+own (the CPU oracle builds only the experts a token touches).
+
+Shapes (hidden ``d``, experts ``E``, top ``K``, shared ``S``, expert
+intermediate ``I``, LoRA rank ``r``):
+
+* ``tiny``   d 512,  E 16,  K 2, S 0, I 256,  r 8   (one layer)
+* ``moe35b`` d 2048, E 256, K 8, S 1, I 512,  r 16  (35B-class layer; also the
+  40-layer stack and the batched / prefill workload)
+* ``tier8b`` d 4096, E 64,  K 4, S 0, I 1024, r 16  (24 layers, host staging)
+
+Value distributions:
+
+* Expert weights are drawn directly in the stored int4 group-64 format:
+  uniform codes in 0..15, and per group an fp16 scale ``s`` uniform in
+  ``[0.9, 1.1] * 0.02 / sqrt(255 / 12)`` and an fp16 zero
+  ``z = -7.5 s + 0.005 * u``, ``u`` uniform in ``[-1, 1]``.  The
+  reconstructed weights then have mean ~0 and standard deviation ~0.02,
+  the scale of N(0, 0.02) weights after int4 quantization.
+* LoRA ``A [r, in]`` ~ N(0, 1/r) and ``B [out, r]`` ~ N(0, 0.01) (second
+  argument = standard deviation), stored fp16.
+* Router and prerouter head weights ``[E, d]`` ~ N(0, 0.02), fp16.
+* Token draws ``xi [d]`` ~ N(0, 1), fp32 (the layer input is their RMS
+  normalization, computed by the code under test).
+* fp32 master weights N(0, 0.02) for the quantizer test.
+"""
+
+import numpy as np
+
+__all__ = [
+    "WORKLOADS", "Workload", "rng", "int4_projection", "fp32_weights",
+    "lora_pair", "bundle", "router_weights", "token_draws", "zipf_logits",
+    "mixing", "ar1_token_draws",
+]
+
+
+class Workload:
+    def __init__(self, wid, name, d, e, k, s, inter, r, layers=1):
+        self.wid, self.name = wid, name
+        self.d, self.E, self.K, self.S, self.I, self.r = d, e, k, s, inter, r
+        self.layers = layers
+        self.a_std = 1.0 / r
+        self.b_std = 0.01
+        self.w_std = 0.02
+        self.lora_alpha = 2 * r           # alpha / r = 32 / 16 = 2
+
+    @property
+    def lora_scale(self):
+        return self.lora_alpha / self.r
+
+    def __repr__(self):
+        return "Workload(%s)" % self.name
+
+
+WORKLOADS = {
+    "tiny": Workload(0, "tiny", 512, 16, 2, 0, 256, 8),
+    "moe35b": Workload(1, "moe35b", 2048, 256, 8, 1, 512, 16, layers=40),
+    "tier8b": Workload(4, "tier8b", 4096, 64, 4, 0, 1024, 16, layers=24),
+}
+
+# tensor ids inside a key
+_T_Q = {"gate": 0, "up": 1, "down": 2}
+_T_SZ = {"gate": 3, "up": 4, "down": 5}
+_T_A = {"gate": 6, "up": 7, "down": 8}
+_T_B = {"gate": 9, "up": 10, "down": 11}
+_ROUTER_ID = 1 << 20
+_TOKEN_BASE = 10 ** 6
+
+
+def rng(*key):
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(k) for k in key])))
+
+
+def int4_projection(key_q, key_sz, out_dim, in_dim, w_std=0.02):
+    """Packed codes ``[out, in/2]`` (even input in the low nibble), fp16 s, z."""
+    q = np.frombuffer(rng(*key_q).bytes(out_dim * in_dim // 2), dtype=np.uint8)
+    q = q.reshape(out_dim, in_dim // 2).copy()
+    g = rng(*key_sz)
+    groups = (out_dim, in_dim // 64)
+    base = w_std / np.sqrt(255.0 / 12.0)
+    s = (base * g.uniform(0.9, 1.1, size=groups)).astype(np.float16)
+    z = (-7.5 * s.astype(np.float64) + 0.005 * g.uniform(-1.0, 1.0, size=groups)).astype(np.float16)
+    return q, s, z
+
+
+def fp32_weights(key, out_dim, in_dim, std=0.02):
+    return rng(*key).normal(0.0, std, size=(out_dim, in_dim)).astype(np.float32)
+
+
+def lora_pair(key_a, key_b, out_dim, in_dim, r, a_std, b_std):
+    a = rng(*key_a).normal(0.0, a_std, size=(r, in_dim)).astype(np.float16)
+    b = rng(*key_b).normal(0.0, b_std, size=(out_dim, r)).astype(np.float16)
+    return a, b
+
+
+def bundle(wl, layer, expert, lora=True, lora_on=("gate", "up", "down")):
+    """Expert ``expert`` of ``layer`` (ids ``E .. E+S-1`` are the shared experts)."""
+    dims = {"gate": (wl.I, wl.d), "up": (wl.I, wl.d), "down": (wl.d, wl.I)}
+    out = {"lora": {}}
+    for p, (o, i) in dims.items():
+        out[p] = int4_projection((wl.wid, layer, expert, _T_Q[p]),
+                                 (wl.wid, layer, expert, _T_SZ[p]), o, i, wl.w_std)
+        if lora and p in lora_on:
+            out["lora"][p] = lora_pair((wl.wid, layer, expert, _T_A[p]),
+                                       (wl.wid, layer, expert, _T_B[p]),
+                                       o, i, wl.r, wl.a_std, wl.b_std)
+        else:
+            out["lora"][p] = None
+    return out
+
+
+def router_weights(wl, layer, kind):
+    """fp16 ``[E, d]``; ``kind`` 0 = the layer's router, 1 = its prerouter head."""
+    return rng(wl.wid, layer, _ROUTER_ID, kind).normal(0.0, 0.02, size=(wl.E, wl.d)).astype(np.float16)
+
+
+def token_draws(wl, t0, count, stream=0):
+    """fp32 ``[count, d]`` N(0, 1) draws for tokens ``t0 .. t0+count-1``."""
+    return np.stack([rng(wl.wid, _TOKEN_BASE + t, stream).standard_normal(wl.d).astype(np.float32)
+                     for t in range(t0, t0 + count)])
+
+
+def zipf_logits(wl, tokens, seed=0, exponent=1.1):
+    """Synthetic router logits ``[T, E]`` fp32 with Zipf popularity.
+
+    ``p_e`` proportional to ``rank_e ** -exponent`` over a seeded permutation of
+    ranks; ``l[t, e] = log p_e + Gumbel(0, 1)``, so the top-K of a row is a
+    sample of K experts without replacement from ``p``.
+    """
+    g = rng(wl.wid, 2 << 20, seed)
+    ranks = g.permutation(wl.E) + 1
+    logp = -exponent * np.log(ranks.astype(np.float64))
+    logp -= np.log(np.sum(np.exp(logp)))
+    gumbel = g.gumbel(0.0, 1.0, size=(tokens, wl.E))
+    return (logp[None, :] + gumbel).astype(np.float32)
+
+
+def mixing(wl, layer):
+    """Residual-mixing stand-in for attention: fp16 ``D [d]`` ~ N(0, 0.5) and a permutation."""
+    g = rng(wl.wid, layer, 3 << 20)
+    d = g.normal(0.0, 0.5, size=wl.d).astype(np.float16)
+    perm = g.permutation(wl.d).astype(np.int32)
+    return d, perm
+
+
+def ar1_token_draws(wl, count, rho, stream=0):
+    """AR(1) token draws ``xi_{t+1} = rho xi_t + sqrt(1 - rho^2) eps``, fp32 ``[count, d]``."""
+    eps = token_draws(wl, 0, count, stream=stream).astype(np.float64)
+    out = np.empty_like(eps)
+    out[0] = eps[0]
+    c = np.sqrt(1.0 - rho * rho)
+    for t in range(1, count):
+        out[t] = rho * out[t - 1] + c * eps[t]
+    return out.astype(np.float32)

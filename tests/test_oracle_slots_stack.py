@@ -1,0 +1,152 @@
+"""Pins for the oracle's slot table, slot policy, decode chain and batched layer (CPU only).
+
+Slot policy: invariants checked by brute force over random traces and a
+hand-traced case.  Decode chain: prediction-as-routing (§3.2) checked on the
+trace itself, the boundary cases (first token, first layer) and determinism.
+Batched layer: equal to the one-token layer on every token (§3.1, Math
+contract).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import slots, stack, batched, expert, routing
+import synth
+
+
+def test_slot_table_bind_lookup_unbind():
+    t = slots.SlotTable(2, 8, 4)
+    t.bind(1, 5, 2)
+    assert t.lookup(1, 5) == 2 and t.lookup(0, 5) == -1
+    t.bind(1, 6, 2)                  # rebinding the slot evicts expert 5
+    assert t.lookup(1, 5) == -1 and t.lookup(1, 6) == 2
+    t.bind(1, 6, 3)                  # moving an expert frees its old slot
+    assert t.expert_in[1][2] == -1 and t.lookup(1, 6) == 3
+    t.unbind(1, 6)
+    assert t.lookup(1, 6) == -1 and t.expert_in[1][3] == -1
+
+
+def test_slot_policy_hand_trace():
+    p = slots.SlotPolicy(1, 8, 4)
+    assert p.stage(0, [1, 2]) == [(1, 0), (2, 1)]
+    assert p.stage(0, [2, 3]) == [(3, 2)]
+    assert p.use(0, [1, 2]) == [0, 1]
+    # pinned: {2, 3} (queued) and {4, 5}; free slot 3 first, then the LRU
+    # unpinned slot, slot 0 (expert 1)
+    assert p.stage(0, [4, 5]) == [(4, 3), (5, 0)]
+    assert p.use(0, [2, 3]) == [1, 2]
+    assert p.use(0, [4, 5]) == [3, 0]
+    with pytest.raises(RuntimeError):
+        p.use(0, [4, 5])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_slot_policy_invariants_random(seed):
+    rs = np.random.default_rng(seed)
+    n_layers, n_exp, k = 3, 16, 4
+    n_slots = 3 * k
+    p = slots.SlotPolicy(n_layers, n_exp, n_slots)
+    queued = [[] for _ in range(n_layers)]
+    for step in range(300):
+        layer = int(rs.integers(n_layers))
+        if queued[layer] and (len(queued[layer]) >= 2 or rs.random() < 0.5):
+            want = queued[layer].pop(0)
+            got = p.use(layer, want)
+            assert [p.table.expert_in[layer][s] for s in got] == want
+            continue
+        experts = [int(e) for e in rs.choice(n_exp, size=k, replace=False)]
+        before = {s: p.table.expert_in[layer][s] for s in range(n_slots)}
+        pinned_experts = set(e for q in queued[layer] for e in q)
+        misses = [e for e in experts if p.table.lookup(layer, e) < 0]
+        copies = p.stage(layer, experts)
+        # copies = misses, in routing order
+        assert [e for e, _ in copies] == misses
+        # nothing queued was evicted, and every member of every queued set is resident
+        for e in pinned_experts | set(experts):
+            assert p.table.lookup(layer, e) >= 0
+        # only copied slots changed
+        changed = {s for s in range(n_slots) if p.table.expert_in[layer][s] != before[s]}
+        assert changed == {s for _, s in copies}
+        queued[layer].append(experts)
+
+
+def _stack_layers(wl, n_layers, with_heads=True):
+    layers = []
+    for n in range(n_layers):
+        d, perm = synth.mixing(wl, n)
+        layers.append({
+            "router": synth.router_weights(wl, n, 0),
+            "head": synth.router_weights(wl, n, 1) if with_heads else None,
+            "mix_d": d, "mix_perm": perm,
+            "routed": (lambda e, n=n: synth.bundle(wl, n, e)),
+            "shared": [synth.bundle(wl, n, wl.E + s) for s in range(wl.S)],
+        })
+    return layers
+
+
+def test_chain_prediction_is_routing():
+    wl = synth.WORKLOADS["tiny"]
+    layers = _stack_layers(wl, 4)
+    xi = synth.token_draws(wl, 0, 3)
+    out = stack.decode_chain(xi, layers, wl.K, wl.lora_scale)
+    for t, recs in enumerate(out):
+        for n, rec in enumerate(recs):
+            if t == 0 or n == 0:
+                assert rec["src"] == "router"
+                _, idx, w = routing.route(layers[n]["router"], rec["x16"], wl.K)
+                assert rec["idx"].tolist() == idx.tolist()
+            else:
+                assert rec["src"] == "pred"
+                prev = out[t - 1][n - 1]
+                assert rec["idx"].tolist() == prev["pred_idx"].tolist()
+                assert np.array_equal(rec["w"], prev["pred_w"])
+            if n + 1 < len(layers):
+                _, pi, _ = routing.route(layers[n]["head"], rec["x16"], wl.K)
+                assert rec["pred_idx"].tolist() == pi.tolist()
+            else:
+                assert "pred_idx" not in rec
+    again = stack.decode_chain(xi, layers, wl.K, wl.lora_scale)
+    for a, b in zip(out, again):
+        for ra, rb in zip(a, b):
+            assert np.array_equal(ra["y"], rb["y"]) and np.array_equal(ra["x16"], rb["x16"])
+
+
+def test_chain_layer_output_matches_single_layer():
+    wl = synth.WORKLOADS["tiny"]
+    layers = _stack_layers(wl, 2)
+    out = stack.decode_chain(synth.token_draws(wl, 0, 2), layers, wl.K, wl.lora_scale)
+    rec = out[1][1]
+    single = expert.moe_layer(rec["x16"], wl.K, layers[1]["routed"], layers[1]["shared"],
+                              wl.lora_scale, routing=(rec["idx"], rec["w"]))
+    assert np.array_equal(single["y"], rec["y"])
+
+
+def test_chain_without_consumers_uses_own_router():
+    wl = synth.WORKLOADS["tiny"]
+    layers = _stack_layers(wl, 3)
+    out = stack.decode_chain(synth.token_draws(wl, 0, 2), layers, wl.K, wl.lora_scale, consumers=set())
+    assert all(rec["src"] == "router" for recs in out for rec in recs)
+
+
+def test_batched_equals_single_token_layer():
+    wl = synth.WORKLOADS["tiny"]
+    t = 5
+    x = routing.rms_norm_f16(synth.token_draws(wl, 0, t))
+    logits = synth.zipf_logits(wl, t, seed=1)
+    routed = lambda e: synth.bundle(wl, 0, e)
+    out = batched.batched_layer(x, logits, wl.K, routed, [], wl.lora_scale)
+    for i in range(t):
+        inds, w = routing.softmax_topk(logits[i], wl.K)
+        one = expert.moe_layer(x[i], wl.K, routed, [], wl.lora_scale, routing=(inds, w))
+        assert out["idx"][i].tolist() == inds.tolist()
+        assert np.array_equal(out["y"][i], one["y"])
+    sub = batched.batched_layer(x, logits, wl.K, routed, [], wl.lora_scale, tokens=[2])
+    assert np.array_equal(sub["y"][2], out["y"][2]) and np.isnan(sub["y"][0]).all()
+
+
+def test_zipf_logits_popularity_is_skewed():
+    wl = synth.WORKLOADS["moe35b"]
+    logits = synth.zipf_logits(wl, 512, seed=0)
+    idx = np.argsort(-logits, axis=1, kind="stable")[:, :wl.K]
+    counts = np.bincount(idx.ravel(), minlength=wl.E)
+    assert counts.max() > 300 and (counts > 0).sum() > 150

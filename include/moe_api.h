@@ -1,0 +1,201 @@
+/*
+ * moe_api.h -- C ABI of the MI355X (gfx950) streaming-MoE decode hot path.
+ *
+ * One MoE layer does the following:
+ * - routes a token: router logits, softmax, top-k (App. A, Softmax-topk);
+ * - predicts the next layer's routing one token ahead with the prerouter head,
+ *   and that prediction is then used as the routing (Sec. 3.2, Motivation and
+ *   Prediction-as-routing);
+ * - runs the selected int4 group-64 SwiGLU experts (Sec. 3.1, Math contract),
+ *   each with the unmerged LoRA delta (alpha/r) B A v (Sec. 3.3, Fig. 1);
+ * - combines the expert outputs with the routing weights.
+ * Expert ids reach their weights through a device-resident slot table, so a
+ * decode step never stacks weights (Sec. 3.1, Executor paths, "staged").
+ *
+ * Conventions for every call below:
+ * - Plain C. Device pointers point to device memory, host pointers to host
+ *   memory. `stream` is a hipStream_t passed as void* (NULL means the null stream).
+ * - The caller owns every buffer passed in: inputs, outputs and workspaces.
+ *   Only the slot-table object and its device table belong to the library.
+ * - The hot-path calls (moe_rmsnorm_f16 through moe_topk) only enqueue work
+ *   on `stream`. They never allocate, never synchronise the host, and are
+ *   safe to capture in a HIP graph.
+ * - Return value: MOE_OK (0) or a negative MOE_E* code. A failed argument
+ *   check enqueues nothing.
+ * - Alignment: device pointers must be 16-byte aligned (MOE_EALIGN otherwise).
+ * - A kernel that meets an expert id outside [0, E) or a non-resident expert
+ *   ORs a MOE_STATUS_* bit into the caller's status word. That expert then
+ *   contributes zeros. The caller reads the status word after the step.
+ * - Not thread-safe for concurrent calls on one slot table.
+ */
+#ifndef MOE_API_H
+#define MOE_API_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes -------------------------------------------------------- */
+#define MOE_OK            0
+#define MOE_EINVAL       (-1)  /* bad spec, shape, NULL pointer or index     */
+#define MOE_EALIGN       (-2)  /* device pointer not 16-byte aligned         */
+#define MOE_ENOTRESIDENT (-3)  /* host-visible lookup of an unbound expert   */
+#define MOE_EHIP         (-4)  /* a HIP runtime call or kernel launch failed */
+#define MOE_ENOMEM       (-5)  /* workspace too small / allocation failed    */
+
+/* ---- device status bits (OR-ed into *status_dev by the kernels) ---------- */
+#define MOE_STATUS_SLOT_MISS 1u  /* routed expert has no resident slot       */
+#define MOE_STATUS_BAD_INDEX 2u  /* expert id outside [0, E)                  */
+
+/* ---- layer description (the MoESpec of Sec. 3) --------------------------- */
+#define MOE_ROUTING_SOFTMAX_TOPK 0   /* App. A, Softmax-topk                    */
+
+typedef struct moe_layer_spec {
+  int32_t d_model;     /* hidden size d; multiple of 64, <= 8192             */
+  int32_t n_experts;   /* routed experts E; 1..1024                          */
+  int32_t top_k;       /* K; 1..min(E, 32)                                   */
+  int32_t n_shared;    /* always-on shared experts S (weight 1.0); 0..4      */
+  int32_t d_expert;    /* expert intermediate size I; multiple of 64, <= 8192 */
+  int32_t group_size;  /* int4 quantization group; must be 64                */
+  int32_t lora_rank;   /* r; 0 (no adapters) or 1..64                        */
+  float   lora_scale;  /* alpha / r, the LoRA delta multiplier (Sec. 3.3)    */
+  int32_t routing;     /* MOE_ROUTING_*                                      */
+  int32_t reserved[7]; /* must be zero                                       */
+} moe_layer_spec;
+
+/*
+ * One int4 group-64 projection W [out x in] of an expert, in device memory
+ * (Sec. 2, Quantization; Sec. 3.1, Executor paths: the three quantized
+ * projections, each with its scales and biases):
+ *   q      uint8 [out][in/2]. Row-major packed codes; byte j of a row holds
+ *          input 2j in the low nibble and input 2j+1 in the high nibble.
+ *   sz     fp16 pairs [out][in/64][2] = (scale s, zero z) of each 64-input group.
+ *          The weight is w = s * q + z.
+ *   lora_a fp16 [r][in] or NULL  (LoRA down-projection A)
+ *   lora_b fp16 [out][r] or NULL (LoRA up-projection B); the delta is
+ *          lora_scale * B (A v), applied only when both are non-NULL.
+ */
+typedef struct moe_proj {
+  const void* q;
+  const void* sz;
+  const void* lora_a;
+  const void* lora_b;
+} moe_proj;
+
+/* One expert: gate and up are [I x d], down is [d x I]. */
+typedef struct moe_bundle {
+  moe_proj gate, up, down;
+} moe_bundle;
+
+/* Check a spec. Returns MOE_OK or MOE_EINVAL. Host only. */
+int moe_spec_check(const moe_layer_spec* spec);
+
+/* Human-readable text of an error code. Static storage. */
+const char* moe_strerror(int code);
+
+/* ---- slot table (Sec. 3.1, Executor paths, "staged": routing indices map
+ *      through a slot table and never leave the device) -------------------- */
+typedef struct moe_slot_table moe_slot_table;
+
+/*
+ * Create a table for n_layers layers. Each layer has n_ids expert ids
+ * (E routed ids first, then the S shared ids E .. E+S-1) and n_slots slots.
+ * Only host memory is allocated here. The device copy is allocated by the
+ * first moe_slot_table_sync. Destroy the table with moe_slot_table_destroy.
+ */
+int moe_slot_table_create(int n_layers, int n_ids, int n_slots, moe_slot_table** out);
+int moe_slot_table_destroy(moe_slot_table* t);
+
+/*
+ * Bind expert `expert` of `layer` to `slot`, whose weights are *bundle (the
+ * table copies the pointers). If the slot held another expert, that expert
+ * becomes unbound. If `expert` was in another slot, that slot becomes free.
+ * Host mirror only: call moe_slot_table_sync to publish.
+ */
+int moe_slot_bind(moe_slot_table* t, int layer, int expert, int slot, const moe_bundle* bundle);
+/* Mark `expert` of `layer` as not resident (host mirror). */
+int moe_slot_unbind(moe_slot_table* t, int layer, int expert);
+/* Slot of `expert` in `layer` from the host mirror, or MOE_ENOTRESIDENT. */
+int moe_slot_lookup(const moe_slot_table* t, int layer, int expert);
+/*
+ * Push the host mirror to the device copy with async copies on `stream`
+ * (the first call allocates the device copy). The mirror is staged in a
+ * library-owned pinned buffer, so the host may change it right after return.
+ */
+int moe_slot_table_sync(moe_slot_table* t, void* stream);
+
+/* ---- hot path ------------------------------------------------------------ */
+
+/*
+ * Layer input: x[t] = fp16(xi[t] / sqrt(mean(xi[t]^2) + 1e-6)) for T rows
+ * of d fp32 values. The normalized value is computed in fp64 and rounded
+ * once to fp16 (round-to-nearest-even).
+ * xi: device fp32 [T][d]; x_f16: device fp16 [T][d].
+ */
+int moe_rmsnorm_f16(const float* xi, int T, int d, void* x_f16, void* stream);
+
+/* Workspace bytes needed by moe_route / moe_preroute / moe_expert_ffn_int4_lora
+ * for T tokens. The caller allocates it and zero-fills it once. The library
+ * leaves its internal counters at zero after every call. Calls that share one
+ * workspace must be ordered on one stream. */
+size_t moe_workspace_bytes(const moe_layer_spec* spec, int T);
+
+/*
+ * Router (App. A, Softmax-topk): fp32 logits l = W x, then the K largest
+ * logits in descending order (ties go to the lower expert id), with weights
+ * w_i = exp(l_i - l_max) / sum over the selected j of exp(l_j - l_max).
+ * x_f16: device fp16 [T][d]; w_router_f16: device fp16 [E][d].
+ * logits_opt: device fp32 [T][E], or NULL if not needed.
+ * idx: device int32 [T][K]; w: device fp32 [T][K].
+ */
+int moe_route(const moe_layer_spec* spec, const void* x_f16, const void* w_router_f16, int T,
+              float* logits_opt, int32_t* idx, float* w, void* workspace, size_t workspace_bytes,
+              void* stream);
+
+/*
+ * Prerouter (Sec. 3.2, Head and Prediction-as-routing): the head of layer N
+ * runs on layer N's input at token t. Its output (same math as moe_route,
+ * with the head weights [E_next][d]) is layer N+1's routing at token t+1.
+ * `next` describes layer N+1.
+ */
+int moe_preroute(const moe_layer_spec* next, const void* x_f16, const void* w_head_f16, int T,
+                 float* logits_opt, int32_t* pred_idx, float* pred_w, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+/*
+ * Experts (Sec. 3.1, Math contract; Sec. 3.3): for every token t and every
+ * list position k in [0, K+S):
+ *   e = idx[t][k] for k < K, else E + (k - K)
+ *   y_experts[t][k] = down(silu(g) * u), where
+ *   g = W_gate x + s_L B_gate (A_gate x), u likewise, and down likewise on h.
+ * Weights are found through `table` (layer `layer`). All arithmetic is fp32.
+ * idx: device int32 [T][K], for example the prerouter's output.
+ * y_experts: device fp32 [T][K+S][d]. status_dev: device uint32.
+ */
+int moe_expert_ffn_int4_lora(const moe_layer_spec* spec, const moe_slot_table* table, int layer,
+                             const void* x_f16, int T, const int32_t* idx, float* y_experts,
+                             uint32_t* status_dev, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/*
+ * Combine (Fig. 1 sum node): y[t] = sum_{k<K} w[t][k] y_experts[t][k]
+ *                                  + sum_{s<S} y_experts[t][K+s].
+ * y: device fp32 [T][d].
+ */
+int moe_combine(const moe_layer_spec* spec, const float* y_experts, const float* w, int T,
+                float* y, void* stream);
+
+/*
+ * Softmax-top-k on given logits (App. A): logits device fp32 [T][E] ->
+ * idx [T][K], w [T][K]. Same selection and weights as moe_route.
+ */
+int moe_topk(const moe_layer_spec* spec, const float* logits, int T, int32_t* idx, float* w,
+             void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_API_H */

@@ -13,10 +13,10 @@ selection uses the biased score and the weights use the raw sigmoid.
 Readings (the paper is silent on these):
 
 * Layer input: ``x = fp16(xi / sqrt(mean(xi^2) + 1e-6))`` with no learned
-  scale.  The scale factor is computed in float64 and the product is rounded
-  to fp32 and then to fp16 (round-to-nearest-even).  The fp16 code of ``x``
-  is decided by floating point, and float64 makes the decision independent
-  of the order of the reduction.
+  scale.  The normalized value is computed in float64 and rounded once to
+  fp16 (round-to-nearest-even).  The fp16 code of ``x`` is decided by
+  floating point, and float64 makes the decision independent of the order
+  of the reduction.
 * Router and head logits are fp32: the exact dot product of fp16 weights and
   fp16 activations (computed in float64, where every product is exact),
   rounded once to fp32.
@@ -40,7 +40,7 @@ def rms_norm_f16(xi, eps=RMS_EPS):
     x64 = xi.astype(np.float64)
     ms = np.mean(x64 * x64, axis=-1, keepdims=True)
     r = 1.0 / np.sqrt(ms + eps)
-    return (x64 * r).astype(np.float32).astype(np.float16)
+    return (x64 * r).astype(np.float16)
 
 
 def logits_fp32(w16, x16):

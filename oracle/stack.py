@@ -31,7 +31,7 @@ def _rmsnorm64(v, eps=RMS_EPS):
 
 
 def _x16(r):
-    return _rmsnorm64(r).astype(np.float32).astype(np.float16)
+    return _rmsnorm64(r).astype(np.float16)
 
 
 def decode_chain(tokens_xi, layers, k, lora_scale, consumers=None):

@@ -1,0 +1,235 @@
+"""ctypes binding of libmoe.so (argument marshalling only).
+
+Every function here converts torch tensors to device pointers, passes the
+current HIP stream and turns negative return codes into :class:`MoeError`.
+All computation happens in the library's HIP kernels.  If the library is
+missing, loading fails with ``ImportError``: there is no fallback path.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoe.so")
+
+c_int, c_int32, c_float, c_void_p, c_size_t = (ctypes.c_int, ctypes.c_int32, ctypes.c_float,
+                                               ctypes.c_void_p, ctypes.c_size_t)
+
+MOE_OK, MOE_EINVAL, MOE_EALIGN, MOE_ENOTRESIDENT, MOE_EHIP, MOE_ENOMEM = 0, -1, -2, -3, -4, -5
+MOE_STATUS_SLOT_MISS, MOE_STATUS_BAD_INDEX = 1, 2
+
+
+class MoeLayerSpec(ctypes.Structure):
+    _fields_ = [("d_model", c_int32), ("n_experts", c_int32), ("top_k", c_int32),
+                ("n_shared", c_int32), ("d_expert", c_int32), ("group_size", c_int32),
+                ("lora_rank", c_int32), ("lora_scale", c_float), ("routing", c_int32),
+                ("reserved", c_int32 * 7)]
+
+
+class MoeProj(ctypes.Structure):
+    _fields_ = [("q", c_void_p), ("sz", c_void_p), ("lora_a", c_void_p), ("lora_b", c_void_p)]
+
+
+class MoeBundle(ctypes.Structure):
+    _fields_ = [("gate", MoeProj), ("up", MoeProj), ("down", MoeProj)]
+
+
+class MoeError(RuntimeError):
+    def __init__(self, code, what):
+        self.code = code
+        super().__init__("%s failed: %s (%d)" % (what, strerror(code), code))
+
+
+_lib = None
+
+# name -> (restype, argtypes) for every symbol declared in include/moe_api.h
+SIGNATURES = {
+    "moe_spec_check": (c_int, [ctypes.POINTER(MoeLayerSpec)]),
+    "moe_strerror": (ctypes.c_char_p, [c_int]),
+    "moe_slot_table_create": (c_int, [c_int, c_int, c_int, ctypes.POINTER(c_void_p)]),
+    "moe_slot_table_destroy": (c_int, [c_void_p]),
+    "moe_slot_bind": (c_int, [c_void_p, c_int, c_int, c_int, ctypes.POINTER(MoeBundle)]),
+    "moe_slot_unbind": (c_int, [c_void_p, c_int, c_int]),
+    "moe_slot_lookup": (c_int, [c_void_p, c_int, c_int]),
+    "moe_slot_table_sync": (c_int, [c_void_p, c_void_p]),
+    "moe_rmsnorm_f16": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p]),
+    "moe_workspace_bytes": (c_size_t, [ctypes.POINTER(MoeLayerSpec), c_int]),
+    "moe_route": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
+                          c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "moe_preroute": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
+                             c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "moe_expert_ffn_int4_lora": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p,
+                                         c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                         c_void_p]),
+    "moe_combine": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
+                            c_void_p]),
+    "moe_topk": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p, c_void_p,
+                         c_void_p]),
+}
+
+
+def lib():
+    """Load libmoe.so once and declare its signatures."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libmoe.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = handle
+    return _lib
+
+
+def strerror(code):
+    return lib().moe_strerror(int(code)).decode()
+
+
+def _check(rc, what):
+    if rc < 0:
+        raise MoeError(rc, what)
+    return rc
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def make_spec(d, n_experts, top_k, n_shared, d_expert, lora_rank, lora_scale, group_size=64):
+    s = MoeLayerSpec()
+    s.d_model, s.n_experts, s.top_k, s.n_shared = d, n_experts, top_k, n_shared
+    s.d_expert, s.group_size, s.lora_rank, s.lora_scale = d_expert, group_size, lora_rank, lora_scale
+    s.routing = 0
+    return s
+
+
+def spec_from_workload(wl):
+    return make_spec(wl.d, wl.E, wl.K, wl.S, wl.I, wl.r, wl.lora_scale)
+
+
+def spec_check(spec):
+    return lib().moe_spec_check(ctypes.byref(spec))
+
+
+def workspace_bytes(spec, T):
+    return int(lib().moe_workspace_bytes(ctypes.byref(spec), int(T)))
+
+
+class SlotTable:
+    """Owner of a library slot table (host mirror + device copy)."""
+
+    def __init__(self, n_layers, n_ids, n_slots):
+        h = c_void_p()
+        _check(lib().moe_slot_table_create(n_layers, n_ids, n_slots, ctypes.byref(h)),
+               "moe_slot_table_create")
+        self.handle = h
+        self.n_layers, self.n_ids, self.n_slots = n_layers, n_ids, n_slots
+        self._keep = {}
+
+    def bind(self, layer, expert, slot, bundle, keep=None):
+        _check(lib().moe_slot_bind(self.handle, layer, expert, slot, ctypes.byref(bundle)),
+               "moe_slot_bind")
+        self._keep[(layer, slot)] = keep
+
+    def unbind(self, layer, expert):
+        _check(lib().moe_slot_unbind(self.handle, layer, expert), "moe_slot_unbind")
+
+    def lookup(self, layer, expert):
+        rc = lib().moe_slot_lookup(self.handle, layer, expert)
+        if rc == MOE_ENOTRESIDENT:
+            return -1
+        return _check(rc, "moe_slot_lookup")
+
+    def sync(self, stream=None):
+        _check(lib().moe_slot_table_sync(self.handle, _stream(stream)), "moe_slot_table_sync")
+
+    def close(self):
+        if self.handle:
+            _check(lib().moe_slot_table_destroy(self.handle), "moe_slot_table_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---- weights: host arrays in the stored format -> device buffers --------------
+
+def upload_projection(qsz, lora, device):
+    """(packed q [out, in/2] uint8, s fp16 [out, in/64], z fp16) + (A, B) | None
+    -> (MoeProj, tensors to keep alive).  s and z are interleaved into the
+    (scale, zero) pairs of the device layout."""
+    import torch
+    q, s, z = qsz
+    qt = torch.from_numpy(np.ascontiguousarray(q)).to(device)
+    sz = np.ascontiguousarray(np.stack([np.asarray(s, np.float16), np.asarray(z, np.float16)], -1))
+    szt = torch.from_numpy(sz).to(device)
+    keep = [qt, szt]
+    p = MoeProj(qt.data_ptr(), szt.data_ptr(), None, None)
+    if lora is not None:
+        at = torch.from_numpy(np.ascontiguousarray(lora[0], dtype=np.float16)).to(device)
+        bt = torch.from_numpy(np.ascontiguousarray(lora[1], dtype=np.float16)).to(device)
+        keep += [at, bt]
+        p.lora_a, p.lora_b = at.data_ptr(), bt.data_ptr()
+    return p, keep
+
+
+def upload_bundle(b, device="cuda"):
+    lo = b.get("lora") or {}
+    g, kg = upload_projection(b["gate"], lo.get("gate"), device)
+    u, ku = upload_projection(b["up"], lo.get("up"), device)
+    d, kd = upload_projection(b["down"], lo.get("down"), device)
+    return MoeBundle(g, u, d), kg + ku + kd
+
+
+# ---- hot path -----------------------------------------------------------------
+
+def rmsnorm_f16(xi, x, stream=None):
+    T, d = xi.shape
+    _check(lib().moe_rmsnorm_f16(_ptr(xi), T, d, _ptr(x), _stream(stream)), "moe_rmsnorm_f16")
+
+
+def route(spec, x, w_router, idx, w, workspace, logits=None, stream=None):
+    T = x.shape[0]
+    _check(lib().moe_route(ctypes.byref(spec), _ptr(x), _ptr(w_router), T, _ptr(logits), _ptr(idx),
+                           _ptr(w), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                           _stream(stream)), "moe_route")
+
+
+def preroute(spec_next, x, w_head, pred_idx, pred_w, workspace, logits=None, stream=None):
+    T = x.shape[0]
+    _check(lib().moe_preroute(ctypes.byref(spec_next), _ptr(x), _ptr(w_head), T, _ptr(logits),
+                              _ptr(pred_idx), _ptr(pred_w), _ptr(workspace),
+                              workspace.numel() * workspace.element_size(), _stream(stream)),
+           "moe_preroute")
+
+
+def expert_ffn(spec, table, layer, x, idx, y_experts, status, workspace, stream=None):
+    T = x.shape[0]
+    _check(lib().moe_expert_ffn_int4_lora(ctypes.byref(spec), table.handle, layer, _ptr(x), T,
+                                          _ptr(idx), _ptr(y_experts), _ptr(status), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(),
+                                          _stream(stream)), "moe_expert_ffn_int4_lora")
+
+
+def combine(spec, y_experts, w, y, stream=None):
+    T = y.shape[0]
+    _check(lib().moe_combine(ctypes.byref(spec), _ptr(y_experts), _ptr(w), T, _ptr(y),
+                             _stream(stream)), "moe_combine")
+
+
+def topk(spec, logits, idx, w, stream=None):
+    T = logits.shape[0]
+    _check(lib().moe_topk(ctypes.byref(spec), _ptr(logits), T, _ptr(idx), _ptr(w), _stream(stream)),
+           "moe_topk")

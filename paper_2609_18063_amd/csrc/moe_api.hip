@@ -1,0 +1,318 @@
+// C ABI of the MoE decode hot path (declarations and contracts in
+// include/moe_api.h): argument checks, the slot table, the workspace layout
+// and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "moe_kernels.h"
+
+struct moe_slot_table {
+  int n_layers = 0, n_ids = 0, n_slots = 0;
+  std::vector<int32_t> slot_of;      // [L][n_ids], -1 = not resident
+  std::vector<int32_t> expert_in;    // [L][n_slots], -1 = free
+  std::vector<moe_bundle> bundles;   // [L][n_slots]
+  // device copy: [slot_of | pad | bundles] in one allocation
+  void* dev = nullptr;
+  size_t dev_bytes = 0, bundles_off = 0;
+  void* pinned = nullptr;
+  hipEvent_t copied = nullptr;
+  bool copy_pending = false;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool pow2_dim(int v) {
+  return v == 256 || v == 512 || v == 1024 || v == 2048 || v == 4096 || v == 8192;
+}
+
+struct WsLayout {
+  size_t counters, logits, gx, ux, h, ag, au, adpart, total;
+};
+
+WsLayout ws_layout(const moe_layer_spec* s, int T) {
+  WsLayout w{};
+  const size_t n = (size_t)(s->top_k + s->n_shared);
+  const size_t r = (size_t)(s->lora_rank > 0 ? s->lora_rank : 1);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = round_up(off + bytes, kAlign);
+    return o;
+  };
+  w.counters = take((size_t)T * sizeof(uint32_t));
+  w.logits = take((size_t)T * s->n_experts * sizeof(float));
+  w.gx = take((size_t)T * n * s->d_expert * sizeof(float));
+  w.ux = take((size_t)T * n * s->d_expert * sizeof(float));
+  w.h = take((size_t)T * n * s->d_expert * sizeof(float));
+  w.ag = take((size_t)T * n * r * sizeof(float));
+  w.au = take((size_t)T * n * r * sizeof(float));
+  w.adpart = take((size_t)T * n * (s->d_expert / 64) * r * sizeof(float));
+  w.total = off;
+  return w;
+}
+
+int from_hip(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_EHIP; }
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_spec_check(const moe_layer_spec* s) {
+  if (!s) return MOE_EINVAL;
+  if (!pow2_dim(s->d_model) || s->d_model < 512) return MOE_EINVAL;
+  if (!pow2_dim(s->d_expert)) return MOE_EINVAL;
+  if (s->n_experts < 1 || s->n_experts > 1024) return MOE_EINVAL;
+  if (s->top_k < 1 || s->top_k > 32 || s->top_k > s->n_experts) return MOE_EINVAL;
+  if (s->n_shared < 0 || s->n_shared > 4) return MOE_EINVAL;
+  if (s->group_size != 64) return MOE_EINVAL;
+  if (s->lora_rank < 0 || s->lora_rank > 64) return MOE_EINVAL;
+  if (!(s->lora_scale == s->lora_scale)) return MOE_EINVAL;
+  if (s->routing != MOE_ROUTING_SOFTMAX_TOPK) return MOE_EINVAL;
+  for (int i = 0; i < 7; ++i)
+    if (s->reserved[i] != 0) return MOE_EINVAL;
+  return MOE_OK;
+}
+
+const char* moe_strerror(int code) {
+  switch (code) {
+    case MOE_OK: return "ok";
+    case MOE_EINVAL: return "invalid argument (spec, shape, null pointer or index)";
+    case MOE_EALIGN: return "device pointer not 16-byte aligned";
+    case MOE_ENOTRESIDENT: return "expert not resident in the slot table";
+    case MOE_EHIP: return "HIP runtime or kernel launch error";
+    case MOE_ENOMEM: return "workspace too small or allocation failed";
+  }
+  return "unknown error";
+}
+
+// ---- slot table ------------------------------------------------------------
+
+int moe_slot_table_create(int n_layers, int n_ids, int n_slots, moe_slot_table** out) {
+  if (!out || n_layers < 1 || n_ids < 1 || n_slots < 1) return MOE_EINVAL;
+  if ((long long)n_layers * n_ids > (1LL << 28) || (long long)n_layers * n_slots > (1LL << 24))
+    return MOE_EINVAL;
+  moe_slot_table* t = new (std::nothrow) moe_slot_table;
+  if (!t) return MOE_ENOMEM;
+  t->n_layers = n_layers;
+  t->n_ids = n_ids;
+  t->n_slots = n_slots;
+  t->slot_of.assign((size_t)n_layers * n_ids, -1);
+  t->expert_in.assign((size_t)n_layers * n_slots, -1);
+  t->bundles.assign((size_t)n_layers * n_slots, moe_bundle{});
+  *out = t;
+  return MOE_OK;
+}
+
+int moe_slot_table_destroy(moe_slot_table* t) {
+  if (!t) return MOE_EINVAL;
+  int rc = MOE_OK;
+  if (t->copied) {
+    if (t->copy_pending && hipEventSynchronize(t->copied) != hipSuccess) rc = MOE_EHIP;
+    (void)hipEventDestroy(t->copied);
+  }
+  if (t->pinned) (void)hipHostFree(t->pinned);
+  if (t->dev) (void)hipFree(t->dev);
+  delete t;
+  return rc;
+}
+
+int moe_slot_bind(moe_slot_table* t, int layer, int expert, int slot, const moe_bundle* b) {
+  if (!t || !b || layer < 0 || layer >= t->n_layers || expert < 0 || expert >= t->n_ids ||
+      slot < 0 || slot >= t->n_slots)
+    return MOE_EINVAL;
+  const moe_proj* ps[3] = {&b->gate, &b->up, &b->down};
+  for (const moe_proj* p : ps) {
+    if (!p->q || !p->sz) return MOE_EINVAL;
+    if (!aligned16(p->q) || !aligned16(p->sz)) return MOE_EALIGN;
+    if ((p->lora_a && !aligned16(p->lora_a)) || (p->lora_b && !aligned16(p->lora_b)))
+      return MOE_EALIGN;
+  }
+  int32_t* so = &t->slot_of[(size_t)layer * t->n_ids];
+  int32_t* ei = &t->expert_in[(size_t)layer * t->n_slots];
+  const int old = ei[slot];
+  if (old >= 0) so[old] = -1;
+  const int prev = so[expert];
+  if (prev >= 0) ei[prev] = -1;
+  so[expert] = slot;
+  ei[slot] = expert;
+  t->bundles[(size_t)layer * t->n_slots + slot] = *b;
+  return MOE_OK;
+}
+
+int moe_slot_unbind(moe_slot_table* t, int layer, int expert) {
+  if (!t || layer < 0 || layer >= t->n_layers || expert < 0 || expert >= t->n_ids)
+    return MOE_EINVAL;
+  int32_t* so = &t->slot_of[(size_t)layer * t->n_ids];
+  const int s = so[expert];
+  if (s >= 0) t->expert_in[(size_t)layer * t->n_slots + s] = -1;
+  so[expert] = -1;
+  return MOE_OK;
+}
+
+int moe_slot_lookup(const moe_slot_table* t, int layer, int expert) {
+  if (!t || layer < 0 || layer >= t->n_layers || expert < 0 || expert >= t->n_ids)
+    return MOE_EINVAL;
+  const int s = t->slot_of[(size_t)layer * t->n_ids + expert];
+  return s >= 0 ? s : MOE_ENOTRESIDENT;
+}
+
+int moe_slot_table_sync(moe_slot_table* t, void* stream) {
+  if (!t) return MOE_EINVAL;
+  const size_t so_bytes = t->slot_of.size() * sizeof(int32_t);
+  const size_t b_off = round_up(so_bytes, kAlign);
+  const size_t total = b_off + t->bundles.size() * sizeof(moe_bundle);
+  if (!t->dev) {
+    if (hipMalloc(&t->dev, total) != hipSuccess) {
+      t->dev = nullptr;
+      return MOE_ENOMEM;
+    }
+    if (hipHostMalloc(&t->pinned, total, hipHostMallocDefault) != hipSuccess) {
+      t->pinned = nullptr;
+      return MOE_ENOMEM;
+    }
+    if (hipEventCreateWithFlags(&t->copied, hipEventDisableTiming) != hipSuccess) return MOE_EHIP;
+    t->dev_bytes = total;
+    t->bundles_off = b_off;
+  }
+  // the staging buffer may still be read by the previous copy
+  if (t->copy_pending && hipEventSynchronize(t->copied) != hipSuccess) return MOE_EHIP;
+  std::memcpy(t->pinned, t->slot_of.data(), so_bytes);
+  std::memcpy(static_cast<char*>(t->pinned) + b_off, t->bundles.data(),
+              t->bundles.size() * sizeof(moe_bundle));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipMemcpyAsync(t->dev, t->pinned, total, hipMemcpyHostToDevice, st) != hipSuccess)
+    return MOE_EHIP;
+  if (hipEventRecord(t->copied, st) != hipSuccess) return MOE_EHIP;
+  t->copy_pending = true;
+  return MOE_OK;
+}
+
+// ---- hot path ----------------------------------------------------------------
+
+int moe_rmsnorm_f16(const float* xi, int T, int d, void* x_f16, void* stream) {
+  if (T < 0 || d < 1) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!xi || !x_f16) return MOE_EINVAL;
+  if (!aligned16(xi) || !aligned16(x_f16)) return MOE_EALIGN;
+  return from_hip(moe::launch_rmsnorm(xi, T, d, static_cast<__half*>(x_f16),
+                                      static_cast<hipStream_t>(stream)));
+}
+
+size_t moe_workspace_bytes(const moe_layer_spec* spec, int T) {
+  if (moe_spec_check(spec) != MOE_OK || T < 0) return 0;
+  return ws_layout(spec, T < 1 ? 1 : T).total;
+}
+
+static int route_common(const moe_layer_spec* s, const void* x, const void* W, int T,
+                        float* logits_opt, int32_t* idx, float* w, void* ws, size_t ws_bytes,
+                        void* stream) {
+  int rc = moe_spec_check(s);
+  if (rc != MOE_OK) return rc;
+  if (T < 0) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!x || !W || !idx || !w || !ws) return MOE_EINVAL;
+  if (!aligned16(x) || !aligned16(W) || !aligned16(ws) || !aligned16(idx) || !aligned16(w) ||
+      (logits_opt && !aligned16(logits_opt)))
+    return MOE_EALIGN;
+  const WsLayout L = ws_layout(s, T);
+  if (ws_bytes < L.total) return MOE_ENOMEM;
+  float* logits = logits_opt ? logits_opt : at<float>(ws, L.logits);
+  return from_hip(moe::launch_route(static_cast<const __half*>(x), static_cast<const __half*>(W),
+                                    T, s->n_experts, s->d_model, s->top_k, logits, idx, w,
+                                    at<uint32_t>(ws, L.counters),
+                                    static_cast<hipStream_t>(stream)));
+}
+
+int moe_route(const moe_layer_spec* spec, const void* x_f16, const void* w_router_f16, int T,
+              float* logits_opt, int32_t* idx, float* w, void* workspace, size_t workspace_bytes,
+              void* stream) {
+  return route_common(spec, x_f16, w_router_f16, T, logits_opt, idx, w, workspace,
+                      workspace_bytes, stream);
+}
+
+int moe_preroute(const moe_layer_spec* next, const void* x_f16, const void* w_head_f16, int T,
+                 float* logits_opt, int32_t* pred_idx, float* pred_w, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  return route_common(next, x_f16, w_head_f16, T, logits_opt, pred_idx, pred_w, workspace,
+                      workspace_bytes, stream);
+}
+
+int moe_expert_ffn_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, int layer,
+                             const void* x_f16, int T, const int32_t* idx, float* y_experts,
+                             uint32_t* status_dev, void* ws, size_t ws_bytes, void* stream) {
+  int rc = moe_spec_check(s);
+  if (rc != MOE_OK) return rc;
+  if (!t || T < 0) return MOE_EINVAL;
+  if (layer < 0 || layer >= t->n_layers || t->n_ids < s->n_experts + s->n_shared)
+    return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!x_f16 || !idx || !y_experts || !ws) return MOE_EINVAL;
+  if (!t->dev) return MOE_EINVAL;  // never synced to the device
+  if (!aligned16(x_f16) || !aligned16(y_experts) || !aligned16(ws) || !aligned16(idx))
+    return MOE_EALIGN;
+  const WsLayout L = ws_layout(s, T);
+  if (ws_bytes < L.total) return MOE_ENOMEM;
+  moe::FfnArgs a{};
+  a.d = s->d_model;
+  a.I = s->d_expert;
+  a.E = s->n_experts;
+  a.K = s->top_k;
+  a.S = s->n_shared;
+  a.r = s->lora_rank;
+  a.n_list = a.K + a.S;
+  a.lora_scale = s->lora_scale;
+  a.x = static_cast<const __half*>(x_f16);
+  a.idx = idx;
+  a.slot_of = reinterpret_cast<const int32_t*>(t->dev) + (size_t)layer * t->n_ids;
+  a.bundles = reinterpret_cast<const moe_bundle*>(static_cast<const char*>(t->dev) + t->bundles_off) +
+              (size_t)layer * t->n_slots;
+  a.status = status_dev;
+  a.gx = at<float>(ws, L.gx);
+  a.ux = at<float>(ws, L.ux);
+  a.h = at<float>(ws, L.h);
+  a.ag = at<float>(ws, L.ag);
+  a.au = at<float>(ws, L.au);
+  a.adpart = at<float>(ws, L.adpart);
+  a.y_experts = y_experts;
+  return from_hip(moe::launch_ffn(a, T, static_cast<hipStream_t>(stream)));
+}
+
+int moe_combine(const moe_layer_spec* s, const float* y_experts, const float* w, int T, float* y,
+                void* stream) {
+  int rc = moe_spec_check(s);
+  if (rc != MOE_OK) return rc;
+  if (T < 0) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!y_experts || !w || !y) return MOE_EINVAL;
+  if (!aligned16(y_experts) || !aligned16(w) || !aligned16(y)) return MOE_EALIGN;
+  return from_hip(moe::launch_combine(y_experts, w, T, s->top_k, s->n_shared, s->d_model, y,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+int moe_topk(const moe_layer_spec* s, const float* logits, int T, int32_t* idx, float* w,
+             void* stream) {
+  int rc = moe_spec_check(s);
+  if (rc != MOE_OK) return rc;
+  if (T < 0) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!logits || !idx || !w) return MOE_EINVAL;
+  if (!aligned16(logits) || !aligned16(idx) || !aligned16(w)) return MOE_EALIGN;
+  return from_hip(moe::launch_topk(logits, T, s->n_experts, s->top_k, idx, w,
+                                   static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,101 @@
+// Device-side helpers shared by the gfx950 kernels of the MoE decode path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+#include "../../include/moe_api.h"
+
+namespace moe {
+
+constexpr int kWave = 64;
+
+// 16-byte vector load / store through the vector memory path.
+struct alignas(16) U4 {
+  uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ U4 ld16(const void* p) {
+  return *reinterpret_cast<const U4*>(p);
+}
+
+// Cross-workgroup data (written by one workgroup and read by another in the
+// same launch) goes through agent-scope atomics so that it is coherent
+// across the XCDs' L2 caches.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Sum over groups of `width` consecutive lanes (width a power of two <= 64).
+__device__ __forceinline__ float group_sum(float v, int width) {
+  for (int off = width >> 1; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) { return group_sum(v, kWave); }
+
+// Dot product of 32 int4 codes (16 bytes, even input in the low nibble) with
+// 32 fp32 activations.  Codes are exact small integers in fp32.
+__device__ __forceinline__ float dot32_q4(const U4& q, const float* x) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = w[i] & 0x0F0F0F0Fu;
+    const uint32_t hi = (w[i] >> 4) & 0x0F0F0F0Fu;
+    const float* xv = x + 8 * i;
+    a0 = fmaf((float)(lo & 0xFFu), xv[0], a0);
+    a1 = fmaf((float)(hi & 0xFFu), xv[1], a1);
+    a0 = fmaf((float)((lo >> 8) & 0xFFu), xv[2], a0);
+    a1 = fmaf((float)((hi >> 8) & 0xFFu), xv[3], a1);
+    a0 = fmaf((float)((lo >> 16) & 0xFFu), xv[4], a0);
+    a1 = fmaf((float)((hi >> 16) & 0xFFu), xv[5], a1);
+    a0 = fmaf((float)(lo >> 24), xv[6], a0);
+    a1 = fmaf((float)(hi >> 24), xv[7], a1);
+  }
+  return a0 + a1;
+}
+
+// Dot product of 8 fp16 weights with 8 fp16 activations, fp32 accumulate.
+__device__ __forceinline__ float dot8_h(const U4& a, const U4& b, float acc) {
+  const uint32_t wa[4] = {a.x, a.y, a.z, a.w};
+  const uint32_t wb[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    __half2 ha = *reinterpret_cast<const __half2*>(&wa[i]);
+    __half2 hb = *reinterpret_cast<const __half2*>(&wb[i]);
+    float2 fa = __half22float2(ha);
+    float2 fb = __half22float2(hb);
+    acc = fmaf(fa.x, fb.x, acc);
+    acc = fmaf(fa.y, fb.y, acc);
+  }
+  return acc;
+}
+
+__device__ __forceinline__ float2 h2f2(uint32_t bits) {
+  return __half22float2(*reinterpret_cast<const __half2*>(&bits));
+}
+
+// Resolve list position k of token t to a bundle, or nullptr (status set).
+__device__ __forceinline__ const moe_bundle* resolve_expert(int k, int K, int E, const int32_t* idx_t,
+                                                            const int32_t* slot_of,
+                                                            const moe_bundle* bundles,
+                                                            uint32_t* status, bool report) {
+  int e = (k < K) ? idx_t[k] : E + (k - K);
+  if (k < K && (e < 0 || e >= E)) {
+    if (report && status) atomicOr(status, MOE_STATUS_BAD_INDEX);
+    return nullptr;
+  }
+  int s = slot_of[e];
+  if (s < 0) {
+    if (report && status) atomicOr(status, MOE_STATUS_SLOT_MISS);
+    return nullptr;
+  }
+  return bundles + s;
+}
+
+}  // namespace moe

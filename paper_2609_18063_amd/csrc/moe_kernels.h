@@ -1,0 +1,37 @@
+// Kernel launch interface used by the C ABI (host side of moe_kernels.hip).
+#pragma once
+
+#include "moe_device.h"
+
+namespace moe {
+
+// Everything the expert kernels need for one layer call.
+struct FfnArgs {
+  int d, I, E, K, S, r, n_list;   // n_list = K + S experts per token
+  float lora_scale;
+  const __half* x;                // [T][d]
+  const int32_t* idx;             // [T][K]
+  const int32_t* slot_of;         // [E + S] of this layer
+  const moe_bundle* bundles;      // [n_slots] of this layer
+  uint32_t* status;               // may be null
+  // workspace
+  float* gx;                      // [T][n][I]
+  float* ux;                      // [T][n][I]
+  float* h;                       // [T][n][I]
+  float* ag;                      // [T][n][r]
+  float* au;                      // [T][n][r]
+  float* adpart;                  // [T][n][I/64][r]
+  float* y_experts;               // [T][n][d]
+};
+
+hipError_t launch_rmsnorm(const float* xi, int T, int d, __half* x, hipStream_t st);
+hipError_t launch_route(const __half* x, const __half* W, int T, int E, int d, int K,
+                        float* logits, int32_t* idx, float* w, uint32_t* counters,
+                        hipStream_t st);
+hipError_t launch_topk(const float* logits, int T, int E, int K, int32_t* idx, float* w,
+                       hipStream_t st);
+hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st);
+hipError_t launch_combine(const float* ye, const float* w, int T, int K, int S, int d, float* y,
+                          hipStream_t st);
+
+}  // namespace moe

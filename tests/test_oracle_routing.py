@@ -164,3 +164,27 @@ def test_sigmoid_group_hand_case():
     assert inds.tolist() == [4, 0]
     s3, s2 = 1 / (1 + np.exp(-3.0)), 1 / (1 + np.exp(-2.0))
     assert np.allclose(w, [2.5 * s3 / (s3 + s2), 2.5 * s2 / (s3 + s2)], rtol=1e-14)
+
+
+def test_rmsnorm_single_rounding_against_high_precision():
+    """The layer input is the fp16 nearest (ties to even) to the exact
+    normalized value: checked with 40-digit decimal arithmetic."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = 40
+    rs = np.random.default_rng(9)
+    xi = rs.normal(0, 2.0, size=(8, 2048)).astype(np.float32)
+    got = routing.rms_norm_f16(xi)
+    for t in range(xi.shape[0]):
+        ds = [Decimal(float(v)) for v in xi[t]]
+        ms = sum(v * v for v in ds) / Decimal(xi.shape[1])
+        r = Decimal(1) / (ms + Decimal("1e-6")).sqrt()
+        for j in range(xi.shape[1]):
+            v = ds[j] * r
+            c = np.float16(float(v))
+            cands = [np.nextafter(c, np.float16(-np.inf)), c, np.nextafter(c, np.float16(np.inf))]
+            dist = [abs(Decimal(float(cc)) - v) for cc in cands]
+            best = min(dist)
+            near = [cc for cc, dd in zip(cands, dist) if dd == best]
+            if len(near) > 1:
+                near = [cc for cc in near if int(cc.view(np.uint16)) % 2 == 0]
+            assert got[t, j].view(np.uint16) == near[0].view(np.uint16), (t, j)

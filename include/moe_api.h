@@ -195,6 +195,18 @@ int moe_combine(const moe_layer_spec* spec, const float* y_experts, const float*
 int moe_topk(const moe_layer_spec* spec, const float* logits, int T, int32_t* idx, float* w,
              void* stream);
 
+/* ---- profiling (not part of the hot path) ------------------------------- */
+#define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */
+
+/*
+ * Arm per-launch timing. The next launch of kernel `which` on the calling
+ * host thread records `start_event` when the kernel starts executing and
+ * `stop_event` when it ends (hipEvent_t values created with timing enabled).
+ * The hook then disarms itself. Do not arm it during graph capture.
+ * Returns MOE_EINVAL for an unknown `which` or NULL events.
+ */
+int moe_profile_arm(int which, void* start_event, void* stop_event);
+
 #ifdef __cplusplus
 }
 #endif

@@ -67,7 +67,10 @@ SIGNATURES = {
                             c_void_p]),
     "moe_topk": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p, c_void_p,
                          c_void_p]),
+    "moe_profile_arm": (c_int, [c_int, c_void_p, c_void_p]),
 }
+
+MOE_PROF_FFN_MAIN = 0
 
 
 def lib():
@@ -233,3 +236,9 @@ def topk(spec, logits, idx, w, stream=None):
     T = logits.shape[0]
     _check(lib().moe_topk(ctypes.byref(spec), _ptr(logits), T, _ptr(idx), _ptr(w), _stream(stream)),
            "moe_topk")
+
+
+def profile_arm(which, start_event, stop_event):
+    """Time the next launch of kernel ``which`` with two hipEvent_t handles (ints)."""
+    _check(lib().moe_profile_arm(which, ctypes.c_void_p(start_event), ctypes.c_void_p(stop_event)),
+           "moe_profile_arm")

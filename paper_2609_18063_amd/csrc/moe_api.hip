@@ -62,6 +62,12 @@ WsLayout ws_layout(const moe_layer_spec* s, int T) {
 
 int from_hip(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_EHIP; }
 
+// Armed per-launch timing events (moe_profile_arm), per host thread.
+struct ProfArm {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+thread_local ProfArm g_prof_ffn;
+
 template <typename T>
 T* at(void* base, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(base) + off);
@@ -288,7 +294,9 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, i
   a.au = at<float>(ws, L.au);
   a.adpart = at<float>(ws, L.adpart);
   a.y_experts = y_experts;
-  return from_hip(moe::launch_ffn(a, T, static_cast<hipStream_t>(stream)));
+  ProfArm arm = g_prof_ffn;
+  g_prof_ffn = ProfArm{};
+  return from_hip(moe::launch_ffn(a, T, static_cast<hipStream_t>(stream), arm.start, arm.stop));
 }
 
 int moe_combine(const moe_layer_spec* s, const float* y_experts, const float* w, int T, float* y,
@@ -313,6 +321,13 @@ int moe_topk(const moe_layer_spec* s, const float* logits, int T, int32_t* idx, 
   if (!aligned16(logits) || !aligned16(idx) || !aligned16(w)) return MOE_EALIGN;
   return from_hip(moe::launch_topk(logits, T, s->n_experts, s->top_k, idx, w,
                                    static_cast<hipStream_t>(stream)));
+}
+
+int moe_profile_arm(int which, void* start_event, void* stop_event) {
+  if (which != MOE_PROF_FFN_MAIN || !start_event || !stop_event) return MOE_EINVAL;
+  g_prof_ffn.start = static_cast<hipEvent_t>(start_event);
+  g_prof_ffn.stop = static_cast<hipEvent_t>(stop_event);
+  return MOE_OK;
 }
 
 }  // extern "C"

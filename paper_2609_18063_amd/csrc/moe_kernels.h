@@ -30,7 +30,10 @@ hipError_t launch_route(const __half* x, const __half* W, int T, int E, int d, i
                         hipStream_t st);
 hipError_t launch_topk(const float* logits, int T, int E, int K, int32_t* idx, float* w,
                        hipStream_t st);
-hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st);
+// prof_start / prof_stop: if non-null, the gate/up kernel is launched with
+// hipExtLaunchKernelGGL and records them around its execution.
+hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st, hipEvent_t prof_start,
+                      hipEvent_t prof_stop);
 hipError_t launch_combine(const float* ye, const float* w, int T, int K, int S, int d, float* y,
                           hipStream_t st);
 

@@ -468,12 +468,16 @@ hipError_t launch_topk(const float* logits, int T, int E, int K, int32_t* idx, f
 }
 
 template <int LPR, int CPL>
-static void gateup(const FfnArgs& a, int T, hipStream_t st) {
+static void gateup(const FfnArgs& a, int T, hipStream_t st, hipEvent_t ps, hipEvent_t pe) {
   constexpr int RP = 4;
   constexpr int PAIRS = 4 * RP * (kWave / LPR);
   const int nblk = (a.I + PAIRS - 1) / PAIRS + (2 * a.r + 3) / 4;
-  hipLaunchKernelGGL((ffn_gateup_kernel<LPR, CPL, RP>), dim3(nblk * a.n_list, T), dim3(256), 0,
-                     st, a);
+  if (ps && pe)
+    hipExtLaunchKernelGGL((ffn_gateup_kernel<LPR, CPL, RP>), dim3(nblk * a.n_list, T), dim3(256),
+                          0, st, ps, pe, 0, a);
+  else
+    hipLaunchKernelGGL((ffn_gateup_kernel<LPR, CPL, RP>), dim3(nblk * a.n_list, T), dim3(256), 0,
+                       st, a);
 }
 
 template <int LPR, int CPL>
@@ -485,14 +489,15 @@ static void down(const FfnArgs& a, int T, hipStream_t st) {
                      a);
 }
 
-static bool dispatch_gateup(const FfnArgs& a, int T, hipStream_t st) {
+static bool dispatch_gateup(const FfnArgs& a, int T, hipStream_t st, hipEvent_t ps,
+                            hipEvent_t pe) {
   switch (a.d) {
-    case 256: gateup<8, 1>(a, T, st); return true;
-    case 512: gateup<16, 1>(a, T, st); return true;
-    case 1024: gateup<32, 1>(a, T, st); return true;
-    case 2048: gateup<64, 1>(a, T, st); return true;
-    case 4096: gateup<64, 2>(a, T, st); return true;
-    case 8192: gateup<64, 4>(a, T, st); return true;
+    case 256: gateup<8, 1>(a, T, st, ps, pe); return true;
+    case 512: gateup<16, 1>(a, T, st, ps, pe); return true;
+    case 1024: gateup<32, 1>(a, T, st, ps, pe); return true;
+    case 2048: gateup<64, 1>(a, T, st, ps, pe); return true;
+    case 4096: gateup<64, 2>(a, T, st, ps, pe); return true;
+    case 8192: gateup<64, 4>(a, T, st, ps, pe); return true;
   }
   return false;
 }
@@ -509,8 +514,9 @@ static bool dispatch_down(const FfnArgs& a, int T, hipStream_t st) {
   return false;
 }
 
-hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st) {
-  if (!dispatch_gateup(a, T, st)) return hipErrorInvalidValue;
+hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st, hipEvent_t prof_start,
+                      hipEvent_t prof_stop) {
+  if (!dispatch_gateup(a, T, st, prof_start, prof_stop)) return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(ffn_h_kernel, dim3((a.I >> 6) * a.n_list, T), dim3(64), 0, st, a);

@@ -22,7 +22,9 @@
  *   safe to capture in a HIP graph.
  * - Return value: MOE_OK (0) or a negative MOE_E* code. A failed argument
  *   check enqueues nothing.
- * - Alignment: device pointers must be 16-byte aligned (MOE_EALIGN otherwise).
+ * - Alignment: device pointers must be 16-byte aligned, except the small
+ *   int32/fp32 arrays idx, w, pred_idx, pred_w and the status word, which
+ *   need 4 bytes (MOE_EALIGN otherwise).
  * - A kernel that meets an expert id outside [0, E) or a non-resident expert
  *   ORs a MOE_STATUS_* bit into the caller's status word. That expert then
  *   contributes zeros. The caller reads the status word after the step.
@@ -188,12 +190,33 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* spec, const moe_slot_table* t
 int moe_combine(const moe_layer_spec* spec, const float* y_experts, const float* w, int T,
                 float* y, void* stream);
 
+/* As moe_combine, but adds into y_inout: y_inout[t] += (the combine of token t).
+ * A decode chain uses it to add the layer output into the residual. */
+int moe_combine_add(const moe_layer_spec* spec, const float* y_experts, const float* w, int T,
+                    float* y_inout, void* stream);
+
 /*
  * Softmax-top-k on given logits (App. A): logits device fp32 [T][E] ->
  * idx [T][K], w [T][K]. Same selection and weights as moe_route.
  */
 int moe_topk(const moe_layer_spec* spec, const float* logits, int T, int32_t* idx, float* w,
              void* stream);
+
+/* ---- decode-chain stand-in for attention ---------------------------------
+ * The paper's decoder runs attention before each MoE layer, and the head of
+ * layer N reads layer N's post-attention norm output (Sec. 3.2, Motivation).
+ * A multi-layer decode chain without attention uses these two O(d) steps on
+ * an fp32 residual r [d] (one token), so that each layer's input depends on
+ * every earlier layer and token:
+ *   moe_chain_token_start: r = xi + rmsnorm(r)   (r = 0 before the first token)
+ *   moe_chain_mix_rmsnorm: r = r + D * r[perm], then x = fp16(rmsnorm(r))
+ * rmsnorm(v) = v / sqrt(mean(v^2) + 1e-6), computed in fp64. The residual
+ * update of token_start is rounded once to fp32, and x is rounded once to
+ * fp16. D: fp16 [d]. perm: int32 [d], a permutation of 0..d-1.
+ * xi, r: fp32 [d]. x_f16: fp16 [d]. d <= 8192. */
+int moe_chain_token_start(const float* xi, int d, float* r_inout, void* stream);
+int moe_chain_mix_rmsnorm(const void* mix_d_f16, const int32_t* perm, int d, float* r_inout,
+                          void* x_f16, void* stream);
 
 /* ---- profiling (not part of the hot path) ------------------------------- */
 #define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */

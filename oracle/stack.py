@@ -40,7 +40,8 @@ def decode_chain(tokens_xi, layers, k, lora_scale, consumers=None):
     ``layers[N]`` is a dict with ``router`` (fp16 [E, d]), ``head`` (fp16
     [E, d] or None), ``mix_d`` (fp16 [d]), ``mix_perm`` (int [d]),
     ``routed(e)`` -> bundle and ``shared`` (list of bundles).
-    Returns a per-token list of per-layer records (x16, idx, w, y, source).
+    Returns a per-token list of per-layer records (x16, idx, w, y, y_experts,
+    source, and the head's prediction).
     """
     nl = len(layers)
     if consumers is None:
@@ -65,7 +66,8 @@ def decode_chain(tokens_xi, layers, k, lora_scale, consumers=None):
             ys = [expert_forward(lay["routed"](int(e)), x16, lora_scale)[0] for e in idx]
             ysh = [expert_forward(b, x16, lora_scale)[0] for b in lay["shared"]]
             y = combine(w, ys, ysh)
-            rec = {"x16": x16, "idx": np.asarray(idx), "w": np.asarray(w), "y": y, "src": src}
+            rec = {"x16": x16, "idx": np.asarray(idx), "w": np.asarray(w), "y": y, "src": src,
+                   "y_experts": ys + ysh}
             if n + 1 < nl and lay.get("head") is not None:
                 pl, pi, pw = preroute(lay["head"], x16, k)
                 pred[(t + 1, n + 1)] = (pi, pw)

@@ -68,6 +68,10 @@ SIGNATURES = {
     "moe_topk": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p, c_void_p,
                          c_void_p]),
     "moe_profile_arm": (c_int, [c_int, c_void_p, c_void_p]),
+    "moe_combine_add": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
+                                c_void_p]),
+    "moe_chain_token_start": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
+    "moe_chain_mix_rmsnorm": (c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_void_p]),
 }
 
 MOE_PROF_FFN_MAIN = 0
@@ -242,3 +246,19 @@ def profile_arm(which, start_event, stop_event):
     """Time the next launch of kernel ``which`` with two hipEvent_t handles (ints)."""
     _check(lib().moe_profile_arm(which, ctypes.c_void_p(start_event), ctypes.c_void_p(stop_event)),
            "moe_profile_arm")
+
+
+def combine_add(spec, y_experts, w, y_inout, stream=None):
+    T = y_inout.shape[0]
+    _check(lib().moe_combine_add(ctypes.byref(spec), _ptr(y_experts), _ptr(w), T, _ptr(y_inout),
+                                 _stream(stream)), "moe_combine_add")
+
+
+def chain_token_start(xi, r, stream=None):
+    _check(lib().moe_chain_token_start(_ptr(xi), r.numel(), _ptr(r), _stream(stream)),
+           "moe_chain_token_start")
+
+
+def chain_mix_rmsnorm(mix_d, perm, r, x, stream=None):
+    _check(lib().moe_chain_mix_rmsnorm(_ptr(mix_d), _ptr(perm), r.numel(), _ptr(r), _ptr(x),
+                                       _stream(stream)), "moe_chain_mix_rmsnorm")

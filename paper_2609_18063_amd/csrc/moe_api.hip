@@ -29,6 +29,7 @@ constexpr size_t kAlign = 256;
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 bool pow2_dim(int v) {
   return v == 256 || v == 512 || v == 1024 || v == 2048 || v == 4096 || v == 8192;
@@ -231,7 +232,7 @@ static int route_common(const moe_layer_spec* s, const void* x, const void* W, i
   if (T < 0) return MOE_EINVAL;
   if (T == 0) return MOE_OK;
   if (!x || !W || !idx || !w || !ws) return MOE_EINVAL;
-  if (!aligned16(x) || !aligned16(W) || !aligned16(ws) || !aligned16(idx) || !aligned16(w) ||
+  if (!aligned16(x) || !aligned16(W) || !aligned16(ws) || !aligned4(idx) || !aligned4(w) ||
       (logits_opt && !aligned16(logits_opt)))
     return MOE_EALIGN;
   const WsLayout L = ws_layout(s, T);
@@ -268,7 +269,8 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, i
   if (T == 0) return MOE_OK;
   if (!x_f16 || !idx || !y_experts || !ws) return MOE_EINVAL;
   if (!t->dev) return MOE_EINVAL;  // never synced to the device
-  if (!aligned16(x_f16) || !aligned16(y_experts) || !aligned16(ws) || !aligned16(idx))
+  if (!aligned16(x_f16) || !aligned16(y_experts) || !aligned16(ws) || !aligned4(idx) ||
+      (status_dev && !aligned4(status_dev)))
     return MOE_EALIGN;
   const WsLayout L = ws_layout(s, T);
   if (ws_bytes < L.total) return MOE_ENOMEM;
@@ -299,16 +301,42 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, i
   return from_hip(moe::launch_ffn(a, T, static_cast<hipStream_t>(stream), arm.start, arm.stop));
 }
 
-int moe_combine(const moe_layer_spec* s, const float* y_experts, const float* w, int T, float* y,
-                void* stream) {
+static int combine_common(const moe_layer_spec* s, const float* y_experts, const float* w, int T,
+                          float* y, int accumulate, void* stream) {
   int rc = moe_spec_check(s);
   if (rc != MOE_OK) return rc;
   if (T < 0) return MOE_EINVAL;
   if (T == 0) return MOE_OK;
   if (!y_experts || !w || !y) return MOE_EINVAL;
-  if (!aligned16(y_experts) || !aligned16(w) || !aligned16(y)) return MOE_EALIGN;
+  if (!aligned16(y_experts) || !aligned4(w) || !aligned16(y)) return MOE_EALIGN;
   return from_hip(moe::launch_combine(y_experts, w, T, s->top_k, s->n_shared, s->d_model, y,
-                                      static_cast<hipStream_t>(stream)));
+                                      accumulate, static_cast<hipStream_t>(stream)));
+}
+
+int moe_combine(const moe_layer_spec* s, const float* y_experts, const float* w, int T, float* y,
+                void* stream) {
+  return combine_common(s, y_experts, w, T, y, 0, stream);
+}
+
+int moe_combine_add(const moe_layer_spec* s, const float* y_experts, const float* w, int T,
+                    float* y_inout, void* stream) {
+  return combine_common(s, y_experts, w, T, y_inout, 1, stream);
+}
+
+int moe_chain_token_start(const float* xi, int d, float* r_inout, void* stream) {
+  if (!xi || !r_inout || d < 1 || d > 8192) return MOE_EINVAL;
+  if (!aligned16(xi) || !aligned16(r_inout)) return MOE_EALIGN;
+  return from_hip(moe::launch_chain_token_start(xi, d, r_inout, static_cast<hipStream_t>(stream)));
+}
+
+int moe_chain_mix_rmsnorm(const void* mix_d_f16, const int32_t* perm, int d, float* r_inout,
+                          void* x_f16, void* stream) {
+  if (!mix_d_f16 || !perm || !r_inout || !x_f16 || d < 1 || d > 8192) return MOE_EINVAL;
+  if (!aligned16(mix_d_f16) || !aligned16(perm) || !aligned16(r_inout) || !aligned16(x_f16))
+    return MOE_EALIGN;
+  return from_hip(moe::launch_chain_mix_rmsnorm(static_cast<const __half*>(mix_d_f16), perm, d,
+                                                r_inout, static_cast<__half*>(x_f16),
+                                                static_cast<hipStream_t>(stream)));
 }
 
 int moe_topk(const moe_layer_spec* s, const float* logits, int T, int32_t* idx, float* w,
@@ -318,7 +346,7 @@ int moe_topk(const moe_layer_spec* s, const float* logits, int T, int32_t* idx, 
   if (T < 0) return MOE_EINVAL;
   if (T == 0) return MOE_OK;
   if (!logits || !idx || !w) return MOE_EINVAL;
-  if (!aligned16(logits) || !aligned16(idx) || !aligned16(w)) return MOE_EALIGN;
+  if (!aligned16(logits) || !aligned4(idx) || !aligned4(w)) return MOE_EALIGN;
   return from_hip(moe::launch_topk(logits, T, s->n_experts, s->top_k, idx, w,
                                    static_cast<hipStream_t>(stream)));
 }

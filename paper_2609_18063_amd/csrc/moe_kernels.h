@@ -35,6 +35,9 @@ hipError_t launch_topk(const float* logits, int T, int E, int K, int32_t* idx, f
 hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st, hipEvent_t prof_start,
                       hipEvent_t prof_stop);
 hipError_t launch_combine(const float* ye, const float* w, int T, int K, int S, int d, float* y,
-                          hipStream_t st);
+                          int accumulate, hipStream_t st);
+hipError_t launch_chain_token_start(const float* xi, int d, float* r, hipStream_t st);
+hipError_t launch_chain_mix_rmsnorm(const __half* mix_d, const int32_t* perm, int d, float* r,
+                                    __half* x, hipStream_t st);
 
 }  // namespace moe

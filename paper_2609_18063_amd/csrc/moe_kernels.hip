@@ -430,7 +430,7 @@ __global__ void __launch_bounds__(256) ffn_down_kernel(FfnArgs a) {
 // ------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ ye,
                                                       const float* __restrict__ w, int K, int S,
-                                                      int d, float* __restrict__ y) {
+                                                      int d, float* __restrict__ y, int accumulate) {
   const int t = blockIdx.y;
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= d) return;
@@ -439,7 +439,57 @@ __global__ void __launch_bounds__(256) combine_kernel(const float* __restrict__ 
   float acc = 0.f;
   for (int k = 0; k < K; ++k) acc = fmaf(w[(size_t)t * K + k], base[(size_t)k * d], acc);
   for (int s = 0; s < S; ++s) acc += base[(size_t)(K + s) * d];
-  y[(size_t)t * d + j] = acc;
+  float* out = y + (size_t)t * d + j;
+  *out = accumulate ? *out + acc : acc;
+}
+
+// ------------------------------------------------------------------------
+// Decode-chain stand-in for attention (one workgroup per call):
+//   token start:  r = xi + rmsnorm(r)         (norm in fp64, r kept fp32)
+//   layer input:  r = r + D * r[perm];  x = fp16(rmsnorm(r))
+// ------------------------------------------------------------------------
+__device__ double block_sum_sq(const float* v, int d, double* red) {
+  double acc = 0.0;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    const double a = v[j];
+    acc += a * a;
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = blockDim.x >> 1; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  const double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+__global__ void __launch_bounds__(256) chain_token_start_kernel(const float* __restrict__ xi, int d,
+                                                                float* __restrict__ r) {
+  __shared__ double red[256];
+  const double inv = 1.0 / sqrt(block_sum_sq(r, d, red) / (double)d + 1e-6);
+  for (int j = threadIdx.x; j < d; j += blockDim.x)
+    r[j] = (float)((double)xi[j] + (double)r[j] * inv);
+}
+
+__global__ void __launch_bounds__(256) chain_mix_rmsnorm_kernel(const __half* __restrict__ mix_d,
+                                                                const int32_t* __restrict__ perm,
+                                                                int d, float* __restrict__ r,
+                                                                __half* __restrict__ x) {
+  extern __shared__ float rs[];
+  __shared__ double red[256];
+  for (int j = threadIdx.x; j < d; j += blockDim.x) rs[j] = r[j];
+  __syncthreads();
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    const int p = perm[j];
+    const float v = (p >= 0 && p < d) ? rs[p] : 0.f;
+    r[j] = fmaf(__half2float(mix_d[j]), v, rs[j]);
+  }
+  __syncthreads();
+  const double inv = 1.0 / sqrt(block_sum_sq(r, d, red) / (double)d + 1e-6);
+  for (int j = threadIdx.x; j < d; j += blockDim.x)
+    x[j] = __half(static_cast<_Float16>((double)r[j] * inv));
 }
 
 // ------------------------------------------------------------------------
@@ -527,8 +577,21 @@ hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st, hipEvent_t prof_s
 }
 
 hipError_t launch_combine(const float* ye, const float* w, int T, int K, int S, int d, float* y,
-                          hipStream_t st) {
-  hipLaunchKernelGGL(combine_kernel, dim3((d + 255) / 256, T), dim3(256), 0, st, ye, w, K, S, d, y);
+                          int accumulate, hipStream_t st) {
+  hipLaunchKernelGGL(combine_kernel, dim3((d + 255) / 256, T), dim3(256), 0, st, ye, w, K, S, d, y,
+                     accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_chain_token_start(const float* xi, int d, float* r, hipStream_t st) {
+  hipLaunchKernelGGL(chain_token_start_kernel, dim3(1), dim3(256), 0, st, xi, d, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_chain_mix_rmsnorm(const __half* mix_d, const int32_t* perm, int d, float* r,
+                                    __half* x, hipStream_t st) {
+  hipLaunchKernelGGL(chain_mix_rmsnorm_kernel, dim3(1), dim3(256), (size_t)d * 4, st, mix_d, perm, d,
+                     r, x);
   return hipGetLastError();
 }
 

@@ -133,6 +133,9 @@ def test_hot_path_argument_checks_need_no_gpu(B):
     assert L.moe_route(sp, ws, ws, -1, None, ws, ws, ws, 1 << 20, None) == B.MOE_EINVAL
     assert L.moe_combine(sp, None, None, 0, None, None) == B.MOE_OK
     assert L.moe_combine(sp, mis, ws, 2, ws, None) == B.MOE_EALIGN
+    odd = ctypes.c_void_p(0x100002)
+    assert L.moe_combine(sp, ws, odd, 2, ws, None) == B.MOE_EALIGN
+    assert L.moe_route(sp, ws, ws, 1, None, odd, ws, ws, 1 << 20, None) == B.MOE_EALIGN
     assert L.moe_topk(sp, None, 1, ws, ws, None) == B.MOE_EINVAL
     assert L.moe_rmsnorm_f16(None, 0, 512, None, None) == B.MOE_OK
     assert L.moe_rmsnorm_f16(mis, 1, 512, ws, None) == B.MOE_EALIGN

@@ -51,6 +51,8 @@ extern "C" {
 /* ---- device status bits (OR-ed into *status_dev by the kernels) ---------- */
 #define MOE_STATUS_SLOT_MISS 1u  /* routed expert has no resident slot       */
 #define MOE_STATUS_BAD_INDEX 2u  /* expert id outside [0, E)                  */
+#define MOE_STATUS_ENGINE_ABORT 4u /* decode engine left a wait on its time limit,
+                                      or ran on an unexpected CU/XCD layout     */
 
 /* ---- layer description (the MoESpec of Sec. 3) --------------------------- */
 #define MOE_ROUTING_SOFTMAX_TOPK 0   /* App. A, Softmax-topk                    */
@@ -217,6 +219,66 @@ int moe_topk(const moe_layer_spec* spec, const float* logits, int T, int32_t* id
 int moe_chain_token_start(const float* xi, int d, float* r_inout, void* stream);
 int moe_chain_mix_rmsnorm(const void* mix_d_f16, const int32_t* perm, int d, float* r_inout,
                           void* x_f16, void* stream);
+
+/* ---- persistent decode engine -------------------------------------------
+ * The same hot path (layer input, routing or prediction-as-routing, experts
+ * with LoRA, combine, head prediction), but many single-token layer steps
+ * run in ONE cooperative launch of 256 workgroups (one per CU; the work
+ * split assumes 8 XCDs of 32 CUs). Workgroups exchange intermediate vectors
+ * through the workspace, so no step pays a kernel launch. This amortises
+ * the per-step graph and launch cost (the paper's engine spends 44 ms of
+ * graph building per step, Sec. 6) down to device-side waits.
+ *
+ * Every wait is bounded. On a time limit the engine ORs
+ * MOE_STATUS_ENGINE_ABORT into *status, sets a sticky abort word in the
+ * workspace, and all workgroups return. After an abort, zero-fill the
+ * workspace before the next call. Supported shapes: moe_engine_supported.
+ * The workspace (moe_engine_workspace_bytes) must be zero-filled before its
+ * first use. Consecutive calls on one workspace must be ordered on one stream.
+ */
+typedef struct moe_engine_layer {
+  const void* router;      /* fp16 [E][d] (the layer's own router)              */
+  const void* head;        /* fp16 [E][d] prerouter head, or NULL               */
+  const void* mix_d;       /* chain only: fp16 [d] (see moe_chain_mix_rmsnorm)  */
+  const int32_t* mix_perm; /* chain only: int32 [d]                             */
+} moe_engine_layer;
+
+/* MOE_OK if the engine handles this layer shape on this device, else MOE_EINVAL. */
+int moe_engine_supported(const moe_layer_spec* spec);
+/* Workspace bytes of the engine for chains of up to n_layers layers. */
+size_t moe_engine_workspace_bytes(const moe_layer_spec* spec, int n_layers);
+
+/*
+ * Independent single-token steps. Step s reads table layer step_layer[s]
+ * (a device int32 array). It computes x = fp16(rmsnorm(xi[s])), the layer's
+ * own routing, the experts, the combine into y[s] (fp32 [d]), and the head's
+ * prediction. layers: a device array indexed by table layer.
+ * The *_rec arrays are optional device arrays [n_steps][K]: routing used and
+ * head prediction.
+ */
+int moe_engine_layers(const moe_layer_spec* spec, const moe_slot_table* table,
+                      const moe_engine_layer* layers, const int32_t* step_layer, int n_steps,
+                      const float* xi, float* y, int32_t* idx_rec, float* w_rec,
+                      int32_t* pidx_rec, float* pw_rec, uint32_t* status, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+/*
+ * Decode chain (Sec. 3.2): n_tokens tokens, numbered first_token .. , each
+ * through the n_layers layers held at table layers 0..n_layers-1, on the
+ * residual r_state (device fp32 [d], in/out; zero before the first token):
+ *   r = xi[t] + rmsnorm(r) at the start of each token, then per layer N:
+ *   r = r + D_N * r[perm_N];  x = fp16(rmsnorm(r));  r = r + layer_N(x).
+ * Layer 0 and every layer of token 0 route by their own router. Layer N >= 1
+ * at token t >= 1 routes by the prediction that the head of layer N-1 made at
+ * token t-1. The predictions persist in the workspace between calls.
+ * Optional records (device, [n_tokens*n_layers] rows in token-major order):
+ * x_rec fp16 [.][d], idx_rec / w_rec / pidx_rec / pw_rec [.][K], y_rec fp32 [.][d].
+ */
+int moe_engine_chain(const moe_layer_spec* spec, const moe_slot_table* table,
+                     const moe_engine_layer* layers, int n_layers, int first_token, int n_tokens,
+                     const float* xi, float* r_state, void* x_rec, int32_t* idx_rec, float* w_rec,
+                     int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status,
+                     void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- profiling (not part of the hot path) ------------------------------- */
 #define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */

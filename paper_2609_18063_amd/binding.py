@@ -36,6 +36,11 @@ class MoeBundle(ctypes.Structure):
     _fields_ = [("gate", MoeProj), ("up", MoeProj), ("down", MoeProj)]
 
 
+class MoeEngineLayer(ctypes.Structure):
+    _fields_ = [("router", c_void_p), ("head", c_void_p), ("mix_d", c_void_p),
+                ("mix_perm", c_void_p)]
+
+
 class MoeError(RuntimeError):
     def __init__(self, code, what):
         self.code = code
@@ -72,6 +77,14 @@ SIGNATURES = {
                                 c_void_p]),
     "moe_chain_token_start": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
     "moe_chain_mix_rmsnorm": (c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_void_p]),
+    "moe_engine_supported": (c_int, [ctypes.POINTER(MoeLayerSpec)]),
+    "moe_engine_workspace_bytes": (c_size_t, [ctypes.POINTER(MoeLayerSpec), c_int]),
+    "moe_engine_layers": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_void_p, c_int,
+                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                  c_void_p, c_void_p, c_size_t, c_void_p]),
+    "moe_engine_chain": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_int,
+                                 c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                 c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
 }
 
 MOE_PROF_FFN_MAIN = 0
@@ -262,3 +275,50 @@ def chain_token_start(xi, r, stream=None):
 def chain_mix_rmsnorm(mix_d, perm, r, x, stream=None):
     _check(lib().moe_chain_mix_rmsnorm(_ptr(mix_d), _ptr(perm), r.numel(), _ptr(r), _ptr(x),
                                        _stream(stream)), "moe_chain_mix_rmsnorm")
+
+
+MOE_STATUS_ENGINE_ABORT = 4
+
+
+def engine_supported(spec):
+    return lib().moe_engine_supported(ctypes.byref(spec)) == MOE_OK
+
+
+def engine_workspace_bytes(spec, n_layers):
+    return int(lib().moe_engine_workspace_bytes(ctypes.byref(spec), int(n_layers)))
+
+
+def engine_layer_array(layers, device="cuda"):
+    """Device array of moe_engine_layer from dicts of device tensors
+    (router, head, mix_d, mix_perm; missing or None -> NULL)."""
+    import torch
+    arr = (MoeEngineLayer * len(layers))()
+    for i, lay in enumerate(layers):
+        def p(k):
+            t = lay.get(k)
+            return None if t is None else t.data_ptr()
+        arr[i] = MoeEngineLayer(p("router"), p("head"), p("mix_d"), p("mix_perm"))
+    raw = np.frombuffer(bytes(arr), dtype=np.uint8).copy()
+    return torch.from_numpy(raw).to(device)
+
+
+def engine_layers(spec, table, layer_arr, step_layer, xi, y, workspace, idx=None, w=None,
+                  pidx=None, pw=None, status=None, stream=None):
+    n = step_layer.numel()
+    _check(lib().moe_engine_layers(ctypes.byref(spec), table.handle, _ptr(layer_arr),
+                                   _ptr(step_layer), n, _ptr(xi), _ptr(y), _ptr(idx), _ptr(w),
+                                   _ptr(pidx), _ptr(pw), _ptr(status), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)),
+           "moe_engine_layers")
+
+
+def engine_chain(spec, table, layer_arr, n_layers, first_token, xi, r_state, workspace,
+                 x_rec=None, idx=None, w=None, pidx=None, pw=None, y_rec=None, status=None,
+                 stream=None):
+    n_tokens = xi.shape[0]
+    _check(lib().moe_engine_chain(ctypes.byref(spec), table.handle, _ptr(layer_arr), n_layers,
+                                  first_token, n_tokens, _ptr(xi), _ptr(r_state), _ptr(x_rec),
+                                  _ptr(idx), _ptr(w), _ptr(pidx), _ptr(pw), _ptr(y_rec),
+                                  _ptr(status), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)),
+           "moe_engine_chain")

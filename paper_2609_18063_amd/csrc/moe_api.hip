@@ -7,6 +7,7 @@
 #include <new>
 #include <vector>
 
+#include "moe_engine.h"
 #include "moe_kernels.h"
 
 struct moe_slot_table {
@@ -349,6 +350,110 @@ int moe_topk(const moe_layer_spec* s, const float* logits, int T, int32_t* idx, 
   if (!aligned16(logits) || !aligned4(idx) || !aligned4(w)) return MOE_EALIGN;
   return from_hip(moe::launch_topk(logits, T, s->n_experts, s->top_k, idx, w,
                                    static_cast<hipStream_t>(stream)));
+}
+
+// ---- persistent decode engine ----------------------------------------------
+
+int moe_engine_supported(const moe_layer_spec* s) {
+  if (moe_spec_check(s) != MOE_OK) return MOE_EINVAL;
+  if (!moe::engine_shape_supported(s->d_model, s->d_expert, s->lora_rank, s->top_k, s->n_shared,
+                                   s->n_experts))
+    return MOE_EINVAL;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_EHIP;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return MOE_EHIP;
+  return cus == 256 ? MOE_OK : MOE_EINVAL;
+}
+
+static constexpr size_t kEngineCtlBytes = 256;
+
+size_t moe_engine_workspace_bytes(const moe_layer_spec* s, int n_layers) {
+  if (moe_spec_check(s) != MOE_OK || n_layers < 0) return 0;
+  moe::EngineArgs a{};
+  const size_t words = moe::engine_workspace_words(s->n_experts, s->d_model, n_layers, &a);
+  return kEngineCtlBytes + words * 8;
+}
+
+static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n_table_layers,
+                         moe::EngineArgs& a, void* ws, size_t ws_bytes, void* stream) {
+  int rc = moe_engine_supported(s);
+  if (rc != MOE_OK) return rc;
+  if (!t || !ws || !a.layers || !a.xi) return MOE_EINVAL;
+  if (!t->dev) return MOE_EINVAL;
+  if (n_table_layers > t->n_layers || t->n_ids < s->n_experts + s->n_shared) return MOE_EINVAL;
+  if (!aligned16(ws) || !aligned16(a.xi) || (a.y && !aligned16(a.y)) ||
+      (a.r_state && !aligned16(a.r_state)) || (a.x_rec && !aligned16(a.x_rec)) ||
+      (a.idx_rec && !aligned4(a.idx_rec)) || (a.w_rec && !aligned4(a.w_rec)) ||
+      (a.pidx_rec && !aligned4(a.pidx_rec)) || (a.pw_rec && !aligned4(a.pw_rec)) ||
+      (a.status && !aligned4(a.status)))
+    return MOE_EALIGN;
+  const size_t words = moe::engine_workspace_words(s->n_experts, s->d_model, a.L, &a);
+  if (ws_bytes < kEngineCtlBytes + words * 8) return MOE_ENOMEM;
+  a.E = s->n_experts;
+  a.K = s->top_k;
+  a.S = s->n_shared;
+  a.r = s->lora_rank;
+  a.lora_scale = s->lora_scale;
+  a.n_ids = t->n_ids;
+  a.n_slots = t->n_slots;
+  a.n_table_layers = t->n_layers;
+  a.slot_of = reinterpret_cast<const int32_t*>(t->dev);
+  a.bundles = reinterpret_cast<const moe_bundle*>(static_cast<const char*>(t->dev) + t->bundles_off);
+  a.ctl = static_cast<uint32_t*>(ws);
+  a.xw = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + kEngineCtlBytes);
+  return from_hip(moe::launch_engine(a, s->d_model, s->d_expert, s->lora_rank,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+int moe_engine_layers(const moe_layer_spec* s, const moe_slot_table* t,
+                      const moe_engine_layer* layers, const int32_t* step_layer, int n_steps,
+                      const float* xi, float* y, int32_t* idx_rec, float* w_rec, int32_t* pidx_rec,
+                      float* pw_rec, uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
+  if (n_steps < 0 || !step_layer || !y) return MOE_EINVAL;
+  if (n_steps == 0) return MOE_OK;
+  moe::EngineArgs a{};
+  a.mode = 0;
+  a.n_steps = n_steps;
+  a.L = 0;
+  a.layers = layers;
+  a.step_layer = step_layer;
+  a.xi = xi;
+  a.y = y;
+  a.idx_rec = idx_rec;
+  a.w_rec = w_rec;
+  a.pidx_rec = pidx_rec;
+  a.pw_rec = pw_rec;
+  a.status = status;
+  return engine_common(s, t, t ? t->n_layers : 0, a, ws, ws_bytes, stream);
+}
+
+int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,
+                     const moe_engine_layer* layers, int n_layers, int first_token, int n_tokens,
+                     const float* xi, float* r_state, void* x_rec, int32_t* idx_rec, float* w_rec,
+                     int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status, void* ws,
+                     size_t ws_bytes, void* stream) {
+  if (n_layers < 1 || n_tokens < 0 || first_token < 0 || !r_state) return MOE_EINVAL;
+  if ((long long)n_tokens * n_layers > (1LL << 30)) return MOE_EINVAL;
+  if (n_tokens == 0) return MOE_OK;
+  moe::EngineArgs a{};
+  a.mode = 1;
+  a.n_steps = n_tokens * n_layers;
+  a.L = n_layers;
+  a.first_token = first_token;
+  a.consumer_lo = 1;
+  a.consumer_hi = n_layers - 1;
+  a.layers = layers;
+  a.xi = xi;
+  a.r_state = r_state;
+  a.x_rec = static_cast<__half*>(x_rec);
+  a.idx_rec = idx_rec;
+  a.w_rec = w_rec;
+  a.pidx_rec = pidx_rec;
+  a.pw_rec = pw_rec;
+  a.y = y_rec;
+  a.status = status;
+  return engine_common(s, t, n_layers, a, ws, ws_bytes, stream);
 }
 
 int moe_profile_arm(int which, void* start_event, void* stop_event) {

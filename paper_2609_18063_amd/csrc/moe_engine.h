@@ -1,0 +1,42 @@
+// Persistent decode engine (moe_engine.hip): launch interface.
+#pragma once
+
+#include "moe_device.h"
+
+namespace moe {
+
+struct EngineArgs {
+  int mode;          // 0: independent single-token steps; 1: decode chain
+  int n_steps;
+  int L;             // chain: layers per token
+  int first_token;   // chain: token index of the first step
+  int consumer_lo, consumer_hi;  // chain: layers that route by the prediction (after token 0)
+  int E, K, S, r;
+  float lora_scale;
+  int n_ids, n_slots, n_table_layers;
+  const int32_t* slot_of;        // slot-table device copy
+  const moe_bundle* bundles;
+  const moe_engine_layer* layers;
+  const int32_t* step_layer;     // mode 0: [n_steps] table layer of each step
+  const float* xi;               // mode 0: [n_steps][d]; mode 1: [n_tokens][d]
+  float* y;                      // mode 0: [n_steps][d] output; mode 1: optional record
+  float* r_state;                // mode 1: [d] residual, in/out
+  __half* x_rec;                 // optional [n_steps][d]
+  int32_t* idx_rec;              // optional [n_steps][K]
+  float* w_rec;
+  int32_t* pidx_rec;
+  float* pw_rec;
+  uint32_t* status;
+  uint32_t* ctl;                 // workspace control words
+  uint64_t* xw;                  // workspace exchange words
+  // exchange-area offsets and per-parity strides (in 64-bit words)
+  size_t xo_logr, xs_logr, xo_loghm, xo_av, xs_av, xo_hv, xs_hv, xo_part, xs_part, xo_rv, xs_rv,
+      xo_logh, xs_logh_layer;
+};
+
+bool engine_shape_supported(int d, int I, int r, int K, int S, int E);
+// Fills the exchange offsets of `a`; returns the exchange area size in words.
+size_t engine_workspace_words(int E, int d, int L, EngineArgs* a);
+hipError_t launch_engine(EngineArgs& a, int d, int I, int r, hipStream_t st);
+
+}  // namespace moe

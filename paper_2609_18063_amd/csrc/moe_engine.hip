@@ -1,0 +1,823 @@
+// Persistent decode engine for gfx950: a sequence of single-token MoE layer
+// steps in one cooperative launch (256 workgroups = one per CU, 8 XCDs of 32).
+//
+// Work split of one step (one token through one layer), per XCD x:
+//   The K routed + S shared experts of the token are laid end to end along
+//   their intermediate dimension (n_list * I rows). XCD x owns the rows
+//   [x*GX, (x+1)*GX), GX = n_list*I/8, as at most three segments of experts.
+//   Its 32 workgroups split the segments' gate/up rows and LoRA-A rows,
+//   compute h = silu(g)*u for their rows, and then split the d rows of the
+//   down projection restricted to the XCD's columns. That is the XCD's
+//   weighted partial of the layer output: the down projection and its LoRA
+//   term are linear in h, so partials over intermediate rows add up.
+//   Reducer workgroups sum the 8 XCD partials for 8 rows each.
+//
+// Cross-workgroup data travels as 8-byte words {tag, fp32 value}, written
+// and polled with agent-scope relaxed atomics. The tag is the step number
+// of a device-side counter that persists across launches, so a reader never
+// takes a stale value for a fresh one. Every wait is bounded. A timeout sets
+// MOE_STATUS_ENGINE_ABORT and a sticky abort word, and every workgroup
+// leaves the kernel. Weights are staged into LDS with direct global->LDS
+// loads (global_load_lds_dwordx4).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "moe_engine.h"
+
+namespace moe {
+namespace eng {
+
+constexpr int NX = 8, NM = 32, NWG = NX * NM, NT = 512, NWV = NT / 64;
+constexpr long kSpinMax = 1L << 20;   // polls of about a microsecond each
+
+// ---------------------------------------------------------------------------
+// tagged exchange words
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void st_tag(uint64_t* p, uint32_t tag, float v) {
+  const uint64_t w = ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v);
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_tag(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_u32(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v;
+}
+
+// One 16-byte direct global->LDS load per lane; lane l writes lds_wave + 16*l.
+__device__ __forceinline__ void lds_copy16(const void* g, void* lds_wave) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_wave, 16, 0, 0);
+}
+
+struct Ctl {
+  uint32_t* ctl;      // [0] tag base, [1] finish counter, [2] abort
+  uint32_t* status;
+};
+
+// Poll `count` tagged words (addr(i) for i < count) until all carry `tag`;
+// store(i, value) each. Every thread takes items threadIdx.x + q*NT. Returns
+// false (after the barrier) if any thread timed out or saw the abort word.
+template <int MAXI, typename AddrF, typename StoreF>
+__device__ bool poll_all(int count, uint32_t tag, AddrF addr, StoreF store, const Ctl& c,
+                         int* sh_abort) {
+  uint32_t pending = 0;
+#pragma unroll
+  for (int q = 0; q < MAXI; ++q)
+    if ((int)threadIdx.x + q * NT < count) pending |= 1u << q;
+  long spin = 0;
+  while (pending) {
+    uint64_t v[MAXI];
+#pragma unroll
+    for (int q = 0; q < MAXI; ++q)
+      if ((pending >> q) & 1u) v[q] = ld_tag(addr(threadIdx.x + q * NT));
+#pragma unroll
+    for (int q = 0; q < MAXI; ++q)
+      if (((pending >> q) & 1u) && (uint32_t)(v[q] >> 32) == tag) {
+        store(threadIdx.x + q * NT, __uint_as_float((uint32_t)v[q]));
+        pending &= ~(1u << q);
+      }
+    if (!pending) break;
+    if (++spin > kSpinMax) {
+      if (c.status) atomicOr(c.status, MOE_STATUS_ENGINE_ABORT);
+      __hip_atomic_store(&c.ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *sh_abort = 1;
+      break;
+    }
+    if ((spin & 63) == 0 && ld_u32(&c.ctl[2])) {
+      *sh_abort = 1;
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  __syncthreads();
+  const bool ok = *sh_abort == 0;
+  __syncthreads();
+  return ok;
+}
+
+// ---------------------------------------------------------------------------
+// per-shape constants
+// ---------------------------------------------------------------------------
+template <int D_, int IE_, int R_, int RMX_, int GXX_, int HRX_, int NSEGX_>
+struct Shape {
+  static constexpr int D = D_;        // hidden size
+  static constexpr int IE = IE_;      // expert intermediate size
+  static constexpr int R = R_;        // LoRA rank
+  static constexpr int RMX = RMX_;    // max gate/up row pairs per workgroup
+  static constexpr int GXX = GXX_;    // max intermediate rows per XCD
+  static constexpr int HRX = HRX_;    // max router (and head) rows per workgroup
+  static constexpr int NSEGX = NSEGX_;  // max expert segments per XCD
+  static constexpr int LPR = D / 32 < 64 ? D / 32 : 64;   // lanes per gate/up row
+  static constexpr int CPL = D / 32 / LPR;                 // 16-byte chunks per lane
+  static constexpr int RPI = 64 / LPR;                     // gate/up rows per wave instruction
+  static constexpr int NAX = (NSEGX * 2 * R + NM - 1) / NM; // max LoRA-A rows per workgroup
+  static constexpr int DR = D / NM;   // down rows per workgroup
+  static constexpr int RR = D / NWG;  // reducer rows per workgroup
+  static constexpr int MAXI_D = (D + NT - 1) / NT;
+  // LDS layout (bytes); staged regions are rounded up to 1 KiB (one wave copy)
+  static constexpr int kb(int b) { return (b + 1023) / 1024 * 1024; }
+  static constexpr int O_GUQ = 0;                                   // [2*RMX][D/2]
+  static constexpr int O_GUS = O_GUQ + kb(2 * RMX * D / 2);         // [2*RMX][D/16]
+  static constexpr int O_AR = O_GUS + kb(2 * RMX * D / 16);         // [NAX][D] fp16
+  static constexpr int O_RT = O_AR + kb(NAX * D * 2);               // [HRX][D] router rows
+  static constexpr int O_HD = O_RT + kb(HRX * D * 2);               // [HRX][D] head rows
+  static constexpr int O_BGU = O_HD + kb(HRX * D * 2);              // [2*RMX][R] fp16
+  static constexpr int O_DQ = O_BGU + kb(2 * RMX * R * 2);          // [DR][GXX/2]
+  static constexpr int O_DS = O_DQ + kb(DR * GXX / 2);              // [DR][NSEGX][IE/16]
+  static constexpr int O_BD = O_DS + kb(DR * NSEGX * IE / 16);      // [DR][NSEGX][R] fp16
+  static constexpr int O_ADR = O_BD + kb(DR * NSEGX * R * 2);       // [R][GXX] fp16
+  static constexpr int O_XF = O_ADR + kb(R * GXX * 2);              // [D] f32
+  static constexpr int O_XH = O_XF + D * 4;                         // [D] f16
+  static constexpr int O_R0 = O_XH + D * 2;                         // [D] f32
+  static constexpr int O_R1 = O_R0 + D * 4;                         // [D] f32
+  static constexpr int O_LG = O_R1 + D * 4;                         // [1024] f32 logits
+  static constexpr int O_HX = O_LG + 1024 * 4;                      // [GXX] f32 h of the XCD
+  static constexpr int O_GXU = O_HX + GXX * 4;                      // [2*RMX] f32
+  static constexpr int O_DP = O_GXU + 2 * RMX * 4;                  // [DR][32] f32 down partials
+  static constexpr int O_AV = O_DP + DR * 32 * 4;                   // [NSEGX][2R] f32
+  static constexpr int O_ADV = O_AV + NSEGX * 2 * R * 4;            // [NSEGX][R] f32
+  static constexpr int O_YL = O_ADV + NSEGX * R * 4;                // [RR][NX] f32
+  static constexpr int O_RED = (O_YL + RR * NX * 4 + 63) / 64 * 64; // [NT] f64 reduction
+  static constexpr int O_MISC = O_RED + NT * 8;                     // small ints / floats
+  static constexpr int LDS_BYTES = O_MISC + 1024;
+};
+
+struct Seg {
+  int k;       // list position (k < K routed, else shared E + k - K)
+  int i0;      // first intermediate row of the expert in this segment
+  int len;     // rows
+  int col0;    // first column of the segment in the XCD's concatenation
+};
+
+struct Misc {
+  int nseg;
+  int abort;
+  int idx[32];
+  float w[32];
+  int pidx[32];
+  float pw[32];
+  Seg seg[4];
+  float segw[4];
+  int segok[4];
+  const moe_bundle* segb[4];
+};
+
+__device__ __forceinline__ float silu(float z) { return z / (1.f + expf(-z)); }
+
+template <class SH>
+__device__ void block_rmsnorm_to_x(const float* v, float* xf, __half* xh, double* red) {
+  double acc = 0.0;
+  for (int j = threadIdx.x; j < SH::D; j += NT) {
+    const double a = v[j];
+    acc += a * a;
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = NT / 2; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  const double inv = 1.0 / sqrt(red[0] / (double)SH::D + 1e-6);
+  __syncthreads();
+  for (int j = threadIdx.x; j < SH::D; j += NT) {
+    const __half h = __half(static_cast<_Float16>((double)v[j] * inv));
+    xh[j] = h;
+    xf[j] = __half2float(h);
+  }
+}
+
+template <class SH>
+__device__ double block_sumsq(const float* v, double* red) {
+  double acc = 0.0;
+  for (int j = threadIdx.x; j < SH::D; j += NT) {
+    const double a = v[j];
+    acc += a * a;
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = NT / 2; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  const double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+// fp16 row (D halves in LDS) . x (fp16 in LDS) by one wave; fp32 accumulate.
+template <class SH>
+__device__ __forceinline__ float wave_dot_h(const __half* row, const __half* xh) {
+  const int lane = threadIdx.x & 63;
+  float acc = 0.f;
+#pragma unroll
+  for (int q = 0; q < SH::D / 512; ++q) {
+    const int c = lane + 64 * q;
+    acc = dot8_h(*reinterpret_cast<const U4*>(row + c * 8), *reinterpret_cast<const U4*>(xh + c * 8),
+                 acc);
+  }
+  return wave_sum(acc);
+}
+
+// Stage `nchunks` 16-byte chunks into LDS region `dst` (1 KiB-padded);
+// src(i) gives chunk i's global address (i < nchunks). Waves take 64-chunk
+// blocks round-robin; lanes past the end re-read chunk 0 into the padding.
+template <typename SrcF>
+__device__ __forceinline__ void stage(char* dst, int nchunks, SrcF src) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int b = wave; b * 64 < nchunks; b += NWV) {
+    const int i = b * 64 + lane;
+    lds_copy16(src(i < nchunks ? i : 0), dst + b * 1024);
+  }
+}
+
+template <class SH>
+__global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  constexpr int D = SH::D, IE = SH::IE, R = SH::R;
+  uint8_t* guq = reinterpret_cast<uint8_t*>(smem + SH::O_GUQ);
+  uint8_t* gus = reinterpret_cast<uint8_t*>(smem + SH::O_GUS);
+  __half* arow = reinterpret_cast<__half*>(smem + SH::O_AR);
+  __half* rtrow = reinterpret_cast<__half*>(smem + SH::O_RT);
+  __half* hdrow = reinterpret_cast<__half*>(smem + SH::O_HD);
+  __half* bgu = reinterpret_cast<__half*>(smem + SH::O_BGU);
+  uint8_t* dq = reinterpret_cast<uint8_t*>(smem + SH::O_DQ);
+  uint8_t* ds = reinterpret_cast<uint8_t*>(smem + SH::O_DS);
+  __half* bd = reinterpret_cast<__half*>(smem + SH::O_BD);
+  __half* adr = reinterpret_cast<__half*>(smem + SH::O_ADR);
+  float* xf = reinterpret_cast<float*>(smem + SH::O_XF);
+  __half* xh = reinterpret_cast<__half*>(smem + SH::O_XH);
+  float* r0 = reinterpret_cast<float*>(smem + SH::O_R0);
+  float* r1 = reinterpret_cast<float*>(smem + SH::O_R1);
+  float* lg = reinterpret_cast<float*>(smem + SH::O_LG);
+  float* hx = reinterpret_cast<float*>(smem + SH::O_HX);
+  float* gxu = reinterpret_cast<float*>(smem + SH::O_GXU);
+  float* dp = reinterpret_cast<float*>(smem + SH::O_DP);
+  float* av = reinterpret_cast<float*>(smem + SH::O_AV);
+  float* adv = reinterpret_cast<float*>(smem + SH::O_ADV);
+  float* yl = reinterpret_cast<float*>(smem + SH::O_YL);
+  double* red = reinterpret_cast<double*>(smem + SH::O_RED);
+  Misc* mi = reinterpret_cast<Misc*>(smem + SH::O_MISC);
+
+  const int g = blockIdx.x;
+  const int x = g % NX, m = g / NX;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const Ctl c{a.ctl, a.status};
+  const int K = a.K, E = a.E;
+  const int n_list = K + a.S;
+  const int GX = n_list * IE / NX;    // rows of this XCD
+  const int RM = GX / NM;             // gate/up row pairs of this workgroup
+  const int LPRD = GX / 32;           // lanes per down row (one 32-column chunk each)
+  const int RPID = 64 / LPRD;         // down rows per wave instruction
+
+  if (threadIdx.x == 0) {
+    mi->abort = 0;
+    if ((int)xcc_id() != x) {  // the work split relies on blockIdx % 8 == XCD
+      if (a.status) atomicOr(a.status, MOE_STATUS_ENGINE_ABORT);
+      __hip_atomic_store(&a.ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      mi->abort = 1;
+    }
+    if (ld_u32(&a.ctl[2])) mi->abort = 1;
+  }
+  const uint32_t base = ld_u32(&a.ctl[0]);
+  __syncthreads();
+
+  // segments of this XCD (fixed for the launch)
+  if (threadIdx.x == 0) {
+    int row = x * GX, end = (x + 1) * GX, n = 0, col = 0;
+    while (row < end && n < SH::NSEGX) {
+      const int k = row / IE, i0 = row % IE;
+      const int len = min(IE - i0, end - row);
+      mi->seg[n] = Seg{k, i0, len, col};
+      ++n;
+      row += len;
+      col += len;
+    }
+    mi->nseg = n;
+  }
+  __syncthreads();
+  const int nseg = mi->nseg;
+
+  uint64_t* const X = a.xw;
+  for (int s = 0; s < a.n_steps && !mi->abort; ++s) {
+    const uint32_t tag = base + (uint32_t)s + 1u;
+    const int par = s & 1;
+    int t = 0, N = 0, lay;
+    bool own_route = true, has_head;
+    if (a.mode == 0) {
+      lay = a.step_layer[s];
+      if (lay < 0 || lay >= a.n_table_layers) {  // uniform across the grid: every workgroup stops
+        if (g == 0 && threadIdx.x == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
+        break;
+      }
+    } else {
+      t = a.first_token + s / a.L;
+      N = s % a.L;
+      lay = N;
+      own_route = t == 0 || N < a.consumer_lo || N > a.consumer_hi;
+    }
+    const moe_engine_layer LY = a.layers[lay];
+    has_head = LY.head != nullptr && (a.mode == 0 || N + 1 < a.L);
+
+    // ---- S0: layer input ------------------------------------------------
+    if (a.mode == 0) {
+      const float* xi = a.xi + (size_t)s * D;
+      for (int j = threadIdx.x; j < D; j += NT) r0[j] = xi[j];
+      __syncthreads();
+      block_rmsnorm_to_x<SH>(r0, xf, xh, red);
+    } else {
+      if (s == 0) {
+        for (int j = threadIdx.x; j < D; j += NT) r0[j] = a.r_state[j];
+        __syncthreads();
+      } else {
+        uint64_t* rv = X + a.xo_rv + (size_t)(par ^ 1) * a.xs_rv;
+        if (!poll_all<SH::MAXI_D>(D, tag - 1u, [&](int i) { return rv + i; },
+                                  [&](int i, float v) { r0[i] = v; }, c, &mi->abort))
+          break;
+      }
+      if (N == 0) {  // token start: r = xi + rmsnorm(r)
+        const double inv = 1.0 / sqrt(block_sumsq<SH>(r0, red) / (double)D + 1e-6);
+        const float* xi = a.xi + (size_t)(s / a.L) * D;
+        for (int j = threadIdx.x; j < D; j += NT) r0[j] = (float)((double)xi[j] + (double)r0[j] * inv);
+        __syncthreads();
+      }
+      const __half* md = reinterpret_cast<const __half*>(LY.mix_d);
+      for (int j = threadIdx.x; j < D; j += NT) {
+        const int p = LY.mix_perm[j];
+        const float v = (p >= 0 && p < D) ? r0[p] : 0.f;
+        r1[j] = fmaf(__half2float(md[j]), v, r0[j]);
+      }
+      __syncthreads();
+      block_rmsnorm_to_x<SH>(r1, xf, xh, red);
+    }
+    __syncthreads();
+    if (g == 0 && a.x_rec)
+      for (int j = threadIdx.x; j < D; j += NT) a.x_rec[(size_t)s * D + j] = xh[j];
+
+    // ---- S1: routing ----------------------------------------------------
+    if (own_route) {
+      uint64_t* lr = X + a.xo_logr + (size_t)par * a.xs_logr;
+      const __half* W = reinterpret_cast<const __half*>(LY.router);
+      stage(smem + SH::O_RT, SH::HRX * D / 8, [&](int i) {
+        const int e = g + NWG * (i / (D / 8));
+        return W + (size_t)(e < E ? e : 0) * D + (i % (D / 8)) * 8;
+      });
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      for (int q = wave; q < SH::HRX; q += NWV) {
+        const int e = g + NWG * q;
+        const float v = wave_dot_h<SH>(rtrow + (size_t)q * D, xh);
+        if (lane == 0 && e < E) st_tag(lr + e, tag, v);
+      }
+      if (!poll_all<2>(E, tag, [&](int i) { return lr + i; }, [&](int i, float v) { lg[i] = v; }, c,
+                       &mi->abort))
+        break;
+    } else {
+      uint64_t* lh = X + a.xo_logh + ((size_t)(t & 1) * a.L + N) * a.xs_logh_layer;
+      if (!poll_all<2>(E, (uint32_t)t + 1u, [&](int i) { return lh + i; },
+                       [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
+        break;
+    }
+    if (wave == 0) wave_topk<false>(lg, E, K, mi->idx, mi->w);
+    __syncthreads();
+    if (g == 0 && threadIdx.x < K) {
+      if (a.idx_rec) a.idx_rec[(size_t)s * K + threadIdx.x] = mi->idx[threadIdx.x];
+      if (a.w_rec) a.w_rec[(size_t)s * K + threadIdx.x] = mi->w[threadIdx.x];
+    }
+    if (threadIdx.x < nseg) {
+      const int q = threadIdx.x;
+      const int k = mi->seg[q].k;
+      const int e = k < K ? mi->idx[k] : E + (k - K);
+      const bool bad = k < K && (e < 0 || e >= E);
+      const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
+      mi->segok[q] = slot >= 0;
+      mi->segb[q] = slot >= 0 ? a.bundles + (size_t)lay * a.n_slots + slot : nullptr;
+      mi->segw[q] = k < K ? mi->w[k] : 1.f;
+      if (m == 0 && a.status) {
+        if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
+        else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
+      }
+    }
+    __syncthreads();
+
+    // ---- S2: stage weights, gate/up rows, LoRA-A rows, head rows --------
+    // gate/up row r of this workgroup: r < RM gate, else up; flattened row
+    // fr = x*GX + m*RM + (r % RM) -> segment and expert row.
+    auto row_seg = [&](int lr) {  // XCD-local row -> segment index
+      int q = 0;
+      while (q + 1 < nseg && lr >= mi->seg[q + 1].col0) ++q;
+      return q;
+    };
+    {
+      constexpr int QCH = D / 32;   // 16-byte code chunks per gate/up row
+      stage(smem + SH::O_GUQ, 2 * RM * QCH, [&](int i) -> const void* {
+        const int rr = i / QCH, ch = i % QCH;
+        const int lr = m * RM + (rr % RM);
+        const int q = row_seg(lr);
+        const moe_bundle* b = mi->segb[q];
+        if (!b) return a.xi;  // any valid address; the row is not used
+        const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
+        const uint8_t* base_q = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.q : b->up.q);
+        return base_q + (size_t)er * (D / 2) + ch * 16;
+      });
+      constexpr int SCH = D / 256;  // 16-byte (scale, zero) chunks per row
+      stage(smem + SH::O_GUS, 2 * RM * SCH, [&](int i) -> const void* {
+        const int rr = i / SCH, ch = i % SCH;
+        const int lr = m * RM + (rr % RM);
+        const int q = row_seg(lr);
+        const moe_bundle* b = mi->segb[q];
+        if (!b) return a.xi;
+        const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
+        const uint8_t* base_s = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.sz : b->up.sz);
+        return base_s + (size_t)er * (D / 16) + ch * 16;
+      });
+      // LoRA-A rows: the XCD's nseg*2R rows, row ar = m + NM*qa
+      stage(smem + SH::O_AR, SH::NAX * (D / 8), [&](int i) -> const void* {
+        const int qa = i / (D / 8), ch = i % (D / 8);
+        const int ar = m + NM * qa;
+        if (ar >= nseg * 2 * R) return a.xi;
+        const int q = ar / (2 * R), rr = ar % (2 * R);
+        const moe_bundle* b = mi->segb[q];
+        const void* A = b ? (rr < R ? b->gate.lora_a : b->up.lora_a) : nullptr;
+        if (!A) return a.xi;
+        return reinterpret_cast<const __half*>(A) + (size_t)(rr % R) * D + ch * 8;
+      });
+      if (has_head) {
+        const __half* Wh = reinterpret_cast<const __half*>(LY.head);
+        stage(smem + SH::O_HD, SH::HRX * (D / 8), [&](int i) {
+          const int e = g + NWG * (i / (D / 8));
+          return Wh + (size_t)(e < E ? e : 0) * D + (i % (D / 8)) * 8;
+        });
+      }
+      // LoRA-B rows of gate / up for this workgroup's rows (R halves each)
+      constexpr int BCH = R * 2 / 16;
+      stage(smem + SH::O_BGU, 2 * RM * BCH, [&](int i) -> const void* {
+        const int rr = i / BCH, ch = i % BCH;
+        const int lr = m * RM + (rr % RM);
+        const int q = row_seg(lr);
+        const moe_bundle* b = mi->segb[q];
+        const void* B = b ? (rr < RM ? b->gate.lora_b : b->up.lora_b) : nullptr;
+        if (!B) return a.xi;
+        const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
+        return reinterpret_cast<const __half*>(B) + (size_t)er * R + ch * 8;
+      });
+      // down rows j = m*DR + jj, restricted to the XCD's columns
+      const int dqch = GX / 32;  // 16-byte chunks per staged down row
+      stage(smem + SH::O_DQ, SH::DR * dqch, [&](int i) -> const void* {
+        const int jj = i / dqch, ch = i % dqch;
+        const int col = ch * 32;
+        const int q = row_seg(col);
+        const moe_bundle* b = mi->segb[q];
+        if (!b) return a.xi;
+        const int ec = mi->seg[q].i0 + (col - mi->seg[q].col0);
+        return reinterpret_cast<const uint8_t*>(b->down.q) + (size_t)(m * SH::DR + jj) * (IE / 2) +
+               ec / 2;
+      });
+      // (scale, zero) of the down rows: the whole row of each segment expert, [jj][q][I/16 B]
+      constexpr int DSCH = IE / 256;  // 16-byte chunks per (scale, zero) row
+      stage(smem + SH::O_DS, SH::DR * SH::NSEGX * DSCH, [&](int i) -> const void* {
+        const int jq = i / DSCH, ch = i % DSCH;
+        const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
+        if (q >= nseg) return a.xi;
+        const moe_bundle* b = mi->segb[q];
+        if (!b) return a.xi;
+        return reinterpret_cast<const uint8_t*>(b->down.sz) + (size_t)(m * SH::DR + jj) * (IE / 16) +
+               ch * 16;
+      });
+      // LoRA-B rows of down: [jj][q][R]
+      stage(smem + SH::O_BD, SH::DR * SH::NSEGX * BCH, [&](int i) -> const void* {
+        const int jq = i / BCH, ch = i % BCH;
+        const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
+        if (q >= nseg) return a.xi;
+        const moe_bundle* b = mi->segb[q];
+        const void* B = b ? b->down.lora_b : nullptr;
+        if (!B) return a.xi;
+        return reinterpret_cast<const __half*>(B) + (size_t)(m * SH::DR + jj) * R + ch * 8;
+      });
+      // LoRA-A of down restricted to the XCD's columns: [kk][GX]
+      const int adch = GX / 8;
+      stage(smem + SH::O_ADR, R * adch, [&](int i) -> const void* {
+        const int kk = i / adch, ch = i % adch;
+        const int col = ch * 8;
+        const int q = row_seg(col);
+        const moe_bundle* b = mi->segb[q];
+        const void* A = b ? b->down.lora_a : nullptr;
+        if (!A) return a.xi;
+        const int ec = mi->seg[q].i0 + (col - mi->seg[q].col0);
+        return reinterpret_cast<const __half*>(A) + (size_t)kk * IE + ec;
+      });
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+
+    // gate/up matvecs (raw): rows r of [gate RM | up RM], LPR lanes per row
+    {
+      const int c0 = lane % SH::LPR, sub = lane / SH::LPR;
+      float xv[SH::CPL][32], xs[SH::CPL];
+#pragma unroll
+      for (int cc = 0; cc < SH::CPL; ++cc) {
+        const int ch = c0 + SH::LPR * cc;
+        float sacc = 0.f;
+#pragma unroll
+        for (int e = 0; e < 32; ++e) {
+          xv[cc][e] = xf[ch * 32 + e];
+          sacc += xv[cc][e];
+        }
+        xs[cc] = sacc;
+      }
+      for (int rg = wave; rg * SH::RPI < 2 * RM; rg += NWV) {
+        const int rr = rg * SH::RPI + sub;
+        const int rrc = rr < 2 * RM ? rr : 0;
+        float acc = 0.f;
+#pragma unroll
+        for (int cc = 0; cc < SH::CPL; ++cc) {
+          const int ch = c0 + SH::LPR * cc;
+          const U4 qv = *reinterpret_cast<const U4*>(guq + (size_t)rrc * (D / 2) + ch * 16);
+          const float2 sz = h2f2(*reinterpret_cast<const uint32_t*>(gus + (size_t)rrc * (D / 16) +
+                                                                     (ch >> 1) * 4));
+          acc += sz.x * dot32_q4(qv, xv[cc]) + sz.y * xs[cc];
+        }
+        acc = group_sum(acc, SH::LPR);
+        if (c0 == 0 && rr < 2 * RM) gxu[rr] = acc;
+      }
+    }
+    // LoRA-A rows -> tagged a-vectors of the XCD
+    {
+      uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
+      for (int qa = wave; qa < SH::NAX; qa += NWV) {
+        const int ar = m + NM * qa;
+        if (ar >= nseg * 2 * R) continue;
+        const int q = ar / (2 * R), rr = ar % (2 * R);
+        const moe_bundle* b = mi->segb[q];
+        const bool has = b && (rr < R ? (b->gate.lora_a && b->gate.lora_b)
+                                      : (b->up.lora_a && b->up.lora_b));
+        const float v = has ? wave_dot_h<SH>(arow + (size_t)qa * D, xh) : 0.f;
+        if (lane == 0) st_tag(AV + q * 2 * R + rr, tag, v);
+      }
+    }
+    // head rows -> tagged logits for the next layer at the next token
+    if (has_head) {
+      uint64_t* lh;
+      uint32_t htag;
+      if (a.mode == 0) {
+        lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
+        htag = tag;
+      } else {
+        lh = X + a.xo_logh + ((size_t)((t + 1) & 1) * a.L + (N + 1)) * a.xs_logh_layer;
+        htag = (uint32_t)t + 2u;
+      }
+      for (int q = wave; q < SH::HRX; q += NWV) {
+        const int e = g + NWG * q;
+        const float v = wave_dot_h<SH>(hdrow + (size_t)q * D, xh);
+        if (lane == 0 && e < E) st_tag(lh + e, htag, v);
+      }
+    }
+    __syncthreads();
+
+    // ---- S3: a-vectors of the XCD -> h of this workgroup's rows ---------
+    {
+      uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
+      if (!poll_all<1>(nseg * 2 * R, tag, [&](int i) { return AV + i; },
+                       [&](int i, float v) { av[i] = v; }, c, &mi->abort))
+        break;
+      uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
+      if ((int)threadIdx.x < RM) {
+        const int i = threadIdx.x;
+        const int lr = m * RM + i;
+        const int q = row_seg(lr);
+        const moe_bundle* b = mi->segb[q];
+        float hv = 0.f;
+        if (b) {
+          float gg = gxu[i], uu = gxu[RM + i];
+          if (b->gate.lora_a && b->gate.lora_b) {
+            float s2 = 0.f;
+            for (int kk = 0; kk < R; ++kk)
+              s2 = fmaf(__half2float(bgu[(size_t)i * R + kk]), av[q * 2 * R + kk], s2);
+            gg = fmaf(a.lora_scale, s2, gg);
+          }
+          if (b->up.lora_a && b->up.lora_b) {
+            float s2 = 0.f;
+            for (int kk = 0; kk < R; ++kk)
+              s2 = fmaf(__half2float(bgu[(size_t)(RM + i) * R + kk]), av[q * 2 * R + R + kk], s2);
+            uu = fmaf(a.lora_scale, s2, uu);
+          }
+          hv = silu(gg) * uu;
+        }
+        st_tag(HV + lr, tag, hv);
+      }
+    }
+
+    // ---- S4: h of the XCD -> down rows -> tagged partial of the output ---
+    {
+      uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
+      if (!poll_all<(SH::GXX + NT - 1) / NT>(GX, tag, [&](int i) { return HV + i; },
+                                            [&](int i, float v) { hx[i] = v; }, c, &mi->abort))
+        break;
+      // a_d[q][kk] = A_down[kk][segment q columns] . h: 16 lanes per (q, kk)
+      for (int pbase = 0; pbase < nseg * R; pbase += NT / 16) {
+        const int p = pbase + (int)threadIdx.x / 16, part = threadIdx.x % 16;
+        float acc = 0.f;
+        if (p < nseg * R) {
+          const int q = p / R, kk = p % R;
+          const int c0 = mi->seg[q].col0, len = mi->seg[q].len;
+          for (int cix = part; cix < len; cix += 16)
+            acc = fmaf(__half2float(adr[(size_t)kk * GX + c0 + cix]), hx[c0 + cix], acc);
+        }
+        acc = group_sum(acc, 16);
+        if (part == 0 && p < nseg * R) adv[p] = acc;
+      }
+      __syncthreads();
+      // down matvec: lane -> 32-column chunk ch (fixed), RPID rows per wave instruction
+      const int ch = lane % LPRD, sub = lane / LPRD;
+      const bool active = sub < RPID;
+      float hv[32], hsum = 0.f, wseg = 0.f;
+      int qseg = 0, egrp = 0;
+      if (active) {
+        qseg = row_seg(ch * 32);
+        wseg = mi->segok[qseg] ? mi->segw[qseg] : 0.f;
+        egrp = (mi->seg[qseg].i0 + (ch * 32 - mi->seg[qseg].col0)) / 64;
+#pragma unroll
+        for (int e = 0; e < 32; ++e) {
+          hv[e] = hx[ch * 32 + e];
+          hsum += hv[e];
+        }
+      }
+      for (int rg = wave; rg * RPID < SH::DR; rg += NWV) {
+        const int jj = rg * RPID + sub;
+        if (active && jj < SH::DR) {
+          const U4 qv = *reinterpret_cast<const U4*>(dq + (size_t)jj * (GX / 2) + ch * 16);
+          // (scale, zero) of the expert group holding XCD-local columns 32*ch ..
+          const float2 sz = h2f2(*reinterpret_cast<const uint32_t*>(
+              ds + ((size_t)jj * SH::NSEGX + qseg) * (IE / 16) + egrp * 4));
+          const float p = wseg * (sz.x * dot32_q4(qv, hv) + sz.y * hsum);
+          dp[jj * 32 + ch] = p;
+        }
+      }
+      __syncthreads();
+      uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part + (size_t)x * D;
+      for (int jj = threadIdx.x; jj < SH::DR; jj += NT) {
+        float acc = 0.f;
+        for (int cc = 0; cc < LPRD; ++cc) acc += dp[jj * 32 + cc];
+        for (int q = 0; q < nseg; ++q) {
+          const moe_bundle* b = mi->segb[q];
+          if (!b || !b->down.lora_a || !b->down.lora_b) continue;
+          float la = 0.f;
+          for (int kk = 0; kk < R; ++kk)
+            la = fmaf(__half2float(bd[((size_t)jj * SH::NSEGX + q) * R + kk]), adv[q * R + kk], la);
+          acc = fmaf(mi->segw[q] * a.lora_scale, la, acc);
+        }
+        st_tag(PART + m * SH::DR + jj, tag, acc);
+      }
+    }
+
+    // ---- S5: reduce the 8 XCD partials of this workgroup's rows ---------
+    {
+      uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part;
+      if (!poll_all<1>(SH::RR * NX, tag,
+                       [&](int i) { return PART + (size_t)(i % NX) * D + g * SH::RR + i / NX; },
+                       [&](int i, float v) { yl[i] = v; }, c, &mi->abort))
+        break;
+      if ((int)threadIdx.x < SH::RR) {
+        const int jr = threadIdx.x, j = g * SH::RR + jr;
+        float y = 0.f;
+        for (int xx = 0; xx < NX; ++xx) y += yl[jr * NX + xx];
+        if (a.mode == 0) {
+          a.y[(size_t)s * D + j] = y;
+        } else {
+          const float rn = r1[j] + y;
+          st_tag(X + a.xo_rv + (size_t)par * a.xs_rv + j, tag, rn);
+          if (a.y) a.y[(size_t)s * D + j] = y;
+          if (s + 1 == a.n_steps) a.r_state[j] = rn;
+        }
+      }
+      // the head's prediction (recorded for tests and callers)
+      if (g == 0 && has_head && (a.pidx_rec || a.pw_rec)) {
+        uint64_t* lh;
+        uint32_t htag;
+        if (a.mode == 0) {
+          lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
+          htag = tag;
+        } else {
+          lh = X + a.xo_logh + ((size_t)((t + 1) & 1) * a.L + (N + 1)) * a.xs_logh_layer;
+          htag = (uint32_t)t + 2u;
+        }
+        if (!poll_all<2>(E, htag, [&](int i) { return lh + i; }, [&](int i, float v) { lg[i] = v; },
+                         c, &mi->abort))
+          break;
+        if (wave == 0) {
+          int32_t* pi = mi->pidx;
+          float* pw = mi->pw;
+          wave_topk<false>(lg, E, K, pi, pw);
+          if (lane < K) {
+            if (a.pidx_rec) a.pidx_rec[(size_t)s * K + lane] = pi[lane];
+            if (a.pw_rec) a.pw_rec[(size_t)s * K + lane] = pw[lane];
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // ---- finish: the last workgroup moves the tag base past this launch ----
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t old = atomicAdd(&a.ctl[1], 1u);
+    if (old == NWG - 1) {
+      __hip_atomic_store(&a.ctl[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.ctl[0], base + (uint32_t)a.n_steps, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// shapes: (D, I, R, max row pairs per workgroup, max rows per XCD, router rows per workgroup)
+using ShapeMoe35b = Shape<2048, 512, 16, 18, 576, 1, 2>;
+using ShapeTiny = Shape<512, 256, 8, 2, 64, 1, 1>;
+
+template <class SH>
+static hipError_t launch(EngineArgs& a, hipStream_t st) {
+  static_assert(SH::LDS_BYTES <= 160 * 1024, "engine LDS budget");
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)engine_kernel<SH>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, SH::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  void* args[] = {&a};
+  return hipLaunchCooperativeKernel((const void*)engine_kernel<SH>, dim3(NWG), dim3(NT), args,
+                                    SH::LDS_BYTES, st);
+}
+
+}  // namespace eng
+
+// number of expert segments of the XCD with the most of them
+static int max_segments(int n_list, int I) {
+  const int GX = n_list * I / eng::NX;
+  int most = 0;
+  for (int x = 0; x < eng::NX; ++x) {
+    int row = x * GX, end = (x + 1) * GX, n = 0;
+    while (row < end) {
+      row += std::min(I - row % I, end - row);
+      ++n;
+    }
+    most = std::max(most, n);
+  }
+  return most;
+}
+
+template <class SH>
+static bool fits(int GX, int n_list, int I) {
+  return GX <= SH::GXX && GX / eng::NM <= SH::RMX && GX / 32 <= 32 &&
+         max_segments(n_list, I) <= SH::NSEGX;
+}
+
+bool engine_shape_supported(int d, int I, int r, int K, int S, int E) {
+  const int n = K + S;
+  if (E > 256 || K > 32) return false;
+  if ((n * I) % (eng::NX * 64) != 0) return false;
+  const int GX = n * I / eng::NX;
+  if (GX % eng::NM != 0 || GX % 64 != 0) return false;
+  if (d == 2048 && I == 512 && r == 16) return fits<eng::ShapeMoe35b>(GX, n, I);
+  if (d == 512 && I == 256 && r == 8) return fits<eng::ShapeTiny>(GX, n, I);
+  return false;
+}
+
+size_t engine_workspace_words(int E, int d, int L, EngineArgs* a) {
+  // offsets in 64-bit words; every area doubled by step parity
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    const size_t o = off;
+    off += (n + 31) / 32 * 32;
+    return o;
+  };
+  const int GXX = 576, NSEGX = 2, R = 64;
+  a->xs_logr = (E + 31) / 32 * 32;
+  a->xo_logr = take(2 * (size_t)a->xs_logr);
+  a->xo_loghm = take(2 * (size_t)a->xs_logr);
+  a->xs_av = (size_t)eng::NX * NSEGX * 2 * R;
+  a->xo_av = take(2 * a->xs_av);
+  a->xs_hv = (size_t)eng::NX * GXX;
+  a->xo_hv = take(2 * a->xs_hv);
+  a->xs_part = (size_t)eng::NX * d;
+  a->xo_part = take(2 * a->xs_part);
+  a->xs_rv = (size_t)d;
+  a->xo_rv = take(2 * a->xs_rv);
+  a->xs_logh_layer = (size_t)(E + 31) / 32 * 32;
+  a->xo_logh = take(2 * (size_t)(L > 0 ? L : 1) * a->xs_logh_layer);
+  return off;
+}
+
+hipError_t launch_engine(EngineArgs& a, int d, int I, int r, hipStream_t st) {
+  if (d == 2048 && I == 512 && r == 16) return eng::launch<eng::ShapeMoe35b>(a, st);
+  if (d == 512 && I == 256 && r == 8) return eng::launch<eng::ShapeTiny>(a, st);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace moe

@@ -40,56 +40,6 @@ __global__ void __launch_bounds__(256) rmsnorm_f16_kernel(const float* __restric
     x[(size_t)t * d + j] = __half(static_cast<_Float16>((double)row[j] * r));
 }
 
-// ------------------------------------------------------------------------
-// Softmax-top-k of one token's logits by one wave.  Selection is on the fp32
-// logits (the softmax is increasing), descending, ties to the lower index;
-// weights are the softmax renormalized over the selected set.
-// ------------------------------------------------------------------------
-constexpr int kTopkVals = 16;  // E <= 64 * 16
-
-template <bool kAgent>
-__device__ void wave_topk(const float* l, int E, int K, int32_t* idx_out, float* w_out) {
-  const int lane = threadIdx.x & 63;
-  float v[kTopkVals];
-#pragma unroll
-  for (int j = 0; j < kTopkVals; ++j) {
-    const int e = lane + 64 * j;
-    float a = -INFINITY;
-    if (e < E) a = kAgent ? ld_agent(l + e) : l[e];
-    v[j] = (a != a) ? -INFINITY : a;
-  }
-  uint32_t taken = 0;
-  float mine = -INFINITY;
-  for (int k = 0; k < K; ++k) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-#pragma unroll
-    for (int j = 0; j < kTopkVals; ++j) {
-      const int e = lane + 64 * j;
-      if (e < E && !((taken >> j) & 1u) && (v[j] > bv || (v[j] == bv && e < bi))) {
-        bv = v[j];
-        bi = e;
-      }
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const float ov = __shfl_xor(bv, off, kWave);
-      const int oi = __shfl_xor(bi, off, kWave);
-      if (ov > bv || (ov == bv && oi < bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
-    if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
-    if (lane == k) mine = bv;
-    if (lane == 0) idx_out[k] = bi;
-  }
-  const float m = __shfl(mine, 0, kWave);
-  const float ex = (lane < K) ? expf(mine - m) : 0.f;
-  const float s = wave_sum(ex);
-  if (lane < K) w_out[lane] = ex / s;
-}
-
 // Router / prerouter logits for one token per grid row, then top-k by the
 // last workgroup of that token to finish (a counter in the workspace, left
 // at zero afterwards).

@@ -1,12 +1,14 @@
-"""Benchmark: one decode step of the 35B-class int4 MoE layer at batch 1.
+"""Benchmark: decode steps of the 35B-class int4 MoE layer at batch 1.
 
 A step is the whole hot path on one token: layer input (RMSNorm -> fp16),
 router + softmax-top-k, prerouter prediction for the next layer, the 8
 routed + 1 shared int4 group-64 SwiGLU experts with the unmerged LoRA delta,
-and the combine.  Steps rotate over 32 resident layer instances (32 x ~520 MB)
-so that weights come from HBM and not from the 256 MB last-level cache.  The
-K timed steps are replayed from one captured HIP graph, inputs resident in
-HBM.  Prints one JSON line.
+and the combine.  Steps rotate over 40 resident layers (40 x ~520 MB), so
+weights come from HBM and not from the 256 MB last-level cache.  The K timed
+steps run in one launch of the persistent decode engine, with the inputs
+already resident in HBM.  Also measured: tokens/s of the 40-layer stack
+(autoregressive, prediction-as-routing) and the per-call path.  Prints one
+JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -78,44 +80,49 @@ class Hip:
         self.lib.hipEventDestroy(ctypes.c_void_p(e))
 
 
-def build_instances(wl, n_inst, torch):
-    """n_inst copies of one seeded layer (all 256 + 1 experts, router, head)
-    at distinct device addresses, bound in one slot table (one table layer
-    per instance, a seeded slot permutation)."""
+def build_stack(wl, n_layers, torch):
+    """n_layers resident layers: one seeded set of 256 + 1 expert bundles
+    uploaded once per layer (distinct device addresses), and per layer a
+    seeded router, prerouter head and residual-mixing stand-in for attention.
+    All experts are bound in one slot table (one table layer per layer, a
+    seeded slot permutation)."""
     import synth
     from paper_2609_18063_amd import binding as B, weights as W
     t0 = time.time()
     n_ids = wl.E + wl.S
     bundles = [synth.bundle(wl, 0, e) for e in range(n_ids)]
-    router = synth.router_weights(wl, 0, 0)
-    head = synth.router_weights(wl, 0, 1)
-    buf, boffs, eoffs = W.pack_host(bundles, extra=[router, head])
-    log("packed one layer instance: %.1f MB in %.1fs" % (buf.nbytes / 1e6, time.time() - t0))
+    buf, boffs, _ = W.pack_host(bundles)
+    del bundles
     host = torch.from_numpy(buf).pin_memory()
-    table = B.SlotTable(n_inst, n_ids, n_ids)
+    log("packed the expert bundles of one layer: %.1f MB in %.1fs" % (buf.nbytes / 1e6,
+                                                                      time.time() - t0))
+    table = B.SlotTable(n_layers, n_ids, n_ids)
     perm = np.random.default_rng(1000).permutation(n_ids)
-    inst = []
-    for i in range(n_inst):
+    layers = []
+    for n in range(n_layers):
         dev = torch.empty(buf.nbytes, dtype=torch.uint8, device="cuda")
         dev.copy_(host, non_blocking=True)
-        W.bind_layer(table, i, dev, boffs, perm)
-        inst.append({
+        W.bind_layer(table, n, dev, boffs, perm)
+        mix_d, mix_perm = synth.mixing(wl, n)
+        layers.append({
             "dev": dev,
-            "router": W.extra_tensor(dev, eoffs[0], router.shape, torch.float16),
-            "head": W.extra_tensor(dev, eoffs[1], head.shape, torch.float16),
+            "router": torch.from_numpy(synth.router_weights(wl, n, 0)).cuda(),
+            "head": torch.from_numpy(synth.router_weights(wl, n, 1)).cuda(),
+            "mix_d": torch.from_numpy(mix_d).cuda(),
+            "mix_perm": torch.from_numpy(mix_perm).cuda(),
         })
     table.sync()
     torch.cuda.synchronize()
-    log("uploaded %d instances (%.1f GB) in %.1fs" % (n_inst, n_inst * buf.nbytes / 1e9,
-                                                        time.time() - t0))
-    return table, inst
+    log("uploaded %d layers (%.1f GB) in %.1fs" % (n_layers, n_layers * buf.nbytes / 1e9,
+                                                     time.time() - t0))
+    return table, layers
 
 
-def step(B, spec, table, inst, i, xi_row, bufs):
-    """Enqueue one decode step of instance ``i`` on the current stream."""
+def step(B, spec, table, lay, i, xi_row, bufs):
+    """Enqueue one decode step of table layer ``i`` through the per-call ABI."""
     B.rmsnorm_f16(xi_row, bufs["x"])
-    B.route(spec, bufs["x"], inst["router"], bufs["idx"], bufs["w"], bufs["ws"])
-    B.preroute(spec, bufs["x"], inst["head"], bufs["pidx"], bufs["pw"], bufs["ws"])
+    B.route(spec, bufs["x"], lay["router"], bufs["idx"], bufs["w"], bufs["ws"])
+    B.preroute(spec, bufs["x"], lay["head"], bufs["pidx"], bufs["pw"], bufs["ws"])
     B.expert_ffn(spec, table, i, bufs["x"], bufs["idx"], bufs["ye"], bufs["status"], bufs["ws"])
     B.combine(spec, bufs["ye"], bufs["w"], bufs["y"])
 
@@ -154,13 +161,63 @@ def cpu_baseline(wl, budget_s=15.0):
                       % (done, per_tok)}
 
 
+def time_launch(torch, fn):
+    """GPU time (ms) of the work ``fn`` enqueues, bracketed by events."""
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1)
+
+
+def per_call_path(B, torch, spec, table, layers, tokens, n_steps, wl, hip):
+    """The same single-token steps through the per-call ABI (7 kernels per
+    step), replayed from a HIP graph: reported for comparison."""
+    n = wl.K + wl.S
+    bufs = {
+        "ws": torch.zeros(B.workspace_bytes(spec, 1), dtype=torch.uint8, device="cuda"),
+        "x": torch.empty(1, wl.d, dtype=torch.float16, device="cuda"),
+        "idx": torch.empty(1, wl.K, dtype=torch.int32, device="cuda"),
+        "w": torch.empty(1, wl.K, dtype=torch.float32, device="cuda"),
+        "pidx": torch.empty(1, wl.K, dtype=torch.int32, device="cuda"),
+        "pw": torch.empty(1, wl.K, dtype=torch.float32, device="cuda"),
+        "ye": torch.empty(1, n, wl.d, dtype=torch.float32, device="cuda"),
+        "y": torch.empty(1, wl.d, dtype=torch.float32, device="cuda"),
+        "status": torch.zeros(1, dtype=torch.int32, device="cuda"),
+    }
+    L = len(layers)
+    step(B, spec, table, layers[0], 0, tokens[0:1], bufs)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+        for j in range(n_steps):
+            step(B, spec, table, layers[j % L], j % L, tokens[j:j + 1], bufs)
+    g.replay()
+    ms = time_launch(torch, g.replay)
+    # per-launch time of the gate/up kernel (hipExtLaunchKernelGGL events)
+    evs = [(hip.event(), hip.event()) for _ in range(100)]
+    for j, (a, b) in enumerate(evs):
+        B.profile_arm(B.MOE_PROF_FFN_MAIN, a, b)
+        B.expert_ffn(spec, table, j % L, bufs["x"], bufs["idx"], bufs["ye"], bufs["status"],
+                     bufs["ws"])
+    torch.cuda.synchronize()
+    gu = float(np.mean([hip.elapsed_ms(a, b) for a, b in evs]))
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    return ms / n_steps, gu
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--instances", type=int, default=32)
-    ap.add_argument("--prof-launches", type=int, default=200)
+    ap.add_argument("--layers", type=int, default=40)
+    ap.add_argument("--stack-tokens", type=int, default=256)
+    ap.add_argument("--per-call-steps", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -176,72 +233,50 @@ def main():
     B.lib()
     wl = synth.WORKLOADS["moe35b"]
     spec = B.spec_from_workload(wl)
+    assert B.engine_supported(spec), "the decode engine does not support this device/shape"
     nb = layer_bytes(wl)
-    K, W = args.steps, args.warmup
-    table, inst = build_instances(wl, args.instances, torch)
-
-    tokens = torch.from_numpy(synth.token_draws(wl, 0, K + W)).cuda()
-    n = wl.K + wl.S
-    bufs = {
-        "ws": torch.zeros(B.workspace_bytes(spec, 1), dtype=torch.uint8, device="cuda"),
-        "x": torch.empty(1, wl.d, dtype=torch.float16, device="cuda"),
-        "idx": torch.empty(1, wl.K, dtype=torch.int32, device="cuda"),
-        "w": torch.empty(1, wl.K, dtype=torch.float32, device="cuda"),
-        "pidx": torch.empty(1, wl.K, dtype=torch.int32, device="cuda"),
-        "pw": torch.empty(1, wl.K, dtype=torch.float32, device="cuda"),
-        "ye": torch.empty(1, n, wl.d, dtype=torch.float32, device="cuda"),
-        "y": torch.empty(1, wl.d, dtype=torch.float32, device="cuda"),
-        "status": torch.zeros(1, dtype=torch.int32, device="cuda"),
-    }
-    # eager run once to load kernels, then capture warmup and timed graphs
-    step(B, spec, table, inst[0], 0, tokens[0:1], bufs)
-    torch.cuda.synchronize()
-    s = torch.cuda.Stream()
-    graphs = {}
-    for name, t0, count in (("warmup", K, W), ("timed", 0, K)):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=s):
-            for j in range(count):
-                i = (t0 + j) % args.instances
-                step(B, spec, table, inst[i], i, tokens[t0 + j:t0 + j + 1], bufs)
-        graphs[name] = g
-    torch.cuda.synchronize()
-    log("captured graphs: %d warmup + %d timed steps" % (W, K))
-
-    if W:
-        graphs["warmup"].replay()
-    torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    wall0 = time.perf_counter()
-    ev0.record()
-    graphs["timed"].replay()
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_total = ev0.elapsed_time(ev1)
-    ms_step = ms_total / K
-    assert int(bufs["status"].item()) == 0, "slot miss or bad index during the benchmark"
-    gbs = nb["step"] * K / (ms_total * 1e-3) / 1e9
-    log("timed %d steps: %.3f ms GPU (%.3f ms wall), %.2f us/step, %.1f GB/s"
-        % (K, ms_total, wall * 1e3, ms_step * 1e3, gbs))
-
-    # per-launch duration of the dominant kernel (gate/up expert stage)
+    K, W, L = args.steps, args.warmup, args.layers
+    table, layers = build_stack(wl, L, torch)
+    arr = B.engine_layer_array(layers)
     hip = Hip()
-    evs = [(hip.event(), hip.event()) for _ in range(args.prof_launches)]
-    for j, (a, b) in enumerate(evs):
-        i = j % args.instances
-        B.profile_arm(B.MOE_PROF_FFN_MAIN, a, b)
-        B.expert_ffn(spec, table, i, bufs["x"], bufs["idx"], bufs["ye"], bufs["status"], bufs["ws"])
-    torch.cuda.synchronize()
-    durs = [hip.elapsed_ms(a, b) for a, b in evs]
-    for a, b in evs:
-        hip.destroy(a)
-        hip.destroy(b)
-    dom_ms = float(np.mean(durs))
-    achieved = nb["gateup"] / (dom_ms * 1e-3) / 1e9
-    log("gate/up kernel: mean %.2f us, median %.2f us over %d launches -> %.1f GB/s"
-        % (dom_ms * 1e3, float(np.median(durs)) * 1e3, len(durs), achieved))
+
+    # ---- single-token layer steps (the layer metric): one engine launch ----
+    tokens = torch.from_numpy(synth.token_draws(wl, 0, K + W)).cuda()
+    step_layer = (torch.arange(K + W, dtype=torch.int32, device="cuda") % L).contiguous()
+    y = torch.empty(K + W, wl.d, dtype=torch.float32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+    if W:
+        B.engine_layers(spec, table, arr, step_layer[K:], tokens[K:], y[K:], ws, status=status)
+    ms_total = time_launch(torch, lambda: B.engine_layers(spec, table, arr, step_layer[:K],
+                                                          tokens[:K], y[:K], ws, status=status))
+    assert int(status.item()) == 0, "engine status %d" % int(status.item())
+    ms_step = ms_total / K
+    gbs = nb["step"] * K / (ms_total * 1e-3) / 1e9
+    log("engine, %d single-token steps in one launch: %.3f ms, %.2f us/step, %.1f GB/s"
+        % (K, ms_total, ms_step * 1e3, gbs))
+
+    # ---- 40-layer stack, autoregressive decode (prediction-as-routing) ----
+    T = args.stack_tokens
+    ws2 = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+    r_state = torch.zeros(wl.d, dtype=torch.float32, device="cuda")
+    stack_tok = torch.from_numpy(synth.token_draws(wl, 0, T + 16, stream=1)).cuda()
+    B.engine_chain(spec, table, arr, L, 0, stack_tok[T:], r_state, ws2, status=status)
+    r_state.zero_()
+    ws2.zero_()
+    ms_chain = time_launch(torch, lambda: B.engine_chain(spec, table, arr, L, 0, stack_tok[:T],
+                                                         r_state, ws2, status=status))
+    assert int(status.item()) == 0, "engine status %d" % int(status.item())
+    tok_s = T / (ms_chain * 1e-3)
+    # per token (t >= 1): 40 x the nine bundles, plus 39 heads and the layer-0 router
+    chain_bytes = T * L * (nb["ffn"] + nb["route"] // 2)
+    chain_gbs = chain_bytes / (ms_chain * 1e-3) / 1e9
+    log("engine, %d-layer stack: %d tokens in %.3f ms -> %.1f tok/s, %.1f GB/s"
+        % (L, T, ms_chain, tok_s, chain_gbs))
+
+    # ---- the per-call path, for comparison ----
+    pc_us, gu_ms = per_call_path(B, torch, spec, table, layers, tokens, args.per_call_steps, wl, hip)
+    log("per-call path: %.2f us/step; its gate/up kernel %.2f us" % (pc_us * 1e3, gu_ms * 1e3))
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
     out = {
@@ -260,21 +295,31 @@ def main():
         "config": {
             "workload": "moe35b decode layer at batch 1: d 2048, 256 experts top-8 + 1 shared, "
                         "I 512, int4 g64 + fp16 (s,z), LoRA r16 on gate/up/down, router + "
-                        "prerouter fp16 [256x2048]; %d rotated layer instances" % args.instances,
+                        "prerouter fp16 [256x2048]; single-token steps rotating over %d resident "
+                        "layers" % L,
             "tokens": K,
             "bytes_per_step": nb["step"],
         },
         "pct_peak_hbm": round(100.0 * gbs / PEAK_HBM_GBS, 2),
+        "stack": {
+            "workload": "%d-layer stack of the moe35b layer, %d autoregressive tokens, "
+                        "prediction-as-routing" % (L, T),
+            "tokens_per_s": round(tok_s, 1),
+            "ms_per_token": round(ms_chain / T, 5),
+            "GB_s": round(chain_gbs, 1),
+        },
+        "per_call_path": {"us_per_step": round(pc_us * 1e3, 3),
+                          "gateup_kernel_us": round(gu_ms * 1e3, 3)},
         "roofline": {
             "bound": "hbm",
-            "kernel": "ffn_gateup_kernel (gate/up int4 matvecs + LoRA A)",
-            "achieved": round(achieved, 2),
+            "kernel": "engine_kernel (persistent; %d single-token layer steps per launch)" % K,
+            "achieved": round(gbs, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "frac": round(gbs / PEAK_HBM_GBS, 4),
             "traffic": None,
-            "bytes_per_launch": nb["gateup"],
-            "mean_launch_us": round(dom_ms * 1e3, 3),
+            "bytes_per_launch": nb["step"] * K,
+            "mean_launch_us": round(ms_total * 1e3, 3),
         },
         "cpu_baseline": cpu,
     }

@@ -282,11 +282,17 @@ int moe_engine_chain(const moe_layer_spec* spec, const moe_slot_table* table,
 
 /* ---- profiling (not part of the hot path) ------------------------------- */
 #define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */
+#define MOE_PROF_ENGINE_PHASES 1 /* the next decode-engine launch writes, for
+                                    workgroups 0, 7 and 255, the device wall clock
+                                    (wall_clock64) at 16 marks of every step into
+                                    start_event, read as a device uint64 array
+                                    [n_steps][3][16]; stop_event is unused */
 
 /*
- * Arm per-launch timing. The next launch of kernel `which` on the calling
- * host thread records `start_event` when the kernel starts executing and
- * `stop_event` when it ends (hipEvent_t values created with timing enabled).
+ * Arm per-launch timing. For MOE_PROF_FFN_MAIN, the next launch of that
+ * kernel on the calling host thread records `start_event` when the kernel
+ * starts executing and `stop_event` when it ends (hipEvent_t values created
+ * with timing enabled). For MOE_PROF_ENGINE_PHASES see above.
  * The hook then disarms itself. Do not arm it during graph capture.
  * Returns MOE_EINVAL for an unknown `which` or NULL events.
  */

@@ -88,6 +88,7 @@ SIGNATURES = {
 }
 
 MOE_PROF_FFN_MAIN = 0
+MOE_PROF_ENGINE_PHASES = 1
 
 
 def lib():

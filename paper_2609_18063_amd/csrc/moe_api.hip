@@ -69,6 +69,7 @@ struct ProfArm {
   hipEvent_t start = nullptr, stop = nullptr;
 };
 thread_local ProfArm g_prof_ffn;
+thread_local void* g_prof_engine_ts = nullptr;
 
 template <typename T>
 T* at(void* base, size_t off) {
@@ -400,6 +401,8 @@ static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n
   a.n_table_layers = t->n_layers;
   a.slot_of = reinterpret_cast<const int32_t*>(t->dev);
   a.bundles = reinterpret_cast<const moe_bundle*>(static_cast<const char*>(t->dev) + t->bundles_off);
+  a.phase_ts = static_cast<uint64_t*>(g_prof_engine_ts);
+  g_prof_engine_ts = nullptr;
   a.ctl = static_cast<uint32_t*>(ws);
   a.xw = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + kEngineCtlBytes);
   return from_hip(moe::launch_engine(a, s->d_model, s->d_expert, s->lora_rank,
@@ -457,6 +460,11 @@ int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,
 }
 
 int moe_profile_arm(int which, void* start_event, void* stop_event) {
+  if (which == MOE_PROF_ENGINE_PHASES) {
+    if (!start_event || !aligned16(start_event)) return MOE_EINVAL;
+    g_prof_engine_ts = start_event;
+    return MOE_OK;
+  }
   if (which != MOE_PROF_FFN_MAIN || !start_event || !stop_event) return MOE_EINVAL;
   g_prof_ffn.start = static_cast<hipEvent_t>(start_event);
   g_prof_ffn.stop = static_cast<hipEvent_t>(stop_event);

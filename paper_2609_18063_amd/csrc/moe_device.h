@@ -31,13 +31,68 @@ __device__ __forceinline__ float ld_agent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Sum over groups of `width` consecutive lanes (width a power of two <= 64).
-__device__ __forceinline__ float group_sum(float v, int width) {
-  for (int off = width >> 1; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+// DPP lane moves (gfx9 data-parallel primitives): a few cycles each, against
+// an LDS round trip for a shuffle.  Controls used: quad_perm [1,0,3,2] (0xB1)
+// and [2,3,0,1] (0x4E), row_half_mirror (0x141), row_mirror (0x140),
+// row_bcast15 (0x142), row_bcast31 (0x143).  `old` is the value a lane keeps
+// when its row is masked off.
+template <int CTRL, int ROWMASK = 0xf>
+__device__ __forceinline__ float dpp_f(float old, float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), CTRL, ROWMASK, 0xf, false));
+}
+template <int CTRL, int ROWMASK = 0xf>
+__device__ __forceinline__ int dpp_i(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROWMASK, 0xf, false);
+}
+
+// Sum over each row of 16 lanes; every lane of the row receives the sum.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f<0xB1>(0.f, v);
+  v += dpp_f<0x4E>(0.f, v);
+  v += dpp_f<0x141>(0.f, v);
+  v += dpp_f<0x140>(0.f, v);
   return v;
 }
 
-__device__ __forceinline__ float wave_sum(float v) { return group_sum(v, kWave); }
+// Sum over the 64 lanes of a wave, returned to every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = row16_sum(v);
+  v += dpp_f<0x142, 0xa>(0.f, v);
+  v += dpp_f<0x143, 0xc>(0.f, v);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// Sum over groups of `width` consecutive lanes (width a power of two <= 64);
+// every lane of a group receives its group's sum.
+__device__ __forceinline__ float group_sum(float v, int width) {
+  if (width >= 64) return wave_sum(v);
+  if (width >= 2) v += dpp_f<0xB1>(0.f, v);
+  if (width >= 4) v += dpp_f<0x4E>(0.f, v);
+  if (width >= 8) v += dpp_f<0x141>(0.f, v);
+  if (width >= 16) v += dpp_f<0x140>(0.f, v);
+  if (width >= 32) v += __shfl_xor(v, 16, kWave);
+  return v;
+}
+
+// (value, index) arg-max over the wave: larger value wins, equal values go
+// to the lower index; the winner is returned to every lane.
+__device__ __forceinline__ void argmax_step(float& v, int& i, float ov, int oi) {
+  if (ov > v || (ov == v && oi < i)) {
+    v = ov;
+    i = oi;
+  }
+}
+__device__ __forceinline__ void wave_argmax(float& v, int& i) {
+  argmax_step(v, i, dpp_f<0xB1>(v, v), dpp_i<0xB1>(i, i));
+  argmax_step(v, i, dpp_f<0x4E>(v, v), dpp_i<0x4E>(i, i));
+  argmax_step(v, i, dpp_f<0x141>(v, v), dpp_i<0x141>(i, i));
+  argmax_step(v, i, dpp_f<0x140>(v, v), dpp_i<0x140>(i, i));
+  argmax_step(v, i, dpp_f<0x142, 0xa>(v, v), dpp_i<0x142, 0xa>(i, i));
+  argmax_step(v, i, dpp_f<0x143, 0xc>(v, v), dpp_i<0x143, 0xc>(i, i));
+  v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+  i = __builtin_amdgcn_readlane(i, 63);
+}
 
 // Dot product of 32 int4 codes (16 bytes, even input in the low nibble) with
 // 32 fp32 activations.  Codes are exact small integers in fp32.
@@ -104,15 +159,18 @@ __device__ __forceinline__ const moe_bundle* resolve_expert(int k, int K, int E,
 // weights are the softmax renormalized over the selected set.
 constexpr int kTopkVals = 16;  // E <= 64 * 16
 
-template <bool kAgent>
+// Branch-free: every lane keeps its values with a taken mask; each of the K
+// rounds takes the lane-local best with selects and one DPP arg-max.
+template <bool kAgent, int NV = kTopkVals>
 __device__ void wave_topk(const float* l, int E, int K, int32_t* idx_out, float* w_out) {
   const int lane = threadIdx.x & 63;
-  float v[kTopkVals];
+  const int nv = (E + 63) >> 6;  // values per lane actually used (<= NV)
+  float v[NV];
 #pragma unroll
-  for (int j = 0; j < kTopkVals; ++j) {
+  for (int j = 0; j < NV; ++j) {
     const int e = lane + 64 * j;
     float a = -INFINITY;
-    if (e < E) a = kAgent ? ld_agent(l + e) : l[e];
+    if (j < nv && e < E) a = kAgent ? ld_agent(l + e) : l[e];
     v[j] = (a != a) ? -INFINITY : a;
   }
   uint32_t taken = 0;
@@ -121,27 +179,19 @@ __device__ void wave_topk(const float* l, int E, int K, int32_t* idx_out, float*
     float bv = -INFINITY;
     int bi = 0x7fffffff;
 #pragma unroll
-    for (int j = 0; j < kTopkVals; ++j) {
+    for (int j = 0; j < NV; ++j) {
       const int e = lane + 64 * j;
-      if (e < E && !((taken >> j) & 1u) && (v[j] > bv || (v[j] == bv && e < bi))) {
-        bv = v[j];
-        bi = e;
-      }
+      const bool cand = (j < nv) & (e < E) & !((taken >> j) & 1u);
+      const bool better = cand & ((v[j] > bv) | ((v[j] == bv) & (e < bi)));
+      bv = better ? v[j] : bv;
+      bi = better ? e : bi;
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const float ov = __shfl_xor(bv, off, kWave);
-      const int oi = __shfl_xor(bi, off, kWave);
-      if (ov > bv || (ov == bv && oi < bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
-    if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
-    if (lane == k) mine = bv;
+    wave_argmax(bv, bi);
+    taken |= ((bi & 63) == lane) ? (1u << ((bi >> 6) & 31)) : 0u;
+    mine = (lane == k) ? bv : mine;
     if (lane == 0) idx_out[k] = bi;
   }
-  const float m = __shfl(mine, 0, kWave);
+  const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine), 0));
   const float ex = (lane < K) ? expf(mine - m) : 0.f;
   const float s = wave_sum(ex);
   if (lane < K) w_out[lane] = ex / s;

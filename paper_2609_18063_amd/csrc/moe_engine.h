@@ -27,11 +27,12 @@ struct EngineArgs {
   int32_t* pidx_rec;
   float* pw_rec;
   uint32_t* status;
+  uint64_t* phase_ts;            // profiling: [n_steps][3][10] wall-clock marks, or null
   uint32_t* ctl;                 // workspace control words
   uint64_t* xw;                  // workspace exchange words
   // exchange-area offsets and per-parity strides (in 64-bit words)
-  size_t xo_logr, xs_logr, xo_loghm, xo_av, xs_av, xo_hv, xs_hv, xo_part, xs_part, xo_rv, xs_rv,
-      xo_logh, xs_logh_layer;
+  size_t xo_logr, xs_logr, xo_loghm, xo_av, xs_av, xo_hv, xs_hv, xo_adp, xs_adp, xo_part, xs_part,
+      xo_rv, xs_rv, xo_logh, xs_logh_layer;
 };
 
 bool engine_shape_supported(int d, int I, int r, int K, int S, int E);

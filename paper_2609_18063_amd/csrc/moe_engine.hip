@@ -132,14 +132,15 @@ struct Shape {
   static constexpr int O_DQ = O_BGU + kb(2 * RMX * R * 2);          // [DR][GXX/2]
   static constexpr int O_DS = O_DQ + kb(DR * GXX / 2);              // [DR][NSEGX][IE/16]
   static constexpr int O_BD = O_DS + kb(DR * NSEGX * IE / 16);      // [DR][NSEGX][R] fp16
-  static constexpr int O_ADR = O_BD + kb(DR * NSEGX * R * 2);       // [R][GXX] fp16
-  static constexpr int O_XF = O_ADR + kb(R * GXX * 2);              // [D] f32
+  static constexpr int O_ADM = O_BD + kb(DR * NSEGX * R * 2);       // [R][NSEGX][32] fp16
+  static constexpr int O_XF = O_ADM + kb(R * NSEGX * 32 * 2);       // [D] f32
   static constexpr int O_XH = O_XF + D * 4;                         // [D] f16
   static constexpr int O_R0 = O_XH + D * 2;                         // [D] f32
   static constexpr int O_R1 = O_R0 + D * 4;                         // [D] f32
   static constexpr int O_LG = O_R1 + D * 4;                         // [1024] f32 logits
   static constexpr int O_HX = O_LG + 1024 * 4;                      // [GXX] f32 h of the XCD
-  static constexpr int O_GXU = O_HX + GXX * 4;                      // [2*RMX] f32
+  static constexpr int O_HL = O_HX + GXX * 4;                       // [RMX] f32 own h
+  static constexpr int O_GXU = O_HL + RMX * 4;                      // [2*RMX] f32
   static constexpr int O_DP = O_GXU + 2 * RMX * 4;                  // [DR][32] f32 down partials
   static constexpr int O_AV = O_DP + DR * 32 * 4;                   // [NSEGX][2R] f32
   static constexpr int O_ADV = O_AV + NSEGX * 2 * R * 4;            // [NSEGX][R] f32
@@ -166,33 +167,33 @@ struct Misc {
   Seg seg[4];
   float segw[4];
   int segok[4];
-  const moe_bundle* segb[4];
+  moe_bundle segbd[4];   // the segments' bundles, copied from the slot table
 };
 
 __device__ __forceinline__ float silu(float z) { return z / (1.f + expf(-z)); }
 
-template <class SH>
-__device__ void block_rmsnorm_to_x(const float* v, float* xf, __half* xh, double* red) {
-  double acc = 0.0;
-  for (int j = threadIdx.x; j < SH::D; j += NT) {
-    const double a = v[j];
-    acc += a * a;
-  }
-  red[threadIdx.x] = acc;
-  __syncthreads();
-  for (int s = NT / 2; s > 0; s >>= 1) {
-    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
-    __syncthreads();
-  }
-  const double inv = 1.0 / sqrt(red[0] / (double)SH::D + 1e-6);
-  __syncthreads();
-  for (int j = threadIdx.x; j < SH::D; j += NT) {
-    const __half h = __half(static_cast<_Float16>((double)v[j] * inv));
-    xh[j] = h;
-    xf[j] = __half2float(h);
-  }
+// fp64 sum over the wave (DPP on the two 32-bit halves of each step's operand)
+template <int CTRL, int ROWMASK = 0xf>
+__device__ __forceinline__ double dpp_d(double v) {
+  const uint64_t b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROWMASK, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, ROWMASK, 0xf, false);
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+__device__ __forceinline__ double wave_sum_f64(double v) {
+  v += dpp_d<0xB1>(v);
+  v += dpp_d<0x4E>(v);
+  v += dpp_d<0x141>(v);
+  v += dpp_d<0x140>(v);
+  v += dpp_d<0x142, 0xa>(v);
+  v += dpp_d<0x143, 0xc>(v);
+  const uint64_t b = __double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)b, 63);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), 63);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// Sum of squares of v[0..D) in fp64 over the workgroup (two barriers).
 template <class SH>
 __device__ double block_sumsq(const float* v, double* red) {
   double acc = 0.0;
@@ -200,15 +201,24 @@ __device__ double block_sumsq(const float* v, double* red) {
     const double a = v[j];
     acc += a * a;
   }
-  red[threadIdx.x] = acc;
+  acc = wave_sum_f64(acc);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();
-  for (int s = NT / 2; s > 0; s >>= 1) {
-    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
-    __syncthreads();
+  double tot = 0.0;
+#pragma unroll
+  for (int w = 0; w < NWV; ++w) tot += red[w];
+  __syncthreads();
+  return tot;
+}
+
+template <class SH>
+__device__ void block_rmsnorm_to_x(const float* v, float* xf, __half* xh, double* red) {
+  const double inv = 1.0 / sqrt(block_sumsq<SH>(v, red) / (double)SH::D + 1e-6);
+  for (int j = threadIdx.x; j < SH::D; j += NT) {
+    const __half h = __half(static_cast<_Float16>((double)v[j] * inv));
+    xh[j] = h;
+    xf[j] = __half2float(h);
   }
-  const double r = red[0];
-  __syncthreads();
-  return r;
 }
 
 // fp16 row (D halves in LDS) . x (fp16 in LDS) by one wave; fp32 accumulate.
@@ -237,6 +247,17 @@ __device__ __forceinline__ void stage(char* dst, int nchunks, SrcF src) {
   }
 }
 
+// Phase timestamps for the profiling hook: thread 0 of workgroups 0, 7 and
+// 255 writes the constant-rate wall clock at up to 16 marks of every step.
+constexpr int kProfMarks = 16;
+__device__ __forceinline__ void mark(const EngineArgs& a, int s, int k) {
+  if (!a.phase_ts || threadIdx.x != 0) return;
+  const int g = blockIdx.x;
+  const int slot = g == 0 ? 0 : (g == 7 ? 1 : (g == NWG - 1 ? 2 : -1));
+  if (slot < 0) return;
+  a.phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
+}
+
 template <class SH>
 __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
@@ -250,7 +271,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   uint8_t* dq = reinterpret_cast<uint8_t*>(smem + SH::O_DQ);
   uint8_t* ds = reinterpret_cast<uint8_t*>(smem + SH::O_DS);
   __half* bd = reinterpret_cast<__half*>(smem + SH::O_BD);
-  __half* adr = reinterpret_cast<__half*>(smem + SH::O_ADR);
+  __half* adm = reinterpret_cast<__half*>(smem + SH::O_ADM);
   float* xf = reinterpret_cast<float*>(smem + SH::O_XF);
   __half* xh = reinterpret_cast<__half*>(smem + SH::O_XH);
   float* r0 = reinterpret_cast<float*>(smem + SH::O_R0);
@@ -258,6 +279,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   float* lg = reinterpret_cast<float*>(smem + SH::O_LG);
   float* hx = reinterpret_cast<float*>(smem + SH::O_HX);
   float* gxu = reinterpret_cast<float*>(smem + SH::O_GXU);
+  float* hl = reinterpret_cast<float*>(smem + SH::O_HL);
   float* dp = reinterpret_cast<float*>(smem + SH::O_DP);
   float* av = reinterpret_cast<float*>(smem + SH::O_AV);
   float* adv = reinterpret_cast<float*>(smem + SH::O_ADV);
@@ -305,6 +327,13 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   const int nseg = mi->nseg;
 
   uint64_t* const X = a.xw;
+  float xi_next[SH::MAXI_D];
+  if (a.mode == 0)
+#pragma unroll
+    for (int q = 0; q < SH::MAXI_D; ++q) {
+      const int j = threadIdx.x + q * NT;
+      xi_next[q] = j < D ? a.xi[j] : 0.f;
+    }
   for (int s = 0; s < a.n_steps && !mi->abort; ++s) {
     const uint32_t tag = base + (uint32_t)s + 1u;
     const int par = s & 1;
@@ -325,10 +354,22 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     const moe_engine_layer LY = a.layers[lay];
     has_head = LY.head != nullptr && (a.mode == 0 || N + 1 < a.L);
 
+    mark(a, s, 0);
     // ---- S0: layer input ------------------------------------------------
     if (a.mode == 0) {
-      const float* xi = a.xi + (size_t)s * D;
-      for (int j = threadIdx.x; j < D; j += NT) r0[j] = xi[j];
+#pragma unroll
+      for (int q = 0; q < SH::MAXI_D; ++q) {
+        const int j = threadIdx.x + q * NT;
+        if (j < D) r0[j] = xi_next[q];
+      }
+      if (s + 1 < a.n_steps) {  // the next step's draws arrive while this step runs
+        const float* xn = a.xi + (size_t)(s + 1) * D;
+#pragma unroll
+        for (int q = 0; q < SH::MAXI_D; ++q) {
+          const int j = threadIdx.x + q * NT;
+          xi_next[q] = j < D ? xn[j] : 0.f;
+        }
+      }
       __syncthreads();
       block_rmsnorm_to_x<SH>(r0, xf, xh, red);
     } else {
@@ -360,6 +401,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     if (g == 0 && a.x_rec)
       for (int j = threadIdx.x; j < D; j += NT) a.x_rec[(size_t)s * D + j] = xh[j];
 
+    mark(a, s, 1);
     // ---- S1: routing ----------------------------------------------------
     if (own_route) {
       uint64_t* lr = X + a.xo_logr + (size_t)par * a.xs_logr;
@@ -375,6 +417,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const float v = wave_dot_h<SH>(rtrow + (size_t)q * D, xh);
         if (lane == 0 && e < E) st_tag(lr + e, tag, v);
       }
+      mark(a, s, 12);
       if (!poll_all<2>(E, tag, [&](int i) { return lr + i; }, [&](int i, float v) { lg[i] = v; }, c,
                        &mi->abort))
         break;
@@ -384,8 +427,10 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
                        [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
         break;
     }
-    if (wave == 0) wave_topk<false>(lg, E, K, mi->idx, mi->w);
+    mark(a, s, 10);
+    if (wave == 0) wave_topk<false, 4>(lg, E, K, mi->idx, mi->w);
     __syncthreads();
+    mark(a, s, 11);
     if (g == 0 && threadIdx.x < K) {
       if (a.idx_rec) a.idx_rec[(size_t)s * K + threadIdx.x] = mi->idx[threadIdx.x];
       if (a.w_rec) a.w_rec[(size_t)s * K + threadIdx.x] = mi->w[threadIdx.x];
@@ -397,7 +442,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       const bool bad = k < K && (e < 0 || e >= E);
       const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
       mi->segok[q] = slot >= 0;
-      mi->segb[q] = slot >= 0 ? a.bundles + (size_t)lay * a.n_slots + slot : nullptr;
+      if (slot >= 0) mi->segbd[q] = a.bundles[(size_t)lay * a.n_slots + slot];
       mi->segw[q] = k < K ? mi->w[k] : 1.f;
       if (m == 0 && a.status) {
         if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
@@ -406,6 +451,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     }
     __syncthreads();
 
+    mark(a, s, 2);
     // ---- S2: stage weights, gate/up rows, LoRA-A rows, head rows --------
     // gate/up row r of this workgroup: r < RM gate, else up; flattened row
     // fr = x*GX + m*RM + (r % RM) -> segment and expert row.
@@ -420,7 +466,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int rr = i / QCH, ch = i % QCH;
         const int lr = m * RM + (rr % RM);
         const int q = row_seg(lr);
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         if (!b) return a.xi;  // any valid address; the row is not used
         const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
         const uint8_t* base_q = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.q : b->up.q);
@@ -431,7 +477,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int rr = i / SCH, ch = i % SCH;
         const int lr = m * RM + (rr % RM);
         const int q = row_seg(lr);
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         if (!b) return a.xi;
         const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
         const uint8_t* base_s = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.sz : b->up.sz);
@@ -443,7 +489,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int ar = m + NM * qa;
         if (ar >= nseg * 2 * R) return a.xi;
         const int q = ar / (2 * R), rr = ar % (2 * R);
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         const void* A = b ? (rr < R ? b->gate.lora_a : b->up.lora_a) : nullptr;
         if (!A) return a.xi;
         return reinterpret_cast<const __half*>(A) + (size_t)(rr % R) * D + ch * 8;
@@ -461,7 +507,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int rr = i / BCH, ch = i % BCH;
         const int lr = m * RM + (rr % RM);
         const int q = row_seg(lr);
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         const void* B = b ? (rr < RM ? b->gate.lora_b : b->up.lora_b) : nullptr;
         if (!B) return a.xi;
         const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
@@ -473,7 +519,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int jj = i / dqch, ch = i % dqch;
         const int col = ch * 32;
         const int q = row_seg(col);
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         if (!b) return a.xi;
         const int ec = mi->seg[q].i0 + (col - mi->seg[q].col0);
         return reinterpret_cast<const uint8_t*>(b->down.q) + (size_t)(m * SH::DR + jj) * (IE / 2) +
@@ -485,7 +531,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int jq = i / DSCH, ch = i % DSCH;
         const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
         if (q >= nseg) return a.xi;
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         if (!b) return a.xi;
         return reinterpret_cast<const uint8_t*>(b->down.sz) + (size_t)(m * SH::DR + jj) * (IE / 16) +
                ch * 16;
@@ -495,27 +541,31 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int jq = i / BCH, ch = i % BCH;
         const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
         if (q >= nseg) return a.xi;
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         const void* B = b ? b->down.lora_b : nullptr;
         if (!B) return a.xi;
         return reinterpret_cast<const __half*>(B) + (size_t)(m * SH::DR + jj) * R + ch * 8;
       });
-      // LoRA-A of down restricted to the XCD's columns: [kk][GX]
-      const int adch = GX / 8;
-      stage(smem + SH::O_ADR, R * adch, [&](int i) -> const void* {
-        const int kk = i / adch, ch = i % adch;
-        const int col = ch * 8;
-        const int q = row_seg(col);
-        const moe_bundle* b = mi->segb[q];
+      // LoRA-A of down at this workgroup's rows: [kk][q][4 chunks of 8 halves]
+      // covering expert rows [e_lo(q) & ~7, e_hi(q)) of each segment q
+      stage(smem + SH::O_ADM, R * SH::NSEGX * 4, [&](int i) -> const void* {
+        const int kk = i / (SH::NSEGX * 4), q = (i / 4) % SH::NSEGX, cch = i % 4;
+        if (q >= nseg) return a.xi;
+        const int lo = max(m * RM, mi->seg[q].col0);
+        const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         const void* A = b ? b->down.lora_a : nullptr;
-        if (!A) return a.xi;
-        const int ec = mi->seg[q].i0 + (col - mi->seg[q].col0);
+        if (!A || lo >= hi) return a.xi;
+        const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
+        int ec = e0 + 8 * cch;
+        if (ec > IE - 8) ec = IE - 8;
         return reinterpret_cast<const __half*>(A) + (size_t)kk * IE + ec;
       });
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
+    mark(a, s, 3);
     // gate/up matvecs (raw): rows r of [gate RM | up RM], LPR lanes per row
     {
       const int c0 = lane % SH::LPR, sub = lane / SH::LPR;
@@ -554,7 +604,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int ar = m + NM * qa;
         if (ar >= nseg * 2 * R) continue;
         const int q = ar / (2 * R), rr = ar % (2 * R);
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         const bool has = b && (rr < R ? (b->gate.lora_a && b->gate.lora_b)
                                       : (b->up.lora_a && b->up.lora_b));
         const float v = has ? wave_dot_h<SH>(arow + (size_t)qa * D, xh) : 0.f;
@@ -580,6 +630,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     }
     __syncthreads();
 
+    mark(a, s, 4);
     // ---- S3: a-vectors of the XCD -> h of this workgroup's rows ---------
     {
       uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
@@ -591,7 +642,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int i = threadIdx.x;
         const int lr = m * RM + i;
         const int q = row_seg(lr);
-        const moe_bundle* b = mi->segb[q];
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
         float hv = 0.f;
         if (b) {
           float gg = gxu[i], uu = gxu[RM + i];
@@ -610,29 +661,54 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           hv = silu(gg) * uu;
         }
         st_tag(HV + lr, tag, hv);
+        hl[i] = hv;
+      }
+      __syncthreads();
+      // partial a_d[q][kk] over this workgroup's rows of segment q -> ADP
+      uint64_t* ADP = X + a.xo_adp + (size_t)par * a.xs_adp +
+                      ((size_t)x * NM + m) * SH::NSEGX * R;
+      for (int p = threadIdx.x; p < nseg * R; p += NT) {
+        const int q = p / R, kk = p % R;
+        const int lo = max(m * RM, mi->seg[q].col0);
+        const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
+        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
+        float acc = 0.f;
+        if (b && b->down.lora_a && b->down.lora_b && lo < hi) {
+          const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
+          for (int lr2 = lo; lr2 < hi; ++lr2) {
+            const int ec = mi->seg[q].i0 + (lr2 - mi->seg[q].col0);
+            acc = fmaf(__half2float(adm[((size_t)kk * SH::NSEGX + q) * 32 + (ec - e0)]),
+                       hl[lr2 - m * RM], acc);
+          }
+        }
+        st_tag(ADP + p, tag, acc);
       }
     }
 
+    mark(a, s, 5);
     // ---- S4: h of the XCD -> down rows -> tagged partial of the output ---
     {
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
       if (!poll_all<(SH::GXX + NT - 1) / NT>(GX, tag, [&](int i) { return HV + i; },
                                             [&](int i, float v) { hx[i] = v; }, c, &mi->abort))
         break;
-      // a_d[q][kk] = A_down[kk][segment q columns] . h: 16 lanes per (q, kk)
-      for (int pbase = 0; pbase < nseg * R; pbase += NT / 16) {
-        const int p = pbase + (int)threadIdx.x / 16, part = threadIdx.x % 16;
-        float acc = 0.f;
-        if (p < nseg * R) {
-          const int q = p / R, kk = p % R;
-          const int c0 = mi->seg[q].col0, len = mi->seg[q].len;
-          for (int cix = part; cix < len; cix += 16)
-            acc = fmaf(__half2float(adr[(size_t)kk * GX + c0 + cix]), hx[c0 + cix], acc);
+      // a_d[q][kk] = sum of the 32 members' partials
+      {
+        uint64_t* ADP = X + a.xo_adp + (size_t)par * a.xs_adp + (size_t)x * NM * SH::NSEGX * R;
+        const int per = nseg * R;
+        if (!poll_all<(NM * SH::NSEGX * R + NT - 1) / NT>(
+                NM * per, tag,
+                [&](int i) { return ADP + (size_t)(i / per) * SH::NSEGX * R + (i % per); },
+                [&](int i, float v) { dp[i] = v; }, c, &mi->abort))
+          break;
+        for (int p = threadIdx.x; p < per; p += NT) {
+          float acc = 0.f;
+          for (int mm = 0; mm < NM; ++mm) acc += dp[mm * per + p];
+          adv[p] = acc;
         }
-        acc = group_sum(acc, 16);
-        if (part == 0 && p < nseg * R) adv[p] = acc;
+        __syncthreads();
       }
-      __syncthreads();
+      mark(a, s, 6);
       // down matvec: lane -> 32-column chunk ch (fixed), RPID rows per wave instruction
       const int ch = lane % LPRD, sub = lane / LPRD;
       const bool active = sub < RPID;
@@ -661,21 +737,28 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       }
       __syncthreads();
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part + (size_t)x * D;
-      for (int jj = threadIdx.x; jj < SH::DR; jj += NT) {
+      // 8 threads per row: chunk partials and LoRA-B terms, then a DPP sum
+      for (int base = 0; base < SH::DR * 8; base += NT) {
+        const int tt = base + (int)threadIdx.x;
+        const int jj = tt >> 3, part = tt & 7;
         float acc = 0.f;
-        for (int cc = 0; cc < LPRD; ++cc) acc += dp[jj * 32 + cc];
-        for (int q = 0; q < nseg; ++q) {
-          const moe_bundle* b = mi->segb[q];
-          if (!b || !b->down.lora_a || !b->down.lora_b) continue;
-          float la = 0.f;
-          for (int kk = 0; kk < R; ++kk)
-            la = fmaf(__half2float(bd[((size_t)jj * SH::NSEGX + q) * R + kk]), adv[q * R + kk], la);
-          acc = fmaf(mi->segw[q] * a.lora_scale, la, acc);
+        if (jj < SH::DR) {
+          for (int cc = part; cc < LPRD; cc += 8) acc += dp[jj * 32 + cc];
+          for (int term = part; term < nseg * R; term += 8) {
+            const int q = term / R, kk = term % R;
+            const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
+            if (!b || !b->down.lora_a || !b->down.lora_b) continue;
+            acc = fmaf(mi->segw[q] * a.lora_scale *
+                           __half2float(bd[((size_t)jj * SH::NSEGX + q) * R + kk]),
+                       adv[q * R + kk], acc);
+          }
         }
-        st_tag(PART + m * SH::DR + jj, tag, acc);
+        acc = group_sum(acc, 8);
+        if (part == 0 && jj < SH::DR) st_tag(PART + m * SH::DR + jj, tag, acc);
       }
     }
 
+    mark(a, s, 7);
     // ---- S5: reduce the 8 XCD partials of this workgroup's rows ---------
     {
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part;
@@ -683,6 +766,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
                        [&](int i) { return PART + (size_t)(i % NX) * D + g * SH::RR + i / NX; },
                        [&](int i, float v) { yl[i] = v; }, c, &mi->abort))
         break;
+      mark(a, s, 8);
       if ((int)threadIdx.x < SH::RR) {
         const int jr = threadIdx.x, j = g * SH::RR + jr;
         float y = 0.f;
@@ -713,7 +797,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         if (wave == 0) {
           int32_t* pi = mi->pidx;
           float* pw = mi->pw;
-          wave_topk<false>(lg, E, K, pi, pw);
+          wave_topk<false, 4>(lg, E, K, pi, pw);
           if (lane < K) {
             if (a.pidx_rec) a.pidx_rec[(size_t)s * K + lane] = pi[lane];
             if (a.pw_rec) a.pw_rec[(size_t)s * K + lane] = pw[lane];
@@ -721,6 +805,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
       }
       __syncthreads();
+      mark(a, s, 9);
     }
   }
 
@@ -805,6 +890,8 @@ size_t engine_workspace_words(int E, int d, int L, EngineArgs* a) {
   a->xo_av = take(2 * a->xs_av);
   a->xs_hv = (size_t)eng::NX * GXX;
   a->xo_hv = take(2 * a->xs_hv);
+  a->xs_adp = (size_t)eng::NX * eng::NM * NSEGX * R;
+  a->xo_adp = take(2 * a->xs_adp);
   a->xs_part = (size_t)eng::NX * d;
   a->xo_part = take(2 * a->xs_part);
   a->xs_rv = (size_t)d;

@@ -185,6 +185,24 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* spec, const moe_slot_table* t
                              void* stream);
 
 /*
+ * Batched decode / prefill experts (Sec. 3.1, Executor paths: the whole-layer
+ * path serves prefill; Math contract: every path gives the same outputs).
+ * Same inputs, outputs and status behaviour as moe_expert_ffn_int4_lora, for
+ * many tokens at once: the (token, expert) pairs are grouped by expert and
+ * each group runs as a dense contraction on the matrix cores. The int4
+ * weights are dequantized to fp16 (w = s q + z, rounded once), the token
+ * activations are fp16, h = silu(g) u is rounded to fp16 between the two
+ * contractions, and lora_scale * (A v) is rounded to fp16 for the LoRA-B
+ * step; every sum accumulates in fp32.
+ * Shapes: d and I multiples of 128, lora_rank <= 16, E + S <= 2048; other
+ * specs give MOE_EINVAL. Uses the workspace of moe_workspace_bytes(spec, T).
+ */
+int moe_expert_ffn_grouped_int4_lora(const moe_layer_spec* spec, const moe_slot_table* table,
+                                     int layer, const void* x_f16, int T, const int32_t* idx,
+                                     float* y_experts, uint32_t* status_dev, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
+/*
  * Combine (Fig. 1 sum node): y[t] = sum_{k<K} w[t][k] y_experts[t][k]
  *                                  + sum_{s<S} y_experts[t][K+s].
  * y: device fp32 [T][d].

@@ -68,6 +68,9 @@ SIGNATURES = {
     "moe_expert_ffn_int4_lora": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p,
                                          c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                          c_void_p]),
+    "moe_expert_ffn_grouped_int4_lora": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int,
+                                                 c_void_p, c_int, c_void_p, c_void_p, c_void_p,
+                                                 c_void_p, c_size_t, c_void_p]),
     "moe_combine": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
                             c_void_p]),
     "moe_topk": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p, c_void_p,
@@ -242,6 +245,17 @@ def expert_ffn(spec, table, layer, x, idx, y_experts, status, workspace, stream=
                                           _ptr(idx), _ptr(y_experts), _ptr(status), _ptr(workspace),
                                           workspace.numel() * workspace.element_size(),
                                           _stream(stream)), "moe_expert_ffn_int4_lora")
+
+
+def expert_ffn_grouped(spec, table, layer, x, idx, y_experts, status, workspace, stream=None):
+    """Batched / prefill experts: same contract as ``expert_ffn``, grouped by expert."""
+    T = x.shape[0]
+    _check(lib().moe_expert_ffn_grouped_int4_lora(ctypes.byref(spec), table.handle, layer, _ptr(x),
+                                                  T, _ptr(idx), _ptr(y_experts), _ptr(status),
+                                                  _ptr(workspace),
+                                                  workspace.numel() * workspace.element_size(),
+                                                  _stream(stream)),
+           "moe_expert_ffn_grouped_int4_lora")
 
 
 def combine(spec, y_experts, w, y, stream=None):

@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "moe_engine.h"
+#include "moe_grouped.h"
 #include "moe_kernels.h"
 
 struct moe_slot_table {
@@ -37,7 +38,10 @@ bool pow2_dim(int v) {
 }
 
 struct WsLayout {
-  size_t counters, logits, gx, ux, h, ag, au, adpart, total;
+  size_t counters, logits, gx, ux, h, ag, au, adpart;
+  size_t g_perm, g_tiles, g_ntiles, g_h;  // grouped (batched) path
+  int g_max_tiles;
+  size_t total;
 };
 
 WsLayout ws_layout(const moe_layer_spec* s, int T) {
@@ -58,6 +62,11 @@ WsLayout ws_layout(const moe_layer_spec* s, int T) {
   w.ag = take((size_t)T * n * r * sizeof(float));
   w.au = take((size_t)T * n * r * sizeof(float));
   w.adpart = take((size_t)T * n * (s->d_expert / 64) * r * sizeof(float));
+  w.g_max_tiles = moe::grouped_max_tiles(T, (int)n, s->n_experts + s->n_shared);
+  w.g_perm = take((size_t)T * n * sizeof(int32_t));
+  w.g_tiles = take((size_t)w.g_max_tiles * sizeof(moe::GroupTile));
+  w.g_ntiles = take(sizeof(int32_t));
+  w.g_h = take((size_t)T * n * s->d_expert * sizeof(__half));
   w.total = off;
   return w;
 }
@@ -301,6 +310,51 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, i
   ProfArm arm = g_prof_ffn;
   g_prof_ffn = ProfArm{};
   return from_hip(moe::launch_ffn(a, T, static_cast<hipStream_t>(stream), arm.start, arm.stop));
+}
+
+int moe_expert_ffn_grouped_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, int layer,
+                                     const void* x_f16, int T, const int32_t* idx, float* y_experts,
+                                     uint32_t* status_dev, void* ws, size_t ws_bytes, void* stream) {
+  int rc = moe_spec_check(s);
+  if (rc != MOE_OK) return rc;
+  if (!t || T < 0) return MOE_EINVAL;
+  if (layer < 0 || layer >= t->n_layers || t->n_ids < s->n_experts + s->n_shared)
+    return MOE_EINVAL;
+  if (!moe::grouped_shape_supported(s->d_model, s->d_expert, s->lora_rank,
+                                    s->n_experts + s->n_shared))
+    return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!x_f16 || !idx || !y_experts || !ws) return MOE_EINVAL;
+  if (!t->dev) return MOE_EINVAL;  // never synced to the device
+  if (!aligned16(x_f16) || !aligned16(y_experts) || !aligned16(ws) || !aligned4(idx) ||
+      (status_dev && !aligned4(status_dev)))
+    return MOE_EALIGN;
+  const WsLayout L = ws_layout(s, T);
+  if (ws_bytes < L.total) return MOE_ENOMEM;
+  moe::GroupedArgs a{};
+  a.T = T;
+  a.d = s->d_model;
+  a.I = s->d_expert;
+  a.E = s->n_experts;
+  a.K = s->top_k;
+  a.S = s->n_shared;
+  a.r = s->lora_rank;
+  a.n_list = a.K + a.S;
+  a.n_ids = t->n_ids;
+  a.lora_scale = s->lora_scale;
+  a.x = static_cast<const __half*>(x_f16);
+  a.idx = idx;
+  a.slot_of = reinterpret_cast<const int32_t*>(t->dev) + (size_t)layer * t->n_ids;
+  a.bundles = reinterpret_cast<const moe_bundle*>(static_cast<const char*>(t->dev) + t->bundles_off) +
+              (size_t)layer * t->n_slots;
+  a.status = status_dev;
+  a.perm = at<int32_t>(ws, L.g_perm);
+  a.tiles = at<moe::GroupTile>(ws, L.g_tiles);
+  a.n_tiles = at<int32_t>(ws, L.g_ntiles);
+  a.max_tiles = L.g_max_tiles;
+  a.h = at<__half>(ws, L.g_h);
+  a.y_experts = y_experts;
+  return from_hip(moe::launch_grouped_ffn(a, static_cast<hipStream_t>(stream)));
 }
 
 static int combine_common(const moe_layer_spec* s, const float* y_experts, const float* w, int T,

@@ -26,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
+PEAK_MFMA_F16_TFS = 2500.0     # MI355X dense fp16 matrix peak, published
 METRIC = "int4 MoE layer achieved HBM GB/s (% peak) at batch 1; tokens/s, 40-layer stack"
 
 
@@ -210,6 +211,54 @@ def per_call_path(B, torch, spec, table, layers, tokens, n_steps, wl, hip):
     return ms / n_steps, gu
 
 
+def batched_path(B, torch, spec, table, wl, L, Ts=(64, 512), reps=20):
+    """Batched decode / prefill on the 35B-class layer (tokens grouped by
+    expert, MFMA contractions): Zipf(1.1) routing through softmax-top-k on
+    given logits, the grouped experts and the combine, rotating over the L
+    resident layers.  Algorithmic bytes: the distinct selected experts + the
+    shared expert (weights and LoRA, read once per batch), x, the logits and
+    y; FLOPs: 2 per weight per token-expert pair, LoRA included."""
+    import synth
+    n = wl.K + wl.S
+    bundle = 2 * proj_bytes(wl.I, wl.d) + proj_bytes(wl.d, wl.I) + \
+        2 * (2 * (wl.r * wl.d + wl.I * wl.r) + wl.r * wl.I + wl.d * wl.r)
+    flops_pair = 2 * (3 * wl.I * wl.d + 2 * (wl.r * wl.d + wl.I * wl.r) + wl.r * wl.I + wl.d * wl.r)
+    res = {}
+    for T in Ts:
+        logits = torch.from_numpy(synth.zipf_logits(wl, T, seed=T)).cuda()
+        xi = torch.from_numpy(synth.token_draws(wl, 300 + T, T)).cuda()
+        x = torch.empty(T, wl.d, dtype=torch.float16, device="cuda")
+        B.rmsnorm_f16(xi, x)
+        idx = torch.empty(T, wl.K, dtype=torch.int32, device="cuda")
+        w = torch.empty(T, wl.K, dtype=torch.float32, device="cuda")
+        ws = torch.zeros(B.workspace_bytes(spec, T), dtype=torch.uint8, device="cuda")
+        ye = torch.empty(T, n, wl.d, dtype=torch.float32, device="cuda")
+        y = torch.empty(T, wl.d, dtype=torch.float32, device="cuda")
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+        def one(i):
+            B.topk(spec, logits, idx, w)
+            B.expert_ffn_grouped(spec, table, i % L, x, idx, ye, status, ws)
+            B.combine(spec, ye, w, y)
+
+        for i in range(3):
+            one(i)
+        ms = time_launch(torch, lambda: [one(i) for i in range(reps)]) / reps
+        assert int(status.item()) == 0, "batched status %d" % int(status.item())
+        distinct = len(np.unique(idx.cpu().numpy()))
+        nbytes = (distinct + wl.S) * bundle + T * wl.d * 2 + T * wl.E * 4 + T * wl.d * 4
+        flops = T * n * flops_pair
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        tfs = flops / (ms * 1e-3) / 1e12
+        res["T%d" % T] = {"us_per_batch": round(ms * 1e3, 2), "tokens_per_s": round(T / (ms * 1e-3), 1),
+                          "distinct_experts": distinct, "bytes": nbytes, "GB_s": round(gbs, 1),
+                          "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "TFLOP_s": round(tfs, 2),
+                          "frac_mfma_fp16": round(tfs / PEAK_MFMA_F16_TFS, 4)}
+        log("batched T=%d: %.1f us per batch, %d distinct experts, %.1f GB/s (%.1f%% of HBM), "
+            "%.1f TFLOP/s" % (T, ms * 1e3, distinct, gbs, 100 * gbs / PEAK_HBM_GBS, tfs))
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -219,6 +268,7 @@ def main():
     ap.add_argument("--stack-tokens", type=int, default=256)
     ap.add_argument("--per-call-steps", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-batched", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only; a multi-GPU (expert-parallel) run is not "
@@ -278,6 +328,8 @@ def main():
     pc_us, gu_ms = per_call_path(B, torch, spec, table, layers, tokens, args.per_call_steps, wl, hip)
     log("per-call path: %.2f us/step; its gate/up kernel %.2f us" % (pc_us * 1e3, gu_ms * 1e3))
 
+    batched = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
+
     cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
     out = {
         "metric": METRIC,
@@ -308,6 +360,7 @@ def main():
             "ms_per_token": round(ms_chain / T, 5),
             "GB_s": round(chain_gbs, 1),
         },
+        "batched": batched,
         "per_call_path": {"us_per_step": round(pc_us * 1e3, 3),
                           "gateup_kernel_us": round(gu_ms * 1e3, 3)},
         "roofline": {

@@ -298,6 +298,78 @@ int moe_engine_chain(const moe_layer_spec* spec, const moe_slot_table* table,
                      int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- host-tier staging -----------------------------------------------------
+ * The staged executor keeps a fixed set of device slots per layer and rewrites
+ * only the slots whose expert changed (Sec. 3.1, Executor paths); head N's
+ * prediction for layer N+1 at token t+1 lets that rewrite start a token early
+ * (Sec. 3.2, Motivation).  Reading of the slot policy (the paper leaves it
+ * open): every layer keeps a FIFO of staged-but-unused expert sets and a FIFO
+ * of sets in use.  Staging a set walks it in routing order; a resident expert
+ * costs nothing; a missing one takes the lowest free slot, else the slot with
+ * the oldest last use among the slots that are not pinned, ties to the lowest
+ * slot id.  Pinned: the slots of the set being staged, of every set still
+ * queued for the layer and of every set in use.  A clock that advances on
+ * every copy and every use orders "last use".  Using a set (in FIFO order; it
+ * must equal the oldest staged set) moves it to the in-use FIFO; releasing the
+ * layer (its kernels on that set finished) unpins the oldest set in use.
+ */
+typedef struct moe_slot_policy moe_slot_policy;
+int moe_slot_policy_create(int n_layers, int n_ids, int n_slots, moe_slot_policy** out);
+int moe_slot_policy_destroy(moe_slot_policy* p);
+/* experts: host int32 [n], distinct ids in [0, n_ids). copies: host int32
+ * [n][2] or NULL, filled with (expert, slot) in issue order. Returns the
+ * number of copies, MOE_EINVAL (bad set), or MOE_ENOMEM (not enough unpinned
+ * slots; the policy is unchanged). */
+int moe_slot_policy_stage(moe_slot_policy* p, int layer, const int32_t* experts, int n,
+                          int32_t* copies);
+/* Consumes the oldest staged set of `layer`, which must equal experts[0..n).
+ * slots: host int32 [n] or NULL. MOE_EINVAL if the set is not the oldest. */
+int moe_slot_policy_use(moe_slot_policy* p, int layer, const int32_t* experts, int n,
+                        int32_t* slots);
+/* The layer finished with its oldest set in use. MOE_EINVAL if none. */
+int moe_slot_policy_release(moe_slot_policy* p, int layer);
+/* Slot of (layer, expert), or MOE_ENOTRESIDENT. */
+int moe_slot_policy_lookup(const moe_slot_policy* p, int layer, int expert);
+
+/* Byte offsets of the tensors of one packed bundle (16-byte aligned), in the
+ * order q, sz, lora_a, lora_b of gate, up and down; -1 for absent LoRA. */
+typedef struct moe_bundle_layout {
+  int64_t gate[4], up[4], down[4];
+} moe_bundle_layout;
+
+typedef struct moe_stager_stats {
+  int64_t stages, uses, copies, bytes;
+} moe_stager_stats;
+
+/*
+ * The policy above driving a slot table: the experts of every layer are packed
+ * bundles of bundle_bytes bytes in caller-owned PINNED host memory
+ * (host_bundles: [n_layers][n_ids] pointers), and the device slots are a
+ * caller-owned pool [n_layers][n_slots] of slot_stride bytes (256-aligned).
+ * The stager owns every binding of `table` (it starts empty; the table must
+ * have been synced once so that its device copy exists).
+ */
+typedef struct moe_stager moe_stager;
+int moe_stager_create(moe_slot_table* table, const moe_bundle_layout* layout, size_t bundle_bytes,
+                      const void* const* host_bundles, void* slot_pool, size_t slot_stride,
+                      moe_stager** out);
+int moe_stager_destroy(moe_stager* s);
+/* Stages a set (policy stage), rewrites the layer's slot-table rows on the
+ * device and copies each missing bundle host -> slot, all enqueued on
+ * copy_stream. Returns the number of copies (copies as in the policy) or an
+ * error. A kernel may read a slot only between the use and the release of a
+ * set that holds it, so unpinned slots are free to overwrite. */
+int moe_stager_stage(moe_stager* s, int layer, const int32_t* experts, int n, void* copy_stream,
+                     int32_t* copies);
+/* Uses the oldest staged set of the layer: compute_stream waits for that
+ * set's copies (no wait when it needed none). slots: host int32 [n] or NULL. */
+int moe_stager_use(moe_stager* s, int layer, const int32_t* experts, int n, void* compute_stream,
+                   int32_t* slots);
+/* The kernels that read the layer's oldest set in use have finished (the host
+ * knows it, e.g. from an event recorded after them): unpin that set. */
+int moe_stager_release(moe_stager* s, int layer);
+int moe_stager_stats_get(const moe_stager* s, moe_stager_stats* out);
+
 /* ---- profiling (not part of the hot path) ------------------------------- */
 #define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */
 #define MOE_PROF_ENGINE_PHASES 1 /* the next decode-engine launch writes, for

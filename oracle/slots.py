@@ -8,15 +8,17 @@ ahead, so the copy for token t+1 overlaps the compute of token t.
 
 Readings (the paper is silent on the policy):
 
-* A layer has ``n_slots`` slots and a queue of staged-but-unused sets.
-  A layer whose routing is not predicted (its own router) stages its set and
-  uses it at once (a synchronous fetch).  Staging a set walks it in routing
-  order; an expert already resident costs
+* A layer has ``n_slots`` slots, a queue of staged-but-unused sets and a
+  queue of sets in use.  A layer whose routing is not predicted (its own
+  router) stages its set and uses it at once (a synchronous fetch).  Staging
+  a set walks it in routing order; an expert already resident costs
   nothing, a missing one takes the lowest free slot, else the slot with the
   oldest last use among the slots that are not pinned, ties to the lowest
   slot id.  Pinned: the slots holding any set still queued for the layer
-  (staged earlier, not yet consumed) and the slots holding members of the
-  set being staged.
+  (staged earlier, not yet consumed), any set in use (consumed, and the
+  layer has not finished with it), and the members of the set being staged.
+* Using a set moves it from the staged queue to the in-use queue; releasing
+  the layer's oldest set in use (its layer finished) unpins it.
 * "Last use" is a counter that advances on every stage-copy and every use.
 * Copies are issued in routing order; each is ``(expert, slot)``.
 """
@@ -57,6 +59,7 @@ class SlotPolicy:
         self.table = SlotTable(n_layers, n_experts, n_slots)
         self.last_use = [[-1] * n_slots for _ in range(n_layers)]
         self.pending = [[] for _ in range(n_layers)]   # FIFO of staged sets
+        self.in_use = [[] for _ in range(n_layers)]    # FIFO of sets in use
         self.clock = 0
 
     def _tick(self):
@@ -68,9 +71,13 @@ class SlotPolicy:
         copy list ``[(expert, slot), ...]``."""
         t = self.table
         keep = set(int(e) for e in experts)
-        for pend in self.pending[layer]:
+        for pend in self.pending[layer] + self.in_use[layer]:
             keep |= set(pend)
         pinned = {t.lookup(layer, e) for e in keep if t.lookup(layer, e) >= 0}
+        misses = [e for e in experts if t.lookup(layer, int(e)) < 0]
+        usable = [s for s in range(t.n_slots) if s not in pinned]
+        if len(misses) > len(usable):      # refuse before changing anything
+            raise RuntimeError("no evictable slot: too few slots")
         copies = []
         for e in experts:
             e = int(e)
@@ -97,7 +104,7 @@ class SlotPolicy:
         t = self.table
         if not self.pending[layer] or self.pending[layer][0] != [int(e) for e in experts]:
             raise RuntimeError("layer %d uses a set that was not staged" % layer)
-        self.pending[layer].pop(0)
+        self.in_use[layer].append(self.pending[layer].pop(0))
         slots = []
         for e in experts:
             s = t.lookup(layer, int(e))
@@ -106,3 +113,9 @@ class SlotPolicy:
             self.last_use[layer][s] = self._tick()
             slots.append(s)
         return slots
+
+    def release(self, layer):
+        """The layer finished with its oldest set in use: unpin it."""
+        if not self.in_use[layer]:
+            raise RuntimeError("layer %d has no set in use" % layer)
+        self.in_use[layer].pop(0)

@@ -41,6 +41,16 @@ class MoeEngineLayer(ctypes.Structure):
                 ("mix_perm", c_void_p)]
 
 
+class MoeBundleLayout(ctypes.Structure):
+    _fields_ = [("gate", ctypes.c_int64 * 4), ("up", ctypes.c_int64 * 4),
+                ("down", ctypes.c_int64 * 4)]
+
+
+class MoeStagerStats(ctypes.Structure):
+    _fields_ = [("stages", ctypes.c_int64), ("uses", ctypes.c_int64), ("copies", ctypes.c_int64),
+                ("bytes", ctypes.c_int64)]
+
+
 class MoeError(RuntimeError):
     def __init__(self, code, what):
         self.code = code
@@ -76,6 +86,19 @@ SIGNATURES = {
     "moe_topk": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p, c_void_p,
                          c_void_p]),
     "moe_profile_arm": (c_int, [c_int, c_void_p, c_void_p]),
+    "moe_slot_policy_create": (c_int, [c_int, c_int, c_int, ctypes.POINTER(c_void_p)]),
+    "moe_slot_policy_destroy": (c_int, [c_void_p]),
+    "moe_slot_policy_stage": (c_int, [c_void_p, c_int, c_void_p, c_int, c_void_p]),
+    "moe_slot_policy_use": (c_int, [c_void_p, c_int, c_void_p, c_int, c_void_p]),
+    "moe_slot_policy_release": (c_int, [c_void_p, c_int]),
+    "moe_slot_policy_lookup": (c_int, [c_void_p, c_int, c_int]),
+    "moe_stager_create": (c_int, [c_void_p, ctypes.POINTER(MoeBundleLayout), c_size_t, c_void_p,
+                                  c_void_p, c_size_t, ctypes.POINTER(c_void_p)]),
+    "moe_stager_destroy": (c_int, [c_void_p]),
+    "moe_stager_stage": (c_int, [c_void_p, c_int, c_void_p, c_int, c_void_p, c_void_p]),
+    "moe_stager_use": (c_int, [c_void_p, c_int, c_void_p, c_int, c_void_p, c_void_p]),
+    "moe_stager_release": (c_int, [c_void_p, c_int]),
+    "moe_stager_stats_get": (c_int, [c_void_p, ctypes.POINTER(MoeStagerStats)]),
     "moe_combine_add": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
                                 c_void_p]),
     "moe_chain_token_start": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
@@ -179,6 +202,99 @@ class SlotTable:
     def close(self):
         if self.handle:
             _check(lib().moe_slot_table_destroy(self.handle), "moe_slot_table_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _i32(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+class SlotPolicy:
+    """The library's host-tier slot policy (host logic only)."""
+
+    def __init__(self, n_layers, n_ids, n_slots):
+        h = c_void_p()
+        _check(lib().moe_slot_policy_create(n_layers, n_ids, n_slots, ctypes.byref(h)),
+               "moe_slot_policy_create")
+        self.handle = h
+
+    def stage(self, layer, experts):
+        e = _i32(experts)
+        out = np.zeros((max(len(e), 1), 2), dtype=np.int32)
+        n = _check(lib().moe_slot_policy_stage(self.handle, layer, e.ctypes.data, len(e),
+                                               out.ctypes.data), "moe_slot_policy_stage")
+        return [tuple(int(v) for v in out[i]) for i in range(n)]
+
+    def use(self, layer, experts):
+        e = _i32(experts)
+        out = np.zeros(max(len(e), 1), dtype=np.int32)
+        _check(lib().moe_slot_policy_use(self.handle, layer, e.ctypes.data, len(e), out.ctypes.data),
+               "moe_slot_policy_use")
+        return out[:len(e)].tolist()
+
+    def release(self, layer):
+        _check(lib().moe_slot_policy_release(self.handle, layer), "moe_slot_policy_release")
+
+    def lookup(self, layer, expert):
+        rc = lib().moe_slot_policy_lookup(self.handle, layer, expert)
+        return -1 if rc == MOE_ENOTRESIDENT else _check(rc, "moe_slot_policy_lookup")
+
+    def close(self):
+        if self.handle:
+            lib().moe_slot_policy_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Stager:
+    """The slot policy driving a slot table: pinned host bundles -> device slots."""
+
+    def __init__(self, table, layout, bundle_bytes, host_ptrs, slot_pool, slot_stride):
+        h = c_void_p()
+        ptrs = (c_void_p * len(host_ptrs))(*host_ptrs)
+        _check(lib().moe_stager_create(table.handle, ctypes.byref(layout), bundle_bytes, ptrs,
+                                       _ptr(slot_pool), slot_stride, ctypes.byref(h)),
+               "moe_stager_create")
+        self.handle = h
+        self.table, self.pool = table, slot_pool
+
+    def stage(self, layer, experts, copy_stream):
+        e = _i32(experts)
+        out = np.zeros((max(len(e), 1), 2), dtype=np.int32)
+        n = _check(lib().moe_stager_stage(self.handle, layer, e.ctypes.data, len(e),
+                                          ctypes.c_void_p(copy_stream.cuda_stream),
+                                          out.ctypes.data), "moe_stager_stage")
+        return [tuple(int(v) for v in out[i]) for i in range(n)]
+
+    def use(self, layer, experts, compute_stream=None):
+        e = _i32(experts)
+        out = np.zeros(max(len(e), 1), dtype=np.int32)
+        _check(lib().moe_stager_use(self.handle, layer, e.ctypes.data, len(e),
+                                    _stream(compute_stream), out.ctypes.data), "moe_stager_use")
+        return out[:len(e)].tolist()
+
+    def release(self, layer):
+        _check(lib().moe_stager_release(self.handle, layer), "moe_stager_release")
+
+    def stats(self):
+        st = MoeStagerStats()
+        _check(lib().moe_stager_stats_get(self.handle, ctypes.byref(st)), "moe_stager_stats_get")
+        return {"stages": st.stages, "uses": st.uses, "copies": st.copies, "bytes": st.bytes}
+
+    def close(self):
+        if self.handle:
+            lib().moe_stager_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

@@ -31,6 +31,10 @@ def test_slot_policy_hand_trace():
     assert p.stage(0, [1, 2]) == [(1, 0), (2, 1)]
     assert p.stage(0, [2, 3]) == [(3, 2)]
     assert p.use(0, [1, 2]) == [0, 1]
+    # {1, 2} is in use: slots 0, 1 and 2 are pinned; the free slot 3 only fits one
+    with pytest.raises(RuntimeError):
+        p.stage(0, [4, 5])
+    p.release(0)
     # pinned: {2, 3} (queued) and {4, 5}; free slot 3 first, then the LRU
     # unpinned slot, slot 0 (expert 1)
     assert p.stage(0, [4, 5]) == [(4, 3), (5, 0)]
@@ -38,6 +42,10 @@ def test_slot_policy_hand_trace():
     assert p.use(0, [4, 5]) == [3, 0]
     with pytest.raises(RuntimeError):
         p.use(0, [4, 5])
+    p.release(0)
+    p.release(0)
+    with pytest.raises(RuntimeError):
+        p.release(0)
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -47,21 +55,28 @@ def test_slot_policy_invariants_random(seed):
     n_slots = 3 * k
     p = slots.SlotPolicy(n_layers, n_exp, n_slots)
     queued = [[] for _ in range(n_layers)]
+    using = [[] for _ in range(n_layers)]
     for step in range(300):
         layer = int(rs.integers(n_layers))
-        if queued[layer] and (len(queued[layer]) >= 2 or rs.random() < 0.5):
+        total = len(queued[layer]) + len(using[layer])   # at most 2 sets pinned + the new one
+        if using[layer] and (rs.random() < 0.3 or (total >= 2 and not queued[layer])):
+            using[layer].pop(0)
+            p.release(layer)
+            continue
+        if queued[layer] and (total >= 2 or rs.random() < 0.5):
             want = queued[layer].pop(0)
             got = p.use(layer, want)
             assert [p.table.expert_in[layer][s] for s in got] == want
+            using[layer].append(want)
             continue
         experts = [int(e) for e in rs.choice(n_exp, size=k, replace=False)]
         before = {s: p.table.expert_in[layer][s] for s in range(n_slots)}
-        pinned_experts = set(e for q in queued[layer] for e in q)
+        pinned_experts = set(e for q in queued[layer] + using[layer] for e in q)
         misses = [e for e in experts if p.table.lookup(layer, e) < 0]
         copies = p.stage(layer, experts)
         # copies = misses, in routing order
         assert [e for e, _ in copies] == misses
-        # nothing queued was evicted, and every member of every queued set is resident
+        # nothing queued or in use was evicted; every member of those sets is resident
         for e in pinned_experts | set(experts):
             assert p.table.lookup(layer, e) >= 0
         # only copied slots changed

@@ -1,0 +1,263 @@
+"""Decode chain with host-tier expert staging (the 8B tier on one GPU).
+
+The experts of every layer live in pinned host memory; each layer has a
+small pool of device slots (3 x top-K).  Per token t and layer N (§3.2,
+Motivation and Prediction-as-routing; §3.1, staged executor):
+
+* layer 0, and every layer of token 0, route with their own router: the host
+  reads the routing back and stages the set on demand (the kernels wait);
+* head N's prediction for layer N+1 at token t+1 is read back one layer
+  later and staged at once, so its copies overlap the rest of token t and
+  the first layers of token t+1;
+* the compute stream waits for exactly the copies of the set it uses, and a
+  set stays pinned until the host knows its kernels finished.
+
+Everything on the device is the library's: the per-call kernels for the
+layer, and the library's stager (policy, slot-table rows, hipMemcpyAsync).
+This module only orders the calls and moves the K routing ids to the host.
+"""
+
+import time
+
+import torch
+
+from . import binding as B
+from . import weights as W
+
+
+def bundle_layout(bundle):
+    """Pack one bundle alone: (packed bytes, MoeBundleLayout)."""
+    buf, boffs, _ = W.pack_host([bundle])
+    d = boffs[0]
+    lay = B.MoeBundleLayout()
+    for p in ("gate", "up", "down"):
+        arr = getattr(lay, p)
+        for i, kind in enumerate(("q", "sz", "a", "b")):
+            arr[i] = d.get((p, kind), -1)
+    return buf, lay
+
+
+class HostPool:
+    """Pinned host memory holding the packed bundles of every layer:
+    ``[n_layers][n_ids]`` bundles of ``stride`` bytes."""
+
+    def __init__(self, n_layers, n_ids, bundle_fn):
+        first, self.layout = bundle_layout(bundle_fn(0, 0))
+        self.bundle_bytes = first.nbytes
+        self.stride = (first.nbytes + 255) // 256 * 256
+        self.n_layers, self.n_ids = n_layers, n_ids
+        self.buf = torch.empty(n_layers * n_ids * self.stride, dtype=torch.uint8, pin_memory=True)
+        host = self.buf.numpy()
+        for n in range(n_layers):
+            for e in range(n_ids):
+                b = first if (n, e) == (0, 0) else bundle_layout(bundle_fn(n, e))[0]
+                o = (n * n_ids + e) * self.stride
+                host[o:o + b.nbytes] = b
+
+    def ptrs(self):
+        base = self.buf.data_ptr()
+        return [base + i * self.stride for i in range(self.n_layers * self.n_ids)]
+
+    def bytes_of(self, layer, expert):
+        o = (layer * self.n_ids + expert) * self.stride
+        return self.buf[o:o + self.bundle_bytes]
+
+
+class TieredChain:
+    """Decode chain of ``len(layers)`` layers whose experts are staged from
+    ``pool`` into ``n_slots`` device slots per layer.
+
+    ``layers``: dicts with device tensors ``router``, ``head`` (None on the
+    last layer), ``mix_d`` and ``mix_perm``, as for the resident chain.
+    """
+
+    def __init__(self, spec, layers, pool, n_slots):
+        self.spec, self.layers, self.host = spec, layers, pool
+        self.L = len(layers)
+        d, K = spec.d_model, spec.top_k
+        self.K = K
+        n_ids = spec.n_experts + spec.n_shared
+        dev = "cuda"
+        self.table = B.SlotTable(self.L, n_ids, n_slots)
+        self.table.sync()
+        self.slots = torch.empty(self.L * n_slots * pool.stride, dtype=torch.uint8, device=dev)
+        self.stager = B.Stager(self.table, pool.layout, pool.bundle_bytes, pool.ptrs(), self.slots,
+                               pool.stride)
+        self.copy_stream = torch.cuda.Stream()      # default priority
+        self.ws = torch.zeros(B.workspace_bytes(spec, 1), dtype=torch.uint8, device=dev)
+        self.r = torch.zeros(1, d, dtype=torch.float32, device=dev)
+        self.x = torch.empty(1, d, dtype=torch.float16, device=dev)
+        self.xi = torch.zeros(1, d, dtype=torch.float32, device=dev)
+        self.own_idx = torch.empty(1, K, dtype=torch.int32, device=dev)
+        self.own_w = torch.empty(1, K, dtype=torch.float32, device=dev)
+        self.pred_idx = torch.zeros(2, self.L, 1, K, dtype=torch.int32, device=dev)
+        self.pred_w = torch.zeros(2, self.L, 1, K, dtype=torch.float32, device=dev)
+        self.own_host = torch.empty(K, dtype=torch.int32, pin_memory=True)
+        self.pred_host = torch.empty(2, self.L, K, dtype=torch.int32, pin_memory=True)
+        self.ye = torch.empty(1, K + spec.n_shared, d, dtype=torch.float32, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.shared = list(range(spec.n_experts, n_ids))
+        self.staged = {}        # (t, n) -> staged host set
+        self.queued = None      # (t + 1, n + 1, event) prediction read back, not yet staged
+        self.used_layers = []   # layers of the sets used and not yet released, in use order
+        self.copy_ms = 0.0
+        self.copy_events = []
+        self.stall_s = 0.0
+        self.log = []           # (t, n, "demand" | "predicted", set, copies)
+        self.ops = []           # every policy call in order: ("stage", n, set, copies) | ("use", n, set) | ("release", n)
+
+    def _release(self, keep):
+        while len(self.used_layers) > keep:
+            n = self.used_layers.pop(0)
+            self.stager.release(n)
+            self.ops.append(("release", n))
+
+    def _stage(self, t, n, experts, kind):
+        s = [int(e) for e in experts] + self.shared
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        start.record(self.copy_stream)
+        copies = self.stager.stage(n, s, self.copy_stream)
+        stop.record(self.copy_stream)
+        if copies:
+            self.copy_events.append((start, stop))
+        self.log.append((t, n, kind, s, copies))
+        self.ops.append(("stage", n, s, copies))
+        return s
+
+    def _process_queued(self):
+        """Head n finished (the event also covers its layer's experts): every
+        set in use but the last one is done; stage the prediction."""
+        if self.queued is None:
+            return
+        tq, nq, ev = self.queued
+        self.queued = None
+        t0 = time.perf_counter()
+        ev.synchronize()
+        self.stall_s += time.perf_counter() - t0
+        self._release(keep=1)
+        self.staged[(tq, nq)] = self._stage(tq, nq, self.pred_host[tq % 2, nq].tolist(), "predicted")
+
+    def run_token(self, t, xi_row, record=None):
+        """One token through all layers; ``xi_row`` is a device fp32 [1, d]."""
+        s = self.spec
+        cur = torch.cuda.current_stream()
+        self.xi.copy_(xi_row)
+        B.chain_token_start(self.xi, self.r)
+        for n, lay in enumerate(self.layers):
+            B.chain_mix_rmsnorm(lay["mix_d"], lay["mix_perm"], self.r, self.x)
+            if t > 0 and n > 0:
+                idx, w = self.pred_idx[t % 2, n], self.pred_w[t % 2, n]
+                st = self.staged.pop((t, n))
+            else:
+                B.route(s, self.x, lay["router"], self.own_idx, self.own_w, self.ws)
+                self.own_host.copy_(self.own_idx[0], non_blocking=True)
+                ev = torch.cuda.Event()
+                ev.record(cur)
+                t0 = time.perf_counter()
+                ev.synchronize()                     # demand: the host needs the routing now
+                self.stall_s += time.perf_counter() - t0
+                self._release(keep=0)
+                st = self._stage(t, n, self.own_host.tolist(), "demand")
+                idx, w = self.own_idx, self.own_w
+            self.stager.use(n, st, cur)
+            self.ops.append(("use", n, st))
+            self.used_layers.append(n)
+            has_head = n + 1 < self.L and lay.get("head") is not None
+            if has_head:
+                nxt = (t + 1) % 2
+                B.preroute(s, self.x, lay["head"], self.pred_idx[nxt, n + 1],
+                           self.pred_w[nxt, n + 1], self.ws)
+            ye = self.ye if record is None else record["ye"][t, n]
+            B.expert_ffn(s, self.table, n, self.x, idx, ye, self.status, self.ws)
+            B.combine_add(s, ye, w, self.r)
+            if record is not None:
+                record["x"][t, n].copy_(self.x[0])
+                record["idx"][t, n].copy_(idx[0])
+                record["w"][t, n].copy_(w[0])
+                if has_head:
+                    record["pidx"][t, n].copy_(self.pred_idx[(t + 1) % 2, n + 1, 0])
+                    record["pw"][t, n].copy_(self.pred_w[(t + 1) % 2, n + 1, 0])
+            # the previous layer's prediction: its kernels are done or nearly so
+            self._process_queued()
+            if has_head:
+                self.pred_host[(t + 1) % 2, n + 1].copy_(self.pred_idx[(t + 1) % 2, n + 1, 0],
+                                                         non_blocking=True)
+                ev = torch.cuda.Event()
+                ev.record(cur)                       # after the layer's experts and combine
+                self.queued = (t + 1, n + 1, ev)
+        self._process_queued()
+
+    def finish(self):
+        """Wait for all work; release every set in use."""
+        torch.cuda.synchronize()
+        self._release(keep=0)
+        self.copy_ms += sum(a.elapsed_time(b) for a, b in self.copy_events)
+        self.copy_events = []
+
+    def new_record(self, T):
+        s = self.spec
+        n = s.top_k + s.n_shared
+        L, d, K = self.L, s.d_model, s.top_k
+        dev = "cuda"
+        return {
+            "x": torch.zeros(T, L, d, dtype=torch.float16, device=dev),
+            "idx": torch.zeros(T, L, K, dtype=torch.int32, device=dev),
+            "w": torch.zeros(T, L, K, dtype=torch.float32, device=dev),
+            "pidx": torch.full((T, L, K), -1, dtype=torch.int32, device=dev),
+            "pw": torch.zeros(T, L, K, dtype=torch.float32, device=dev),
+            "ye": torch.zeros(T, L, 1, n, d, dtype=torch.float32, device=dev),
+        }
+
+    def run(self, xi_tokens, record=False):
+        """Eager run over device fp32 draws ``[T, d]``; returns the record or None."""
+        T = xi_tokens.shape[0]
+        rec = self.new_record(T) if record else None
+        self.r.zero_()
+        for t in range(T):
+            self.run_token(t, xi_tokens[t:t + 1], record=rec)
+        self.finish()
+        return rec
+
+    def slot_bytes(self, layer, slot):
+        o = (layer * self.table.n_slots + slot) * self.host.stride
+        return self.slots[o:o + self.host.bundle_bytes]
+
+    def close(self):
+        self.stager.close()
+        self.table.close()
+
+
+def set_overlap(log, L):
+    """Mean fraction of a layer's set kept from the previous token."""
+    last, kept, n = {}, 0, 0
+    for t, layer, _, s, _ in log:
+        if layer in last:
+            kept += len(set(s) & set(last[layer]))
+            n += len(s)
+        last[layer] = s
+    return kept / n if n else 0.0
+
+
+def resident_table(spec, pool, layers):
+    """Every bundle of ``pool`` copied to the device and bound (no staging):
+    the all-resident reference for the same weights.  Returns (table, keep)."""
+    L, n_ids = pool.n_layers, pool.n_ids
+    dev = pool.buf.to("cuda")
+    table = B.SlotTable(L, n_ids, n_ids)
+    base = dev.data_ptr()
+    lay = pool.layout
+    for n in range(L):
+        for e in range(n_ids):
+            o = base + (n * n_ids + e) * pool.stride
+            projs = []
+            for p in ("gate", "up", "down"):
+                f = list(getattr(lay, p))
+                projs.append(B.MoeProj(o + f[0], o + f[1], None if f[2] < 0 else o + f[2],
+                                       None if f[3] < 0 else o + f[3]))
+            table.bind(n, e, e, B.MoeBundle(*projs), keep=dev)
+    table.sync()
+    return table, dev
+
+
+__all__ = ["HostPool", "TieredChain", "bundle_layout", "set_overlap", "resident_table"]

@@ -259,6 +259,84 @@ def batched_path(B, torch, spec, table, wl, L, Ts=(64, 512), reps=20):
     return res
 
 
+def tier_path(B, torch, T=64, L=24, rho=0.5):
+    """The 8B tier with host-tier staging: 24 layers whose 64 experts per
+    layer live in pinned host memory, 3 x top-4 device slots per layer; the
+    experts of layer N+1 at token t+1 are copied while token t runs (the
+    prerouter's prediction), layer 0 and token 0 load on demand.  Reported
+    beside the staged wall time: the same chain with every expert resident
+    (compute only, HIP-graph replay), the copy engine's busy time, and their
+    overlap = (t_copy + t_compute - t_wall) / min(t_copy, t_compute)."""
+    import synth
+    from paper_2609_18063_amd import chain as C, tier
+    wl = synth.WORKLOADS["tier8b"]
+    spec = B.spec_from_workload(wl)
+    nb = layer_bytes(wl)
+    t0 = time.time()
+    pool = tier.HostPool(L, wl.E + wl.S, lambda n, e: synth.bundle(wl, n, e), replicate=True)
+    log("8B tier: %d layers x %d bundles of %.2f MB in pinned host memory (%.1f GB) in %.1fs"
+        % (L, pool.n_ids, pool.bundle_bytes / 1e6, pool.buf.numel() / 1e9, time.time() - t0))
+    layers = []
+    for n in range(L):
+        mix_d, mix_perm = synth.mixing(wl, n)
+        layers.append({
+            "router": torch.from_numpy(synth.router_weights(wl, n, 0)).cuda(),
+            "head": None if n + 1 == L else torch.from_numpy(synth.router_weights(wl, n, 1)).cuda(),
+            "mix_d": torch.from_numpy(mix_d).cuda(),
+            "mix_perm": torch.from_numpy(mix_perm).cuda(),
+        })
+    xi = torch.from_numpy(synth.ar1_token_draws(wl, T, rho)).cuda()
+    n_slots = 3 * wl.K
+    ch = tier.TieredChain(spec, layers, pool, n_slots)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ch.run(xi)
+    wall = time.perf_counter() - w0
+    assert int(ch.status.item()) == 0, "tier status %d" % int(ch.status.item())
+    st = ch.stager.stats()
+    copy_s = ch.copy_ms * 1e-3
+    ch.close()
+    # the same chain, every expert resident: compute only
+    table, keep = tier.resident_table(spec, pool, layers)
+    dc = C.DeviceChain(spec, table, layers)
+    dc.capture()
+    dc.reset()
+
+    def replay_all():
+        for t in range(T):
+            dc.xi.copy_(xi[t:t + 1])
+            dc.replay_token(t)
+
+    compute_s = time_launch(torch, replay_all) * 1e-3
+    table.close()
+    del keep
+    tok_bytes = L * (nb["ffn"] + nb["route"] // 2)
+    overlap = (copy_s + compute_s - wall) / min(copy_s, compute_s) if copy_s > 0 else None
+    res = {
+        "workload": "8B tier: d 4096, 64 experts top-4, I 1024, int4 g64, LoRA r16, %d layers, "
+                    "%d tokens (AR(1) draws, rho %.2f), %d HBM slots per layer, experts in "
+                    "pinned host memory" % (L, T, rho, n_slots),
+        "tokens_per_s": round(T / wall, 2),
+        "ms_per_token": round(wall * 1e3 / T, 3),
+        "compute_only_ms_per_token": round(compute_s * 1e3 / T, 4),
+        "kernel_GB_s": round(tok_bytes * T / compute_s / 1e9, 1),
+        "h2d_GB_s": round(st["bytes"] / copy_s / 1e9, 2) if copy_s > 0 else None,
+        "copy_ms_per_token": round(copy_s * 1e3 / T, 3),
+        "misses_per_token": round(st["copies"] / T, 2),
+        "MiB_per_token": round(st["bytes"] / T / 2 ** 20, 1),
+        "MiB_per_load": round(pool.bundle_bytes / 2 ** 20, 3),
+        "stall_ms_per_token": round((wall - compute_s) * 1e3 / T, 3),
+        "host_wait_ms_per_token": round(ch.stall_s * 1e3 / T, 3),
+        "overlap": None if overlap is None else round(overlap, 3),
+        "adjacent_set_overlap": round(tier.set_overlap(ch.log, L), 3),
+    }
+    log("8B tier staged: %.1f tok/s, %.2f misses/token, H2D %.1f GB/s, compute-only %.3f ms/token, "
+        "overlap %s" % (res["tokens_per_s"], res["misses_per_token"], res["h2d_GB_s"] or 0,
+                        res["compute_only_ms_per_token"], res["overlap"]))
+    del pool
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -269,6 +347,8 @@ def main():
     ap.add_argument("--per-call-steps", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
+    ap.add_argument("--no-tier", action="store_true")
+    ap.add_argument("--tier-tokens", type=int, default=64)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only; a multi-GPU (expert-parallel) run is not "
@@ -330,6 +410,8 @@ def main():
 
     batched = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
 
+    tier_res = None if args.no_tier else tier_path(B, torch, T=args.tier_tokens)
+
     cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
     out = {
         "metric": METRIC,
@@ -361,6 +443,7 @@ def main():
             "GB_s": round(chain_gbs, 1),
         },
         "batched": batched,
+        "host_tier": tier_res,
         "per_call_path": {"us_per_step": round(pc_us * 1e3, 3),
                           "gateup_kernel_us": round(gu_ms * 1e3, 3)},
         "roofline": {

@@ -306,7 +306,8 @@ int moe_stager_create(moe_slot_table* table, const moe_bundle_layout* layout, si
 int moe_stager_destroy(moe_stager* s) {
   if (!s) return MOE_OK;
   for (auto& q : s->set_ev)
-    for (hipEvent_t e : q) (void)hipEventDestroy(e);
+    for (hipEvent_t e : q)
+      if (e) (void)hipEventDestroy(e);  // null: a set that needed no copy
   for (hipEvent_t e : s->free_ev) (void)hipEventDestroy(e);
   for (hipEvent_t e : s->ring_ev)
     if (e) {

@@ -41,14 +41,21 @@ class HostPool:
     """Pinned host memory holding the packed bundles of every layer:
     ``[n_layers][n_ids]`` bundles of ``stride`` bytes."""
 
-    def __init__(self, n_layers, n_ids, bundle_fn):
+    def __init__(self, n_layers, n_ids, bundle_fn, replicate=False):
+        """``bundle_fn(layer, expert)`` gives a bundle; with ``replicate`` only
+        layer 0's bundles are built and every layer holds a copy of them (at
+        its own addresses)."""
         first, self.layout = bundle_layout(bundle_fn(0, 0))
         self.bundle_bytes = first.nbytes
         self.stride = (first.nbytes + 255) // 256 * 256
         self.n_layers, self.n_ids = n_layers, n_ids
         self.buf = torch.empty(n_layers * n_ids * self.stride, dtype=torch.uint8, pin_memory=True)
         host = self.buf.numpy()
+        per_layer = n_ids * self.stride
         for n in range(n_layers):
+            if replicate and n > 0:
+                host[n * per_layer:(n + 1) * per_layer] = host[:per_layer]
+                continue
             for e in range(n_ids):
                 b = first if (n, e) == (0, 0) else bundle_layout(bundle_fn(n, e))[0]
                 o = (n * n_ids + e) * self.stride

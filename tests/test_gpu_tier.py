@@ -145,3 +145,14 @@ def test_tier_matches_oracle_chain(tiered):
     stats = compare_chain(tiered["rec"], ref, tiered["np_layers"], wl, L_TEST)
     print("tier8b staged chain:", stats)
     assert stats["layers"] >= L_TEST * 2, stats
+
+
+def test_tier_close_leaves_no_hip_error(tiered, torch_cuda):
+    """Destroying the stager (with sets that needed no copy still queued or
+    retired) leaves no error behind for the next HIP call."""
+    torch = torch_cuda
+    ch = tiered["chain"]
+    ch.close()
+    x = torch.ones(1024, device="cuda")
+    assert float((x * 2).sum().item()) == 2048.0
+    torch.cuda.synchronize()

@@ -349,6 +349,10 @@ def main():
     ap.add_argument("--no-batched", action="store_true")
     ap.add_argument("--no-tier", action="store_true")
     ap.add_argument("--tier-tokens", type=int, default=64)
+    ap.add_argument("--only-engine", action="store_true",
+                    help="time the engine launch only (for counter runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain device copy of 1 GiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only; a multi-GPU (expert-parallel) run is not "
@@ -385,6 +389,17 @@ def main():
     gbs = nb["step"] * K / (ms_total * 1e-3) / 1e9
     log("engine, %d single-token steps in one launch: %.3f ms, %.2f us/step, %.1f GB/s"
         % (K, ms_total, ms_step * 1e3, gbs))
+
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)                      # reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
+    if args.only_engine:
+        print(json.dumps({"engine_us_per_step": round(ms_step * 1e3, 3), "GB_s": round(gbs, 2)}),
+              flush=True)
+        return
 
     # ---- 40-layer stack, autoregressive decode (prediction-as-routing) ----
     T = args.stack_tokens

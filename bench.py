@@ -15,6 +15,7 @@ JSON line.
 
 import argparse
 import ctypes
+import hashlib
 import json
 import os
 import sys
@@ -28,6 +29,32 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
 PEAK_MFMA_F16_TFS = 2500.0     # MI355X dense fp16 matrix peak, published
 METRIC = "int4 MoE layer achieved HBM GB/s (% peak) at batch 1; tokens/s, 40-layer stack"
+
+
+ENGINE_SOURCES = ("paper_2609_18063_amd/csrc/moe_engine.hip", "paper_2609_18063_amd/csrc/moe_engine.h",
+                  "paper_2609_18063_amd/csrc/moe_device.h")
+TRAFFIC_PROFILE = "profiles/moe35b_engine_hbm_traffic.md"
+
+
+def measured_traffic(steps):
+    """HBM bytes of one engine launch of ``steps`` steps, from the committed
+    calibrated counter summary; None if the engine sources changed since the
+    counters were taken (or the summary is missing)."""
+    try:
+        text = open(os.path.join(ROOT, TRAFFIC_PROFILE)).read()
+        h = hashlib.sha256()
+        for f in ENGINE_SOURCES:
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        if ": " in line and line.split(": ", 1)[0] in ("traffic_bytes_per_step", "source_sha256"):
+            k, v = line.split(": ", 1)
+            vals[k] = v.strip()
+    if vals.get("source_sha256") != h.hexdigest() or "traffic_bytes_per_step" not in vals:
+        return None
+    return int(vals["traffic_bytes_per_step"]) * steps
 
 
 def log(*a):
@@ -468,7 +495,8 @@ def main():
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(gbs / PEAK_HBM_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(K),
+            "traffic_source": TRAFFIC_PROFILE,
             "bytes_per_launch": nb["step"] * K,
             "mean_launch_us": round(ms_total * 1e3, 3),
         },

@@ -77,23 +77,6 @@ __device__ __forceinline__ float group_sum(float v, int width) {
 
 // (value, index) arg-max over the wave: larger value wins, equal values go
 // to the lower index; the winner is returned to every lane.
-__device__ __forceinline__ void argmax_step(float& v, int& i, float ov, int oi) {
-  if (ov > v || (ov == v && oi < i)) {
-    v = ov;
-    i = oi;
-  }
-}
-__device__ __forceinline__ void wave_argmax(float& v, int& i) {
-  argmax_step(v, i, dpp_f<0xB1>(v, v), dpp_i<0xB1>(i, i));
-  argmax_step(v, i, dpp_f<0x4E>(v, v), dpp_i<0x4E>(i, i));
-  argmax_step(v, i, dpp_f<0x141>(v, v), dpp_i<0x141>(i, i));
-  argmax_step(v, i, dpp_f<0x140>(v, v), dpp_i<0x140>(i, i));
-  argmax_step(v, i, dpp_f<0x142, 0xa>(v, v), dpp_i<0x142, 0xa>(i, i));
-  argmax_step(v, i, dpp_f<0x143, 0xc>(v, v), dpp_i<0x143, 0xc>(i, i));
-  v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-  i = __builtin_amdgcn_readlane(i, 63);
-}
-
 // Dot product of 32 int4 codes (16 bytes, even input in the low nibble) with
 // 32 fp32 activations.  Codes are exact small integers in fp32.
 __device__ __forceinline__ float dot32_q4(const U4& q, const float* x) {
@@ -157,44 +140,100 @@ __device__ __forceinline__ const moe_bundle* resolve_expert(int k, int K, int E,
 // Softmax-top-k of one token's logits by one wave.  Selection is on the fp32
 // logits (the softmax is increasing), descending, ties to the lower index;
 // weights are the softmax renormalized over the selected set.
+//
+// Each logit becomes a 32-bit order key (NaN as -inf, -0 as +0).  The K-th
+// largest key T is found bit by bit from the top: a candidate stays if at
+// least K keys reach it (one ballot and a scalar popcount per key register).
+// The selected set is every key above T plus the lowest-index keys equal to
+// T; its K members are compacted to LDS and ranked against each other.
 constexpr int kTopkVals = 16;  // E <= 64 * 16
 
-// Branch-free: every lane keeps its values with a taken mask; each of the K
-// rounds takes the lane-local best with selects and one DPP arg-max.
+__device__ __forceinline__ uint32_t topk_key(float v) {
+  if (v != v) v = -INFINITY;
+  if (v == 0.f) v = 0.f;
+  const uint32_t b = __float_as_uint(v);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float topk_key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+// scratch: LDS, at least 2 * 32 words, private to the calling wave.
 template <bool kAgent, int NV = kTopkVals>
-__device__ void wave_topk(const float* l, int E, int K, int32_t* idx_out, float* w_out) {
+__device__ void wave_topk(const float* l, int E, int K, int32_t* idx_out, float* w_out,
+                          uint32_t* scratch) {
   const int lane = threadIdx.x & 63;
-  const int nv = (E + 63) >> 6;  // values per lane actually used (<= NV)
-  float v[NV];
+  uint32_t key[NV];
+  bool valid[NV];
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int e = lane + 64 * j;
-    float a = -INFINITY;
-    if (j < nv && e < E) a = kAgent ? ld_agent(l + e) : l[e];
-    v[j] = (a != a) ? -INFINITY : a;
+    valid[j] = e < E;
+    key[j] = valid[j] ? topk_key(kAgent ? ld_agent(l + e) : l[e]) : 0u;
   }
-  uint32_t taken = 0;
-  float mine = -INFINITY;
-  for (int k = 0; k < K; ++k) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
+  // T: the largest value with at least K keys >= T (invalid positions count as
+  // key 0, which no real key equals: -inf is 0x007FFFFF)
+  uint32_t T = 0;
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t cand = T | (1u << b);
+    int cnt = 0;
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int e = lane + 64 * j;
-      const bool cand = (j < nv) & (e < E) & !((taken >> j) & 1u);
-      const bool better = cand & ((v[j] > bv) | ((v[j] == bv) & (e < bi)));
-      bv = better ? v[j] : bv;
-      bi = better ? e : bi;
-    }
-    wave_argmax(bv, bi);
-    taken |= ((bi & 63) == lane) ? (1u << ((bi >> 6) & 31)) : 0u;
-    mine = (lane == k) ? bv : mine;
-    if (lane == 0) idx_out[k] = bi;
+    for (int j = 0; j < NV; ++j) cnt += __popcll(__ballot(valid[j] && key[j] >= cand));
+    if (cnt >= K) T = cand;
   }
-  const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine), 0));
-  const float ex = (lane < K) ? expf(mine - m) : 0.f;
+  // keys above T are in; keys equal to T fill the rest, lowest index first
+  int n_gt = 0;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) n_gt += __popcll(__ballot(valid[j] && key[j] > T));
+  const int need = K - n_gt;
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  int eq_before = 0, sel_before = 0;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const bool eq = valid[j] && key[j] == T;
+    const uint64_t meq = __ballot(eq);
+    const int eq_rank = eq_before + __popcll(meq & below);
+    const bool sel = (valid[j] && key[j] > T) || (eq && eq_rank < need);
+    const uint64_t msel = __ballot(sel);
+    if (sel) {
+      const int ci = sel_before + __popcll(msel & below);
+      scratch[2 * ci] = key[j];
+      scratch[2 * ci + 1] = (uint32_t)(lane + 64 * j);
+    }
+    eq_before += __popcll(meq);
+    sel_before += __popcll(msel);
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  // rank of member `lane` among the K: larger key first, then lower index
+  uint32_t mk = 0, mi = 0;
+  int rank = 0;
+  if (lane < K) {
+    mk = scratch[2 * lane];
+    mi = scratch[2 * lane + 1];
+    for (int q = 0; q < K; ++q) {
+      const uint32_t ok = scratch[2 * q], oi = scratch[2 * q + 1];
+      rank += (ok > mk) || (ok == mk && oi < mi);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  if (lane < K) {
+    scratch[2 * rank] = mk;
+    scratch[2 * rank + 1] = mi;
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  // lane r holds the r-th selected logit; weights as a softmax over the set
+  const float v = lane < K ? topk_key_value(scratch[2 * lane]) : 0.f;
+  const int id = lane < K ? (int)scratch[2 * lane + 1] : 0;
+  const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float ex = (lane < K) ? expf(v - m) : 0.f;
   const float s = wave_sum(ex);
-  if (lane < K) w_out[lane] = ex / s;
+  if (lane < K) {
+    idx_out[lane] = id;
+    w_out[lane] = ex / s;
+  }
 }
 
 }  // namespace moe

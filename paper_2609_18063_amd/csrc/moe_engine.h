@@ -32,7 +32,7 @@ struct EngineArgs {
   uint64_t* xw;                  // workspace exchange words
   // exchange-area offsets and per-parity strides (in 64-bit words)
   size_t xo_logr, xs_logr, xo_loghm, xo_av, xs_av, xo_hv, xs_hv, xo_adp, xs_adp, xo_part, xs_part,
-      xo_rv, xs_rv, xo_logh, xs_logh_layer;
+      xo_rv, xs_rv, xo_logh, xs_logh_layer, xo_pred, xs_pred;
 };
 
 bool engine_shape_supported(int d, int I, int r, int K, int S, int E);

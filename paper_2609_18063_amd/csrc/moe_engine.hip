@@ -17,8 +17,18 @@
 // of a device-side counter that persists across launches, so a reader never
 // takes a stale value for a fresh one. Every wait is bounded. A timeout sets
 // MOE_STATUS_ENGINE_ABORT and a sticky abort word, and every workgroup
-// leaves the kernel. Weights are staged into LDS with direct global->LDS
-// loads (global_load_lds_dwordx4).
+// leaves the kernel.
+//
+// Weights are staged into LDS with direct global->LDS loads
+// (global_load_lds_dwordx4) issued by waves 4-7 only; waves 0-3 make every
+// other global access. The vector-memory counter of a wave is in order, so
+// this split lets a prefetch stay in flight while waves 0-3 poll. Each LDS
+// region is refilled for step s+1 as soon as step s has read it: router and
+// head rows always (a layer's weights are known ahead), the expert weights
+// when step s+1 is routed by a prediction made at the previous token
+// (Sec. 3.2, Prediction-as-routing: the next layer's experts are known
+// before the current layer finishes), in which case its routing is computed
+// during step s as well.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -30,6 +40,11 @@ namespace eng {
 
 constexpr int NX = 8, NM = 32, NWG = NX * NM, NT = 512, NWV = NT / 64;
 constexpr long kSpinMax = 1L << 20;   // polls of about a microsecond each
+// Waves 0 .. kStageW0-1 make every global access of a step except the weight
+// staging (polls, exchange stores, inputs, records); waves kStageW0 .. issue
+// the staging loads and nothing that would make them wait for those loads.
+constexpr int kStageW0 = 4;
+constexpr int NPT = kStageW0 * 64;    // polling threads
 
 // ---------------------------------------------------------------------------
 // tagged exchange words
@@ -51,10 +66,26 @@ __device__ __forceinline__ unsigned xcc_id() {
   return v;
 }
 
-// One 16-byte direct global->LDS load per lane; lane l writes lds_wave + 16*l.
-__device__ __forceinline__ void lds_copy16(const void* g, void* lds_wave) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_wave, 16, 0, 0);
+// One 16-byte direct global->LDS load per lane (lane l writes lds_wave +
+// 16 l), from inline assembly: the compiler does not track it, so a prefetch
+// stays in flight across later barriers and polls.  The issuing wave waits
+// for it with dma_wait() before the barrier that hands the data over.
+// M0 (the LDS destination) is saved and restored around the load, since the
+// compiler reserves it; one wait state separates the M0 write from its use.
+__device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_wave;
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off nt\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(g)
+      : "memory");
 }
+__device__ __forceinline__ void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 struct Ctl {
   uint32_t* ctl;      // [0] tag base, [1] finish counter, [2] abort
@@ -62,25 +93,28 @@ struct Ctl {
 };
 
 // Poll `count` tagged words (addr(i) for i < count) until all carry `tag`;
-// store(i, value) each. Every thread takes items threadIdx.x + q*NT. Returns
-// false (after the barrier) if any thread timed out or saw the abort word.
+// store(i, value) each. The polling threads (threadIdx.x < NPT) take items
+// threadIdx.x + q*NPT; every thread meets the two barriers. Returns false
+// (after the barrier) if any thread timed out or saw the abort word.
 template <int MAXI, typename AddrF, typename StoreF>
 __device__ bool poll_all(int count, uint32_t tag, AddrF addr, StoreF store, const Ctl& c,
                          int* sh_abort) {
   uint32_t pending = 0;
+  if ((int)threadIdx.x < NPT) {
 #pragma unroll
-  for (int q = 0; q < MAXI; ++q)
-    if ((int)threadIdx.x + q * NT < count) pending |= 1u << q;
+    for (int q = 0; q < MAXI; ++q)
+      if ((int)threadIdx.x + q * NPT < count) pending |= 1u << q;
+  }
   long spin = 0;
   while (pending) {
     uint64_t v[MAXI];
 #pragma unroll
     for (int q = 0; q < MAXI; ++q)
-      if ((pending >> q) & 1u) v[q] = ld_tag(addr(threadIdx.x + q * NT));
+      if ((pending >> q) & 1u) v[q] = ld_tag(addr(threadIdx.x + q * NPT));
 #pragma unroll
     for (int q = 0; q < MAXI; ++q)
       if (((pending >> q) & 1u) && (uint32_t)(v[q] >> 32) == tag) {
-        store(threadIdx.x + q * NT, __uint_as_float((uint32_t)v[q]));
+        store(threadIdx.x + q * NPT, __uint_as_float((uint32_t)v[q]));
         pending &= ~(1u << q);
       }
     if (!pending) break;
@@ -120,7 +154,8 @@ struct Shape {
   static constexpr int NAX = (NSEGX * 2 * R + NM - 1) / NM; // max LoRA-A rows per workgroup
   static constexpr int DR = D / NM;   // down rows per workgroup
   static constexpr int RR = D / NWG;  // reducer rows per workgroup
-  static constexpr int MAXI_D = (D + NT - 1) / NT;
+  static constexpr int MAXI_P = (D + NPT - 1) / NPT;  // per polling thread: D items
+  static constexpr int MAXI_E = 1;                      // E <= NPT logits
   // LDS layout (bytes); staged regions are rounded up to 1 KiB (one wave copy)
   static constexpr int kb(int b) { return (b + 1023) / 1024 * 1024; }
   static constexpr int O_GUQ = 0;                                   // [2*RMX][D/2]
@@ -133,13 +168,13 @@ struct Shape {
   static constexpr int O_DS = O_DQ + kb(DR * GXX / 2);              // [DR][NSEGX][IE/16]
   static constexpr int O_BD = O_DS + kb(DR * NSEGX * IE / 16);      // [DR][NSEGX][R] fp16
   static constexpr int O_ADM = O_BD + kb(DR * NSEGX * R * 2);       // [R][NSEGX][32] fp16
-  static constexpr int O_XF = O_ADM + kb(R * NSEGX * 32 * 2);       // [D] f32
-  static constexpr int O_XH = O_XF + D * 4;                         // [D] f16
+  static constexpr int O_XF = O_ADM + kb(R * NSEGX * 32 * 2);       // [D] f32, pad32 layout
+  static constexpr int O_XH = O_XF + (D + D / 32) * 4;              // [D] f16
   static constexpr int O_R0 = O_XH + D * 2;                         // [D] f32
   static constexpr int O_R1 = O_R0 + D * 4;                         // [D] f32
   static constexpr int O_LG = O_R1 + D * 4;                         // [1024] f32 logits
-  static constexpr int O_HX = O_LG + 1024 * 4;                      // [GXX] f32 h of the XCD
-  static constexpr int O_HL = O_HX + GXX * 4;                       // [RMX] f32 own h
+  static constexpr int O_HX = O_LG + 1024 * 4;                      // [GXX] f32 h of the XCD, pad32
+  static constexpr int O_HL = O_HX + (GXX + GXX / 32) * 4;          // [RMX] f32 own h
   static constexpr int O_GXU = O_HL + RMX * 4;                      // [2*RMX] f32
   static constexpr int O_DP = O_GXU + 2 * RMX * 4;                  // [DR][32] f32 down partials
   static constexpr int O_AV = O_DP + DR * 32 * 4;                   // [NSEGX][2R] f32
@@ -147,7 +182,7 @@ struct Shape {
   static constexpr int O_YL = O_ADV + NSEGX * R * 4;                // [RR][NX] f32
   static constexpr int O_RED = (O_YL + RR * NX * 4 + 63) / 64 * 64; // [NT] f64 reduction
   static constexpr int O_MISC = O_RED + NT * 8;                     // small ints / floats
-  static constexpr int LDS_BYTES = O_MISC + 1024;
+  static constexpr int LDS_BYTES = O_MISC + 2048;
 };
 
 struct Seg {
@@ -157,20 +192,82 @@ struct Seg {
   int col0;    // first column of the segment in the XCD's concatenation
 };
 
-struct Misc {
-  int nseg;
-  int abort;
+// The routing of one step and the bundles of the XCD's segments under it.
+struct Route {
+  int step;              // the step this routing belongs to (-1: none)
   int idx[32];
   float w[32];
-  int pidx[32];
-  float pw[32];
-  Seg seg[4];
-  float segw[4];
   int segok[4];
+  float segw[4];
   moe_bundle segbd[4];   // the segments' bundles, copied from the slot table
 };
 
+struct Misc {
+  int nseg;
+  int abort;
+  int gu_step, dn_step, rt_step, hd_step;  // the step whose weights each LDS region holds
+  int pidx[32];
+  float pw[32];
+  Seg seg[4];
+  Route rt[2];           // by step parity: this step and the next one
+};
+
 __device__ __forceinline__ float silu(float z) { return z / (1.f + expf(-z)); }
+
+// Softmax-top-k of E <= 256 fp32 logits in LDS, by the workgroup (every
+// thread calls it; three barriers).  Logit i gets a 64-bit key (order key of
+// the value, then ~index: ties go to the lower index); its rank is the count
+// of larger keys, from two half-counts by threads i and i + 256 (eight
+// independent compares per step; the key array is padded with zeros, which
+// no real key is below).  The K smallest ranks land in `sorted`, and wave 0
+// forms the weights exactly as the one-wave top-k does.
+// keys: LDS [256] u64; part: LDS [256] int; sorted: LDS [32] u64.
+__device__ void block_topk(const float* l, int E, int K, int32_t* idx_out, float* w_out,
+                           uint64_t* keys, int* part, uint64_t* sorted) {
+  const int tid = threadIdx.x;
+  const int i = tid & 255, half = tid >> 8;
+  const int E16 = (E + 15) & ~15;
+  if (tid < E16)
+    keys[tid] = tid < E ? ((uint64_t)topk_key(l[tid]) << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)tid)
+                        : 0ull;
+  __syncthreads();
+  int rank = 0;
+  uint64_t mine = 0;
+  if (i < E) {
+    mine = keys[i];
+    const int j0 = half * (E16 >> 1), j1 = j0 + (E16 >> 1);
+    for (int j = j0; j < j1; j += 8) {
+      const uint64_t k0 = keys[j], k1 = keys[j + 1], k2 = keys[j + 2], k3 = keys[j + 3];
+      const uint64_t k4 = keys[j + 4], k5 = keys[j + 5], k6 = keys[j + 6], k7 = keys[j + 7];
+      rank += (k0 > mine) + (k1 > mine) + (k2 > mine) + (k3 > mine) + (k4 > mine) + (k5 > mine) +
+              (k6 > mine) + (k7 > mine);
+    }
+    if (half) part[i] = rank;
+  }
+  __syncthreads();
+  if (half == 0 && i < E) {
+    rank += part[i];
+    if (rank < K) sorted[rank] = mine;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    const int lane = tid;
+    const uint64_t k = lane < K ? sorted[lane] : 0;
+    const float v = lane < K ? topk_key_value((uint32_t)(k >> 32)) : 0.f;
+    const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float ex = (lane < K) ? expf(v - m) : 0.f;
+    const float sum = wave_sum(ex);
+    if (lane < K) {
+      idx_out[lane] = (int)(0xFFFFFFFFu - (uint32_t)k);
+      w_out[lane] = ex / sum;
+    }
+  }
+}
+
+// LDS index of element i of a vector that lanes read in 32-element chunks
+// (lane l reading chunk l): one pad word per chunk puts the 64 lanes' reads of
+// the same element in 64 different banks.
+__device__ __forceinline__ int pad32(int i) { return i + (i >> 5); }
 
 // fp64 sum over the wave (DPP on the two 32-bit halves of each step's operand)
 template <int CTRL, int ROWMASK = 0xf>
@@ -217,7 +314,7 @@ __device__ void block_rmsnorm_to_x(const float* v, float* xf, __half* xh, double
   for (int j = threadIdx.x; j < SH::D; j += NT) {
     const __half h = __half(static_cast<_Float16>((double)v[j] * inv));
     xh[j] = h;
-    xf[j] = __half2float(h);
+    xf[pad32(j)] = __half2float(h);
   }
 }
 
@@ -236,14 +333,21 @@ __device__ __forceinline__ float wave_dot_h(const __half* row, const __half* xh)
 }
 
 // Stage `nchunks` 16-byte chunks into LDS region `dst` (1 KiB-padded);
-// src(i) gives chunk i's global address (i < nchunks). Waves take 64-chunk
-// blocks round-robin; lanes past the end re-read chunk 0 into the padding.
+// src(i) gives chunk i's global address (i < nchunks). Waves w0 .. w0+nw-1
+// issue the loads, in 64-chunk blocks round-robin; lanes past the end re-read
+// chunk 0 into the padding. The loads stay in flight until those waves call
+// dma_wait().
+struct Waves {
+  int w0, nw;
+};
+constexpr Waves kAll{0, NWV}, kPollW{0, kStageW0}, kStageW{kStageW0, NWV - kStageW0};
 template <typename SrcF>
-__device__ __forceinline__ void stage(char* dst, int nchunks, SrcF src) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int b = wave; b * 64 < nchunks; b += NWV) {
+__device__ __forceinline__ void stage(char* dst, int nchunks, Waves ws, SrcF src) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (wave < ws.w0 || wave >= ws.w0 + ws.nw) return;
+  for (int b = wave - ws.w0; b * 64 < nchunks; b += ws.nw) {
     const int i = b * 64 + lane;
-    lds_copy16(src(i < nchunks ? i : 0), dst + b * 1024);
+    dma16(src(i < nchunks ? i : 0), dst + b * 1024);
   }
 }
 
@@ -256,6 +360,32 @@ __device__ __forceinline__ void mark(const EngineArgs& a, int s, int k) {
   const int slot = g == 0 ? 0 : (g == 7 ? 1 : (g == NWG - 1 ? 2 : -1));
   if (slot < 0) return;
   a.phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
+}
+
+// Where step s runs: token, layer, routing source, head.
+struct StepInfo {
+  int t, N, lay;
+  bool own;   // routed by the layer's own router (else by the previous token's head)
+  bool head;  // the layer's head runs (prediction for the next layer)
+  bool ok;    // the layer index is valid
+};
+
+__device__ __forceinline__ StepInfo step_info(const EngineArgs& a, int s) {
+  StepInfo f;
+  f.t = 0;
+  f.N = 0;
+  if (a.mode == 0) {
+    f.lay = a.step_layer[s];
+    f.own = true;
+  } else {
+    f.t = a.first_token + s / a.L;
+    f.N = s % a.L;
+    f.lay = f.N;
+    f.own = f.t == 0 || f.N < a.consumer_lo || f.N > a.consumer_hi;
+  }
+  f.ok = f.lay >= 0 && f.lay < a.n_table_layers;
+  f.head = f.ok && a.layers[f.lay].head != nullptr && (a.mode == 0 || f.N + 1 < a.L);
+  return f;
 }
 
 template <class SH>
@@ -289,7 +419,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 
   const int g = blockIdx.x;
   const int x = g % NX, m = g / NX;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const bool poller = (int)threadIdx.x < NPT;
   const Ctl c{a.ctl, a.status};
   const int K = a.K, E = a.E;
   const int n_list = K + a.S;
@@ -300,6 +431,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 
   if (threadIdx.x == 0) {
     mi->abort = 0;
+    mi->gu_step = mi->dn_step = mi->rt_step = mi->hd_step = -1;
+    mi->rt[0].step = mi->rt[1].step = -1;
     if ((int)xcc_id() != x) {  // the work split relies on blockIdx % 8 == XCD
       if (a.status) atomicOr(a.status, MOE_STATUS_ENGINE_ABORT);
       __hip_atomic_store(&a.ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -325,92 +458,246 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   }
   __syncthreads();
   const int nseg = mi->nseg;
+  auto row_seg = [&](int lr) {  // XCD-local row -> segment index
+    int q = 0;
+    while (q + 1 < nseg && lr >= mi->seg[q + 1].col0) ++q;
+    return q;
+  };
+
+  // ---- staging of a step's weights (issued by the staging waves) ----------
+  // gate/up codes, their (scale, zero), the XCD's LoRA-A rows of gate/up
+  auto stage_gu = [&](const Route& Rt, Waves ws) {
+    constexpr int QCH = D / 32;   // 16-byte code chunks per gate/up row
+    stage(smem + SH::O_GUQ, 2 * RM * QCH, ws, [&](int i) -> const void* {
+      const int rr = i / QCH, ch = i % QCH;
+      const int lr = m * RM + (rr % RM);
+      const int q = row_seg(lr);
+      if (!Rt.segok[q]) return a.xi;  // any valid address; the row is not used
+      const moe_bundle* b = &Rt.segbd[q];
+      const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
+      const uint8_t* base_q = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.q : b->up.q);
+      return base_q + (size_t)er * (D / 2) + ch * 16;
+    });
+    constexpr int SCH = D / 256;  // 16-byte (scale, zero) chunks per row
+    stage(smem + SH::O_GUS, 2 * RM * SCH, ws, [&](int i) -> const void* {
+      const int rr = i / SCH, ch = i % SCH;
+      const int lr = m * RM + (rr % RM);
+      const int q = row_seg(lr);
+      if (!Rt.segok[q]) return a.xi;
+      const moe_bundle* b = &Rt.segbd[q];
+      const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
+      const uint8_t* base_s = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.sz : b->up.sz);
+      return base_s + (size_t)er * (D / 16) + ch * 16;
+    });
+    stage(smem + SH::O_AR, SH::NAX * (D / 8), ws, [&](int i) -> const void* {
+      const int qa = i / (D / 8), ch = i % (D / 8);
+      const int ar = m + NM * qa;
+      if (ar >= nseg * 2 * R) return a.xi;
+      const int q = ar / (2 * R), rr = ar % (2 * R);
+      if (!Rt.segok[q]) return a.xi;
+      const moe_bundle* b = &Rt.segbd[q];
+      const void* A = rr < R ? b->gate.lora_a : b->up.lora_a;
+      if (!A) return a.xi;
+      return reinterpret_cast<const __half*>(A) + (size_t)(rr % R) * D + ch * 8;
+    });
+  };
+  // LoRA-B of gate/up (read while h is formed), the down rows restricted to
+  // the XCD's columns, their (scale, zero), LoRA-B and LoRA-A of down
+  auto stage_dn = [&](const Route& Rt, Waves ws) {
+    constexpr int BCH = R * 2 / 16;
+    stage(smem + SH::O_BGU, 2 * RM * BCH, ws, [&](int i) -> const void* {
+      const int rr = i / BCH, ch = i % BCH;
+      const int lr = m * RM + (rr % RM);
+      const int q = row_seg(lr);
+      if (!Rt.segok[q]) return a.xi;
+      const moe_bundle* b = &Rt.segbd[q];
+      const void* B = rr < RM ? b->gate.lora_b : b->up.lora_b;
+      if (!B) return a.xi;
+      const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
+      return reinterpret_cast<const __half*>(B) + (size_t)er * R + ch * 8;
+    });
+    const int dqch = GX / 32;  // 16-byte chunks per staged down row
+    stage(smem + SH::O_DQ, SH::DR * dqch, ws, [&](int i) -> const void* {
+      const int jj = i / dqch, ch = i % dqch;
+      const int col = ch * 32;
+      const int q = row_seg(col);
+      if (!Rt.segok[q]) return a.xi;
+      const moe_bundle* b = &Rt.segbd[q];
+      const int ec = mi->seg[q].i0 + (col - mi->seg[q].col0);
+      return reinterpret_cast<const uint8_t*>(b->down.q) + (size_t)(m * SH::DR + jj) * (IE / 2) +
+             ec / 2;
+    });
+    constexpr int DSCH = IE / 256;  // 16-byte chunks per (scale, zero) row
+    stage(smem + SH::O_DS, SH::DR * SH::NSEGX * DSCH, ws, [&](int i) -> const void* {
+      const int jq = i / DSCH, ch = i % DSCH;
+      const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
+      if (q >= nseg || !Rt.segok[q]) return a.xi;
+      const moe_bundle* b = &Rt.segbd[q];
+      return reinterpret_cast<const uint8_t*>(b->down.sz) + (size_t)(m * SH::DR + jj) * (IE / 16) +
+             ch * 16;
+    });
+    stage(smem + SH::O_BD, SH::DR * SH::NSEGX * BCH, ws, [&](int i) -> const void* {
+      const int jq = i / BCH, ch = i % BCH;
+      const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
+      if (q >= nseg || !Rt.segok[q]) return a.xi;
+      const void* B = Rt.segbd[q].down.lora_b;
+      if (!B) return a.xi;
+      return reinterpret_cast<const __half*>(B) + (size_t)(m * SH::DR + jj) * R + ch * 8;
+    });
+    // LoRA-A of down at this workgroup's rows: [kk][q][4 chunks of 8 halves]
+    // covering expert rows [e_lo(q) & ~7, e_hi(q)) of each segment q
+    stage(smem + SH::O_ADM, R * SH::NSEGX * 4, ws, [&](int i) -> const void* {
+      const int kk = i / (SH::NSEGX * 4), q = (i / 4) % SH::NSEGX, cch = i % 4;
+      if (q >= nseg || !Rt.segok[q]) return a.xi;
+      const int lo = max(m * RM, mi->seg[q].col0);
+      const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
+      const void* A = Rt.segbd[q].down.lora_a;
+      if (!A || lo >= hi) return a.xi;
+      const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
+      int ec = e0 + 8 * cch;
+      if (ec > IE - 8) ec = IE - 8;
+      return reinterpret_cast<const __half*>(A) + (size_t)kk * IE + ec;
+    });
+  };
+  auto stage_rows = [&](int off, const void* W, Waves ws) {  // router or head rows of this workgroup
+    const __half* Wh = reinterpret_cast<const __half*>(W);
+    stage(smem + off, SH::HRX * (D / 8), ws, [&](int i) {
+      const int e = g + NWG * (i / (D / 8));
+      return Wh + (size_t)(e < E ? e : 0) * D + (i % (D / 8)) * 8;
+    });
+  };
+  // The slots of the XCD's segments under routing Rt.idx/w (threads < nseg,
+  // wave 0); one barrier.
+  auto resolve_route = [&](Route& Rt, int lay, int step) {
+    if ((int)threadIdx.x < nseg) {
+      const int q = threadIdx.x;
+      const int k = mi->seg[q].k;
+      const int e = k < K ? Rt.idx[k] : E + (k - K);
+      const bool bad = k < K && (e < 0 || e >= E);
+      const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
+      Rt.segok[q] = slot >= 0;
+      if (slot >= 0) Rt.segbd[q] = a.bundles[(size_t)lay * a.n_slots + slot];
+      Rt.segw[q] = k < K ? Rt.w[k] : 1.f;
+      if (m == 0 && a.status) {
+        if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
+        else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
+      }
+    }
+    if (threadIdx.x == 0) Rt.step = step;
+    __syncthreads();
+  };
+  // Softmax-top-k of the logits in lg (wave 0), then resolve_route.
+  uint64_t* tk_keys = reinterpret_cast<uint64_t*>(lg + 256);          // [256] after the logits
+  int* tk_part = reinterpret_cast<int*>(lg + 768);                    // [256]
+  uint64_t* tk_sorted = reinterpret_cast<uint64_t*>(red);             // [32]; red is free here
+  auto compute_route = [&](Route& Rt, int lay, int step) {
+    block_topk(lg, E, K, Rt.idx, Rt.w, tk_keys, tk_part, tk_sorted);
+    __syncthreads();
+    mark(a, step, 15);
+    resolve_route(Rt, lay, step);
+  };
+  // The published prediction (ids and weights) that routes layer N at token t.
+  auto pred_of = [&](int t, int N) {
+    return a.xw + a.xo_pred + ((size_t)(t & 1) * a.L + N) * a.xs_pred;
+  };
+  // Route a consumer step from its published prediction; false on abort.
+  auto route_from_pred = [&](Route& Rt, int t, int N, int lay, int step) {
+    uint64_t* pw = pred_of(t, N);
+    if (!poll_all<1>(2 * K, (uint32_t)t + 1u, [&](int i) { return pw + i; },
+                     [&](int i, float v) {
+                       if (i < K) Rt.idx[i] = __float_as_int(v);
+                       else Rt.w[i - K] = v;
+                     },
+                     c, &mi->abort))
+      return false;
+    resolve_route(Rt, lay, step);
+    return true;
+  };
+  // the head logits that route layer N at token t (written at token t - 1)
+  auto logh_of = [&](int t, int N) {
+    return a.xw + a.xo_logh + ((size_t)(t & 1) * a.L + N) * a.xs_logh_layer;
+  };
 
   uint64_t* const X = a.xw;
-  float xi_next[SH::MAXI_D];
-  if (a.mode == 0)
+  float xi_next[SH::MAXI_P];
+  if (a.mode == 0 && poller)
 #pragma unroll
-    for (int q = 0; q < SH::MAXI_D; ++q) {
-      const int j = threadIdx.x + q * NT;
+    for (int q = 0; q < SH::MAXI_P; ++q) {
+      const int j = threadIdx.x + q * NPT;
       xi_next[q] = j < D ? a.xi[j] : 0.f;
     }
   for (int s = 0; s < a.n_steps && !mi->abort; ++s) {
     const uint32_t tag = base + (uint32_t)s + 1u;
     const int par = s & 1;
-    int t = 0, N = 0, lay;
-    bool own_route = true, has_head;
-    if (a.mode == 0) {
-      lay = a.step_layer[s];
-      if (lay < 0 || lay >= a.n_table_layers) {  // uniform across the grid: every workgroup stops
-        if (g == 0 && threadIdx.x == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
-        break;
-      }
-    } else {
-      t = a.first_token + s / a.L;
-      N = s % a.L;
-      lay = N;
-      own_route = t == 0 || N < a.consumer_lo || N > a.consumer_hi;
+    const StepInfo f = step_info(a, s);
+    if (!f.ok) {  // uniform across the grid: every workgroup stops
+      if (g == 0 && threadIdx.x == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
+      break;
     }
+    const int t = f.t, N = f.N, lay = f.lay;
+    const bool has_head = f.head;
     const moe_engine_layer LY = a.layers[lay];
-    has_head = LY.head != nullptr && (a.mode == 0 || N + 1 < a.L);
+    Route& Rt = mi->rt[par];
 
     mark(a, s, 0);
-    // ---- S0: layer input ------------------------------------------------
+    // ---- S0: layer input (global reads by the polling waves only) --------
     if (a.mode == 0) {
+      if (poller) {
 #pragma unroll
-      for (int q = 0; q < SH::MAXI_D; ++q) {
-        const int j = threadIdx.x + q * NT;
-        if (j < D) r0[j] = xi_next[q];
-      }
-      if (s + 1 < a.n_steps) {  // the next step's draws arrive while this step runs
-        const float* xn = a.xi + (size_t)(s + 1) * D;
+        for (int q = 0; q < SH::MAXI_P; ++q) {
+          const int j = threadIdx.x + q * NPT;
+          if (j < D) r0[j] = xi_next[q];
+        }
+        if (s + 1 < a.n_steps) {  // the next step's draws arrive while this step runs
+          const float* xn = a.xi + (size_t)(s + 1) * D;
 #pragma unroll
-        for (int q = 0; q < SH::MAXI_D; ++q) {
-          const int j = threadIdx.x + q * NT;
-          xi_next[q] = j < D ? xn[j] : 0.f;
+          for (int q = 0; q < SH::MAXI_P; ++q) {
+            const int j = threadIdx.x + q * NPT;
+            xi_next[q] = j < D ? xn[j] : 0.f;
+          }
         }
       }
       __syncthreads();
       block_rmsnorm_to_x<SH>(r0, xf, xh, red);
     } else {
       if (s == 0) {
-        for (int j = threadIdx.x; j < D; j += NT) r0[j] = a.r_state[j];
+        if (poller)
+          for (int j = threadIdx.x; j < D; j += NPT) r0[j] = a.r_state[j];
         __syncthreads();
       } else {
         uint64_t* rv = X + a.xo_rv + (size_t)(par ^ 1) * a.xs_rv;
-        if (!poll_all<SH::MAXI_D>(D, tag - 1u, [&](int i) { return rv + i; },
+        if (!poll_all<SH::MAXI_P>(D, tag - 1u, [&](int i) { return rv + i; },
                                   [&](int i, float v) { r0[i] = v; }, c, &mi->abort))
           break;
       }
       if (N == 0) {  // token start: r = xi + rmsnorm(r)
         const double inv = 1.0 / sqrt(block_sumsq<SH>(r0, red) / (double)D + 1e-6);
         const float* xi = a.xi + (size_t)(s / a.L) * D;
-        for (int j = threadIdx.x; j < D; j += NT) r0[j] = (float)((double)xi[j] + (double)r0[j] * inv);
+        if (poller)
+          for (int j = threadIdx.x; j < D; j += NPT) r0[j] = (float)((double)xi[j] + (double)r0[j] * inv);
         __syncthreads();
       }
-      const __half* md = reinterpret_cast<const __half*>(LY.mix_d);
-      for (int j = threadIdx.x; j < D; j += NT) {
-        const int p = LY.mix_perm[j];
-        const float v = (p >= 0 && p < D) ? r0[p] : 0.f;
-        r1[j] = fmaf(__half2float(md[j]), v, r0[j]);
+      if (poller) {
+        const __half* md = reinterpret_cast<const __half*>(LY.mix_d);
+        for (int j = threadIdx.x; j < D; j += NPT) {
+          const int p = LY.mix_perm[j];
+          const float v = (p >= 0 && p < D) ? r0[p] : 0.f;
+          r1[j] = fmaf(__half2float(md[j]), v, r0[j]);
+        }
       }
       __syncthreads();
       block_rmsnorm_to_x<SH>(r1, xf, xh, red);
     }
     __syncthreads();
-    if (g == 0 && a.x_rec)
-      for (int j = threadIdx.x; j < D; j += NT) a.x_rec[(size_t)s * D + j] = xh[j];
+    if (g == 0 && a.x_rec && poller)
+      for (int j = threadIdx.x; j < D; j += NPT) a.x_rec[(size_t)s * D + j] = xh[j];
 
     mark(a, s, 1);
     // ---- S1: routing ----------------------------------------------------
-    if (own_route) {
+    if (f.own) {
       uint64_t* lr = X + a.xo_logr + (size_t)par * a.xs_logr;
-      const __half* W = reinterpret_cast<const __half*>(LY.router);
-      stage(smem + SH::O_RT, SH::HRX * D / 8, [&](int i) {
-        const int e = g + NWG * (i / (D / 8));
-        return W + (size_t)(e < E ? e : 0) * D + (i % (D / 8)) * 8;
-      });
-      __builtin_amdgcn_s_waitcnt(0);
+      if (mi->rt_step != s) stage_rows(SH::O_RT, LY.router, kAll);
+      dma_wait();
       __syncthreads();
       for (int q = wave; q < SH::HRX; q += NWV) {
         const int e = g + NWG * q;
@@ -418,154 +705,66 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         if (lane == 0 && e < E) st_tag(lr + e, tag, v);
       }
       mark(a, s, 12);
-      if (!poll_all<2>(E, tag, [&](int i) { return lr + i; }, [&](int i, float v) { lg[i] = v; }, c,
-                       &mi->abort))
+      if (!poll_all<SH::MAXI_E>(E, tag, [&](int i) { return lr + i; },
+                                [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
         break;
-    } else {
-      uint64_t* lh = X + a.xo_logh + ((size_t)(t & 1) * a.L + N) * a.xs_logh_layer;
-      if (!poll_all<2>(E, (uint32_t)t + 1u, [&](int i) { return lh + i; },
-                       [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
-        break;
+      mark(a, s, 10);
+      compute_route(Rt, lay, s);
+    } else if (Rt.step != s) {  // not routed ahead (first step of a launch)
+      if (!route_from_pred(Rt, t, N, lay, s)) break;
     }
-    mark(a, s, 10);
-    if (wave == 0) wave_topk<false, 4>(lg, E, K, mi->idx, mi->w);
-    __syncthreads();
     mark(a, s, 11);
     if (g == 0 && threadIdx.x < K) {
-      if (a.idx_rec) a.idx_rec[(size_t)s * K + threadIdx.x] = mi->idx[threadIdx.x];
-      if (a.w_rec) a.w_rec[(size_t)s * K + threadIdx.x] = mi->w[threadIdx.x];
+      if (a.idx_rec) a.idx_rec[(size_t)s * K + threadIdx.x] = Rt.idx[threadIdx.x];
+      if (a.w_rec) a.w_rec[(size_t)s * K + threadIdx.x] = Rt.w[threadIdx.x];
     }
-    if (threadIdx.x < nseg) {
-      const int q = threadIdx.x;
-      const int k = mi->seg[q].k;
-      const int e = k < K ? mi->idx[k] : E + (k - K);
-      const bool bad = k < K && (e < 0 || e >= E);
-      const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
-      mi->segok[q] = slot >= 0;
-      if (slot >= 0) mi->segbd[q] = a.bundles[(size_t)lay * a.n_slots + slot];
-      mi->segw[q] = k < K ? mi->w[k] : 1.f;
-      if (m == 0 && a.status) {
-        if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
-        else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
-      }
-    }
-    __syncthreads();
 
     mark(a, s, 2);
-    // ---- S2: stage weights, gate/up rows, LoRA-A rows, head rows --------
-    // gate/up row r of this workgroup: r < RM gate, else up; flattened row
-    // fr = x*GX + m*RM + (r % RM) -> segment and expert row.
-    auto row_seg = [&](int lr) {  // XCD-local row -> segment index
-      int q = 0;
-      while (q + 1 < nseg && lr >= mi->seg[q + 1].col0) ++q;
-      return q;
-    };
+    // ---- S2: weights of this step (unless staged ahead), then compute ----
+    // Staged now: gate/up and head rows by waves 0-3 (needed at once), down by
+    // waves 4-7 (needed from S3 on). Staged ahead: waves 4-7 wait for it here.
     {
-      constexpr int QCH = D / 32;   // 16-byte code chunks per gate/up row
-      stage(smem + SH::O_GUQ, 2 * RM * QCH, [&](int i) -> const void* {
-        const int rr = i / QCH, ch = i % QCH;
-        const int lr = m * RM + (rr % RM);
-        const int q = row_seg(lr);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        if (!b) return a.xi;  // any valid address; the row is not used
-        const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
-        const uint8_t* base_q = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.q : b->up.q);
-        return base_q + (size_t)er * (D / 2) + ch * 16;
-      });
-      constexpr int SCH = D / 256;  // 16-byte (scale, zero) chunks per row
-      stage(smem + SH::O_GUS, 2 * RM * SCH, [&](int i) -> const void* {
-        const int rr = i / SCH, ch = i % SCH;
-        const int lr = m * RM + (rr % RM);
-        const int q = row_seg(lr);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        if (!b) return a.xi;
-        const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
-        const uint8_t* base_s = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.sz : b->up.sz);
-        return base_s + (size_t)er * (D / 16) + ch * 16;
-      });
-      // LoRA-A rows: the XCD's nseg*2R rows, row ar = m + NM*qa
-      stage(smem + SH::O_AR, SH::NAX * (D / 8), [&](int i) -> const void* {
-        const int qa = i / (D / 8), ch = i % (D / 8);
-        const int ar = m + NM * qa;
-        if (ar >= nseg * 2 * R) return a.xi;
-        const int q = ar / (2 * R), rr = ar % (2 * R);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        const void* A = b ? (rr < R ? b->gate.lora_a : b->up.lora_a) : nullptr;
-        if (!A) return a.xi;
-        return reinterpret_cast<const __half*>(A) + (size_t)(rr % R) * D + ch * 8;
-      });
-      if (has_head) {
-        const __half* Wh = reinterpret_cast<const __half*>(LY.head);
-        stage(smem + SH::O_HD, SH::HRX * (D / 8), [&](int i) {
-          const int e = g + NWG * (i / (D / 8));
-          return Wh + (size_t)(e < E ? e : 0) * D + (i % (D / 8)) * 8;
-        });
-      }
-      // LoRA-B rows of gate / up for this workgroup's rows (R halves each)
-      constexpr int BCH = R * 2 / 16;
-      stage(smem + SH::O_BGU, 2 * RM * BCH, [&](int i) -> const void* {
-        const int rr = i / BCH, ch = i % BCH;
-        const int lr = m * RM + (rr % RM);
-        const int q = row_seg(lr);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        const void* B = b ? (rr < RM ? b->gate.lora_b : b->up.lora_b) : nullptr;
-        if (!B) return a.xi;
-        const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
-        return reinterpret_cast<const __half*>(B) + (size_t)er * R + ch * 8;
-      });
-      // down rows j = m*DR + jj, restricted to the XCD's columns
-      const int dqch = GX / 32;  // 16-byte chunks per staged down row
-      stage(smem + SH::O_DQ, SH::DR * dqch, [&](int i) -> const void* {
-        const int jj = i / dqch, ch = i % dqch;
-        const int col = ch * 32;
-        const int q = row_seg(col);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        if (!b) return a.xi;
-        const int ec = mi->seg[q].i0 + (col - mi->seg[q].col0);
-        return reinterpret_cast<const uint8_t*>(b->down.q) + (size_t)(m * SH::DR + jj) * (IE / 2) +
-               ec / 2;
-      });
-      // (scale, zero) of the down rows: the whole row of each segment expert, [jj][q][I/16 B]
-      constexpr int DSCH = IE / 256;  // 16-byte chunks per (scale, zero) row
-      stage(smem + SH::O_DS, SH::DR * SH::NSEGX * DSCH, [&](int i) -> const void* {
-        const int jq = i / DSCH, ch = i % DSCH;
-        const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
-        if (q >= nseg) return a.xi;
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        if (!b) return a.xi;
-        return reinterpret_cast<const uint8_t*>(b->down.sz) + (size_t)(m * SH::DR + jj) * (IE / 16) +
-               ch * 16;
-      });
-      // LoRA-B rows of down: [jj][q][R]
-      stage(smem + SH::O_BD, SH::DR * SH::NSEGX * BCH, [&](int i) -> const void* {
-        const int jq = i / BCH, ch = i % BCH;
-        const int jj = jq / SH::NSEGX, q = jq % SH::NSEGX;
-        if (q >= nseg) return a.xi;
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        const void* B = b ? b->down.lora_b : nullptr;
-        if (!B) return a.xi;
-        return reinterpret_cast<const __half*>(B) + (size_t)(m * SH::DR + jj) * R + ch * 8;
-      });
-      // LoRA-A of down at this workgroup's rows: [kk][q][4 chunks of 8 halves]
-      // covering expert rows [e_lo(q) & ~7, e_hi(q)) of each segment q
-      stage(smem + SH::O_ADM, R * SH::NSEGX * 4, [&](int i) -> const void* {
-        const int kk = i / (SH::NSEGX * 4), q = (i / 4) % SH::NSEGX, cch = i % 4;
-        if (q >= nseg) return a.xi;
-        const int lo = max(m * RM, mi->seg[q].col0);
-        const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        const void* A = b ? b->down.lora_a : nullptr;
-        if (!A || lo >= hi) return a.xi;
-        const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
-        int ec = e0 + 8 * cch;
-        if (ec > IE - 8) ec = IE - 8;
-        return reinterpret_cast<const __half*>(A) + (size_t)kk * IE + ec;
-      });
+      const bool gu_now = mi->gu_step != s, dn_now = mi->dn_step != s;
+      const bool hd_now = has_head && mi->hd_step != s;
+      if (gu_now) stage_gu(Rt, kPollW);
+      if (hd_now) stage_rows(SH::O_HD, LY.head, kPollW);
+      if (dn_now) stage_dn(Rt, kStageW);
+      if (wave < kStageW0 ? (gu_now || hd_now) : !dn_now) dma_wait();
+      __syncthreads();
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
 
     mark(a, s, 3);
+    // LoRA-A rows first, so that their exchange overlaps the gate/up rows
+    {
+      uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
+      for (int qa = wave; qa < SH::NAX; qa += NWV) {
+        const int ar = m + NM * qa;
+        if (ar >= nseg * 2 * R) continue;
+        const int q = ar / (2 * R), rr = ar % (2 * R);
+        const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
+        const bool has = b && (rr < R ? (b->gate.lora_a && b->gate.lora_b)
+                                      : (b->up.lora_a && b->up.lora_b));
+        const float v = has ? wave_dot_h<SH>(arow + (size_t)qa * D, xh) : 0.f;
+        if (lane == 0) st_tag(AV + q * 2 * R + rr, tag, v);
+      }
+    }
+    // head rows -> tagged logits for the next layer at the next token
+    if (has_head) {
+      uint64_t* lh;
+      uint32_t htag;
+      if (a.mode == 0) {
+        lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
+        htag = tag;
+      } else {
+        lh = logh_of(t + 1, N + 1);
+        htag = (uint32_t)t + 2u;
+      }
+      for (int q = wave; q < SH::HRX; q += NWV) {
+        const int e = g + NWG * q;
+        const float v = wave_dot_h<SH>(hdrow + (size_t)q * D, xh);
+        if (lane == 0 && e < E) st_tag(lh + e, htag, v);
+      }
+    }
     // gate/up matvecs (raw): rows r of [gate RM | up RM], LPR lanes per row
     {
       const int c0 = lane % SH::LPR, sub = lane / SH::LPR;
@@ -576,7 +775,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         float sacc = 0.f;
 #pragma unroll
         for (int e = 0; e < 32; ++e) {
-          xv[cc][e] = xf[ch * 32 + e];
+          xv[cc][e] = xf[pad32(ch * 32 + e)];
           sacc += xv[cc][e];
         }
         xs[cc] = sacc;
@@ -597,52 +796,47 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         if (c0 == 0 && rr < 2 * RM) gxu[rr] = acc;
       }
     }
-    // LoRA-A rows -> tagged a-vectors of the XCD
-    {
-      uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
-      for (int qa = wave; qa < SH::NAX; qa += NWV) {
-        const int ar = m + NM * qa;
-        if (ar >= nseg * 2 * R) continue;
-        const int q = ar / (2 * R), rr = ar % (2 * R);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
-        const bool has = b && (rr < R ? (b->gate.lora_a && b->gate.lora_b)
-                                      : (b->up.lora_a && b->up.lora_b));
-        const float v = has ? wave_dot_h<SH>(arow + (size_t)qa * D, xh) : 0.f;
-        if (lane == 0) st_tag(AV + q * 2 * R + rr, tag, v);
-      }
-    }
-    // head rows -> tagged logits for the next layer at the next token
-    if (has_head) {
-      uint64_t* lh;
-      uint32_t htag;
-      if (a.mode == 0) {
-        lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
-        htag = tag;
-      } else {
-        lh = X + a.xo_logh + ((size_t)((t + 1) & 1) * a.L + (N + 1)) * a.xs_logh_layer;
-        htag = (uint32_t)t + 2u;
-      }
-      for (int q = wave; q < SH::HRX; q += NWV) {
-        const int e = g + NWG * q;
-        const float v = wave_dot_h<SH>(hdrow + (size_t)q * D, xh);
-        if (lane == 0 && e < E) st_tag(lh + e, htag, v);
-      }
-    }
     __syncthreads();
 
     mark(a, s, 4);
+    // ---- ahead: the next step's router / head rows, and for a step routed
+    // by a prediction, its routing and its gate/up weights ----------------
+    if (wave >= kStageW0) dma_wait();  // this step's down weights (read from S3 on)
+    int nxt_dn = -1;  // the next step, if its routing is known here
+    if (s + 1 < a.n_steps) {
+      const StepInfo f1 = step_info(a, s + 1);
+      if (f1.ok) {
+        const moe_engine_layer L1 = a.layers[f1.lay];
+        if (f1.own) stage_rows(SH::O_RT, L1.router, kStageW);
+        if (f1.head) stage_rows(SH::O_HD, L1.head, kStageW);
+        if (!f1.own) {
+          Route& R1 = mi->rt[par ^ 1];
+          if (!route_from_pred(R1, f1.t, f1.N, f1.lay, s + 1)) break;
+          stage_gu(R1, kStageW);
+          nxt_dn = s + 1;
+        }
+        if (threadIdx.x == 0) {
+          if (f1.own) mi->rt_step = s + 1;
+          if (f1.head) mi->hd_step = s + 1;
+          if (!f1.own) mi->gu_step = s + 1;
+        }
+      }
+    }
+
+    mark(a, s, 13);
     // ---- S3: a-vectors of the XCD -> h of this workgroup's rows ---------
     {
       uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
-      if (!poll_all<1>(nseg * 2 * R, tag, [&](int i) { return AV + i; },
-                       [&](int i, float v) { av[i] = v; }, c, &mi->abort))
+      if (!poll_all<(SH::NSEGX * 2 * R + NPT - 1) / NPT>(
+              nseg * 2 * R, tag, [&](int i) { return AV + i; }, [&](int i, float v) { av[i] = v; }, c,
+              &mi->abort))
         break;
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
       if ((int)threadIdx.x < RM) {
         const int i = threadIdx.x;
         const int lr = m * RM + i;
         const int q = row_seg(lr);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
+        const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
         float hv = 0.f;
         if (b) {
           float gg = gxu[i], uu = gxu[RM + i];
@@ -671,7 +865,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int q = p / R, kk = p % R;
         const int lo = max(m * RM, mi->seg[q].col0);
         const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
-        const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
+        const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
         float acc = 0.f;
         if (b && b->down.lora_a && b->down.lora_b && lo < hi) {
           const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
@@ -689,14 +883,14 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     // ---- S4: h of the XCD -> down rows -> tagged partial of the output ---
     {
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
-      if (!poll_all<(SH::GXX + NT - 1) / NT>(GX, tag, [&](int i) { return HV + i; },
-                                            [&](int i, float v) { hx[i] = v; }, c, &mi->abort))
+      if (!poll_all<(SH::GXX + NPT - 1) / NPT>(GX, tag, [&](int i) { return HV + i; },
+                                              [&](int i, float v) { hx[pad32(i)] = v; }, c, &mi->abort))
         break;
       // a_d[q][kk] = sum of the 32 members' partials
       {
         uint64_t* ADP = X + a.xo_adp + (size_t)par * a.xs_adp + (size_t)x * NM * SH::NSEGX * R;
         const int per = nseg * R;
-        if (!poll_all<(NM * SH::NSEGX * R + NT - 1) / NT>(
+        if (!poll_all<(NM * SH::NSEGX * R + NPT - 1) / NPT>(
                 NM * per, tag,
                 [&](int i) { return ADP + (size_t)(i / per) * SH::NSEGX * R + (i % per); },
                 [&](int i, float v) { dp[i] = v; }, c, &mi->abort))
@@ -716,11 +910,11 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       int qseg = 0, egrp = 0;
       if (active) {
         qseg = row_seg(ch * 32);
-        wseg = mi->segok[qseg] ? mi->segw[qseg] : 0.f;
+        wseg = Rt.segok[qseg] ? Rt.segw[qseg] : 0.f;
         egrp = (mi->seg[qseg].i0 + (ch * 32 - mi->seg[qseg].col0)) / 64;
 #pragma unroll
         for (int e = 0; e < 32; ++e) {
-          hv[e] = hx[ch * 32 + e];
+          hv[e] = hx[pad32(ch * 32 + e)];
           hsum += hv[e];
         }
       }
@@ -738,17 +932,17 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       __syncthreads();
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part + (size_t)x * D;
       // 8 threads per row: chunk partials and LoRA-B terms, then a DPP sum
-      for (int base = 0; base < SH::DR * 8; base += NT) {
-        const int tt = base + (int)threadIdx.x;
+      for (int b0 = 0; b0 < SH::DR * 8; b0 += NT) {
+        const int tt = b0 + (int)threadIdx.x;
         const int jj = tt >> 3, part = tt & 7;
         float acc = 0.f;
         if (jj < SH::DR) {
           for (int cc = part; cc < LPRD; cc += 8) acc += dp[jj * 32 + cc];
           for (int term = part; term < nseg * R; term += 8) {
             const int q = term / R, kk = term % R;
-            const moe_bundle* b = mi->segok[q] ? &mi->segbd[q] : nullptr;
+            const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
             if (!b || !b->down.lora_a || !b->down.lora_b) continue;
-            acc = fmaf(mi->segw[q] * a.lora_scale *
+            acc = fmaf(Rt.segw[q] * a.lora_scale *
                            __half2float(bd[((size_t)jj * SH::NSEGX + q) * R + kk]),
                        adv[q * R + kk], acc);
           }
@@ -757,14 +951,41 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         if (part == 0 && jj < SH::DR) st_tag(PART + m * SH::DR + jj, tag, acc);
       }
     }
+    __syncthreads();
 
     mark(a, s, 7);
+    // ---- ahead: the down weights of a step routed ahead -------------------
+    if (nxt_dn >= 0) {
+      stage_dn(mi->rt[par ^ 1], kStageW);
+      if (threadIdx.x == 0) mi->dn_step = nxt_dn;
+    }
+
+    mark(a, s, 14);
     // ---- S5: reduce the 8 XCD partials of this workgroup's rows ---------
+    // One workgroup per step also turns the head's logits into the predicted
+    // routing (top-k on a staging wave while the polling waves wait for the
+    // partials) and publishes it for the next token's consumer layer.
     {
+      const bool pred_wg = has_head && g == s % NWG && (a.mode == 1 || a.pidx_rec || a.pw_rec);
+      uint64_t* lh = nullptr;
+      uint32_t htag = 0;
+      if (pred_wg) {
+        if (a.mode == 0) {
+          lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
+          htag = tag;
+        } else {
+          lh = logh_of(t + 1, N + 1);
+          htag = (uint32_t)t + 2u;
+        }
+        if (!poll_all<SH::MAXI_E>(E, htag, [&](int i) { return lh + i; },
+                                  [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
+          break;
+        block_topk(lg, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_sorted);
+      }
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part;
-      if (!poll_all<1>(SH::RR * NX, tag,
-                       [&](int i) { return PART + (size_t)(i % NX) * D + g * SH::RR + i / NX; },
-                       [&](int i, float v) { yl[i] = v; }, c, &mi->abort))
+      if (!poll_all<(SH::RR * NX + NPT - 1) / NPT>(
+              SH::RR * NX, tag, [&](int i) { return PART + (size_t)(i % NX) * D + g * SH::RR + i / NX; },
+              [&](int i, float v) { yl[i] = v; }, c, &mi->abort))
         break;
       mark(a, s, 8);
       if ((int)threadIdx.x < SH::RR) {
@@ -780,36 +1001,24 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           if (s + 1 == a.n_steps) a.r_state[j] = rn;
         }
       }
-      // the head's prediction (recorded for tests and callers)
-      if (g == 0 && has_head && (a.pidx_rec || a.pw_rec)) {
-        uint64_t* lh;
-        uint32_t htag;
-        if (a.mode == 0) {
-          lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
-          htag = tag;
-        } else {
-          lh = X + a.xo_logh + ((size_t)((t + 1) & 1) * a.L + (N + 1)) * a.xs_logh_layer;
-          htag = (uint32_t)t + 2u;
+      if (pred_wg && (int)threadIdx.x < K) {
+        const int i = threadIdx.x;
+        if (a.mode == 1) {
+          uint64_t* pw = pred_of(t + 1, N + 1);
+          st_tag(pw + i, htag, __int_as_float(mi->pidx[i]));
+          st_tag(pw + K + i, htag, mi->pw[i]);
         }
-        if (!poll_all<2>(E, htag, [&](int i) { return lh + i; }, [&](int i, float v) { lg[i] = v; },
-                         c, &mi->abort))
-          break;
-        if (wave == 0) {
-          int32_t* pi = mi->pidx;
-          float* pw = mi->pw;
-          wave_topk<false, 4>(lg, E, K, pi, pw);
-          if (lane < K) {
-            if (a.pidx_rec) a.pidx_rec[(size_t)s * K + lane] = pi[lane];
-            if (a.pw_rec) a.pw_rec[(size_t)s * K + lane] = pw[lane];
-          }
-        }
+        if (a.pidx_rec) a.pidx_rec[(size_t)s * K + i] = mi->pidx[i];
+        if (a.pw_rec) a.pw_rec[(size_t)s * K + i] = mi->pw[i];
       }
       __syncthreads();
       mark(a, s, 9);
     }
   }
 
-  // ---- finish: the last workgroup moves the tag base past this launch ----
+  // ---- finish: wait for any staging still in flight; the last workgroup
+  // moves the tag base past this launch ------------------------------------
+  if (wave >= kStageW0) dma_wait();
   __syncthreads();
   if (threadIdx.x == 0) {
     const uint32_t old = atomicAdd(&a.ctl[1], 1u);
@@ -898,6 +1107,8 @@ size_t engine_workspace_words(int E, int d, int L, EngineArgs* a) {
   a->xo_rv = take(2 * a->xs_rv);
   a->xs_logh_layer = (size_t)(E + 31) / 32 * 32;
   a->xo_logh = take(2 * (size_t)(L > 0 ? L : 1) * a->xs_logh_layer);
+  a->xs_pred = 64;  // K ids + K weights, K <= 32
+  a->xo_pred = take(2 * (size_t)(L > 0 ? L : 1) * a->xs_pred);
   return off;
 }
 

@@ -81,6 +81,7 @@ __global__ void __launch_bounds__(256) route_kernel(const __half* __restrict__ x
   __threadfence();
   __syncthreads();
   __shared__ int last;
+  __shared__ uint32_t tk_scratch[64];
   if (threadIdx.x == 0) {
     const uint32_t prev = atomicAdd(&counters[t], 1u);
     last = (prev == gridDim.x - 1);
@@ -88,7 +89,7 @@ __global__ void __launch_bounds__(256) route_kernel(const __half* __restrict__ x
   __syncthreads();
   if (!last) return;
   __threadfence();
-  if (wave == 0) wave_topk<true>(lt, E, K, idx + (size_t)t * K, wout + (size_t)t * K);
+  if (wave == 0) wave_topk<true>(lt, E, K, idx + (size_t)t * K, wout + (size_t)t * K, tk_scratch);
   if (threadIdx.x == 0)
     __hip_atomic_store(&counters[t], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -96,8 +97,9 @@ __global__ void __launch_bounds__(256) route_kernel(const __half* __restrict__ x
 __global__ void __launch_bounds__(64) topk_kernel(const float* __restrict__ logits, int E, int K,
                                                   int32_t* __restrict__ idx,
                                                   float* __restrict__ w) {
+  __shared__ uint32_t tk_scratch[64];
   const int t = blockIdx.x;
-  wave_topk<false>(logits + (size_t)t * E, E, K, idx + (size_t)t * K, w + (size_t)t * K);
+  wave_topk<false>(logits + (size_t)t * E, E, K, idx + (size_t)t * K, w + (size_t)t * K, tk_scratch);
 }
 
 // ------------------------------------------------------------------------

@@ -809,16 +809,13 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const moe_engine_layer L1 = a.layers[f1.lay];
         if (f1.own) stage_rows(SH::O_RT, L1.router, kStageW);
         if (f1.head) stage_rows(SH::O_HD, L1.head, kStageW);
-        if (!f1.own) {
+        if (!f1.own) {  // routing known ahead; its weights are staged in its own step
           Route& R1 = mi->rt[par ^ 1];
           if (!route_from_pred(R1, f1.t, f1.N, f1.lay, s + 1)) break;
-          stage_gu(R1, kStageW);
-          nxt_dn = s + 1;
         }
         if (threadIdx.x == 0) {
           if (f1.own) mi->rt_step = s + 1;
           if (f1.head) mi->hd_step = s + 1;
-          if (!f1.own) mi->gu_step = s + 1;
         }
       }
     }

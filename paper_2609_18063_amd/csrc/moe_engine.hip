@@ -168,8 +168,8 @@ struct Shape {
   static constexpr int O_DS = O_DQ + kb(DR * GXX / 2);              // [DR][NSEGX][IE/16]
   static constexpr int O_BD = O_DS + kb(DR * NSEGX * IE / 16);      // [DR][NSEGX][R] fp16
   static constexpr int O_ADM = O_BD + kb(DR * NSEGX * R * 2);       // [R][NSEGX][32] fp16
-  static constexpr int O_XF = O_ADM + kb(R * NSEGX * 32 * 2);       // [D] f32, pad32 layout
-  static constexpr int O_XH = O_XF + (D + D / 32) * 4;              // [D] f16
+  static constexpr int O_XQ = O_ADM + kb(R * NSEGX * 32 * 2);       // [D] f16, pair order
+  static constexpr int O_XH = O_XQ + D * 2;                         // [D] f16
   static constexpr int O_R0 = O_XH + D * 2;                         // [D] f32
   static constexpr int O_R1 = O_R0 + D * 4;                         // [D] f32
   static constexpr int O_LG = O_R1 + D * 4;                         // [1024] f32 logits
@@ -264,6 +264,8 @@ __device__ void block_topk(const float* l, int E, int K, int32_t* idx_out, float
   }
 }
 
+typedef _Float16 hv2 __attribute__((ext_vector_type(2)));
+
 // LDS index of element i of a vector that lanes read in 32-element chunks
 // (lane l reading chunk l): one pad word per chunk puts the 64 lanes' reads of
 // the same element in 64 different banks.
@@ -308,13 +310,21 @@ __device__ double block_sumsq(const float* v, double* red) {
   return tot;
 }
 
+// Position of input j in the pair order of x: inside each group of 8 the
+// halves run x0,x4,x1,x5,x2,x6,x3,x7, the order in which the nibbles of one
+// code dword pair up under a 0x000F000F mask at shifts 0, 4, 8, 12.
+__device__ __forceinline__ int pair_pos(int j) {
+  const int r = j & 7;
+  return (j & ~7) + (r < 4 ? 2 * r : 2 * (r - 4) + 1);
+}
+
 template <class SH>
-__device__ void block_rmsnorm_to_x(const float* v, float* xf, __half* xh, double* red) {
+__device__ void block_rmsnorm_to_x(const float* v, __half* xq, __half* xh, double* red) {
   const double inv = 1.0 / sqrt(block_sumsq<SH>(v, red) / (double)SH::D + 1e-6);
   for (int j = threadIdx.x; j < SH::D; j += NT) {
     const __half h = __half(static_cast<_Float16>((double)v[j] * inv));
     xh[j] = h;
-    xf[pad32(j)] = __half2float(h);
+    xq[pair_pos(j)] = h;
   }
 }
 
@@ -402,7 +412,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   uint8_t* ds = reinterpret_cast<uint8_t*>(smem + SH::O_DS);
   __half* bd = reinterpret_cast<__half*>(smem + SH::O_BD);
   __half* adm = reinterpret_cast<__half*>(smem + SH::O_ADM);
-  float* xf = reinterpret_cast<float*>(smem + SH::O_XF);
+  __half* xq = reinterpret_cast<__half*>(smem + SH::O_XQ);
   __half* xh = reinterpret_cast<__half*>(smem + SH::O_XH);
   float* r0 = reinterpret_cast<float*>(smem + SH::O_R0);
   float* r1 = reinterpret_cast<float*>(smem + SH::O_R1);
@@ -658,7 +668,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
       }
       __syncthreads();
-      block_rmsnorm_to_x<SH>(r0, xf, xh, red);
+      block_rmsnorm_to_x<SH>(r0, xq, xh, red);
     } else {
       if (s == 0) {
         if (poller)
@@ -686,7 +696,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
       }
       __syncthreads();
-      block_rmsnorm_to_x<SH>(r1, xf, xh, red);
+      block_rmsnorm_to_x<SH>(r1, xq, xh, red);
     }
     __syncthreads();
     if (g == 0 && a.x_rec && poller)
@@ -759,28 +769,40 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         lh = logh_of(t + 1, N + 1);
         htag = (uint32_t)t + 2u;
       }
-      for (int q = wave; q < SH::HRX; q += NWV) {
+      for (int q = (wave + NWV - 2) % NWV; q < SH::HRX; q += NWV) {  // from wave 2 on
         const int e = g + NWG * q;
         const float v = wave_dot_h<SH>(hdrow + (size_t)q * D, xh);
         if (lane == 0 && e < E) st_tag(lh + e, htag, v);
       }
     }
-    // gate/up matvecs (raw): rows r of [gate RM | up RM], LPR lanes per row
+    // gate/up matvecs (raw): rows r of [gate RM | up RM], LPR lanes per row.
+    // Codes become fp16 pairs q * 2^-24 (exact subnormals) under one mask and
+    // meet x in its pair order in v_dot2_f32_f16; the 2^24 goes into the
+    // scale. Rows are dealt from wave 7 down, so the waves that carry the
+    // LoRA-A and head rows get fewer of them.
     {
       const int c0 = lane % SH::LPR, sub = lane / SH::LPR;
-      float xv[SH::CPL][32], xs[SH::CPL];
+      hv2 xp[SH::CPL][16];
+      float xs[SH::CPL];
+      const hv2 one2 = {(_Float16)1.0f, (_Float16)1.0f};
 #pragma unroll
       for (int cc = 0; cc < SH::CPL; ++cc) {
         const int ch = c0 + SH::LPR * cc;
+        const U4* src = reinterpret_cast<const U4*>(xq + ch * 32);
         float sacc = 0.f;
 #pragma unroll
-        for (int e = 0; e < 32; ++e) {
-          xv[cc][e] = xf[pad32(ch * 32 + e)];
-          sacc += xv[cc][e];
+        for (int i = 0; i < 4; ++i) {
+          const U4 v = src[i];
+          xp[cc][4 * i + 0] = __builtin_bit_cast(hv2, v.x);
+          xp[cc][4 * i + 1] = __builtin_bit_cast(hv2, v.y);
+          xp[cc][4 * i + 2] = __builtin_bit_cast(hv2, v.z);
+          xp[cc][4 * i + 3] = __builtin_bit_cast(hv2, v.w);
         }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sacc = __builtin_amdgcn_fdot2(xp[cc][i], one2, sacc, false);
         xs[cc] = sacc;
       }
-      for (int rg = wave; rg * SH::RPI < 2 * RM; rg += NWV) {
+      for (int rg = NWV - 1 - wave; rg * SH::RPI < 2 * RM; rg += NWV) {
         const int rr = rg * SH::RPI + sub;
         const int rrc = rr < 2 * RM ? rr : 0;
         float acc = 0.f;
@@ -790,7 +812,17 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           const U4 qv = *reinterpret_cast<const U4*>(guq + (size_t)rrc * (D / 2) + ch * 16);
           const float2 sz = h2f2(*reinterpret_cast<const uint32_t*>(gus + (size_t)rrc * (D / 16) +
                                                                      (ch >> 1) * 4));
-          acc += sz.x * dot32_q4(qv, xv[cc]) + sz.y * xs[cc];
+          const uint32_t wd[4] = {qv.x, qv.y, qv.z, qv.w};
+          float d = 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int mm = 0; mm < 4; ++mm) {
+              const uint32_t p = (wd[i] >> (4 * mm)) & 0x000F000Fu;
+              d = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, p), xp[cc][4 * i + mm], d, false);
+            }
+          }
+          acc += (sz.x * 16777216.f) * d + sz.y * xs[cc];
         }
         acc = group_sum(acc, SH::LPR);
         if (c0 == 0 && rr < 2 * RM) gxu[rr] = acc;

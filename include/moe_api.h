@@ -254,6 +254,8 @@ int moe_chain_mix_rmsnorm(const void* mix_d_f16, const int32_t* perm, int d, flo
  * The workspace (moe_engine_workspace_bytes) must be zero-filled before its
  * first use. Consecutive calls on one workspace must be ordered on one stream.
  */
+/* All four pointers are device addresses, 16-byte aligned (the engine stages
+ * them into LDS with 16-byte loads). */
 typedef struct moe_engine_layer {
   const void* router;      /* fp16 [E][d] (the layer's own router)              */
   const void* head;        /* fp16 [E][d] prerouter head, or NULL               */

@@ -182,7 +182,9 @@ struct Shape {
   static constexpr int O_YL = O_ADV + NSEGX * R * 4;                // [RR][NX] f32
   static constexpr int O_RED = (O_YL + RR * NX * 4 + 63) / 64 * 64; // [NT] f64 reduction
   static constexpr int O_MISC = O_RED + NT * 8;                     // small ints / floats
-  static constexpr int LDS_BYTES = O_MISC + 2048;
+  static constexpr int O_MD = O_MISC + 2048;                        // [D] f16 mixing scales
+  static constexpr int O_MP = O_MD + kb(D * 2);                     // [D] i32 mixing permutation
+  static constexpr int LDS_BYTES = O_MP + kb(D * 4);
 };
 
 struct Seg {
@@ -199,13 +201,15 @@ struct Route {
   float w[32];
   int segok[4];
   float segw[4];
+  int lg_gate[4], lg_up[4], lg_down[4];  // the segment's adapter on that projection is applied
+  float dsc[4];          // segw * lora_scale where the down adapter is applied, else 0
   moe_bundle segbd[4];   // the segments' bundles, copied from the slot table
 };
 
 struct Misc {
   int nseg;
   int abort;
-  int gu_step, dn_step, rt_step, hd_step;  // the step whose weights each LDS region holds
+  int gu_step, dn_step, rt_step, hd_step, mix_step;  // the step whose data each LDS region holds
   int pidx[32];
   float pw[32];
   Seg seg[4];
@@ -441,7 +445,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 
   if (threadIdx.x == 0) {
     mi->abort = 0;
-    mi->gu_step = mi->dn_step = mi->rt_step = mi->hd_step = -1;
+    mi->gu_step = mi->dn_step = mi->rt_step = mi->hd_step = mi->mix_step = -1;
     mi->rt[0].step = mi->rt[1].step = -1;
     if ((int)xcc_id() != x) {  // the work split relies on blockIdx % 8 == XCD
       if (a.status) atomicOr(a.status, MOE_STATUS_ENGINE_ABORT);
@@ -569,6 +573,12 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       return reinterpret_cast<const __half*>(A) + (size_t)kk * IE + ec;
     });
   };
+  auto stage_mix = [&](const moe_engine_layer& L, Waves ws) {  // mixing scales and permutation
+    const char* md = reinterpret_cast<const char*>(L.mix_d);
+    const char* mp = reinterpret_cast<const char*>(L.mix_perm);
+    stage(smem + SH::O_MD, D * 2 / 16, ws, [&](int i) { return md + (size_t)i * 16; });
+    stage(smem + SH::O_MP, D * 4 / 16, ws, [&](int i) { return mp + (size_t)i * 16; });
+  };
   auto stage_rows = [&](int off, const void* W, Waves ws) {  // router or head rows of this workgroup
     const __half* Wh = reinterpret_cast<const __half*>(W);
     stage(smem + off, SH::HRX * (D / 8), ws, [&](int i) {
@@ -586,8 +596,15 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       const bool bad = k < K && (e < 0 || e >= E);
       const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
       Rt.segok[q] = slot >= 0;
-      if (slot >= 0) Rt.segbd[q] = a.bundles[(size_t)lay * a.n_slots + slot];
+      moe_bundle b{};
+      if (slot >= 0) b = a.bundles[(size_t)lay * a.n_slots + slot];
+      Rt.segbd[q] = b;
       Rt.segw[q] = k < K ? Rt.w[k] : 1.f;
+      const bool lora = slot >= 0 && a.r > 0;
+      Rt.lg_gate[q] = lora && b.gate.lora_a && b.gate.lora_b;
+      Rt.lg_up[q] = lora && b.up.lora_a && b.up.lora_b;
+      Rt.lg_down[q] = lora && b.down.lora_a && b.down.lora_b;
+      Rt.dsc[q] = Rt.lg_down[q] ? Rt.segw[q] * a.lora_scale : 0.f;
       if (m == 0 && a.status) {
         if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
         else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
@@ -670,6 +687,12 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       __syncthreads();
       block_rmsnorm_to_x<SH>(r0, xq, xh, red);
     } else {
+      // the layer's mixing data: staged ahead by waves 4-7, else now
+      if (wave >= kStageW0) dma_wait();
+      if (mi->mix_step != s) {
+        stage_mix(LY, kAll);
+        dma_wait();
+      }
       if (s == 0) {
         if (poller)
           for (int j = threadIdx.x; j < D; j += NPT) r0[j] = a.r_state[j];
@@ -687,10 +710,11 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           for (int j = threadIdx.x; j < D; j += NPT) r0[j] = (float)((double)xi[j] + (double)r0[j] * inv);
         __syncthreads();
       }
-      if (poller) {
-        const __half* md = reinterpret_cast<const __half*>(LY.mix_d);
-        for (int j = threadIdx.x; j < D; j += NPT) {
-          const int p = LY.mix_perm[j];
+      {
+        const __half* md = reinterpret_cast<const __half*>(smem + SH::O_MD);
+        const int* mp = reinterpret_cast<const int*>(smem + SH::O_MP);
+        for (int j = threadIdx.x; j < D; j += NT) {
+          const int p = mp[j];
           const float v = (p >= 0 && p < D) ? r0[p] : 0.f;
           r1[j] = fmaf(__half2float(md[j]), v, r0[j]);
         }
@@ -751,9 +775,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int ar = m + NM * qa;
         if (ar >= nseg * 2 * R) continue;
         const int q = ar / (2 * R), rr = ar % (2 * R);
-        const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
-        const bool has = b && (rr < R ? (b->gate.lora_a && b->gate.lora_b)
-                                      : (b->up.lora_a && b->up.lora_b));
+        const bool has = rr < R ? Rt.lg_gate[q] : Rt.lg_up[q];
         const float v = has ? wave_dot_h<SH>(arow + (size_t)qa * D, xh) : 0.f;
         if (lane == 0) st_tag(AV + q * 2 * R + rr, tag, v);
       }
@@ -841,6 +863,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const moe_engine_layer L1 = a.layers[f1.lay];
         if (f1.own) stage_rows(SH::O_RT, L1.router, kStageW);
         if (f1.head) stage_rows(SH::O_HD, L1.head, kStageW);
+        if (a.mode == 1) stage_mix(L1, kStageW);
         if (!f1.own) {  // routing known ahead; its weights are staged in its own step
           Route& R1 = mi->rt[par ^ 1];
           if (!route_from_pred(R1, f1.t, f1.N, f1.lay, s + 1)) break;
@@ -848,6 +871,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         if (threadIdx.x == 0) {
           if (f1.own) mi->rt_step = s + 1;
           if (f1.head) mi->hd_step = s + 1;
+          if (a.mode == 1) mi->mix_step = s + 1;
         }
       }
     }
@@ -865,17 +889,16 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int i = threadIdx.x;
         const int lr = m * RM + i;
         const int q = row_seg(lr);
-        const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
         float hv = 0.f;
-        if (b) {
+        if (Rt.segok[q]) {
           float gg = gxu[i], uu = gxu[RM + i];
-          if (b->gate.lora_a && b->gate.lora_b) {
+          if (Rt.lg_gate[q]) {
             float s2 = 0.f;
             for (int kk = 0; kk < R; ++kk)
               s2 = fmaf(__half2float(bgu[(size_t)i * R + kk]), av[q * 2 * R + kk], s2);
             gg = fmaf(a.lora_scale, s2, gg);
           }
-          if (b->up.lora_a && b->up.lora_b) {
+          if (Rt.lg_up[q]) {
             float s2 = 0.f;
             for (int kk = 0; kk < R; ++kk)
               s2 = fmaf(__half2float(bgu[(size_t)(RM + i) * R + kk]), av[q * 2 * R + R + kk], s2);
@@ -894,9 +917,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int q = p / R, kk = p % R;
         const int lo = max(m * RM, mi->seg[q].col0);
         const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
-        const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
         float acc = 0.f;
-        if (b && b->down.lora_a && b->down.lora_b && lo < hi) {
+        if (Rt.lg_down[q] && lo < hi) {
           const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
           for (int lr2 = lo; lr2 < hi; ++lr2) {
             const int ec = mi->seg[q].i0 + (lr2 - mi->seg[q].col0);
@@ -969,11 +991,10 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           for (int cc = part; cc < LPRD; cc += 8) acc += dp[jj * 32 + cc];
           for (int term = part; term < nseg * R; term += 8) {
             const int q = term / R, kk = term % R;
-            const moe_bundle* b = Rt.segok[q] ? &Rt.segbd[q] : nullptr;
-            if (!b || !b->down.lora_a || !b->down.lora_b) continue;
-            acc = fmaf(Rt.segw[q] * a.lora_scale *
-                           __half2float(bd[((size_t)jj * SH::NSEGX + q) * R + kk]),
-                       adv[q * R + kk], acc);
+            const float sc = Rt.dsc[q];
+            if (sc != 0.f)
+              acc = fmaf(sc * __half2float(bd[((size_t)jj * SH::NSEGX + q) * R + kk]), adv[q * R + kk],
+                         acc);
           }
         }
         acc = group_sum(acc, 8);

@@ -218,40 +218,50 @@ struct Misc {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.f + expf(-z)); }
 
-// Softmax-top-k of E <= 256 fp32 logits in LDS, by the workgroup (every
-// thread calls it; three barriers).  Logit i gets a 64-bit key (order key of
-// the value, then ~index: ties go to the lower index); its rank is the count
-// of larger keys, from two half-counts by threads i and i + 256 (eight
-// independent compares per step; the key array is padded with zeros, which
-// no real key is below).  The K smallest ranks land in `sorted`, and wave 0
-// forms the weights exactly as the one-wave top-k does.
-// keys: LDS [256] u64; part: LDS [256] int; sorted: LDS [32] u64.
+// Softmax-top-k of the E <= 256 logits in l (512 threads; K <= 32 <= E), ties
+// to the lower index: key = order(l) << 32 | ~index, largest keys first.
+// Stage 1 ranks each group of 64 keys within its group (two waves per group,
+// 32 comparisons a lane); a group's K best become candidates. Stage 2 ranks
+// the 4K candidates among themselves: every key larger than one of the
+// overall top K is itself in its group's top K, so for those keys the rank
+// among the candidates is the overall rank, and every other key has at least
+// K larger candidates. Scratch: keys [256], part [256], cand [128], sorted [32].
 __device__ void block_topk(const float* l, int E, int K, int32_t* idx_out, float* w_out,
-                           uint64_t* keys, int* part, uint64_t* sorted) {
+                           uint64_t* keys, int* part, uint64_t* cand, uint64_t* sorted) {
   const int tid = threadIdx.x;
   const int i = tid & 255, half = tid >> 8;
-  const int E16 = (E + 15) & ~15;
-  if (tid < E16)
+  const int NC = 4 * K;
+  if (tid < 256)
     keys[tid] = tid < E ? ((uint64_t)topk_key(l[tid]) << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)tid)
-                        : 0ull;
+                        : 0ull;  // below every real key
+  else if (tid - 256 < NC)
+    cand[tid - 256] = 0ull;
   __syncthreads();
-  int rank = 0;
-  uint64_t mine = 0;
-  if (i < E) {
-    mine = keys[i];
-    const int j0 = half * (E16 >> 1), j1 = j0 + (E16 >> 1);
-    for (int j = j0; j < j1; j += 8) {
+  const uint64_t mine = keys[i];
+  {
+    const int j0 = (i & ~63) + half * 32;  // uniform across the wave
+    int rank = 0;
+#pragma unroll
+    for (int j = j0; j < j0 + 32; j += 8) {
       const uint64_t k0 = keys[j], k1 = keys[j + 1], k2 = keys[j + 2], k3 = keys[j + 3];
       const uint64_t k4 = keys[j + 4], k5 = keys[j + 5], k6 = keys[j + 6], k7 = keys[j + 7];
       rank += (k0 > mine) + (k1 > mine) + (k2 > mine) + (k3 > mine) + (k4 > mine) + (k5 > mine) +
               (k6 > mine) + (k7 > mine);
     }
     if (half) part[i] = rank;
+    __syncthreads();
+    if (!half) {
+      rank += part[i];
+      if (rank < K) cand[(i >> 6) * K + rank] = mine;  // padding keys of a group share one slot
+    }
   }
   __syncthreads();
-  if (half == 0 && i < E) {
-    rank += part[i];
-    if (rank < K) sorted[rank] = mine;
+  if (tid < NC) {
+    const uint64_t me = cand[tid];
+    int rank = 0;
+    for (int j = 0; j < NC; j += 4)
+      rank += (cand[j] > me) + (cand[j + 1] > me) + (cand[j + 2] > me) + (cand[j + 3] > me);
+    if (rank < K) sorted[rank] = me;
   }
   __syncthreads();
   if (tid < 64) {
@@ -616,9 +626,10 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   // Softmax-top-k of the logits in lg (wave 0), then resolve_route.
   uint64_t* tk_keys = reinterpret_cast<uint64_t*>(lg + 256);          // [256] after the logits
   int* tk_part = reinterpret_cast<int*>(lg + 768);                    // [256]
-  uint64_t* tk_sorted = reinterpret_cast<uint64_t*>(red);             // [32]; red is free here
+  uint64_t* tk_cand = reinterpret_cast<uint64_t*>(red);               // [128]; red is free here
+  uint64_t* tk_sorted = tk_cand + 128;                                 // [32]
   auto compute_route = [&](Route& Rt, int lay, int step) {
-    block_topk(lg, E, K, Rt.idx, Rt.w, tk_keys, tk_part, tk_sorted);
+    block_topk(lg, E, K, Rt.idx, Rt.w, tk_keys, tk_part, tk_cand, tk_sorted);
     __syncthreads();
     mark(a, step, 15);
     resolve_route(Rt, lay, step);
@@ -1030,7 +1041,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         if (!poll_all<SH::MAXI_E>(E, htag, [&](int i) { return lh + i; },
                                   [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
           break;
-        block_topk(lg, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_sorted);
+        block_topk(lg, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_cand, tk_sorted);
       }
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part;
       if (!poll_all<(SH::RR * NX + NPT - 1) / NPT>(

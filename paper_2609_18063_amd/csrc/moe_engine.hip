@@ -664,6 +664,34 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       const int j = threadIdx.x + q * NPT;
       xi_next[q] = j < D ? a.xi[j] : 0.f;
     }
+  // The predicted routing of a step with a head is formed by one workgroup
+  // (g == step % NWG) one step later, between publishing its share of the
+  // next exchange and polling it, so that the top-k stays off the path every
+  // workgroup waits on. Pending: the step (or -1), its head logits and tag.
+  int pend_s = -1, pend_t = 0, pend_N = 0;
+  const uint64_t* pend_lh = nullptr;
+  uint32_t pend_htag = 0;
+  auto flush_pred = [&]() -> bool {
+    if (pend_s < 0) return true;
+    const int ps = pend_s;
+    pend_s = -1;
+    if (!poll_all<SH::MAXI_E>(E, pend_htag, [&](int i) { return pend_lh + i; },
+                              [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
+      return false;
+    block_topk(lg, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_cand, tk_sorted);
+    if ((int)threadIdx.x < K) {  // the lanes that wrote pidx / pw
+      const int i = threadIdx.x;
+      if (a.mode == 1) {
+        uint64_t* pw = pred_of(pend_t + 1, pend_N + 1);
+        st_tag(pw + i, pend_htag, __int_as_float(mi->pidx[i]));
+        st_tag(pw + K + i, pend_htag, mi->pw[i]);
+      }
+      if (a.pidx_rec) a.pidx_rec[(size_t)ps * K + i] = mi->pidx[i];
+      if (a.pw_rec) a.pw_rec[(size_t)ps * K + i] = mi->pw[i];
+    }
+    __syncthreads();
+    return true;
+  };
   for (int s = 0; s < a.n_steps && !mi->abort; ++s) {
     const uint32_t tag = base + (uint32_t)s + 1u;
     const int par = s & 1;
@@ -709,6 +737,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           for (int j = threadIdx.x; j < D; j += NPT) r0[j] = a.r_state[j];
         __syncthreads();
       } else {
+        if (!flush_pred()) break;
         uint64_t* rv = X + a.xo_rv + (size_t)(par ^ 1) * a.xs_rv;
         if (!poll_all<SH::MAXI_P>(D, tag - 1u, [&](int i) { return rv + i; },
                                   [&](int i, float v) { r0[i] = v; }, c, &mi->abort))
@@ -749,6 +778,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const float v = wave_dot_h<SH>(rtrow + (size_t)q * D, xh);
         if (lane == 0 && e < E) st_tag(lr + e, tag, v);
       }
+      if (!flush_pred()) break;
       mark(a, s, 12);
       if (!poll_all<SH::MAXI_E>(E, tag, [&](int i) { return lr + i; },
                                 [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
@@ -1023,25 +1053,18 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 
     mark(a, s, 14);
     // ---- S5: reduce the 8 XCD partials of this workgroup's rows ---------
-    // One workgroup per step also turns the head's logits into the predicted
-    // routing (top-k on a staging wave while the polling waves wait for the
-    // partials) and publishes it for the next token's consumer layer.
     {
-      const bool pred_wg = has_head && g == s % NWG && (a.mode == 1 || a.pidx_rec || a.pw_rec);
-      uint64_t* lh = nullptr;
-      uint32_t htag = 0;
-      if (pred_wg) {
+      if (has_head && g == s % NWG && (a.mode == 1 || a.pidx_rec || a.pw_rec)) {
+        pend_s = s;
+        pend_t = t;
+        pend_N = N;
         if (a.mode == 0) {
-          lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
-          htag = tag;
+          pend_lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
+          pend_htag = tag;
         } else {
-          lh = logh_of(t + 1, N + 1);
-          htag = (uint32_t)t + 2u;
+          pend_lh = logh_of(t + 1, N + 1);
+          pend_htag = (uint32_t)t + 2u;
         }
-        if (!poll_all<SH::MAXI_E>(E, htag, [&](int i) { return lh + i; },
-                                  [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
-          break;
-        block_topk(lg, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_cand, tk_sorted);
       }
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part;
       if (!poll_all<(SH::RR * NX + NPT - 1) / NPT>(
@@ -1062,20 +1085,12 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           if (s + 1 == a.n_steps) a.r_state[j] = rn;
         }
       }
-      if (pred_wg && (int)threadIdx.x < K) {
-        const int i = threadIdx.x;
-        if (a.mode == 1) {
-          uint64_t* pw = pred_of(t + 1, N + 1);
-          st_tag(pw + i, htag, __int_as_float(mi->pidx[i]));
-          st_tag(pw + K + i, htag, mi->pw[i]);
-        }
-        if (a.pidx_rec) a.pidx_rec[(size_t)s * K + i] = mi->pidx[i];
-        if (a.pw_rec) a.pw_rec[(size_t)s * K + i] = mi->pw[i];
-      }
       __syncthreads();
       mark(a, s, 9);
     }
   }
+
+  if (!mi->abort) flush_pred();  // the last step's prediction
 
   // ---- finish: wait for any staging still in flight; the last workgroup
   // moves the tag base past this launch ------------------------------------

@@ -376,9 +376,9 @@ int moe_stager_stats_get(const moe_stager* s, moe_stager_stats* out);
 #define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */
 #define MOE_PROF_ENGINE_PHASES 1 /* the next decode-engine launch writes, for
                                     workgroups 0, 7 and 255, the device wall clock
-                                    (wall_clock64) at 16 marks of every step into
+                                    (wall_clock64) at 24 marks of every step into
                                     start_event, read as a device uint64 array
-                                    [n_steps][3][16]; stop_event is unused */
+                                    [n_steps][3][24]; stop_event is unused */
 
 /*
  * Arm per-launch timing. For MOE_PROF_FFN_MAIN, the next launch of that

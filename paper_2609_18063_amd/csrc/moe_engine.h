@@ -27,7 +27,7 @@ struct EngineArgs {
   int32_t* pidx_rec;
   float* pw_rec;
   uint32_t* status;
-  uint64_t* phase_ts;            // profiling: [n_steps][3][10] wall-clock marks, or null
+  uint64_t* phase_ts;            // profiling: [n_steps][3][24] wall-clock marks, or null
   uint32_t* ctl;                 // workspace control words
   uint64_t* xw;                  // workspace exchange words
   // exchange-area offsets and per-parity strides (in 64-bit words)

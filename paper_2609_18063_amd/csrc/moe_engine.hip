@@ -85,7 +85,16 @@ __device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
       : "s"(lds), "v"(g)
       : "memory");
 }
-__device__ __forceinline__ void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// The compiler does not see the copies above as memory instructions, so the
+// builtin wait follows: it tells the compiler that nothing of its own is
+// outstanding either. Otherwise a wait it places for one of its own loads or
+// stores (a register reused right after a store, say) can land inside a copy
+// loop, where it drains every copy issued so far on each iteration.
+// simm16 0x0F70: vmcnt 0, expcnt and lgkmcnt unconstrained.
+__device__ __forceinline__ void dma_wait() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+}
 
 struct Ctl {
   uint32_t* ctl;      // [0] tag base, [1] finish counter, [2] abort
@@ -209,7 +218,7 @@ struct Route {
 struct Misc {
   int nseg;
   int abort;
-  int gu_step, dn_step, rt_step, hd_step, mix_step;  // the step whose data each LDS region holds
+  int rt_step, hd_step, mix_step;  // the step whose data each LDS region holds
   int pidx[32];
   float pw[32];
   Seg seg[4];
@@ -306,14 +315,8 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-// Sum of squares of v[0..D) in fp64 over the workgroup (two barriers).
-template <class SH>
-__device__ double block_sumsq(const float* v, double* red) {
-  double acc = 0.0;
-  for (int j = threadIdx.x; j < SH::D; j += NT) {
-    const double a = v[j];
-    acc += a * a;
-  }
+// Sum of one fp64 value per thread over the workgroup (two barriers).
+__device__ double block_sum_f64(double acc, double* red) {
   acc = wave_sum_f64(acc);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();
@@ -324,6 +327,42 @@ __device__ double block_sumsq(const float* v, double* red) {
   return tot;
 }
 
+// Sum of squares of v[0..D) in fp64 over the workgroup (two barriers).
+template <class SH>
+__device__ double block_sumsq(const float* v, double* red) {
+  static_assert(SH::D % NT == 0, "D is a multiple of the workgroup size");
+  double acc = 0.0;
+#pragma unroll
+  for (int q = 0; q < SH::D / NT; ++q) {
+    const double a = v[threadIdx.x + q * NT];
+    acc += a * a;
+  }
+  return block_sum_f64(acc, red);
+}
+
+// 1 / sqrt(m) in fp64 for m > 0: the fp32 estimate refined by two Newton
+// steps, within a few fp64 ulps (x is rounded to fp16 afterwards).
+__device__ __forceinline__ double rsqrt_f64(double m) {
+  double y = (double)rsqrtf((float)m);
+  y = y * (1.5 - 0.5 * m * y * y);
+  y = y * (1.5 - 0.5 * m * y * y);
+  return y;
+}
+
+// fp64 -> fp16 rounded once to nearest even: the value is first narrowed to
+// fp32 rounding to odd (truncated, last bit set when bits were dropped), and
+// an odd-rounded value with 13 spare bits rounds to fp16 as the exact one does.
+__device__ __forceinline__ __half f64_to_h(double d) {
+  float f = (float)d;
+  const double back = (double)f;
+  if (back != d) {
+    uint32_t u = __float_as_uint(f);
+    if (fabs(back) > fabs(d)) u -= 1u;  // rounded away from zero: step back
+    f = __uint_as_float(u | 1u);
+  }
+  return __float2half_rn(f);
+}
+
 // Position of input j in the pair order of x: inside each group of 8 the
 // halves run x0,x4,x1,x5,x2,x6,x3,x7, the order in which the nibbles of one
 // code dword pair up under a 0x000F000F mask at shifts 0, 4, 8, 12.
@@ -332,14 +371,31 @@ __device__ __forceinline__ int pair_pos(int j) {
   return (j & ~7) + (r < 4 ? 2 * r : 2 * (r - 4) + 1);
 }
 
+// x = fp16(v * rms(v)^-1) of the D values in vv (this thread's: v[tid + q NT]),
+// written to xh (natural order) and xq (pair order).
 template <class SH>
-__device__ void block_rmsnorm_to_x(const float* v, __half* xq, __half* xh, double* red) {
-  const double inv = 1.0 / sqrt(block_sumsq<SH>(v, red) / (double)SH::D + 1e-6);
-  for (int j = threadIdx.x; j < SH::D; j += NT) {
-    const __half h = __half(static_cast<_Float16>((double)v[j] * inv));
+__device__ __forceinline__ void rmsnorm_regs_to_x(const float (&vv)[SH::D / NT], double acc,
+                                                  __half* xq, __half* xh, double* red) {
+  const double inv = rsqrt_f64(block_sum_f64(acc, red) / (double)SH::D + 1e-6);
+#pragma unroll
+  for (int q = 0; q < SH::D / NT; ++q) {
+    const int j = threadIdx.x + q * NT;
+    const __half h = f64_to_h((double)vv[q] * inv);
     xh[j] = h;
     xq[pair_pos(j)] = h;
   }
+}
+
+template <class SH>
+__device__ void block_rmsnorm_to_x(const float* v, __half* xq, __half* xh, double* red) {
+  float vv[SH::D / NT];
+  double acc = 0.0;
+#pragma unroll
+  for (int q = 0; q < SH::D / NT; ++q) {
+    vv[q] = v[threadIdx.x + q * NT];
+    acc += (double)vv[q] * (double)vv[q];
+  }
+  rmsnorm_regs_to_x<SH>(vv, acc, xq, xh, red);
 }
 
 // fp16 row (D halves in LDS) . x (fp16 in LDS) by one wave; fp32 accumulate.
@@ -377,7 +433,7 @@ __device__ __forceinline__ void stage(char* dst, int nchunks, Waves ws, SrcF src
 
 // Phase timestamps for the profiling hook: thread 0 of workgroups 0, 7 and
 // 255 writes the constant-rate wall clock at up to 16 marks of every step.
-constexpr int kProfMarks = 16;
+constexpr int kProfMarks = 24;
 __device__ __forceinline__ void mark(const EngineArgs& a, int s, int k) {
   if (!a.phase_ts || threadIdx.x != 0) return;
   const int g = blockIdx.x;
@@ -455,7 +511,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 
   if (threadIdx.x == 0) {
     mi->abort = 0;
-    mi->gu_step = mi->dn_step = mi->rt_step = mi->hd_step = mi->mix_step = -1;
+    mi->rt_step = mi->hd_step = mi->mix_step = -1;
     mi->rt[0].step = mi->rt[1].step = -1;
     if ((int)xcc_id() != x) {  // the work split relies on blockIdx % 8 == XCD
       if (a.status) atomicOr(a.status, MOE_STATUS_ENGINE_ABORT);
@@ -598,27 +654,32 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   };
   // The slots of the XCD's segments under routing Rt.idx/w (threads < nseg,
   // wave 0); one barrier.
+  // Segment q of routing Rt: expert e (routed: id idx[k]; shared: E + k - K)
+  // with weight wk, resolved to its slot and bundle.
+  auto resolve_seg = [&](Route& Rt, int lay, int q, int e, float wk) {
+    const int k = mi->seg[q].k;
+    const bool bad = k < K && (e < 0 || e >= E);
+    const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
+    Rt.segok[q] = slot >= 0;
+    moe_bundle b{};
+    if (slot >= 0) b = a.bundles[(size_t)lay * a.n_slots + slot];
+    Rt.segbd[q] = b;
+    Rt.segw[q] = k < K ? wk : 1.f;
+    const bool lora = slot >= 0 && a.r > 0;
+    Rt.lg_gate[q] = lora && b.gate.lora_a && b.gate.lora_b;
+    Rt.lg_up[q] = lora && b.up.lora_a && b.up.lora_b;
+    Rt.lg_down[q] = lora && b.down.lora_a && b.down.lora_b;
+    Rt.dsc[q] = Rt.lg_down[q] ? Rt.segw[q] * a.lora_scale : 0.f;
+    if (m == 0 && a.status) {
+      if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
+      else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
+    }
+  };
   auto resolve_route = [&](Route& Rt, int lay, int step) {
     if ((int)threadIdx.x < nseg) {
       const int q = threadIdx.x;
       const int k = mi->seg[q].k;
-      const int e = k < K ? Rt.idx[k] : E + (k - K);
-      const bool bad = k < K && (e < 0 || e >= E);
-      const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
-      Rt.segok[q] = slot >= 0;
-      moe_bundle b{};
-      if (slot >= 0) b = a.bundles[(size_t)lay * a.n_slots + slot];
-      Rt.segbd[q] = b;
-      Rt.segw[q] = k < K ? Rt.w[k] : 1.f;
-      const bool lora = slot >= 0 && a.r > 0;
-      Rt.lg_gate[q] = lora && b.gate.lora_a && b.gate.lora_b;
-      Rt.lg_up[q] = lora && b.up.lora_a && b.up.lora_b;
-      Rt.lg_down[q] = lora && b.down.lora_a && b.down.lora_b;
-      Rt.dsc[q] = Rt.lg_down[q] ? Rt.segw[q] * a.lora_scale : 0.f;
-      if (m == 0 && a.status) {
-        if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
-        else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
-      }
+      resolve_seg(Rt, lay, q, k < K ? Rt.idx[k] : E + (k - K), k < K ? Rt.w[k] : 1.f);
     }
     if (threadIdx.x == 0) Rt.step = step;
     __syncthreads();
@@ -650,6 +711,45 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       return false;
     resolve_route(Rt, lay, step);
     return true;
+  };
+  // The same by one wave alone (no workgroup barrier): lane u < 2K polls word
+  // u of the prediction (ids, then weights), lanes q < nseg resolve segment q.
+  // The caller's next barrier hands Rt to the workgroup. On a timeout or an
+  // abort it raises the abort flag the next poll_all reports.
+  auto route_from_pred_wave = [&](Route& Rt, int t, int N, int lay, int step) {
+    const uint64_t* pw = pred_of(t, N);
+    uint64_t v = 0;
+    bool ok = true;
+    if (lane < 2 * K) {
+      long spin = 0;
+      for (;;) {
+        v = ld_tag(pw + lane);
+        if ((uint32_t)(v >> 32) == (uint32_t)t + 1u) break;
+        if (++spin > kSpinMax) {
+          if (c.status) atomicOr(c.status, MOE_STATUS_ENGINE_ABORT);
+          __hip_atomic_store(&c.ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ok = false;
+          break;
+        }
+        if ((spin & 63) == 0 && ld_u32(&c.ctl[2])) {
+          ok = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    if (__any(!ok)) {
+      if (lane == 0) mi->abort = 1;
+      return;
+    }
+    const int word = (int)(uint32_t)v;
+    if (lane < K) Rt.idx[lane] = word;
+    else if (lane < 2 * K) Rt.w[lane - K] = __int_as_float(word);
+    const int kq = lane < nseg ? mi->seg[lane].k : 0;
+    const int ek = __shfl(word, kq < K ? kq : 0, kWave);
+    const float wk = __int_as_float(__shfl(word, kq < K ? K + kq : 0, kWave));
+    if (lane < nseg) resolve_seg(Rt, lay, lane, kq < K ? ek : E + (kq - K), wk);
+    if (lane == 0) Rt.step = step;
   };
   // the head logits that route layer N at token t (written at token t - 1)
   auto logh_of = [&](int t, int N) {
@@ -732,35 +832,50 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         stage_mix(LY, kAll);
         dma_wait();
       }
+      // a pending prediction; then wave 4 routes the next step where a
+      // prediction gives it (published at least a step ago) while waves 0-3
+      // poll the residual
+      if (!flush_pred()) break;
+      mark(a, s, 16);
+      if (wave == kStageW0 && s + 1 < a.n_steps) {
+        const StepInfo f1 = step_info(a, s + 1);
+        if (f1.ok && !f1.own) route_from_pred_wave(mi->rt[par ^ 1], f1.t, f1.N, f1.lay, s + 1);
+      }
       if (s == 0) {
         if (poller)
           for (int j = threadIdx.x; j < D; j += NPT) r0[j] = a.r_state[j];
         __syncthreads();
       } else {
-        if (!flush_pred()) break;
         uint64_t* rv = X + a.xo_rv + (size_t)(par ^ 1) * a.xs_rv;
         if (!poll_all<SH::MAXI_P>(D, tag - 1u, [&](int i) { return rv + i; },
                                   [&](int i, float v) { r0[i] = v; }, c, &mi->abort))
           break;
       }
+      mark(a, s, 17);
       if (N == 0) {  // token start: r = xi + rmsnorm(r)
-        const double inv = 1.0 / sqrt(block_sumsq<SH>(r0, red) / (double)D + 1e-6);
+        const double inv = rsqrt_f64(block_sumsq<SH>(r0, red) / (double)D + 1e-6);
         const float* xi = a.xi + (size_t)(s / a.L) * D;
         if (poller)
           for (int j = threadIdx.x; j < D; j += NPT) r0[j] = (float)((double)xi[j] + (double)r0[j] * inv);
         __syncthreads();
       }
-      {
+      {  // r1 = r + d * r[perm] (kept in registers too), then x = rmsnorm(r1)
         const __half* md = reinterpret_cast<const __half*>(smem + SH::O_MD);
         const int* mp = reinterpret_cast<const int*>(smem + SH::O_MP);
-        for (int j = threadIdx.x; j < D; j += NT) {
+        float vv[SH::D / NT];
+        double acc = 0.0;
+#pragma unroll
+        for (int q = 0; q < SH::D / NT; ++q) {
+          const int j = threadIdx.x + q * NT;
           const int p = mp[j];
           const float v = (p >= 0 && p < D) ? r0[p] : 0.f;
-          r1[j] = fmaf(__half2float(md[j]), v, r0[j]);
+          vv[q] = fmaf(__half2float(md[j]), v, r0[j]);
+          r1[j] = vv[q];
+          acc += (double)vv[q] * (double)vv[q];
         }
+        mark(a, s, 18);
+        rmsnorm_regs_to_x<SH>(vv, acc, xq, xh, red);
       }
-      __syncthreads();
-      block_rmsnorm_to_x<SH>(r1, xq, xh, red);
     }
     __syncthreads();
     if (g == 0 && a.x_rec && poller)
@@ -795,16 +910,15 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     }
 
     mark(a, s, 2);
-    // ---- S2: weights of this step (unless staged ahead), then compute ----
-    // Staged now: gate/up and head rows by waves 0-3 (needed at once), down by
-    // waves 4-7 (needed from S3 on). Staged ahead: waves 4-7 wait for it here.
+    // ---- S2: expert weights of this step, then compute ------------------
+    // Gate/up rows (and head rows, unless staged ahead) by waves 0-3, needed
+    // at once; down rows by waves 4-7, needed from S3 on.
     {
-      const bool gu_now = mi->gu_step != s, dn_now = mi->dn_step != s;
-      const bool hd_now = has_head && mi->hd_step != s;
-      if (gu_now) stage_gu(Rt, kPollW);
-      if (hd_now) stage_rows(SH::O_HD, LY.head, kPollW);
-      if (dn_now) stage_dn(Rt, kStageW);
-      if (wave < kStageW0 ? (gu_now || hd_now) : !dn_now) dma_wait();
+      dma_wait();  // nothing outstanding here: keeps the copy loops free of waits
+      stage_gu(Rt, kPollW);
+      if (has_head && mi->hd_step != s) stage_rows(SH::O_HD, LY.head, kPollW);
+      stage_dn(Rt, kStageW);
+      if (wave < kStageW0) dma_wait();
       __syncthreads();
     }
 
@@ -894,21 +1008,20 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     __syncthreads();
 
     mark(a, s, 4);
-    // ---- ahead: the next step's router / head rows, and for a step routed
-    // by a prediction, its routing and its gate/up weights ----------------
+    // ---- ahead: the next step's router / head rows and mixing data --------
+    // (expert weights are staged in their own step: staging them here delays
+    // the exchanges queued behind the copies)
     if (wave >= kStageW0) dma_wait();  // this step's down weights (read from S3 on)
-    int nxt_dn = -1;  // the next step, if its routing is known here
     if (s + 1 < a.n_steps) {
       const StepInfo f1 = step_info(a, s + 1);
       if (f1.ok) {
         const moe_engine_layer L1 = a.layers[f1.lay];
+        // every pointer arrives before the first copy is issued (a wait for a
+        // later one would also drain the copies issued before it)
+        asm volatile("" ::"v"(L1.router), "v"(L1.head), "v"(L1.mix_d), "v"(L1.mix_perm));
         if (f1.own) stage_rows(SH::O_RT, L1.router, kStageW);
         if (f1.head) stage_rows(SH::O_HD, L1.head, kStageW);
         if (a.mode == 1) stage_mix(L1, kStageW);
-        if (!f1.own) {  // routing known ahead; its weights are staged in its own step
-          Route& R1 = mi->rt[par ^ 1];
-          if (!route_from_pred(R1, f1.t, f1.N, f1.lay, s + 1)) break;
-        }
         if (threadIdx.x == 0) {
           if (f1.own) mi->rt_step = s + 1;
           if (f1.head) mi->hd_step = s + 1;
@@ -1045,11 +1158,6 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     __syncthreads();
 
     mark(a, s, 7);
-    // ---- ahead: the down weights of a step routed ahead -------------------
-    if (nxt_dn >= 0) {
-      stage_dn(mi->rt[par ^ 1], kStageW);
-      if (threadIdx.x == 0) mi->dn_step = nxt_dn;
-    }
 
     mark(a, s, 14);
     // ---- S5: reduce the 8 XCD partials of this workgroup's rows ---------

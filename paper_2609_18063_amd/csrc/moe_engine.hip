@@ -182,8 +182,8 @@ struct Shape {
   static constexpr int O_R0 = O_XH + D * 2;                         // [D] f32
   static constexpr int O_R1 = O_R0 + D * 4;                         // [D] f32
   static constexpr int O_LG = O_R1 + D * 4;                         // [1024] f32 logits
-  static constexpr int O_HX = O_LG + 1024 * 4;                      // [GXX] f32 h of the XCD, pad32
-  static constexpr int O_HL = O_HX + (GXX + GXX / 32) * 4;          // [RMX] f32 own h
+  static constexpr int O_HX = O_LG + 1024 * 4;                      // [GXX/32][36] f32 h of the XCD
+  static constexpr int O_HL = O_HX + GXX / 32 * 36 * 4;             // [RMX] f32 own h
   static constexpr int O_GXU = O_HL + RMX * 4;                      // [2*RMX] f32
   static constexpr int O_DP = O_GXU + 2 * RMX * 4;                  // [DR][32] f32 down partials
   static constexpr int O_AV = O_DP + DR * 32 * 4;                   // [NSEGX][2R] f32
@@ -292,7 +292,10 @@ typedef _Float16 hv2 __attribute__((ext_vector_type(2)));
 // LDS index of element i of a vector that lanes read in 32-element chunks
 // (lane l reading chunk l): one pad word per chunk puts the 64 lanes' reads of
 // the same element in 64 different banks.
-__device__ __forceinline__ int pad32(int i) { return i + (i >> 5); }
+// Position of h entry i in LDS: each 32-entry chunk (one down lane's
+// columns) starts 36 floats after the previous, so that lanes of different
+// chunks read it with 16-byte loads on disjoint banks.
+__device__ __forceinline__ int hx_pos(int i) { return (i >> 5) * 36 + (i & 31); }
 
 // fp64 sum over the wave (DPP on the two 32-bit halves of each step's operand)
 template <int CTRL, int ROWMASK = 0xf>
@@ -450,11 +453,12 @@ struct StepInfo {
   bool ok;    // the layer index is valid
 };
 
+template <int MODE>
 __device__ __forceinline__ StepInfo step_info(const EngineArgs& a, int s) {
   StepInfo f;
   f.t = 0;
   f.N = 0;
-  if (a.mode == 0) {
+  if (MODE == 0) {
     f.lay = a.step_layer[s];
     f.own = true;
   } else {
@@ -464,11 +468,13 @@ __device__ __forceinline__ StepInfo step_info(const EngineArgs& a, int s) {
     f.own = f.t == 0 || f.N < a.consumer_lo || f.N > a.consumer_hi;
   }
   f.ok = f.lay >= 0 && f.lay < a.n_table_layers;
-  f.head = f.ok && a.layers[f.lay].head != nullptr && (a.mode == 0 || f.N + 1 < a.L);
+  f.head = f.ok && a.layers[f.lay].head != nullptr && (MODE == 0 || f.N + 1 < a.L);
   return f;
 }
 
-template <class SH>
+// MODE 0: independent single-token steps; MODE 1: the decode chain. One
+// kernel per mode keeps each loop body small enough for the instruction cache.
+template <class SH, int MODE>
 __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   constexpr int D = SH::D, IE = SH::IE, R = SH::R;
@@ -758,7 +764,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 
   uint64_t* const X = a.xw;
   float xi_next[SH::MAXI_P];
-  if (a.mode == 0 && poller)
+  if (MODE == 0 && poller)
 #pragma unroll
     for (int q = 0; q < SH::MAXI_P; ++q) {
       const int j = threadIdx.x + q * NPT;
@@ -781,7 +787,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     block_topk(lg, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_cand, tk_sorted);
     if ((int)threadIdx.x < K) {  // the lanes that wrote pidx / pw
       const int i = threadIdx.x;
-      if (a.mode == 1) {
+      if (MODE == 1) {
         uint64_t* pw = pred_of(pend_t + 1, pend_N + 1);
         st_tag(pw + i, pend_htag, __int_as_float(mi->pidx[i]));
         st_tag(pw + K + i, pend_htag, mi->pw[i]);
@@ -795,7 +801,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   for (int s = 0; s < a.n_steps && !mi->abort; ++s) {
     const uint32_t tag = base + (uint32_t)s + 1u;
     const int par = s & 1;
-    const StepInfo f = step_info(a, s);
+    const StepInfo f = step_info<MODE>(a, s);
     if (!f.ok) {  // uniform across the grid: every workgroup stops
       if (g == 0 && threadIdx.x == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
       break;
@@ -807,7 +813,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 
     mark(a, s, 0);
     // ---- S0: layer input (global reads by the polling waves only) --------
-    if (a.mode == 0) {
+    if (MODE == 0) {
       if (poller) {
 #pragma unroll
         for (int q = 0; q < SH::MAXI_P; ++q) {
@@ -838,7 +844,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       if (!flush_pred()) break;
       mark(a, s, 16);
       if (wave == kStageW0 && s + 1 < a.n_steps) {
-        const StepInfo f1 = step_info(a, s + 1);
+        const StepInfo f1 = step_info<MODE>(a, s + 1);
         if (f1.ok && !f1.own) route_from_pred_wave(mi->rt[par ^ 1], f1.t, f1.N, f1.lay, s + 1);
       }
       if (s == 0) {
@@ -939,7 +945,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     if (has_head) {
       uint64_t* lh;
       uint32_t htag;
-      if (a.mode == 0) {
+      if (MODE == 0) {
         lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
         htag = tag;
       } else {
@@ -1013,7 +1019,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     // the exchanges queued behind the copies)
     if (wave >= kStageW0) dma_wait();  // this step's down weights (read from S3 on)
     if (s + 1 < a.n_steps) {
-      const StepInfo f1 = step_info(a, s + 1);
+      const StepInfo f1 = step_info<MODE>(a, s + 1);
       if (f1.ok) {
         const moe_engine_layer L1 = a.layers[f1.lay];
         // every pointer arrives before the first copy is issued (a wait for a
@@ -1021,11 +1027,11 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         asm volatile("" ::"v"(L1.router), "v"(L1.head), "v"(L1.mix_d), "v"(L1.mix_perm));
         if (f1.own) stage_rows(SH::O_RT, L1.router, kStageW);
         if (f1.head) stage_rows(SH::O_HD, L1.head, kStageW);
-        if (a.mode == 1) stage_mix(L1, kStageW);
+        if (MODE == 1) stage_mix(L1, kStageW);
         if (threadIdx.x == 0) {
           if (f1.own) mi->rt_step = s + 1;
           if (f1.head) mi->hd_step = s + 1;
-          if (a.mode == 1) mi->mix_step = s + 1;
+          if (MODE == 1) mi->mix_step = s + 1;
         }
       }
     }
@@ -1038,49 +1044,60 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
               nseg * 2 * R, tag, [&](int i) { return AV + i; }, [&](int i, float v) { av[i] = v; }, c,
               &mi->abort))
         break;
+      mark(a, s, 19);
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
-      if ((int)threadIdx.x < RM) {
-        const int i = threadIdx.x;
+      // 16 lanes per row: the LoRA-B terms of gate and up, then a DPP sum
+      static_assert(SH::RMX * 16 <= NT, "one 16-lane group per gate/up row");
+      if ((int)threadIdx.x < RM * 16) {
+        const int i = threadIdx.x >> 4, kl = threadIdx.x & 15;
         const int lr = m * RM + i;
         const int q = row_seg(lr);
-        float hv = 0.f;
-        if (Rt.segok[q]) {
-          float gg = gxu[i], uu = gxu[RM + i];
-          if (Rt.lg_gate[q]) {
-            float s2 = 0.f;
-            for (int kk = 0; kk < R; ++kk)
-              s2 = fmaf(__half2float(bgu[(size_t)i * R + kk]), av[q * 2 * R + kk], s2);
-            gg = fmaf(a.lora_scale, s2, gg);
-          }
-          if (Rt.lg_up[q]) {
-            float s2 = 0.f;
-            for (int kk = 0; kk < R; ++kk)
-              s2 = fmaf(__half2float(bgu[(size_t)(RM + i) * R + kk]), av[q * 2 * R + R + kk], s2);
-            uu = fmaf(a.lora_scale, s2, uu);
-          }
-          hv = silu(gg) * uu;
+        const bool ok = Rt.segok[q], lgg = ok && Rt.lg_gate[q], lgu = ok && Rt.lg_up[q];
+        float sg = 0.f, su = 0.f;
+        for (int kk = kl; kk < R; kk += 16) {
+          if (lgg) sg = fmaf(__half2float(bgu[(size_t)i * R + kk]), av[q * 2 * R + kk], sg);
+          if (lgu) su = fmaf(__half2float(bgu[(size_t)(RM + i) * R + kk]), av[q * 2 * R + R + kk], su);
         }
-        st_tag(HV + lr, tag, hv);
-        hl[i] = hv;
+        sg = group_sum(sg, 16);
+        su = group_sum(su, 16);
+        if (kl == 0) {
+          float hv = 0.f;
+          if (ok) {
+            const float gg = lgg ? fmaf(a.lora_scale, sg, gxu[i]) : gxu[i];
+            const float uu = lgu ? fmaf(a.lora_scale, su, gxu[RM + i]) : gxu[RM + i];
+            hv = silu(gg) * uu;
+          }
+          st_tag(HV + lr, tag, hv);
+          hl[i] = hv;
+        }
       }
       __syncthreads();
+      mark(a, s, 20);
       // partial a_d[q][kk] over this workgroup's rows of segment q -> ADP
       uint64_t* ADP = X + a.xo_adp + (size_t)par * a.xs_adp +
                       ((size_t)x * NM + m) * SH::NSEGX * R;
-      for (int p = threadIdx.x; p < nseg * R; p += NT) {
-        const int q = p / R, kk = p % R;
-        const int lo = max(m * RM, mi->seg[q].col0);
-        const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
-        float acc = 0.f;
-        if (Rt.lg_down[q] && lo < hi) {
-          const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
-          for (int lr2 = lo; lr2 < hi; ++lr2) {
-            const int ec = mi->seg[q].i0 + (lr2 - mi->seg[q].col0);
-            acc = fmaf(__half2float(adm[((size_t)kk * SH::NSEGX + q) * 32 + (ec - e0)]),
-                       hl[lr2 - m * RM], acc);
+      // 16 lanes per term (q, kk), rows dealt over the lanes, then a DPP sum
+      static_assert(SH::NSEGX * SH::R * 16 <= NT, "one 16-lane group per down-LoRA term");
+      {
+        const int p = threadIdx.x >> 4, sub = threadIdx.x & 15;
+        if (p < SH::NSEGX * R) {  // whole 16-lane groups
+          float acc = 0.f;
+          if (p < nseg * R) {
+            const int q = p / R, kk = p % R;
+            const int lo = max(m * RM, mi->seg[q].col0);
+            const int hi = min(m * RM + RM, mi->seg[q].col0 + mi->seg[q].len);
+            if (Rt.lg_down[q] && lo < hi) {
+              const int e0 = (mi->seg[q].i0 + (lo - mi->seg[q].col0)) & ~7;
+              for (int lr2 = lo + sub; lr2 < hi; lr2 += 16) {
+                const int ec = mi->seg[q].i0 + (lr2 - mi->seg[q].col0);
+                acc = fmaf(__half2float(adm[((size_t)kk * SH::NSEGX + q) * 32 + (ec - e0)]),
+                           hl[lr2 - m * RM], acc);
+              }
+            }
           }
+          acc = group_sum(acc, 16);
+          if (sub == 0 && p < nseg * R) st_tag(ADP + p, tag, acc);
         }
-        st_tag(ADP + p, tag, acc);
       }
     }
 
@@ -1089,7 +1106,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     {
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
       if (!poll_all<(SH::GXX + NPT - 1) / NPT>(GX, tag, [&](int i) { return HV + i; },
-                                              [&](int i, float v) { hx[pad32(i)] = v; }, c, &mi->abort))
+                                              [&](int i, float v) { hx[hx_pos(i)] = v; }, c, &mi->abort))
         break;
       // a_d[q][kk] = sum of the 32 members' partials
       {
@@ -1117,12 +1134,18 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         qseg = row_seg(ch * 32);
         wseg = Rt.segok[qseg] ? Rt.segw[qseg] : 0.f;
         egrp = (mi->seg[qseg].i0 + (ch * 32 - mi->seg[qseg].col0)) / 64;
+        const float4* hp = reinterpret_cast<const float4*>(hx + ch * 36);
 #pragma unroll
-        for (int e = 0; e < 32; ++e) {
-          hv[e] = hx[pad32(ch * 32 + e)];
-          hsum += hv[e];
+        for (int e4 = 0; e4 < 8; ++e4) {
+          const float4 v4 = hp[e4];
+          hv[4 * e4] = v4.x;
+          hv[4 * e4 + 1] = v4.y;
+          hv[4 * e4 + 2] = v4.z;
+          hv[4 * e4 + 3] = v4.w;
+          hsum += (v4.x + v4.y) + (v4.z + v4.w);
         }
       }
+      mark(a, s, 21);
       for (int rg = wave; rg * RPID < SH::DR; rg += NWV) {
         const int jj = rg * RPID + sub;
         if (active && jj < SH::DR) {
@@ -1135,6 +1158,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
       }
       __syncthreads();
+      mark(a, s, 22);
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part + (size_t)x * D;
       // 8 threads per row: chunk partials and LoRA-B terms, then a DPP sum
       for (int b0 = 0; b0 < SH::DR * 8; b0 += NT) {
@@ -1162,11 +1186,11 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     mark(a, s, 14);
     // ---- S5: reduce the 8 XCD partials of this workgroup's rows ---------
     {
-      if (has_head && g == s % NWG && (a.mode == 1 || a.pidx_rec || a.pw_rec)) {
+      if (has_head && g == s % NWG && (MODE == 1 || a.pidx_rec || a.pw_rec)) {
         pend_s = s;
         pend_t = t;
         pend_N = N;
-        if (a.mode == 0) {
+        if (MODE == 0) {
           pend_lh = X + a.xo_loghm + (size_t)par * a.xs_logr;
           pend_htag = tag;
         } else {
@@ -1184,7 +1208,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         const int jr = threadIdx.x, j = g * SH::RR + jr;
         float y = 0.f;
         for (int xx = 0; xx < NX; ++xx) y += yl[jr * NX + xx];
-        if (a.mode == 0) {
+        if (MODE == 0) {
           a.y[(size_t)s * D + j] = y;
         } else {
           const float rn = r1[j] + y;
@@ -1218,19 +1242,24 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
 using ShapeMoe35b = Shape<2048, 512, 16, 18, 576, 1, 2>;
 using ShapeTiny = Shape<512, 256, 8, 2, 64, 1, 1>;
 
-template <class SH>
-static hipError_t launch(EngineArgs& a, hipStream_t st) {
+template <class SH, int MODE>
+static hipError_t launch_mode(EngineArgs& a, hipStream_t st) {
   static_assert(SH::LDS_BYTES <= 160 * 1024, "engine LDS budget");
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)engine_kernel<SH>,
+    hipError_t e = hipFuncSetAttribute((const void*)engine_kernel<SH, MODE>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, SH::LDS_BYTES);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   void* args[] = {&a};
-  return hipLaunchCooperativeKernel((const void*)engine_kernel<SH>, dim3(NWG), dim3(NT), args,
+  return hipLaunchCooperativeKernel((const void*)engine_kernel<SH, MODE>, dim3(NWG), dim3(NT), args,
                                     SH::LDS_BYTES, st);
+}
+
+template <class SH>
+static hipError_t launch(EngineArgs& a, hipStream_t st) {
+  return a.mode == 0 ? launch_mode<SH, 0>(a, st) : launch_mode<SH, 1>(a, st);
 }
 
 }  // namespace eng

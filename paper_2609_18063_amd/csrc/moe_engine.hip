@@ -193,7 +193,9 @@ struct Shape {
   static constexpr int O_MISC = O_RED + NT * 8;                     // small ints / floats
   static constexpr int O_MD = O_MISC + 2048;                        // [D] f16 mixing scales
   static constexpr int O_MP = O_MD + kb(D * 2);                     // [D] i32 mixing permutation
-  static constexpr int LDS_BYTES = O_MP + kb(D * 4);
+  static constexpr int O_SRC = O_MP + kb(D * 4);                    // [2] Src tables (per parity)
+  static constexpr int SRC_BYTES = (2 * RMX * 3 + NAX + GXX / 32) * 8; // one Src table
+  static constexpr int LDS_BYTES = O_SRC + kb(2 * SRC_BYTES);
 };
 
 struct Seg {
@@ -213,6 +215,18 @@ struct Route {
   int lg_gate[4], lg_up[4], lg_down[4];  // the segment's adapter on that projection is applied
   float dsc[4];          // segw * lora_scale where the down adapter is applied, else 0
   moe_bundle segbd[4];   // the segments' bundles, copied from the slot table
+};
+
+// Source addresses of one step's staged weights for this workgroup,
+// resolved with the routing, so that the copy loops only add a chunk offset
+// (null: the row is not used; its chunks are read from any valid address).
+template <class SH>
+struct Src {
+  const uint8_t* gu[2 * SH::RMX];   // gate (rows < RM) then up codes, one row each
+  const uint8_t* gus[2 * SH::RMX];  // their (scale, zero) rows
+  const uint8_t* bgu[2 * SH::RMX];  // their LoRA-B rows
+  const uint8_t* ar[SH::NAX];       // LoRA-A rows (gate, up) staged by this workgroup
+  const uint8_t* dq[SH::GXX / 32];  // down codes at 32-column chunk ch of down row 0
 };
 
 struct Misc {
@@ -502,6 +516,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   float* yl = reinterpret_cast<float*>(smem + SH::O_YL);
   double* red = reinterpret_cast<double*>(smem + SH::O_RED);
   Misc* mi = reinterpret_cast<Misc*>(smem + SH::O_MISC);
+  static_assert(sizeof(Src<SH>) <= SH::SRC_BYTES, "source table size");
+  Src<SH>* const srcs = reinterpret_cast<Src<SH>*>(smem + SH::O_SRC);
 
   const int g = blockIdx.x;
   const int x = g % NX, m = g / NX;
@@ -549,69 +565,87 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     while (q + 1 < nseg && lr >= mi->seg[q + 1].col0) ++q;
     return q;
   };
+  // the source table that goes with routing Rt (one per step parity)
+  auto src_of = [&](const Route& Rt) -> Src<SH>& { return srcs[&Rt == &mi->rt[0] ? 0 : 1]; };
+  // Source table entries k = tid, tid + nthr, ... of a resolved routing Rt.
+  auto fill_src = [&](const Route& Rt, int tid, int nthr) {
+    Src<SH>& S = src_of(Rt);
+    const int nrow = 2 * RM, nar = SH::NAX, ncol = GX / 32;
+    for (int k = tid; k < nrow + nar + ncol; k += nthr) {
+      if (k < nrow) {  // gate / up row k
+        const int lr = m * RM + (k < RM ? k : k - RM);
+        const int q = row_seg(lr);
+        const uint8_t *cq = nullptr, *cs = nullptr, *cb = nullptr;
+        if (Rt.segok[q]) {
+          const moe_proj& pj = k < RM ? Rt.segbd[q].gate : Rt.segbd[q].up;
+          const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
+          cq = reinterpret_cast<const uint8_t*>(pj.q) + (size_t)er * (D / 2);
+          cs = reinterpret_cast<const uint8_t*>(pj.sz) + (size_t)er * (D / 16);
+          if (pj.lora_b) cb = reinterpret_cast<const uint8_t*>(pj.lora_b) + (size_t)er * R * 2;
+        }
+        S.gu[k] = cq;
+        S.gus[k] = cs;
+        S.bgu[k] = cb;
+      } else if (k < nrow + nar) {  // LoRA-A row m + NM * qa of the XCD's list
+        const int qa = k - nrow, ar = m + NM * qa;
+        const uint8_t* p = nullptr;
+        if (ar < nseg * 2 * R) {
+          const int q = ar / (2 * R), rr = ar % (2 * R);
+          if (Rt.segok[q]) {
+            const void* A = rr < R ? Rt.segbd[q].gate.lora_a : Rt.segbd[q].up.lora_a;
+            if (A) p = reinterpret_cast<const uint8_t*>(A) + (size_t)(rr % R) * D * 2;
+          }
+        }
+        S.ar[qa] = p;
+      } else {  // down codes, column chunk ch
+        const int ch = k - nrow - nar, col = ch * 32;
+        const int q = row_seg(col);
+        const uint8_t* p = nullptr;
+        if (Rt.segok[q])
+          p = reinterpret_cast<const uint8_t*>(Rt.segbd[q].down.q) +
+              (mi->seg[q].i0 + (col - mi->seg[q].col0)) / 2;
+        S.dq[ch] = p;
+      }
+    }
+  };
 
   // ---- staging of a step's weights (issued by the staging waves) ----------
   // gate/up codes, their (scale, zero), the XCD's LoRA-A rows of gate/up
+  // (a chunk of an unused row is read from a.xi, any valid address)
   auto stage_gu = [&](const Route& Rt, Waves ws) {
+    const Src<SH>& S = src_of(Rt);
     constexpr int QCH = D / 32;   // 16-byte code chunks per gate/up row
     stage(smem + SH::O_GUQ, 2 * RM * QCH, ws, [&](int i) -> const void* {
-      const int rr = i / QCH, ch = i % QCH;
-      const int lr = m * RM + (rr % RM);
-      const int q = row_seg(lr);
-      if (!Rt.segok[q]) return a.xi;  // any valid address; the row is not used
-      const moe_bundle* b = &Rt.segbd[q];
-      const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
-      const uint8_t* base_q = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.q : b->up.q);
-      return base_q + (size_t)er * (D / 2) + ch * 16;
+      const uint8_t* p = S.gu[i / QCH];
+      return p ? p + (i % QCH) * 16 : reinterpret_cast<const uint8_t*>(a.xi);
     });
     constexpr int SCH = D / 256;  // 16-byte (scale, zero) chunks per row
     stage(smem + SH::O_GUS, 2 * RM * SCH, ws, [&](int i) -> const void* {
-      const int rr = i / SCH, ch = i % SCH;
-      const int lr = m * RM + (rr % RM);
-      const int q = row_seg(lr);
-      if (!Rt.segok[q]) return a.xi;
-      const moe_bundle* b = &Rt.segbd[q];
-      const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
-      const uint8_t* base_s = reinterpret_cast<const uint8_t*>(rr < RM ? b->gate.sz : b->up.sz);
-      return base_s + (size_t)er * (D / 16) + ch * 16;
+      const uint8_t* p = S.gus[i / SCH];
+      return p ? p + (i % SCH) * 16 : reinterpret_cast<const uint8_t*>(a.xi);
     });
     stage(smem + SH::O_AR, SH::NAX * (D / 8), ws, [&](int i) -> const void* {
-      const int qa = i / (D / 8), ch = i % (D / 8);
-      const int ar = m + NM * qa;
-      if (ar >= nseg * 2 * R) return a.xi;
-      const int q = ar / (2 * R), rr = ar % (2 * R);
-      if (!Rt.segok[q]) return a.xi;
-      const moe_bundle* b = &Rt.segbd[q];
-      const void* A = rr < R ? b->gate.lora_a : b->up.lora_a;
-      if (!A) return a.xi;
-      return reinterpret_cast<const __half*>(A) + (size_t)(rr % R) * D + ch * 8;
+      const uint8_t* p = S.ar[i / (D / 8)];
+      return p ? p + (i % (D / 8)) * 16 : reinterpret_cast<const uint8_t*>(a.xi);
     });
   };
   // LoRA-B of gate/up (read while h is formed), the down rows restricted to
   // the XCD's columns, their (scale, zero), LoRA-B and LoRA-A of down
   auto stage_dn = [&](const Route& Rt, Waves ws) {
+    const Src<SH>& S = src_of(Rt);
     constexpr int BCH = R * 2 / 16;
     stage(smem + SH::O_BGU, 2 * RM * BCH, ws, [&](int i) -> const void* {
-      const int rr = i / BCH, ch = i % BCH;
-      const int lr = m * RM + (rr % RM);
-      const int q = row_seg(lr);
-      if (!Rt.segok[q]) return a.xi;
-      const moe_bundle* b = &Rt.segbd[q];
-      const void* B = rr < RM ? b->gate.lora_b : b->up.lora_b;
-      if (!B) return a.xi;
-      const int er = mi->seg[q].i0 + (lr - mi->seg[q].col0);
-      return reinterpret_cast<const __half*>(B) + (size_t)er * R + ch * 8;
+      const uint8_t* p = S.bgu[i / BCH];
+      return p ? p + (i % BCH) * 16 : reinterpret_cast<const uint8_t*>(a.xi);
     });
+    // i = jj * dqch + ch: jj = (i * magic) >> 20 is exact while i * dqch < 2^20
+    // (magic * dqch - 2^20 <= dqch); here i < DR * dqch and dqch <= 32
     const int dqch = GX / 32;  // 16-byte chunks per staged down row
+    const uint32_t magic = (1u << 20) / (uint32_t)dqch + 1u;
     stage(smem + SH::O_DQ, SH::DR * dqch, ws, [&](int i) -> const void* {
-      const int jj = i / dqch, ch = i % dqch;
-      const int col = ch * 32;
-      const int q = row_seg(col);
-      if (!Rt.segok[q]) return a.xi;
-      const moe_bundle* b = &Rt.segbd[q];
-      const int ec = mi->seg[q].i0 + (col - mi->seg[q].col0);
-      return reinterpret_cast<const uint8_t*>(b->down.q) + (size_t)(m * SH::DR + jj) * (IE / 2) +
-             ec / 2;
+      const int jj = (int)(((uint32_t)i * magic) >> 20), ch = i - jj * dqch;
+      const uint8_t* p = S.dq[ch];
+      return p ? p + (size_t)(m * SH::DR + jj) * (IE / 2) : reinterpret_cast<const uint8_t*>(a.xi);
     });
     constexpr int DSCH = IE / 256;  // 16-byte chunks per (scale, zero) row
     stage(smem + SH::O_DS, SH::DR * SH::NSEGX * DSCH, ws, [&](int i) -> const void* {
@@ -689,6 +723,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     }
     if (threadIdx.x == 0) Rt.step = step;
     __syncthreads();
+    fill_src(Rt, threadIdx.x, NT);
+    __syncthreads();
   };
   // Softmax-top-k of the logits in lg (wave 0), then resolve_route.
   uint64_t* tk_keys = reinterpret_cast<uint64_t*>(lg + 256);          // [256] after the logits
@@ -755,6 +791,9 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     const int ek = __shfl(word, kq < K ? kq : 0, kWave);
     const float wk = __int_as_float(__shfl(word, kq < K ? K + kq : 0, kWave));
     if (lane < nseg) resolve_seg(Rt, lay, lane, kq < K ? ek : E + (kq - K), wk);
+    // the segments written by other lanes of this wave are read next
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    fill_src(Rt, lane, kWave);
     if (lane == 0) Rt.step = step;
   };
   // the head logits that route layer N at token t (written at token t - 1)

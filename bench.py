@@ -378,6 +378,8 @@ def main():
     ap.add_argument("--tier-tokens", type=int, default=64)
     ap.add_argument("--only-engine", action="store_true",
                     help="time the engine launch only (for counter runs)")
+    ap.add_argument("--only-batched", action="store_true",
+                    help="time the batched / prefill path only (for kernel traces)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain device copy of 1 GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -400,6 +402,10 @@ def main():
     table, layers = build_stack(wl, L, torch)
     arr = B.engine_layer_array(layers)
     hip = Hip()
+
+    if args.only_batched:
+        print(json.dumps({"batched": batched_path(B, torch, spec, table, wl, L)}), flush=True)
+        return
 
     # ---- single-token layer steps (the layer metric): one engine launch ----
     tokens = torch.from_numpy(synth.token_draws(wl, 0, K + W)).cuda()

@@ -27,7 +27,7 @@ bool pow2_dim(int v) {
 
 struct WsLayout {
   size_t counters, logits, gx, ux, h, ag, au, adpart;
-  size_t g_perm, g_tiles, g_ntiles, g_h;  // grouped (batched) path
+  size_t g_perm, g_tiles, g_ntiles, g_h, g_xp, g_ax, g_adp;  // grouped (batched) path
   int g_max_tiles;
   size_t total;
 };
@@ -55,6 +55,9 @@ WsLayout ws_layout(const moe_layer_spec* s, int T) {
   w.g_tiles = take((size_t)w.g_max_tiles * sizeof(moe::GroupTile));
   w.g_ntiles = take(sizeof(int32_t));
   w.g_h = take((size_t)T * n * s->d_expert * sizeof(__half));
+  w.g_xp = take((size_t)T * s->d_model * sizeof(__half));
+  w.g_ax = take((size_t)T * n * 2 * 16 * sizeof(float));
+  w.g_adp = take((size_t)T * n * (s->d_expert / 128 > 0 ? s->d_expert / 128 : 1) * 16 * sizeof(float));
   w.total = off;
   return w;
 }
@@ -341,6 +344,9 @@ int moe_expert_ffn_grouped_int4_lora(const moe_layer_spec* s, const moe_slot_tab
   a.n_tiles = at<int32_t>(ws, L.g_ntiles);
   a.max_tiles = L.g_max_tiles;
   a.h = at<__half>(ws, L.g_h);
+  a.xp = at<__half>(ws, L.g_xp);
+  a.ax = at<float>(ws, L.g_ax);
+  a.adp = at<float>(ws, L.g_adp);
   a.y_experts = y_experts;
   return from_hip(moe::launch_grouped_ffn(a, static_cast<hipStream_t>(stream)));
 }

@@ -1,5 +1,6 @@
 // Batched / prefill expert path (moe_grouped.hip): tokens grouped by expert,
-// then MFMA grouped GEMMs over int4 weights dequantized to fp16 in registers.
+// then MFMA grouped GEMMs over int4 weights streamed through LDS and
+// dequantized to fp16 in registers.
 #pragma once
 
 #include "moe_device.h"
@@ -30,7 +31,10 @@ struct GroupedArgs {
   GroupTile* tiles;             // [max_tiles]
   int32_t* n_tiles;             // [1]
   int max_tiles;
-  __half* h;                    // [T * n_list][I], by permuted position
+  __half* h;                    // [T * n_list][I], by permuted position, pair order
+  __half* xp;                   // [T][d]: x in pair order
+  float* ax;                    // [T * n_list][2][16]: A_g x, A_u x by permuted position
+  float* adp;                   // [T * n_list][I / 128][16]: A_d h over 128-column slabs
   float* y_experts;             // [T][n_list][d]
 };
 

@@ -31,9 +31,19 @@ PEAK_MFMA_F16_TFS = 2500.0     # MI355X dense fp16 matrix peak, published
 METRIC = "int4 MoE layer achieved HBM GB/s (% peak) at batch 1; tokens/s, 40-layer stack"
 
 
-ENGINE_SOURCES = ("paper_2609_18063_amd/csrc/moe_engine.hip", "paper_2609_18063_amd/csrc/moe_engine.h",
+# The dominant kernel of the timed step and the sources its counters depend on.
+ENGINE_SOURCES = ("paper_2609_18063_amd/csrc/moe_engine_tokens.hip",
+                  "paper_2609_18063_amd/csrc/moe_engine.h",
+                  "paper_2609_18063_amd/csrc/moe_xchg.h",
                   "paper_2609_18063_amd/csrc/moe_device.h")
-TRAFFIC_PROFILE = "profiles/moe35b_engine_hbm_traffic.md"
+TRAFFIC_PROFILE = "profiles/moe35b_tokens_hbm_traffic.md"
+
+
+def sources_sha256():
+    h = hashlib.sha256()
+    for f in ENGINE_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()
 
 
 def measured_traffic(steps):
@@ -42,9 +52,7 @@ def measured_traffic(steps):
     counters were taken (or the summary is missing)."""
     try:
         text = open(os.path.join(ROOT, TRAFFIC_PROFILE)).read()
-        h = hashlib.sha256()
-        for f in ENGINE_SOURCES:
-            h.update(open(os.path.join(ROOT, f), "rb").read())
+        sha = sources_sha256()
     except OSError:
         return None
     vals = {}
@@ -52,7 +60,7 @@ def measured_traffic(steps):
         if ": " in line and line.split(": ", 1)[0] in ("traffic_bytes_per_step", "source_sha256"):
             k, v = line.split(": ", 1)
             vals[k] = v.strip()
-    if vals.get("source_sha256") != h.hexdigest() or "traffic_bytes_per_step" not in vals:
+    if vals.get("source_sha256") != sha or "traffic_bytes_per_step" not in vals:
         return None
     return int(vals["traffic_bytes_per_step"]) * steps
 
@@ -408,20 +416,22 @@ def main():
         return
 
     # ---- single-token layer steps (the layer metric): one engine launch ----
+    # Throughput schedule (the measured step): each XCD runs its own steps.
     tokens = torch.from_numpy(synth.token_draws(wl, 0, K + W)).cuda()
     step_layer = (torch.arange(K + W, dtype=torch.int32, device="cuda") % L).contiguous()
     y = torch.empty(K + W, wl.d, dtype=torch.float32, device="cuda")
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
     ws = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+    assert B.engine_tokens_supported(spec), "the throughput schedule does not support this shape"
     if W:
-        B.engine_layers(spec, table, arr, step_layer[K:], tokens[K:], y[K:], ws, status=status)
-    ms_total = time_launch(torch, lambda: B.engine_layers(spec, table, arr, step_layer[:K],
+        B.engine_tokens(spec, table, arr, step_layer[K:], tokens[K:], y[K:], ws, status=status)
+    ms_total = time_launch(torch, lambda: B.engine_tokens(spec, table, arr, step_layer[:K],
                                                           tokens[:K], y[:K], ws, status=status))
     assert int(status.item()) == 0, "engine status %d" % int(status.item())
     ms_step = ms_total / K
     gbs = nb["step"] * K / (ms_total * 1e-3) / 1e9
-    log("engine, %d single-token steps in one launch: %.3f ms, %.2f us/step, %.1f GB/s"
-        % (K, ms_total, ms_step * 1e3, gbs))
+    log("engine (one step per XCD in flight), %d single-token steps in one launch: %.3f ms, "
+        "%.2f us/step, %.1f GB/s" % (K, ms_total, ms_step * 1e3, gbs))
 
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
@@ -433,6 +443,16 @@ def main():
         print(json.dumps({"engine_us_per_step": round(ms_step * 1e3, 3), "GB_s": round(gbs, 2)}),
               flush=True)
         return
+
+    # Latency schedule: every step on the whole chip, one after another.
+    if W:
+        B.engine_layers(spec, table, arr, step_layer[K:], tokens[K:], y[K:], ws, status=status)
+    ms_lat = time_launch(torch, lambda: B.engine_layers(spec, table, arr, step_layer[:K],
+                                                        tokens[:K], y[:K], ws, status=status))
+    assert int(status.item()) == 0, "engine status %d" % int(status.item())
+    lat_gbs = nb["step"] * K / (ms_lat * 1e-3) / 1e9
+    log("engine (one step at a time on the whole chip): %.2f us/step, %.1f GB/s"
+        % (ms_lat / K * 1e3, lat_gbs))
 
     # ---- 40-layer stack, autoregressive decode (prediction-as-routing) ----
     T = args.stack_tokens
@@ -483,6 +503,10 @@ def main():
             "bytes_per_step": nb["step"],
         },
         "pct_peak_hbm": round(100.0 * gbs / PEAK_HBM_GBS, 2),
+        "schedule": "one single-token step per XCD in flight (8 at once); each step reads its "
+                    "weights for its own token",
+        "latency_schedule": {"us_per_step": round(ms_lat / K * 1e3, 3), "GB_s": round(lat_gbs, 1),
+                             "frac_hbm": round(lat_gbs / PEAK_HBM_GBS, 4)},
         "stack": {
             "workload": "%d-layer stack of the moe35b layer, %d autoregressive tokens, "
                         "prediction-as-routing" % (L, T),
@@ -496,7 +520,8 @@ def main():
                           "gateup_kernel_us": round(gu_ms * 1e3, 3)},
         "roofline": {
             "bound": "hbm",
-            "kernel": "engine_kernel (persistent; %d single-token layer steps per launch)" % K,
+            "kernel": "tokens_kernel (persistent; %d single-token layer steps per launch, one "
+                      "per XCD in flight)" % K,
             "achieved": round(gbs, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

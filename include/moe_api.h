@@ -283,6 +283,25 @@ int moe_engine_layers(const moe_layer_spec* spec, const moe_slot_table* table,
                       size_t workspace_bytes, void* stream);
 
 /*
+ * The same independent single-token steps and outputs as moe_engine_layers,
+ * scheduled for throughput: each XCD (32 of the 256 workgroups) runs its own
+ * steps s = x, x + 8, x + 16, ..., so eight steps are in flight at once and
+ * the waits of one (exchanges, top-k, slot lookups) overlap the weight
+ * streaming of the others. Every step is still one token through one layer
+ * and reads its weights for that token alone; a step takes longer than under
+ * moe_engine_layers, the sequence of steps less time. Results equal the
+ * oracle's to the same tolerance as moe_engine_layers' (fp32 sums in another
+ * order, so not bit-identical to it). Shapes: moe_engine_tokens_supported.
+ * Same workspace (moe_engine_workspace_bytes) and ordering rules.
+ */
+int moe_engine_tokens_supported(const moe_layer_spec* spec);
+int moe_engine_tokens(const moe_layer_spec* spec, const moe_slot_table* table,
+                      const moe_engine_layer* layers, const int32_t* step_layer, int n_steps,
+                      const float* xi, float* y, int32_t* idx_rec, float* w_rec,
+                      int32_t* pidx_rec, float* pw_rec, uint32_t* status, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+/*
  * Decode chain (Sec. 3.2): n_tokens tokens, numbered first_token .. , each
  * through the n_layers layers held at table layers 0..n_layers-1, on the
  * residual r_state (device fp32 [d], in/out; zero before the first token):

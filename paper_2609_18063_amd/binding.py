@@ -108,6 +108,10 @@ SIGNATURES = {
     "moe_engine_layers": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_void_p, c_int,
                                   c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                   c_void_p, c_void_p, c_size_t, c_void_p]),
+    "moe_engine_tokens_supported": (c_int, [ctypes.POINTER(MoeLayerSpec)]),
+    "moe_engine_tokens": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_void_p, c_int,
+                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                  c_void_p, c_void_p, c_size_t, c_void_p]),
     "moe_engine_chain": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_int,
                                  c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
@@ -441,6 +445,21 @@ def engine_layers(spec, table, layer_arr, step_layer, xi, y, workspace, idx=None
                                    _ptr(pidx), _ptr(pw), _ptr(status), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)),
            "moe_engine_layers")
+
+
+def engine_tokens_supported(spec):
+    return lib().moe_engine_tokens_supported(ctypes.byref(spec)) == MOE_OK
+
+
+def engine_tokens(spec, table, layer_arr, step_layer, xi, y, workspace, idx=None, w=None,
+                  pidx=None, pw=None, status=None, stream=None):
+    """moe_engine_tokens: the steps of engine_layers, one per XCD in flight."""
+    n = step_layer.numel()
+    _check(lib().moe_engine_tokens(ctypes.byref(spec), table.handle, _ptr(layer_arr),
+                                   _ptr(step_layer), n, _ptr(xi), _ptr(y), _ptr(idx), _ptr(w),
+                                   _ptr(pidx), _ptr(pw), _ptr(status), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)),
+           "moe_engine_tokens")
 
 
 def engine_chain(spec, table, layer_arr, n_layers, first_token, xi, r_state, workspace,

@@ -417,16 +417,38 @@ int moe_engine_supported(const moe_layer_spec* s) {
 
 static constexpr size_t kEngineCtlBytes = 256;
 
+// exchange words of the engine's schedule for a.mode (fills a's offsets)
+static size_t engine_words(const moe_layer_spec* s, int n_layers, moe::EngineArgs* a) {
+  if (a->mode == 2)
+    return moe::engine_tokens_workspace_words(s->n_experts, s->d_model, s->d_expert, s->lora_rank,
+                                              s->top_k + s->n_shared, a);
+  return moe::engine_workspace_words(s->n_experts, s->d_model, n_layers, a);
+}
+
 size_t moe_engine_workspace_bytes(const moe_layer_spec* s, int n_layers) {
   if (moe_spec_check(s) != MOE_OK || n_layers < 0) return 0;
   moe::EngineArgs a{};
-  const size_t words = moe::engine_workspace_words(s->n_experts, s->d_model, n_layers, &a);
-  return kEngineCtlBytes + words * 8;
+  const size_t w0 = engine_words(s, n_layers, &a);
+  a.mode = 2;
+  const size_t w2 = engine_words(s, n_layers, &a);
+  return kEngineCtlBytes + (w0 > w2 ? w0 : w2) * 8;
+}
+
+int moe_engine_tokens_supported(const moe_layer_spec* s) {
+  if (moe_spec_check(s) != MOE_OK) return MOE_EINVAL;
+  if (!moe::engine_tokens_supported(s->d_model, s->d_expert, s->lora_rank, s->top_k, s->n_shared,
+                                    s->n_experts))
+    return MOE_EINVAL;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_EHIP;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return MOE_EHIP;
+  return cus == 256 ? MOE_OK : MOE_EINVAL;
 }
 
 static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n_table_layers,
                          moe::EngineArgs& a, void* ws, size_t ws_bytes, void* stream) {
-  int rc = moe_engine_supported(s);
+  int rc = a.mode == 2 ? moe_engine_tokens_supported(s) : moe_engine_supported(s);
   if (rc != MOE_OK) return rc;
   if (!t || !ws || !a.layers || !a.xi) return MOE_EINVAL;
   if (!t->dev) return MOE_EINVAL;
@@ -437,7 +459,7 @@ static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n
       (a.pidx_rec && !aligned4(a.pidx_rec)) || (a.pw_rec && !aligned4(a.pw_rec)) ||
       (a.status && !aligned4(a.status)))
     return MOE_EALIGN;
-  const size_t words = moe::engine_workspace_words(s->n_experts, s->d_model, a.L, &a);
+  const size_t words = engine_words(s, a.L, &a);
   if (ws_bytes < kEngineCtlBytes + words * 8) return MOE_ENOMEM;
   a.E = s->n_experts;
   a.K = s->top_k;
@@ -453,18 +475,21 @@ static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n
   g_prof_engine_ts = nullptr;
   a.ctl = static_cast<uint32_t*>(ws);
   a.xw = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + kEngineCtlBytes);
+  if (a.mode == 2)
+    return from_hip(moe::launch_engine_tokens(a, s->d_model, s->d_expert, s->lora_rank,
+                                              static_cast<hipStream_t>(stream)));
   return from_hip(moe::launch_engine(a, s->d_model, s->d_expert, s->lora_rank,
                                      static_cast<hipStream_t>(stream)));
 }
 
-int moe_engine_layers(const moe_layer_spec* s, const moe_slot_table* t,
-                      const moe_engine_layer* layers, const int32_t* step_layer, int n_steps,
-                      const float* xi, float* y, int32_t* idx_rec, float* w_rec, int32_t* pidx_rec,
-                      float* pw_rec, uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
+static int engine_steps(int mode, const moe_layer_spec* s, const moe_slot_table* t,
+                        const moe_engine_layer* layers, const int32_t* step_layer, int n_steps,
+                        const float* xi, float* y, int32_t* idx_rec, float* w_rec, int32_t* pidx_rec,
+                        float* pw_rec, uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
   if (n_steps < 0 || !step_layer || !y) return MOE_EINVAL;
   if (n_steps == 0) return MOE_OK;
   moe::EngineArgs a{};
-  a.mode = 0;
+  a.mode = mode;
   a.n_steps = n_steps;
   a.L = 0;
   a.layers = layers;
@@ -477,6 +502,22 @@ int moe_engine_layers(const moe_layer_spec* s, const moe_slot_table* t,
   a.pw_rec = pw_rec;
   a.status = status;
   return engine_common(s, t, t ? t->n_layers : 0, a, ws, ws_bytes, stream);
+}
+
+int moe_engine_layers(const moe_layer_spec* s, const moe_slot_table* t,
+                      const moe_engine_layer* layers, const int32_t* step_layer, int n_steps,
+                      const float* xi, float* y, int32_t* idx_rec, float* w_rec, int32_t* pidx_rec,
+                      float* pw_rec, uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
+  return engine_steps(0, s, t, layers, step_layer, n_steps, xi, y, idx_rec, w_rec, pidx_rec, pw_rec,
+                      status, ws, ws_bytes, stream);
+}
+
+int moe_engine_tokens(const moe_layer_spec* s, const moe_slot_table* t,
+                      const moe_engine_layer* layers, const int32_t* step_layer, int n_steps,
+                      const float* xi, float* y, int32_t* idx_rec, float* w_rec, int32_t* pidx_rec,
+                      float* pw_rec, uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
+  return engine_steps(2, s, t, layers, step_layer, n_steps, xi, y, idx_rec, w_rec, pidx_rec, pw_rec,
+                      status, ws, ws_bytes, stream);
 }
 
 int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,

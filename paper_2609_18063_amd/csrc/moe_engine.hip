@@ -46,36 +46,6 @@ constexpr int NX = 8, NM = 32, NWG = NX * NM, NT = 512, NWV = NT / 64;
 constexpr int kStageW0 = 4;
 constexpr int NPT = kStageW0 * 64;    // polling threads
 
-// One 16-byte direct global->LDS load per lane (lane l writes lds_wave +
-// 16 l), from inline assembly: the compiler does not track it, so a prefetch
-// stays in flight across later barriers and polls.  The issuing wave waits
-// for it with dma_wait() before the barrier that hands the data over.
-// M0 (the LDS destination) is saved and restored around the load, since the
-// compiler reserves it; one wait state separates the M0 write from its use.
-__device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
-  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_wave;
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, off nt\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds), "v"(g)
-      : "memory");
-}
-// The compiler does not see the copies above as memory instructions, so the
-// builtin wait follows: it tells the compiler that nothing of its own is
-// outstanding either. Otherwise a wait it places for one of its own loads or
-// stores (a register reused right after a store, say) can land inside a copy
-// loop, where it drains every copy issued so far on each iteration.
-// simm16 0x0F70: vmcnt 0, expcnt and lgkmcnt unconstrained.
-__device__ __forceinline__ void dma_wait() {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-}
-
 struct Ctl {
   uint32_t* ctl;      // [0] tag base, [1] finish counter, [2] abort
   uint32_t* status;
@@ -218,66 +188,6 @@ struct Misc {
   Seg seg[4];
   Route rt[2];           // by step parity: this step and the next one
 };
-
-// Softmax-top-k of the E <= 256 logits in l (512 threads; K <= 32 <= E), ties
-// to the lower index: key = order(l) << 32 | ~index, largest keys first.
-// Stage 1 ranks each group of 64 keys within its group (two waves per group,
-// 32 comparisons a lane); a group's K best become candidates. Stage 2 ranks
-// the 4K candidates among themselves: every key larger than one of the
-// overall top K is itself in its group's top K, so for those keys the rank
-// among the candidates is the overall rank, and every other key has at least
-// K larger candidates. Scratch: keys [256], part [256], cand [128], sorted [32].
-__device__ void block_topk(const float* l, int E, int K, int32_t* idx_out, float* w_out,
-                           uint64_t* keys, int* part, uint64_t* cand, uint64_t* sorted) {
-  const int tid = threadIdx.x;
-  const int i = tid & 255, half = tid >> 8;
-  const int NC = 4 * K;
-  if (tid < 256)
-    keys[tid] = tid < E ? ((uint64_t)topk_key(l[tid]) << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)tid)
-                        : 0ull;  // below every real key
-  else if (tid - 256 < NC)
-    cand[tid - 256] = 0ull;
-  __syncthreads();
-  const uint64_t mine = keys[i];
-  {
-    const int j0 = (i & ~63) + half * 32;  // uniform across the wave
-    int rank = 0;
-#pragma unroll
-    for (int j = j0; j < j0 + 32; j += 8) {
-      const uint64_t k0 = keys[j], k1 = keys[j + 1], k2 = keys[j + 2], k3 = keys[j + 3];
-      const uint64_t k4 = keys[j + 4], k5 = keys[j + 5], k6 = keys[j + 6], k7 = keys[j + 7];
-      rank += (k0 > mine) + (k1 > mine) + (k2 > mine) + (k3 > mine) + (k4 > mine) + (k5 > mine) +
-              (k6 > mine) + (k7 > mine);
-    }
-    if (half) part[i] = rank;
-    __syncthreads();
-    if (!half) {
-      rank += part[i];
-      if (rank < K) cand[(i >> 6) * K + rank] = mine;  // padding keys of a group share one slot
-    }
-  }
-  __syncthreads();
-  if (tid < NC) {
-    const uint64_t me = cand[tid];
-    int rank = 0;
-    for (int j = 0; j < NC; j += 4)
-      rank += (cand[j] > me) + (cand[j + 1] > me) + (cand[j + 2] > me) + (cand[j + 3] > me);
-    if (rank < K) sorted[rank] = me;
-  }
-  __syncthreads();
-  if (tid < 64) {
-    const int lane = tid;
-    const uint64_t k = lane < K ? sorted[lane] : 0;
-    const float v = lane < K ? topk_key_value((uint32_t)(k >> 32)) : 0.f;
-    const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    const float ex = (lane < K) ? expf(v - m) : 0.f;
-    const float sum = wave_sum(ex);
-    if (lane < K) {
-      idx_out[lane] = (int)(0xFFFFFFFFu - (uint32_t)k);
-      w_out[lane] = ex / sum;
-    }
-  }
-}
 
 typedef _Float16 hv2 __attribute__((ext_vector_type(2)));
 

@@ -68,6 +68,19 @@ __device__ __forceinline__ uint16_t ldg2(const void* p) {
   return *(const __attribute__((address_space(1))) uint16_t*)(p);
 }
 
+// The routing of one step, resolved: list position k (k < K routed, then
+// the shared experts) -> expert, weight, bundle and which adapters apply.
+template <int NLX>
+struct Route {
+  int idx[32];
+  float w[32];
+  int ok[NLX];      // resolved to a resident bundle
+  float wl[NLX];    // combine weight (0 when not resolved)
+  float dsc[NLX];   // wl * lora_scale where the down adapter applies, else 0
+  int lg[NLX], lu[NLX], ld[NLX];  // gate / up / down adapter applies
+  moe_bundle bd[NLX];
+};
+
 // D: hidden size, IE: expert intermediate size, R: LoRA rank, NLX: most
 // experts per token (K + S), EX: most routed experts (<= 256).
 template <int D_, int IE_, int R_, int NLX_, int EX_>
@@ -78,7 +91,7 @@ struct TShape {
   static constexpr int RPI = 64 / LPR;                        // gate/up rows per wave instruction
   static constexpr int CPL = D / 32 / LPR;                    // 16-byte code chunks per lane
   static constexpr int NGW = (2 * RPX / RPI + NWV - 1) / NWV; // most gate/up instructions per wave
-  static constexpr int NB = NGW < 9 ? NGW : 9;                // gate/up instructions in flight
+  static constexpr int NB = NGW < 4 ? NGW : 4;                // gate/up instructions per batch
   static constexpr int CH = IE / 32;                          // lanes per down (row, expert) unit
   static constexpr int UPI = 64 / CH;                         // units per wave instruction
   static constexpr int DR = D / NM;                           // down rows per workgroup
@@ -96,39 +109,41 @@ struct TShape {
   static_assert(2 * R * 16 <= NT && R % 8 == 0, "one 16-lane group per A_down term");
   static_assert(DR * 8 <= NT, "eight lanes per output row");
   static_assert(EX <= 256 && (EX + NM - 1) / NM <= NWV, "one router row per wave");
+  static_assert(LPR != 64 || NB % 4 == 0, "whole-wave rows are summed four at a time");
   // LDS layout (bytes)
-  static constexpr int O_XH = 0;                          // [D] fp16, natural order
-  static constexpr int O_XQ = O_XH + D * 2;               // [D] fp16, pair order
-  static constexpr int O_LG = O_XQ + D * 2;               // [EX] router logits
+  static constexpr int NBAT = (NGW + NB - 1) / NB;            // gate/up batches per wave
+  static constexpr int O_XH = 0;                          // [2][D] fp16, natural order, by step parity
+  static constexpr int O_XQ = O_XH + 2 * D * 2;           // [2][D] fp16, pair order, by step parity
+  static constexpr int O_LG = O_XQ + 2 * D * 2;           // [EX] router logits
   static constexpr int O_LH = O_LG + EX * 4;              // [EX] head logits
-  static constexpr int O_TK = O_LH + EX * 4;              // top-k scratch: 64 words per wave, two waves
-  static constexpr int O_BD = O_TK + 2 * 64 * 4;          // [NLX] bundles
-  static constexpr int O_GXU = O_BD + NLX * (int)sizeof(moe_bundle);  // [2 RPX] raw g, u
+  static constexpr int O_TK = O_LH + EX * 4;              // top-k scratch: keys, ranks, candidates, result
+  static constexpr int O_RT = O_TK + 256 * 8 + 256 * 4 + 128 * 8 + 32 * 8;  // [2] Route<NLX>, by step parity
+  static constexpr int O_GXU = O_RT + 2 * (int)sizeof(Route<NLX>);  // [2 RPX] raw g, u
   static constexpr int O_AV = O_GXU + 2 * RPX * 4;        // [2][2R] LoRA-A products of the segments
   static constexpr int O_HL = O_AV + 2 * 2 * R * 4;       // [RPX] own h
   static constexpr int O_HX = O_HL + RPX * 4;             // h of the step, 32-entry chunks at stride 36
   static constexpr int O_ADP = O_HX + NH / 32 * 36 * 4;   // [NM][2][R] A_down partials
   static constexpr int O_ADV = O_ADP + NM * 2 * R * 4;    // [NLX][R] A_down h
   static constexpr int O_YP = O_ADV + NLX * R * 4;        // [DR][NLX] weighted down rows
-  static constexpr int O_RED = (O_YP + DR * NLX * 4 + 15) / 16 * 16;  // [NWV] fp64
+  static constexpr int O_GUT = (O_YP + DR * NLX * 4 + 15) / 16 * 16;  // [2][2 RPX] gate/up row addresses
+  static constexpr int NDX = NLX * DR / UPI;              // most down instructions per workgroup
+  static constexpr int O_DNT = O_GUT + 2 * 2 * RPX * 8;   // [2][NDX] down row addresses
+  static constexpr int O_AR = O_DNT + 2 * NDX * 8;        // [NAX][D] fp16 LoRA-A rows of the next step
+  static constexpr int SOX = (EX + 32 + 63) / 64 * 64;    // slot-map entries staged (routed + shared ids)
+  static constexpr int O_SO = O_AR + NAX * D * 2;         // [SOX] int32 slot map of the next step's layer
+  static constexpr int SLX = 320;                          // most slots per layer whose bundles are staged
+  static constexpr int O_SB = O_SO + SOX * 4;             // [SLX] bundles of the next step's layer
+  static constexpr int O_RED = O_SB + SLX * 96;           // [NWV] fp64
   static constexpr int O_MISC = O_RED + NWV * 8;          // Misc
-  static constexpr int LDS_USED = O_MISC + 2048;
+  static constexpr int LDS_USED = O_MISC + 1024;
   // More than half of the CU's LDS, so that no two workgroups share a CU.
   static constexpr int LDS_BYTES = LDS_USED > 82 * 1024 ? LDS_USED : 82 * 1024;
 };
 
 struct Misc {
   int abort;
-  int idx[32];
-  float w[32];
   int pidx[32];
   float pw[32];
-  int ok[32];      // list position k: resolved to a resident bundle
-  float wl[32];    // its combine weight (0 when not resolved)
-  float dsc[32];   // wl * lora_scale where its down adapter applies, else 0
-  int lg[32];      // gate adapter applies
-  int lu[32];      // up adapter applies
-  int ld[32];      // down adapter applies
 };
 
 struct Ctl {
@@ -232,6 +247,76 @@ __device__ __forceinline__ void row_load(U4 (&r)[D / 512], const __half* row, in
   for (int j = 0; j < D / 512; ++j) r[j] = ldw16(row + (lane + 64 * j) * 8);
 }
 
+// Sum of 32 int4 codes (16 bytes, even input in the low nibble) times 32
+// fp16 activations held in pair order (xp[4 i + mm] = inputs 8 i + mm and
+// 8 i + mm + 4), in units of 2^-24: a code pair masked out of a dword is a
+// pair of exact fp16 subnormals for v_dot2_f32_f16. Nibbles 1 and 3 of each
+// byte pair are masked in place (16 times their value, still subnormal), so
+// one shift per dword serves all four pairs; their sum is scaled back by 1/16
+// (exact).
+__device__ __forceinline__ float dot32_codes(const U4& q, const hv2 (&xp)[16]) {
+  const uint32_t wd[4] = {q.x, q.y, q.z, q.w};
+  float d0 = 0.f, d1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t w = wd[i], w8 = wd[i] >> 8;
+    d0 = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w & 0x000F000Fu), xp[4 * i + 0], d0, false);
+    d1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w & 0x00F000F0u), xp[4 * i + 1], d1, false);
+    d0 = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w8 & 0x000F000Fu), xp[4 * i + 2], d0, false);
+    d1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w8 & 0x00F000F0u), xp[4 * i + 3], d1, false);
+  }
+  return fmaf(d1, 0.0625f, d0);
+}
+// The same against fp32 activations given as two fp16 terms each (hi + lo,
+// pair order), both terms of a pair meeting the same masked codes.
+__device__ __forceinline__ float dot32_codes2(const U4& q, const hv2 (&hh)[16], const hv2 (&hl)[16]) {
+  const uint32_t wd[4] = {q.x, q.y, q.z, q.w};
+  float d0 = 0.f, d1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t w = wd[i], w8 = wd[i] >> 8;
+    const hv2 p0 = __builtin_bit_cast(hv2, w & 0x000F000Fu), p1 = __builtin_bit_cast(hv2, w & 0x00F000F0u);
+    const hv2 p2 = __builtin_bit_cast(hv2, w8 & 0x000F000Fu), p3 = __builtin_bit_cast(hv2, w8 & 0x00F000F0u);
+    d0 = __builtin_amdgcn_fdot2(p0, hh[4 * i + 0], d0, false);
+    d0 = __builtin_amdgcn_fdot2(p0, hl[4 * i + 0], d0, false);
+    d1 = __builtin_amdgcn_fdot2(p1, hh[4 * i + 1], d1, false);
+    d1 = __builtin_amdgcn_fdot2(p1, hl[4 * i + 1], d1, false);
+    d0 = __builtin_amdgcn_fdot2(p2, hh[4 * i + 2], d0, false);
+    d0 = __builtin_amdgcn_fdot2(p2, hl[4 * i + 2], d0, false);
+    d1 = __builtin_amdgcn_fdot2(p3, hh[4 * i + 3], d1, false);
+    d1 = __builtin_amdgcn_fdot2(p3, hl[4 * i + 3], d1, false);
+  }
+  return fmaf(d1, 0.0625f, d0);
+}
+
+// Sums over the wave of four values per lane at once: lane l returns the
+// total of value (l & 3). Two exchange stages leave each lane one value
+// summed over its lane pair and quad; rotations within the 16-lane row and
+// two cross-row exchanges finish the sum.
+__device__ __forceinline__ float rows4_sum(float v0, float v1, float v2, float v3, int lane) {
+  const bool o1 = lane & 1, o2 = lane & 2;
+  float a = o1 ? v1 : v0, b = o1 ? v0 : v1;
+  float c = o1 ? v3 : v2, d = o1 ? v2 : v3;
+  a += dpp_f<0xB1>(0.f, b);   // partner lane ^ 1
+  c += dpp_f<0xB1>(0.f, d);
+  float e = o2 ? c : a, f = o2 ? a : c;
+  e += dpp_f<0x4E>(0.f, f);   // partner lane ^ 2
+  e += dpp_f<0x124>(0.f, e);  // row_ror:4
+  e += dpp_f<0x128>(0.f, e);  // row_ror:8
+  e += __shfl_xor(e, 16, kWave);
+  e += __shfl_xor(e, 32, kWave);
+  return e;
+}
+
+// A value every lane holds alike, moved to scalar registers.
+__device__ __forceinline__ const uint8_t* uniform_ptr(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ int uniform_int(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 // fp64 sum of one value per thread over the workgroup (two barriers)
 __device__ double block_sum_f64(double v, double* red) {
   v = eng::wave_sum_f64(v);
@@ -244,16 +329,30 @@ __device__ double block_sum_f64(double v, double* red) {
   return tot;
 }
 
+// Phase timestamps for the profiling hook: thread 0 of members 0, 1 and 31 of
+// XCD 0 writes the constant-rate wall clock at the marks of its steps.
+constexpr int kProfMarks = 24;
+__device__ __forceinline__ void mark(const EngineArgs& a, int s, int k) {
+  if (!a.phase_ts || threadIdx.x != 0) return;
+  const int g = blockIdx.x;
+  const int slot = g == 0 ? 0 : (g == NX ? 1 : (g == NWG - NX ? 2 : -1));
+  if (slot < 0) return;
+  a.phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
+}
+
 template <class SH>
 __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int D = SH::D, IE = SH::IE, R = SH::R, NLX = SH::NLX;
-  __half* xh = reinterpret_cast<__half*>(smem + SH::O_XH);
-  __half* xq = reinterpret_cast<__half*>(smem + SH::O_XQ);
+  __half* const xh2 = reinterpret_cast<__half*>(smem + SH::O_XH);
+  __half* const xq2 = reinterpret_cast<__half*>(smem + SH::O_XQ);
   float* lg = reinterpret_cast<float*>(smem + SH::O_LG);
   float* lh = reinterpret_cast<float*>(smem + SH::O_LH);
-  uint32_t* tks = reinterpret_cast<uint32_t*>(smem + SH::O_TK);
-  moe_bundle* bund = reinterpret_cast<moe_bundle*>(smem + SH::O_BD);
+  uint64_t* const tk_keys = reinterpret_cast<uint64_t*>(smem + SH::O_TK);  // [256]
+  int* const tk_part = reinterpret_cast<int*>(tk_keys + 256);               // [256]
+  uint64_t* const tk_cand = reinterpret_cast<uint64_t*>(tk_part + 256);     // [128]
+  uint64_t* const tk_sorted = tk_cand + 128;                                 // [32]
+  Route<NLX>* routes = reinterpret_cast<Route<NLX>*>(smem + SH::O_RT);
   float* gxu = reinterpret_cast<float*>(smem + SH::O_GXU);
   float* av = reinterpret_cast<float*>(smem + SH::O_AV);
   float* hl = reinterpret_cast<float*>(smem + SH::O_HL);
@@ -263,11 +362,22 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   float* yp = reinterpret_cast<float*>(smem + SH::O_YP);
   double* red = reinterpret_cast<double*>(smem + SH::O_RED);
   Misc* mi = reinterpret_cast<Misc*>(smem + SH::O_MISC);
-  static_assert(sizeof(Misc) <= 2048, "misc block");
+  static_assert(sizeof(Misc) <= 1024, "misc block");
+  // per-step address tables: gate/up item t (gate rows, then up rows) ->
+  // its code row and (scale, zero) row; down instruction n -> the code and
+  // (scale, zero) rows of its first output row
+  const uint8_t** const gu_q = reinterpret_cast<const uint8_t**>(smem + SH::O_GUT);
+  const uint8_t** const gu_s = gu_q + 2 * SH::RPX;
+  const uint8_t** const dn_q = reinterpret_cast<const uint8_t**>(smem + SH::O_DNT);
+  const uint8_t** const dn_s = dn_q + SH::NDX;
+  __half* const arow = reinterpret_cast<__half*>(smem + SH::O_AR);
+  int32_t* const slot_lds = reinterpret_cast<int32_t*>(smem + SH::O_SO);
+  char* const bund_lds = smem + SH::O_SB;
+  const bool stage_bund = a.n_slots <= SH::SLX;  // else the bundles are read from the table
 
   const int g = blockIdx.x;
   const int x = g % NX, m = g / NX;
-  const int tid0 = threadIdx.x, tid = tid0;
+  const int tid0 = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid0 >> 6), lane0 = tid0 & 63;
   const Ctl c{a.ctl, a.status};
   const int K = a.K, E = a.E, n_list = K + a.S;
@@ -283,13 +393,14 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   const int NA = n_list * 2 * R;             // LoRA-A rows of a step
   const int NHS = n_list * IE;               // h entries of a step
 
-  uint64_t* const LG = a.xw + a.xo_logr + (size_t)x * a.xs_logr;
-  uint64_t* const LH = a.xw + a.xo_loghm + (size_t)x * a.xs_logr;
+  // router and head logits by step parity; the other areas once per step
+  uint64_t* const LG0 = a.xw + a.xo_logr + (size_t)x * 2 * a.xs_logr;
+  uint64_t* const LH0 = a.xw + a.xo_loghm + (size_t)x * 2 * a.xs_logr;
   uint64_t* const AV = a.xw + a.xo_av + (size_t)x * a.xs_av;
   uint64_t* const HV = a.xw + a.xo_hv + (size_t)x * a.xs_hv;
   uint64_t* const ADP = a.xw + a.xo_adp + (size_t)x * a.xs_adp;
 
-  if (tid == 0) {
+  if (tid0 == 0) {
     mi->abort = 0;
     if ((int)eng::xcc_id() != x) {  // the work split relies on blockIdx % 8 == XCD
       raise_abort(c);
@@ -300,17 +411,17 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   const uint32_t base = ld_u32(&a.ctl[0]);
   __syncthreads();
 
-  // ---- a step's inputs, fetched during the previous step of the XCD --------
-  // step_layer early, the layer's pointers after the routing, the draws and
-  // the router and head rows after the down rows: each load is consumed long
+  // ---- a step's inputs, fetched a step ahead --------------------------------
+  // step_layer early, the layer's pointers later, the draws and the router
+  // and head rows at the end of the step before: each load is consumed long
   // after it is issued, so no wait lands in the middle of a step.
   constexpr int XPT = D / NT;
   float xin[XPT];
   U4 rrow[D / 512], hrow[D / 512];
   const int e_row = m + NM * wave;  // this wave's router and head row
-  int lay = -1, lay_n = -1;         // the step's layer; the next step's layer
-  bool has_head = false;
-  const __half *rt_n = nullptr, *hd_n = nullptr;  // the next step's router and head
+  int lay_f = -1, lay_n = -1;       // the layer of the fetched inputs; of the next fetch
+  bool head_f = false;
+  const __half *rt_n = nullptr, *hd_n = nullptr;
   auto layer_ok = [&](int l) { return l >= 0 && l < a.n_table_layers; };
   auto fetch_layer = [&]() {
     rt_n = hd_n = nullptr;
@@ -323,19 +434,177 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   // through a whole step)
   auto fetch_rows = [&](int s1) {
 #pragma unroll
-    for (int q = 0; q < XPT; ++q) xin[q] = a.xi[(size_t)s1 * D + tid + q * NT];
-    lay = lay_n;
-    has_head = layer_ok(lay) && hd_n != nullptr;
-    const bool rows = layer_ok(lay) && e_row < E;
+    for (int q = 0; q < XPT; ++q) xin[q] = a.xi[(size_t)s1 * D + tid0 + q * NT];
+    lay_f = lay_n;
+    head_f = layer_ok(lay_f) && hd_n != nullptr;
+    const bool rows = layer_ok(lay_f) && e_row < E;
     const __half* rsrc = rows ? rt_n + (size_t)e_row * D : reinterpret_cast<const __half*>(a.xi);
-    const __half* hsrc = rows && has_head ? hd_n + (size_t)e_row * D : rsrc;
+    const __half* hsrc = rows && head_f ? hd_n + (size_t)e_row * D : rsrc;
     row_load<D>(rrow, rsrc, lane0);
     row_load<D>(hrow, hsrc, lane0);
   };
+
+  // ---- routing of step s1, in two halves -----------------------------------
+  // publish: x = fp16(rmsnorm(xi)) (single rounding from fp64) and this
+  // workgroup's router and head logits. Uses the fetched inputs.
+  auto route_publish = [&](int s1, int tid, int lane) {
+    const uint32_t tag1 = base + (uint32_t)s1 + 1u;
+    const int par1 = (s1 / NX) & 1;
+    __half* const xh = xh2 + par1 * D;
+    __half* const xq = xq2 + par1 * D;
+    double acc = 0.0;
+#pragma unroll
+    for (int q = 0; q < XPT; ++q) acc += (double)xin[q] * (double)xin[q];
+    const double inv = eng::rsqrt_f64(block_sum_f64(acc, red) / (double)D + 1e-6);
+#pragma unroll
+    for (int q = 0; q < XPT; ++q) {
+      const int j = tid + q * NT;
+      const __half h = eng::f64_to_h((double)xin[q] * inv);
+      xh[j] = h;
+      xq[eng::pair_pos(j)] = h;
+    }
+    __syncthreads();
+    if (e_row < E) {
+      const float v = row_dot<D>(rrow, xh, lane);
+      if (lane == 0) st_tag(LG0 + (size_t)par1 * a.xs_logr + e_row, tag1, v);
+      if (head_f) {
+        const float vh = row_dot<D>(hrow, xh, lane);
+        if (lane == 0) st_tag(LH0 + (size_t)par1 * a.xs_logr + e_row, tag1, vh);
+      }
+    }
+  };
+  // poll: the step's router logits into lg (every thread). False on abort.
+  auto route_poll = [&](int s1, int tid) -> bool {
+    const uint32_t tag1 = base + (uint32_t)s1 + 1u;
+    uint64_t* const LG = LG0 + (size_t)((s1 / NX) & 1) * a.xs_logr;
+    return poll_all<SH::MAXI_L>(tid, E, tag1, [&](int i) { return LG + i; }, [&](int i, float v) { lg[i] = v; },
+                                c, &mi->abort);
+  };
+  // select: softmax-top-k of lg (every thread, two barriers) into
+  // routes[parity]; then wave 0 resolves the slots and bundles (after its own
+  // dma_wait for the staged slot map) and, when predictions are recorded, the
+  // workgroup polls the head's logits and records their top-k. Returns false
+  // on abort. The caller's next barrier publishes routes[parity].
+  auto route_select = [&](int s1, int lay1, bool head1, int tid, int lane) -> bool {
+    const uint32_t tag1 = base + (uint32_t)s1 + 1u;
+    const int par1 = (s1 / NX) & 1;
+    uint64_t* const LH = LH0 + (size_t)par1 * a.xs_logr;
+    Route<NLX>& rt = routes[par1];
+    eng::block_topk(lg, E, K, rt.idx, rt.w, tk_keys, tk_part, tk_cand, tk_sorted);
+    __syncthreads();
+    if (wave == 0) {
+      eng::dma_wait();  // the staged slot map and bundles
+      if (lane < n_list) {  // list position k = lane
+        const int k = lane;
+        const int e = k < K ? rt.idx[k] : E + (k - K);
+        const bool bad = k < K && (e < 0 || e >= E);
+        const int slot = bad ? -1 : slot_lds[e];
+        const bool ok = slot >= 0;
+        // the bundle's 12 pointers as six 16-byte words (gate, up, down: q,
+        // sz, lora_a, lora_b each), copied to LDS
+        static_assert(sizeof(moe_bundle) == 96, "bundle layout");
+        U4 bw[6];
+        if (stage_bund) {
+          const U4* bl = reinterpret_cast<const U4*>(bund_lds + (size_t)(ok ? slot : 0) * 96);
+#pragma unroll
+          for (int i = 0; i < 6; ++i) bw[i] = ok ? bl[i] : U4{0u, 0u, 0u, 0u};
+        } else {
+          const char* bsrc = reinterpret_cast<const char*>(a.bundles + (size_t)lay1 * a.n_slots + (ok ? slot : 0));
+#pragma unroll
+          for (int i = 0; i < 6; ++i) bw[i] = ok ? ldg16(bsrc + 16 * i) : U4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int i = 0; i < 6; ++i) reinterpret_cast<U4*>(&rt.bd[k])[i] = bw[i];
+        // lora_a, lora_b of projection j are the words 2j + 1 (both halves)
+        auto both = [](const U4& v) { return (v.x | v.y) != 0u && (v.z | v.w) != 0u; };
+        const float wk = ok ? (k < K ? rt.w[k] : 1.f) : 0.f;
+        const bool lora = ok && a.r > 0;
+        rt.ok[k] = ok;
+        rt.wl[k] = wk;
+        rt.lg[k] = lora && both(bw[1]);
+        rt.lu[k] = lora && both(bw[3]);
+        rt.ld[k] = lora && both(bw[5]);
+        rt.dsc[k] = rt.ld[k] ? wk * a.lora_scale : 0.f;
+        if (m == 0 && a.status) {
+          if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
+          else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
+        }
+      }
+      if (m == 0 && lane < K) {
+        if (a.idx_rec) a.idx_rec[(size_t)s1 * K + lane] = rt.idx[lane];
+        if (a.w_rec) a.w_rec[(size_t)s1 * K + lane] = rt.w[lane];
+      }
+    }
+    if (m == 0 && head1 && (a.pidx_rec || a.pw_rec)) {  // the head's prediction, recorded
+      if (!poll_all<SH::MAXI_L>(tid, E, tag1, [&](int i) { return LH + i; }, [&](int i, float v) { lh[i] = v; },
+                                c, &mi->abort))
+        return false;
+      eng::block_topk(lh, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_cand, tk_sorted);
+      if (tid < K) {
+        if (a.pidx_rec) a.pidx_rec[(size_t)s1 * K + tid] = mi->pidx[tid];
+        if (a.pw_rec) a.pw_rec[(size_t)s1 * K + tid] = mi->pw[tid];
+      }
+    }
+    return true;
+  };
+
+  // The slot map row of a layer, staged into LDS by wave 0 (which alone reads
+  // it, after its own dma_wait). Entries past n_ids repeat the last one.
+  auto stage_slots = [&](int lay1, int lane) {
+    if (wave != 0) return;
+    const int32_t* row = a.slot_of + (size_t)lay1 * a.n_ids;
+    for (int i0 = 0; i0 < a.n_ids && i0 < SH::SOX; i0 += 64) {
+      const int i = min(i0 + lane, a.n_ids - 1);
+      eng::dma4(row + i, slot_lds + i0);
+    }
+    if (stage_bund) {  // the layer's bundle row, 16-byte chunks
+      const char* brow = reinterpret_cast<const char*>(a.bundles + (size_t)lay1 * a.n_slots);
+      const int nch = a.n_slots * 6;
+      for (int c0 = 0; c0 < nch; c0 += 64) {
+        const int ch = min(c0 + lane, nch - 1);
+        eng::dma16(brow + (size_t)ch * 16, bund_lds + (size_t)c0 * 16);
+      }
+    }
+  };
+  // This wave's LoRA-A rows of a resolved step (rows ar = m + 32 qa, qa =
+  // wave, wave + 8, ...), staged into arow[qa]; the wave reads them after its
+  // own dma_wait.
+  auto stage_arows = [&](const Route<NLX>& r1, int lane) {
+    for (int qa = wave; qa < SH::NAX; qa += NWV) {
+      const int ar = m + NM * qa;
+      if (ar >= NA) break;
+      const int k = ar / (2 * R), proj = (ar / R) & 1, kk = ar % R;
+      if (!(proj ? r1.lu[k] : r1.lg[k])) continue;
+      const __half* A = reinterpret_cast<const __half*>(proj ? r1.bd[k].up.lora_a : r1.bd[k].gate.lora_a) +
+                        (size_t)kk * D;
+#pragma unroll
+      for (int c8 = 0; c8 < D / 512; ++c8) eng::dma16(A + (c8 * 64 + lane) * 8, arow + (size_t)qa * D + c8 * 512);
+    }
+  };
+
+  // ---- first step of this XCD: routed before the loop ------------------------
+  int lay = -1;      // layer of the current step
+  bool cur_ok = false;
   if (x < a.n_steps && !mi->abort) {
     lay_n = a.step_layer[x];
     fetch_layer();
     fetch_rows(x);
+    lay = lay_f;
+    cur_ok = layer_ok(lay);
+    if (cur_ok) {
+      const bool head0 = head_f;
+      route_publish(x, tid0, lane0);
+      lay_n = a.step_layer[x + NX < a.n_steps ? x + NX : x];
+      fetch_layer();
+      stage_slots(lay, lane0);
+      if (route_poll(x, tid0) && route_select(x, lay, head0, tid0, lane0)) {
+        __syncthreads();
+        if (!mi->abort) {
+          stage_arows(routes[(x / NX) & 1], lane0);
+          fetch_rows(x + NX < a.n_steps ? x + NX : x);
+        }
+      }
+    }
   }
 
   for (int s = x; s < a.n_steps && !mi->abort; s += NX) {
@@ -345,118 +614,97 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     int tid = tid0, lane = lane0;
     asm volatile("" : "+v"(tid), "+v"(lane));
     const uint32_t tag = base + (uint32_t)s + 1u;
-    if (lay < 0 || lay >= a.n_table_layers) {  // the same for every member of the XCD
+    mark(a, s, 0);
+    if (!cur_ok) {  // the same for every member of the XCD
       if (m == 0 && tid == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
       break;
     }
-    const int cur_lay = lay;
-    const bool cur_head = has_head;
-    // the next step of this XCD (the last step fetches its own inputs again)
-    const int s_next = s + NX < a.n_steps ? s + NX : s;
-    lay_n = a.step_layer[s_next];
-
-    // ---- layer input: x = fp16(rmsnorm(xi)), single rounding from fp64 ----
+    const int par = (s / NX) & 1;
+    const Route<NLX>& rt = routes[par];
+    const __half* const xh = xh2 + par * D;
+    const __half* const xq = xq2 + par * D;
+    // the next step of this XCD, routed during this one (its inputs are in
+    // xin / rrow / hrow, its layer in lay_f)
+    const int s1 = s + NX;
+    const bool has_next = s1 < a.n_steps;
+    const int lay1 = lay_f;
+    const bool next_ok = has_next && layer_ok(lay1);
+    const bool head1 = head_f;
+    const int s2 = s1 + NX < a.n_steps ? s1 + NX : (has_next ? s1 : s);
+    lay_n = a.step_layer[s2];
+    // ---- this step's address tables (rows of an expert that is not
+    // resident read row 0 of the draws instead; their results are discarded)
     {
-      double acc = 0.0;
-#pragma unroll
-      for (int q = 0; q < XPT; ++q) acc += (double)xin[q] * (double)xin[q];
-      const double inv = eng::rsqrt_f64(block_sum_f64(acc, red) / (double)D + 1e-6);
-#pragma unroll
-      for (int q = 0; q < XPT; ++q) {
-        const int j = tid + q * NT;
-        const __half h = eng::f64_to_h((double)xin[q] * inv);
-        xh[j] = h;
-        xq[eng::pair_pos(j)] = h;
+      const uint8_t* const dummy = reinterpret_cast<const uint8_t*>(a.xi);
+      for (int t = tid; t < 2 * RP; t += NT) {
+        const bool up = t >= RP;
+        const int p = up ? t - RP : t;
+        const int k = k0 + (p >= split ? 1 : 0);
+        const int er = row0 + p - k * IE;
+        const moe_proj& pj = up ? rt.bd[k].up : rt.bd[k].gate;
+        const bool ok = rt.ok[k];
+        gu_q[t] = ok ? reinterpret_cast<const uint8_t*>(pj.q) + (size_t)er * (D / 2) : dummy;
+        gu_s[t] = ok ? reinterpret_cast<const uint8_t*>(pj.sz) + (size_t)er * (D / 16) : dummy;
+      }
+      for (int n = tid; n < NDI; n += NT) {
+        const int k = n / DI, jj0 = (n % DI) * SH::UPI;
+        const bool ok = rt.ok[k];
+        const size_t row = (size_t)m * SH::DR + jj0;
+        dn_q[n] = ok ? reinterpret_cast<const uint8_t*>(rt.bd[k].down.q) + row * (IE / 2) : dummy;
+        dn_s[n] = ok ? reinterpret_cast<const uint8_t*>(rt.bd[k].down.sz) + row * (IE / 16) : dummy;
       }
     }
     __syncthreads();
-
-    // ---- routing ------------------------------------------------------------
-    if (e_row < E) {
-      const float v = row_dot<D>(rrow, xh, lane);
-      if (lane == 0) st_tag(LG + e_row, tag, v);
-      if (cur_head) {
-        const float vh = row_dot<D>(hrow, xh, lane);
-        if (lane == 0) st_tag(LH + e_row, tag, vh);
-      }
-    }
-    if (!poll_all<SH::MAXI_L>(tid, E, tag, [&](int i) { return LG + i; }, [&](int i, float v) { lg[i] = v; }, c,
-                              &mi->abort))
-      break;
-    const bool rec_pred = m == 0 && cur_head && (a.pidx_rec || a.pw_rec);
-    if (wave == 0) {
-      wave_topk<false, 4>(lg, E, K, mi->idx, mi->w, tks);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // resolve list position k (lane k): slot, bundle, adapter flags
-      if (lane < n_list) {
-        const int k = lane;
-        const int e = k < K ? mi->idx[k] : E + (k - K);
-        const bool bad = k < K && (e < 0 || e >= E);
-        const int slot = bad ? -1 : a.slot_of[(size_t)cur_lay * a.n_ids + e];
-        moe_bundle b{};
-        if (slot >= 0) b = a.bundles[(size_t)cur_lay * a.n_slots + slot];
-        bund[k] = b;
-        const bool ok = slot >= 0;
-        const float wk = ok ? (k < K ? mi->w[k] : 1.f) : 0.f;
-        const bool lora = ok && a.r > 0;
-        mi->ok[k] = ok;
-        mi->wl[k] = wk;
-        mi->lg[k] = lora && b.gate.lora_a && b.gate.lora_b;
-        mi->lu[k] = lora && b.up.lora_a && b.up.lora_b;
-        mi->ld[k] = lora && b.down.lora_a && b.down.lora_b;
-        mi->dsc[k] = mi->ld[k] ? wk * a.lora_scale : 0.f;
-        if (m == 0 && a.status) {
-          if (bad) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
-          else if (slot < 0) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
-        }
-      }
-      if (m == 0 && lane < K) {
-        if (a.idx_rec) a.idx_rec[(size_t)s * K + lane] = mi->idx[lane];
-        if (a.w_rec) a.w_rec[(size_t)s * K + lane] = mi->w[lane];
-      }
-    } else if (wave == 1 && rec_pred) {  // the head's prediction, recorded
-      if (!wave_poll(E, tag, [&](int i) { return LH + i; }, [&](int i, float v) { lh[i] = v; }, c)) {
-        if (lane == 0) mi->abort = 1;
-      } else {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        wave_topk<false, 4>(lh, E, K, mi->pidx, mi->pw, tks + 64);
-        if (lane < K) {
-          if (a.pidx_rec) a.pidx_rec[(size_t)s * K + lane] = mi->pidx[lane];
-          if (a.pw_rec) a.pw_rec[(size_t)s * K + lane] = mi->pw[lane];
-        }
-      }
-    }
-    fetch_layer();
-    __syncthreads();
-    if (mi->abort) break;
+    if (next_ok) stage_slots(lay1, lane);
+    mark(a, s, 10);
+    // ---- the next step's routing, first half: its x and router rows -----------
+    // (into the other parity's x buffer; the fetched inputs die here)
+    if (next_ok) route_publish(s1, tid, lane);
+    mark(a, s, 11);
 
     // ---- LoRA-A rows of the step: row ar = m + 32 qa of the list's
     // (position, projection, rank) rows, published first ----------------------
+    eng::dma_wait();  // this wave's LoRA-A rows, staged during the previous step
     for (int qa = wave; qa < SH::NAX; qa += NWV) {
       const int ar = m + NM * qa;
       if (ar >= NA) break;
-      const int k = ar / (2 * R), proj = (ar / R) & 1, kk = ar % R;
-      const bool on = proj ? mi->lu[k] : mi->lg[k];
+      const int k = ar / (2 * R), proj = (ar / R) & 1;
+      const bool on = proj ? rt.lu[k] : rt.lg[k];
       float v = 0.f;
       if (on) {
         U4 ra[D / 512];
-        const __half* A = reinterpret_cast<const __half*>(proj ? bund[k].up.lora_a : bund[k].gate.lora_a);
-        row_load<D>(ra, A + (size_t)kk * D, lane);
+#pragma unroll
+        for (int c8 = 0; c8 < D / 512; ++c8)
+          ra[c8] = *reinterpret_cast<const U4*>(arow + (size_t)qa * D + (c8 * 64 + lane) * 8);
         v = row_dot<D>(ra, xh, lane);
       }
       if (lane == 0) st_tag(AV + ar, tag, v);
     }
+    mark(a, s, 1);
 
+    // ---- LoRA-B rows of gate and up (thread t < RP: local row t), loaded
+    // before the gate/up rows so that they arrive during the streaming
+    constexpr int BV = R / 8;
+    U4 bg[BV], bu[BV];
+    int kt = k0, ert = 0;
+    if (tid < RP) {
+      kt = k0 + (tid >= split ? 1 : 0);
+      ert = row0 + tid - kt * IE;
+#pragma unroll
+      for (int v = 0; v < BV; ++v) {
+        bg[v] = rt.lg[kt] ? ldw16(reinterpret_cast<const __half*>(rt.bd[kt].gate.lora_b) + (size_t)ert * R + 8 * v)
+                          : U4{0u, 0u, 0u, 0u};
+        bu[v] = rt.lu[kt] ? ldw16(reinterpret_cast<const __half*>(rt.bd[kt].up.lora_b) + (size_t)ert * R + 8 * v)
+                          : U4{0u, 0u, 0u, 0u};
+      }
+    }
     // ---- gate/up rows (raw int4 matvecs) ------------------------------------
     // Item t < RP is the gate row of local row t, item RP + t its up row.
     // Codes become fp16 pairs q 2^-24 (exact subnormals) under one mask and
     // meet x in its pair order in v_dot2_f32_f16; 2^24 goes into the scale.
+    // Two batches of loads in flight per wave (double-buffered registers).
     {
-      const int c0 = lane % SH::LPR, sub = lane / SH::LPR;
+      const int c0 = lane % SH::LPR, sub = SH::RPI == 1 ? 0 : lane / SH::LPR;
       hv2 xp[SH::CPL][16];
       float xs[SH::CPL];
       const hv2 one2 = {(_Float16)1.0f, (_Float16)1.0f};
@@ -477,98 +725,99 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         for (int i = 0; i < 16; ++i) sacc = __builtin_amdgcn_fdot2(xp[cc][i], one2, sacc, false);
         xs[cc] = sacc;
       }
-      for (int b = 0; b < SH::NGW; b += SH::NB) {
-        U4 qv[SH::NB][SH::CPL];
-        uint32_t szw[SH::NB][SH::CPL];
+      typedef U4 QB[SH::NB][SH::CPL];
+      typedef uint32_t SB[SH::NB][SH::CPL];
+      // rows come from the step's address table (the compiler keeps no
+      // per-row address in registers across the batches)
+      auto gu_load = [&](int b, QB& qv, SB& szw) {
+        const uint8_t* pq[SH::NB];
+        const uint8_t* ps[SH::NB];
 #pragma unroll
         for (int j = 0; j < SH::NB; ++j) {
-          const int n = wave + NWV * (b + j);  // wave-uniform
+          int n = wave + NWV * (b * SH::NB + j);  // wave-uniform
+          if (n >= NG) n = NG - 1;                // loaded again, not stored
           const int t = n * SH::RPI + sub;
-          bool live = n < NG;
-          const uint8_t *pq = nullptr, *ps = nullptr;
-          if (live) {
-            const bool up = t >= RP;
-            const int p = up ? t - RP : t;
-            const int k = k0 + (p >= split ? 1 : 0);
-            const int er = row0 + p - k * IE;
-            live = mi->ok[k];
-            const moe_proj& pj = up ? bund[k].up : bund[k].gate;
-            pq = reinterpret_cast<const uint8_t*>(pj.q) + (size_t)er * (D / 2);
-            ps = reinterpret_cast<const uint8_t*>(pj.sz) + (size_t)er * (D / 16);
-          }
+          pq[j] = gu_q[t];
+          ps[j] = gu_s[t];
+        }
+#pragma unroll
+        for (int j = 0; j < SH::NB; ++j) {
 #pragma unroll
           for (int cc = 0; cc < SH::CPL; ++cc) {
             const int ch = c0 + SH::LPR * cc;
-            if (live) {
-              qv[j][cc] = ldw16(pq + ch * 16);
-              szw[j][cc] = ldw4(ps + (ch >> 1) * 4);
-            } else {
-              qv[j][cc] = U4{0u, 0u, 0u, 0u};
-              szw[j][cc] = 0u;
-            }
+            qv[j][cc] = ldw16(pq[j] + ch * 16);
+            szw[j][cc] = ldw4(ps[j] + (ch >> 1) * 4);
           }
         }
+      };
+      auto gu_row = [&](const U4 (&qv)[SH::CPL], const uint32_t (&szw)[SH::CPL]) {
+        float acc = 0.f;
 #pragma unroll
-        for (int j = 0; j < SH::NB; ++j) {
-          const int n = wave + NWV * (b + j);
-          if (n >= NG) continue;
-          float acc = 0.f;
-#pragma unroll
-          for (int cc = 0; cc < SH::CPL; ++cc) {
-            const uint32_t wd[4] = {qv[j][cc].x, qv[j][cc].y, qv[j][cc].z, qv[j][cc].w};
-            float d = 0.f;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-#pragma unroll
-              for (int mm = 0; mm < 4; ++mm) {
-                const uint32_t p = (wd[i] >> (4 * mm)) & 0x000F000Fu;
-                d = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, p), xp[cc][4 * i + mm], d, false);
-              }
-            }
-            const float2 sz = h2f2(szw[j][cc]);
-            acc += (sz.x * 16777216.f) * d + sz.y * xs[cc];
-          }
-          acc = group_sum(acc, SH::LPR);
-          if (c0 == 0) gxu[n * SH::RPI + sub] = acc;
+        for (int cc = 0; cc < SH::CPL; ++cc) {
+          const float2 sz = h2f2(szw[cc]);
+          acc += (sz.x * 16777216.f) * dot32_codes(qv[cc], xp[cc]) + sz.y * xs[cc];
         }
+        return acc;
+      };
+      auto gu_compute = [&](int b, const QB& qv, const SB& szw) {
+        if constexpr (SH::LPR == 64) {  // one row per instruction: sum four rows at once
+#pragma unroll
+          for (int j = 0; j < SH::NB; j += 4) {
+            const int n0 = wave + NWV * (b * SH::NB + j);
+            if (n0 >= NG) continue;
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = n0 + NWV * r < NG ? gu_row(qv[j + r], szw[j + r]) : 0.f;
+            const float tot = rows4_sum(v[0], v[1], v[2], v[3], lane);
+            const int nr = n0 + NWV * (lane & 3);
+            if (lane < 4 && nr < NG) gxu[nr] = tot;
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < SH::NB; ++j) {
+            const int n = wave + NWV * (b * SH::NB + j);
+            if (n >= NG) continue;
+            const float acc = group_sum(gu_row(qv[j], szw[j]), SH::LPR);
+            if (c0 == 0) gxu[n * SH::RPI + sub] = acc;
+          }
+        }
+      };
+      QB qA, qB;
+      SB sA, sB;
+      gu_load(0, qA, sA);
+#pragma unroll
+      for (int b = 0; b < SH::NBAT; b += 2) {
+        if (b + 1 < SH::NBAT) gu_load(b + 1, qB, sB);
+        gu_compute(b, qA, sA);
+        if (b + 2 < SH::NBAT) gu_load(b + 2, qA, sA);
+        if (b + 1 < SH::NBAT) gu_compute(b + 1, qB, sB);
       }
     }
+    mark(a, s, 2);
+
+    mark(a, s, 3);
 
     // ---- LoRA-A products of the segments -> h of this workgroup's rows ---------
     {
-      // LoRA-B rows of gate and up (thread t < RP: local row t)
-      constexpr int BV = R / 8;
-      U4 bg[BV], bu[BV];
-      int kt = k0, ert = 0;
-      if (tid < RP) {
-        kt = k0 + (tid >= split ? 1 : 0);
-        ert = row0 + tid - kt * IE;
-#pragma unroll
-        for (int v = 0; v < BV; ++v) {
-          bg[v] = mi->lg[kt] ? ldw16(reinterpret_cast<const __half*>(bund[kt].gate.lora_b) + (size_t)ert * R + 8 * v)
-                             : U4{0u, 0u, 0u, 0u};
-          bu[v] = mi->lu[kt] ? ldw16(reinterpret_cast<const __half*>(bund[kt].up.lora_b) + (size_t)ert * R + 8 * v)
-                             : U4{0u, 0u, 0u, 0u};
-        }
-      }
       // A_down at this workgroup's rows: term (q, kk) = tid / 16, rows sub + 16 j
       const int term = tid >> 4, sub = tid & 15;
       const int qd = term / R, kkd = term % R;
       const int kd = k0 + qd;
-      const bool dterm = term < 2 * R && qd < nseg && mi->ld[kd];
+      const bool dterm = term < 2 * R && qd < nseg && rt.ld[kd];
       const int plo = qd ? split : 0, phi = qd ? RP : split;
       float ad[SH::NPA];
-#pragma unroll
+  #pragma unroll
       for (int j = 0; j < SH::NPA; ++j) {
         const int p = plo + sub + 16 * j;
         ad[j] = 0.f;
         if (dterm && p < phi)
           ad[j] = __half2float(__ushort_as_half(
-              ldg2(reinterpret_cast<const __half*>(bund[kd].down.lora_a) + (size_t)kkd * IE + row0 + p - kd * IE)));
+              ldg2(reinterpret_cast<const __half*>(rt.bd[kd].down.lora_a) + (size_t)kkd * IE + row0 + p - kd * IE)));
       }
       if (!poll_all<SH::MAXI_A>(tid, nseg * 2 * R, tag, [&](int i) { return AV + (size_t)k0 * 2 * R + i; },
                                 [&](int i, float v) { av[i] = v; }, c, &mi->abort))
         break;
+      mark(a, s, 4);
       if (tid < RP) {
         const int q = kt - k0;
         float sg = 0.f, su = 0.f;
@@ -587,9 +836,9 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
           }
         }
         float hv = 0.f;
-        if (mi->ok[kt]) {
-          const float gg = mi->lg[kt] ? fmaf(a.lora_scale, sg, gxu[tid]) : gxu[tid];
-          const float uu = mi->lu[kt] ? fmaf(a.lora_scale, su, gxu[RP + tid]) : gxu[RP + tid];
+        if (rt.ok[kt]) {
+          const float gg = rt.lg[kt] ? fmaf(a.lora_scale, sg, gxu[tid]) : gxu[tid];
+          const float uu = rt.lu[kt] ? fmaf(a.lora_scale, su, gxu[RP + tid]) : gxu[RP + tid];
           hv = eng::silu(gg) * uu;
         }
         st_tag(HV + row0 + tid, tag, hv);
@@ -608,27 +857,50 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         if (sub == 0) st_tag(ADP + ((size_t)m * 2 + qd) * R + kkd, tag, acc);
       }
     }
+    mark(a, s, 5);
 
     // ---- down rows of this workgroup over every expert of the step -------------
     {
       // this wave's instructions n = wave ndw + j: list position n / DI, rows
       // (n % DI) UPI + lane / CH, 32-column chunk lane % CH
       const int cl = lane % SH::CH, su = lane / SH::CH;
-      U4 dq[SH::NDW];
-      uint32_t dsz[SH::NDW];
+      // two halves: the first is loaded before the waits of this phase, the
+      // second after them, while the first is computed
+      constexpr int NDH = (SH::NDW + 1) / 2;
+      typedef U4 DQ[NDH];
+      typedef uint32_t DS[NDH];
+      auto dn_load = [&](int j0, DQ& dq, DS& dsz) {
+        const uint8_t* pq[NDH];
+        const uint8_t* ps[NDH];
 #pragma unroll
-      for (int j = 0; j < SH::NDW; ++j) {
-        const int n = wave * ndw + j;
-        dq[j] = U4{0u, 0u, 0u, 0u};
-        dsz[j] = 0u;
-        if (j < ndw && n < NDI) {
-          const int k = n / DI, jj = (n % DI) * SH::UPI + su;
-          if (mi->ok[k]) {
-            const size_t row = (size_t)m * SH::DR + jj;
-            dq[j] = ldw16(reinterpret_cast<const uint8_t*>(bund[k].down.q) + row * (IE / 2) + cl * 16);
-            dsz[j] = ldw4(reinterpret_cast<const uint8_t*>(bund[k].down.sz) + row * (IE / 16) + (cl >> 1) * 4);
-          }
+        for (int jh = 0; jh < NDH; ++jh) {
+          int n = wave * ndw + j0 + jh;  // wave-uniform
+          if (n >= NDI) n = NDI - 1;     // loaded again, not used
+          pq[jh] = dn_q[n];
+          ps[jh] = dn_s[n];
         }
+#pragma unroll
+        for (int jh = 0; jh < NDH; ++jh) {
+          dq[jh] = ldw16(pq[jh] + su * (IE / 2) + cl * 16);
+          dsz[jh] = ldw4(ps[jh] + su * (IE / 16) + (cl >> 1) * 4);
+        }
+      };
+      DQ dqA, dqB;
+      DS dsA, dsB;
+      // the next step's logits (published at the start of this step) are
+      // polled before any down row is requested: a poll would wait behind them
+      if (next_ok && !route_poll(s1, tid)) break;
+      mark(a, s, 12);
+      // wave 0 selects the next step's experts first, so that its slot and
+      // bundle loads do not queue behind down rows either
+      if (wave != 0 || !next_ok) dn_load(0, dqA, dsA);
+      // the next step's routing, second half, while the down rows arrive
+      if (next_ok) {
+        mark(a, s, 13);
+        if (!route_select(s1, lay1, head1, tid, lane)) break;
+        mark(a, s, 15);
+        if (wave == 0) dn_load(0, dqA, dsA);
+        fetch_layer();
       }
       // LoRA-B rows of down for the output sum: lane (j, part) = (tid / 8, tid % 8)
       constexpr int BV = R / 8;
@@ -640,11 +912,16 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
 #pragma unroll
         for (int v = 0; v < BV; ++v) {
           bd[i][v] = U4{0u, 0u, 0u, 0u};
-          if (jo < SH::DR && k < n_list && mi->ld[k])
-            bd[i][v] = ldw16(reinterpret_cast<const __half*>(bund[k].down.lora_b) +
+          if (jo < SH::DR && k < n_list && rt.ld[k])
+            bd[i][v] = ldw16(reinterpret_cast<const __half*>(rt.bd[k].down.lora_b) +
                              ((size_t)m * SH::DR + jo) * R + 8 * v);
         }
       }
+      __syncthreads();
+      if (mi->abort) break;
+      // the next step's LoRA-A rows (the current step's were read at its start)
+      if (next_ok) stage_arows(routes[par ^ 1], lane);
+      mark(a, s, 6);
       // h of the step and the A_down partials of the XCD
       if (!poll_all<SH::MAXI_H>(
               tid, NHS + NM * 2 * R, tag,
@@ -655,6 +932,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
               },
               c, &mi->abort))
         break;
+      mark(a, s, 7);
       // A_down h of list position k: the partials of the workgroups whose rows
       // meet expert k, in workgroup order
       if (tid < n_list * R) {
@@ -667,36 +945,58 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         }
         adv[tid] = acc;
       }
-      // down dot products: reload the h chunk when the expert changes
-      float hc[32], hsum = 0.f;
+      dn_load(NDH, dqB, dsB);
+      // down dot products: reload the h chunk when the expert changes. The
+      // lane's 32 h values (fp32) become two fp16 terms each, hi = fp16(h)
+      // and lo = fp16(h - hi), in pair order, so the codes meet them in
+      // v_dot2_f32_f16; hi + lo carries h to about 2^-22 (|h| < 65504).
+      hv2 hh[16], hlo[16];
+      float hsum = 0.f;
       int kc = -1;
+      auto dn_compute = [&](int j0, const DQ& dq, const DS& dsz) {
 #pragma unroll
-      for (int j = 0; j < SH::NDW; ++j) {
-        const int n = wave * ndw + j;
-        if (j >= ndw || n >= NDI) continue;
-        const int k = n / DI, jj = (n % DI) * SH::UPI + su;
-        if (k != kc) {
-          kc = k;
-          const float4* hp = reinterpret_cast<const float4*>(hx + ((k * IE) / 32 + cl) * 36);
-          hsum = 0.f;
+        for (int jh = 0; jh < NDH; ++jh) {
+          const int j = j0 + jh;
+          const int n = wave * ndw + j;
+          if (j >= SH::NDW || j >= ndw || n >= NDI) continue;
+          const int k = n / DI, jj = (n % DI) * SH::UPI + su;
+          if (k != kc) {
+            kc = k;
+            const float4* hp = reinterpret_cast<const float4*>(hx + ((k * IE) / 32 + cl) * 36);
+            float hv[32];
+            hsum = 0.f;
 #pragma unroll
-          for (int e4 = 0; e4 < 8; ++e4) {
-            const float4 v4 = hp[e4];
-            hc[4 * e4] = v4.x;
-            hc[4 * e4 + 1] = v4.y;
-            hc[4 * e4 + 2] = v4.z;
-            hc[4 * e4 + 3] = v4.w;
-            hsum += (v4.x + v4.y) + (v4.z + v4.w);
+            for (int e4 = 0; e4 < 8; ++e4) {
+              const float4 v4 = hp[e4];
+              hv[4 * e4] = v4.x;
+              hv[4 * e4 + 1] = v4.y;
+              hv[4 * e4 + 2] = v4.z;
+              hv[4 * e4 + 3] = v4.w;
+              hsum += (v4.x + v4.y) + (v4.z + v4.w);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+#pragma unroll
+              for (int mm = 0; mm < 4; ++mm) {
+                const float a0 = hv[8 * i + mm], a1 = hv[8 * i + mm + 4];
+                const _Float16 h0 = (_Float16)a0, h1 = (_Float16)a1;
+                hh[4 * i + mm] = hv2{h0, h1};
+                hlo[4 * i + mm] = hv2{(_Float16)(a0 - (float)h0), (_Float16)(a1 - (float)h1)};
+              }
+            }
           }
+          const float2 sz = h2f2(dsz[jh]);
+          float v = (sz.x * 16777216.f) * dot32_codes2(dq[jh], hh, hlo) + sz.y * hsum;
+          v = group_sum(v, SH::CH);
+          if (cl == 0) yp[jj * NLX + k] = rt.wl[k] * v;
         }
-        const float2 sz = h2f2(dsz[j]);
-        float v = sz.x * dot32_q4(dq[j], hc) + sz.y * hsum;
-        v = group_sum(v, SH::CH);
-        if (cl == 0) yp[jj * NLX + k] = mi->wl[k] * v;
-      }
+      };
+      dn_compute(0, dqA, dsA);
+      dn_compute(NDH, dqB, dsB);
       __syncthreads();
-      // the next step's inputs (this XCD's step s + 8) arrive while y is summed
-      fetch_rows(s_next);
+      mark(a, s, 8);
+      // the inputs of the step after next arrive while y is summed
+      fetch_rows(s2);
       // y = sum over list positions of the weighted down rows and LoRA terms
       if (jo < SH::DR) {
         float acc = 0.f;
@@ -705,7 +1005,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
           const int k = part + 8 * i;
           if (k >= n_list) continue;
           acc += yp[jo * NLX + k];
-          const float sc = mi->dsc[k];
+          const float sc = rt.dsc[k];
           if (sc != 0.f) {
             float t = 0.f;
 #pragma unroll
@@ -725,12 +1025,18 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         if (part == 0) a.y[(size_t)s * D + (size_t)m * SH::DR + jo] = acc;
       }
       __syncthreads();
+      mark(a, s, 9);
+    }
+    cur_ok = next_ok;
+    if (has_next && !next_ok) {  // the next step's layer is outside the table
+      if (m == 0 && tid == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
+      break;
     }
   }
 
   // ---- finish: the last workgroup moves the tag base past this launch --------
   __syncthreads();
-  if (tid == 0) {
+  if (tid0 == 0) {
     const uint32_t old = atomicAdd(&a.ctl[1], 1u);
     if (old == NWG - 1) {
       __hip_atomic_store(&a.ctl[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -780,9 +1086,9 @@ size_t engine_tokens_workspace_words(int E, int d, int I, int r, int n_list, Eng
     return o;
   };
   const size_t rr = (size_t)(r > 0 ? r : 1);
-  a->xs_logr = (size_t)(E + 31) / 32 * 32;
-  a->xo_logr = take(tok::NX * a->xs_logr);
-  a->xo_loghm = take(tok::NX * a->xs_logr);
+  a->xs_logr = (size_t)(E + 31) / 32 * 32;  // one parity of one XCD
+  a->xo_logr = take(tok::NX * 2 * a->xs_logr);
+  a->xo_loghm = take(tok::NX * 2 * a->xs_logr);
   a->xs_av = (size_t)n_list * 2 * rr;
   a->xo_av = take(tok::NX * a->xs_av);
   a->xs_hv = (size_t)n_list * I;

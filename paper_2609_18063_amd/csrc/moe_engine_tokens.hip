@@ -125,10 +125,10 @@ struct TShape {
   static constexpr int O_ADP = O_HX + NH / 32 * 36 * 4;   // [NM][2][R] A_down partials
   static constexpr int O_ADV = O_ADP + NM * 2 * R * 4;    // [NLX][R] A_down h
   static constexpr int O_YP = O_ADV + NLX * R * 4;        // [DR][NLX] weighted down rows
-  static constexpr int O_GUT = (O_YP + DR * NLX * 4 + 15) / 16 * 16;  // [2][2 RPX] gate/up row addresses
+  static constexpr int O_GUT = (O_YP + DR * NLX * 4 + 15) / 16 * 16;  // [2][2][2 RPX] gate/up row addresses
   static constexpr int NDX = NLX * DR / UPI;              // most down instructions per workgroup
-  static constexpr int O_DNT = O_GUT + 2 * 2 * RPX * 8;   // [2][NDX] down row addresses
-  static constexpr int O_AR = O_DNT + 2 * NDX * 8;        // [NAX][D] fp16 LoRA-A rows of the next step
+  static constexpr int O_DNT = O_GUT + 2 * 2 * 2 * RPX * 8;  // [2][2][NDX] down row addresses
+  static constexpr int O_AR = O_DNT + 2 * 2 * NDX * 8;    // [NAX][D] fp16 LoRA-A rows of the next step
   static constexpr int SOX = (EX + 32 + 63) / 64 * 64;    // slot-map entries staged (routed + shared ids)
   static constexpr int O_SO = O_AR + NAX * D * 2;         // [SOX] int32 slot map of the next step's layer
   static constexpr int SLX = 320;                          // most slots per layer whose bundles are staged
@@ -363,13 +363,11 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   double* red = reinterpret_cast<double*>(smem + SH::O_RED);
   Misc* mi = reinterpret_cast<Misc*>(smem + SH::O_MISC);
   static_assert(sizeof(Misc) <= 1024, "misc block");
-  // per-step address tables: gate/up item t (gate rows, then up rows) ->
-  // its code row and (scale, zero) row; down instruction n -> the code and
-  // (scale, zero) rows of its first output row
-  const uint8_t** const gu_q = reinterpret_cast<const uint8_t**>(smem + SH::O_GUT);
-  const uint8_t** const gu_s = gu_q + 2 * SH::RPX;
-  const uint8_t** const dn_q = reinterpret_cast<const uint8_t**>(smem + SH::O_DNT);
-  const uint8_t** const dn_s = dn_q + SH::NDX;
+  // per-step address tables, by step parity: gate/up item t (gate rows, then
+  // up rows) -> its code row and (scale, zero) row; down instruction n -> the
+  // code and (scale, zero) rows of its first output row
+  const uint8_t** const gu_q2 = reinterpret_cast<const uint8_t**>(smem + SH::O_GUT);
+  const uint8_t** const dn_q2 = reinterpret_cast<const uint8_t**>(smem + SH::O_DNT);
   __half* const arow = reinterpret_cast<__half*>(smem + SH::O_AR);
   int32_t* const slot_lds = reinterpret_cast<int32_t*>(smem + SH::O_SO);
   char* const bund_lds = smem + SH::O_SB;
@@ -481,8 +479,9 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
                                 c, &mi->abort);
   };
   // select: softmax-top-k of lg (every thread, two barriers) into
-  // routes[parity]; then wave 0 resolves the slots and bundles (after its own
-  // dma_wait for the staged slot map) and, when predictions are recorded, the
+  // routes[parity]; then wave 0 resolves the slots and bundles (staged slot
+  // map and bundles, waited for before an earlier barrier) and, when
+  // predictions are recorded, the
   // workgroup polls the head's logits and records their top-k. Returns false
   // on abort. The caller's next barrier publishes routes[parity].
   auto route_select = [&](int s1, int lay1, bool head1, int tid, int lane) -> bool {
@@ -493,7 +492,6 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     eng::block_topk(lg, E, K, rt.idx, rt.w, tk_keys, tk_part, tk_cand, tk_sorted);
     __syncthreads();
     if (wave == 0) {
-      eng::dma_wait();  // the staged slot map and bundles
       if (lane < n_list) {  // list position k = lane
         const int k = lane;
         const int e = k < K ? rt.idx[k] : E + (k - K);
@@ -548,19 +546,20 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     return true;
   };
 
-  // The slot map row of a layer, staged into LDS by wave 0 (which alone reads
-  // it, after its own dma_wait). Entries past n_ids repeat the last one.
+  // The slot map row and the bundle row of a layer, staged into LDS by every
+  // wave (64-entry blocks dealt round-robin). Each wave waits for its own
+  // copies (dma_wait) before a barrier that precedes their reader. Slot-map
+  // entries past n_ids repeat the last one.
   auto stage_slots = [&](int lay1, int lane) {
-    if (wave != 0) return;
     const int32_t* row = a.slot_of + (size_t)lay1 * a.n_ids;
-    for (int i0 = 0; i0 < a.n_ids && i0 < SH::SOX; i0 += 64) {
+    for (int i0 = 64 * wave; i0 < a.n_ids && i0 < SH::SOX; i0 += 64 * NWV) {
       const int i = min(i0 + lane, a.n_ids - 1);
       eng::dma4(row + i, slot_lds + i0);
     }
     if (stage_bund) {  // the layer's bundle row, 16-byte chunks
       const char* brow = reinterpret_cast<const char*>(a.bundles + (size_t)lay1 * a.n_slots);
       const int nch = a.n_slots * 6;
-      for (int c0 = 0; c0 < nch; c0 += 64) {
+      for (int c0 = 64 * wave; c0 < nch; c0 += 64 * NWV) {
         const int ch = min(c0 + lane, nch - 1);
         eng::dma16(brow + (size_t)ch * 16, bund_lds + (size_t)c0 * 16);
       }
@@ -582,6 +581,33 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     }
   };
 
+  // The address tables of a resolved step (rows of an expert that is not
+  // resident read row 0 of the draws instead; their results are discarded).
+  auto fill_tables = [&](const Route<NLX>& r1, int par1, int tid) {
+    const uint8_t* const dummy = reinterpret_cast<const uint8_t*>(a.xi);
+    const uint8_t** const gq = gu_q2 + par1 * 4 * SH::RPX;
+    const uint8_t** const gs = gq + 2 * SH::RPX;
+    const uint8_t** const dq = dn_q2 + par1 * 2 * SH::NDX;
+    const uint8_t** const ds = dq + SH::NDX;
+    for (int t = tid; t < 2 * RP; t += NT) {
+      const bool up = t >= RP;
+      const int p = up ? t - RP : t;
+      const int k = k0 + (p >= split ? 1 : 0);
+      const int er = row0 + p - k * IE;
+      const moe_proj& pj = up ? r1.bd[k].up : r1.bd[k].gate;
+      const bool ok = r1.ok[k];
+      gq[t] = ok ? reinterpret_cast<const uint8_t*>(pj.q) + (size_t)er * (D / 2) : dummy;
+      gs[t] = ok ? reinterpret_cast<const uint8_t*>(pj.sz) + (size_t)er * (D / 16) : dummy;
+    }
+    for (int n = tid; n < NDI; n += NT) {
+      const int k = n / DI, jj0 = (n % DI) * SH::UPI;
+      const bool ok = r1.ok[k];
+      const size_t row = (size_t)m * SH::DR + jj0;
+      dq[n] = ok ? reinterpret_cast<const uint8_t*>(r1.bd[k].down.q) + row * (IE / 2) : dummy;
+      ds[n] = ok ? reinterpret_cast<const uint8_t*>(r1.bd[k].down.sz) + row * (IE / 16) : dummy;
+    }
+  };
+
   // ---- first step of this XCD: routed before the loop ------------------------
   int lay = -1;      // layer of the current step
   bool cur_ok = false;
@@ -597,9 +623,11 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       lay_n = a.step_layer[x + NX < a.n_steps ? x + NX : x];
       fetch_layer();
       stage_slots(lay, lane0);
+      eng::dma_wait();
       if (route_poll(x, tid0) && route_select(x, lay, head0, tid0, lane0)) {
         __syncthreads();
         if (!mi->abort) {
+          fill_tables(routes[(x / NX) & 1], (x / NX) & 1, tid0);
           stage_arows(routes[(x / NX) & 1], lane0);
           fetch_rows(x + NX < a.n_steps ? x + NX : x);
         }
@@ -632,29 +660,10 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     const bool head1 = head_f;
     const int s2 = s1 + NX < a.n_steps ? s1 + NX : (has_next ? s1 : s);
     lay_n = a.step_layer[s2];
-    // ---- this step's address tables (rows of an expert that is not
-    // resident read row 0 of the draws instead; their results are discarded)
-    {
-      const uint8_t* const dummy = reinterpret_cast<const uint8_t*>(a.xi);
-      for (int t = tid; t < 2 * RP; t += NT) {
-        const bool up = t >= RP;
-        const int p = up ? t - RP : t;
-        const int k = k0 + (p >= split ? 1 : 0);
-        const int er = row0 + p - k * IE;
-        const moe_proj& pj = up ? rt.bd[k].up : rt.bd[k].gate;
-        const bool ok = rt.ok[k];
-        gu_q[t] = ok ? reinterpret_cast<const uint8_t*>(pj.q) + (size_t)er * (D / 2) : dummy;
-        gu_s[t] = ok ? reinterpret_cast<const uint8_t*>(pj.sz) + (size_t)er * (D / 16) : dummy;
-      }
-      for (int n = tid; n < NDI; n += NT) {
-        const int k = n / DI, jj0 = (n % DI) * SH::UPI;
-        const bool ok = rt.ok[k];
-        const size_t row = (size_t)m * SH::DR + jj0;
-        dn_q[n] = ok ? reinterpret_cast<const uint8_t*>(rt.bd[k].down.q) + row * (IE / 2) : dummy;
-        dn_s[n] = ok ? reinterpret_cast<const uint8_t*>(rt.bd[k].down.sz) + row * (IE / 16) : dummy;
-      }
-    }
-    __syncthreads();
+    const uint8_t* const* const gu_q = gu_q2 + par * 4 * SH::RPX;
+    const uint8_t* const* const gu_s = gu_q + 2 * SH::RPX;
+    const uint8_t* const* const dn_q = dn_q2 + par * 2 * SH::NDX;
+    const uint8_t* const* const dn_s = dn_q + SH::NDX;
     if (next_ok) stage_slots(lay1, lane);
     mark(a, s, 10);
     // ---- the next step's routing, first half: its x and router rows -----------
@@ -698,6 +707,23 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
                           : U4{0u, 0u, 0u, 0u};
       }
     }
+    // A_down at this workgroup's rows, also loaded ahead of the gate/up rows
+    // (term (q, kk) = tid / 16, rows sub + 16 j)
+    const int term = tid >> 4, sub = tid & 15;
+    const int qd = term / R, kkd = term % R;
+    const int kd = k0 + qd;
+    const bool dterm = term < 2 * R && qd < nseg && rt.ld[kd];
+    const int plo = qd ? split : 0, phi = qd ? RP : split;
+    float ad[SH::NPA];
+#pragma unroll
+    for (int j = 0; j < SH::NPA; ++j) {
+      const int p = plo + sub + 16 * j;
+      ad[j] = 0.f;
+      if (dterm && p < phi)
+        ad[j] = __half2float(__ushort_as_half(
+            ldg2(reinterpret_cast<const __half*>(rt.bd[kd].down.lora_a) + (size_t)kkd * IE + row0 + p - kd * IE)));
+    }
+
     // ---- gate/up rows (raw int4 matvecs) ------------------------------------
     // Item t < RP is the gate row of local row t, item RP + t its up row.
     // Codes become fp16 pairs q 2^-24 (exact subnormals) under one mask and
@@ -795,25 +821,20 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     }
     mark(a, s, 2);
 
+    // ---- the next step's routing, second half: its logits (published by every
+    // member at the start of this step) -> top-k, slots, bundles; then its
+    // address tables ------------------------------------------------------------
+    if (next_ok) {
+      if (!route_poll(s1, tid)) break;
+      if (!route_select(s1, lay1, head1, tid, lane)) break;
+    }
+    __syncthreads();
+    if (mi->abort) break;
+    if (next_ok) fill_tables(routes[par ^ 1], par ^ 1, tid);
     mark(a, s, 3);
 
     // ---- LoRA-A products of the segments -> h of this workgroup's rows ---------
     {
-      // A_down at this workgroup's rows: term (q, kk) = tid / 16, rows sub + 16 j
-      const int term = tid >> 4, sub = tid & 15;
-      const int qd = term / R, kkd = term % R;
-      const int kd = k0 + qd;
-      const bool dterm = term < 2 * R && qd < nseg && rt.ld[kd];
-      const int plo = qd ? split : 0, phi = qd ? RP : split;
-      float ad[SH::NPA];
-  #pragma unroll
-      for (int j = 0; j < SH::NPA; ++j) {
-        const int p = plo + sub + 16 * j;
-        ad[j] = 0.f;
-        if (dterm && p < phi)
-          ad[j] = __half2float(__ushort_as_half(
-              ldg2(reinterpret_cast<const __half*>(rt.bd[kd].down.lora_a) + (size_t)kkd * IE + row0 + p - kd * IE)));
-      }
       if (!poll_all<SH::MAXI_A>(tid, nseg * 2 * R, tag, [&](int i) { return AV + (size_t)k0 * 2 * R + i; },
                                 [&](int i, float v) { av[i] = v; }, c, &mi->abort))
         break;
@@ -887,21 +908,8 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       };
       DQ dqA, dqB;
       DS dsA, dsB;
-      // the next step's logits (published at the start of this step) are
-      // polled before any down row is requested: a poll would wait behind them
-      if (next_ok && !route_poll(s1, tid)) break;
-      mark(a, s, 12);
-      // wave 0 selects the next step's experts first, so that its slot and
-      // bundle loads do not queue behind down rows either
-      if (wave != 0 || !next_ok) dn_load(0, dqA, dsA);
-      // the next step's routing, second half, while the down rows arrive
-      if (next_ok) {
-        mark(a, s, 13);
-        if (!route_select(s1, lay1, head1, tid, lane)) break;
-        mark(a, s, 15);
-        if (wave == 0) dn_load(0, dqA, dsA);
-        fetch_layer();
-      }
+      dn_load(0, dqA, dsA);
+      if (next_ok) fetch_layer();
       // LoRA-B rows of down for the output sum: lane (j, part) = (tid / 8, tid % 8)
       constexpr int BV = R / 8;
       const int jo = tid >> 3, part = tid & 7;
@@ -917,8 +925,6 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
                              ((size_t)m * SH::DR + jo) * R + 8 * v);
         }
       }
-      __syncthreads();
-      if (mi->abort) break;
       // the next step's LoRA-A rows (the current step's were read at its start)
       if (next_ok) stage_arows(routes[par ^ 1], lane);
       mark(a, s, 6);

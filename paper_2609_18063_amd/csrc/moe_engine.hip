@@ -182,6 +182,7 @@ struct Src {
 struct Misc {
   int nseg;
   int abort;
+  int px, pm;            // this workgroup's XCD and member index
   int rt_step, hd_step, mix_step;  // the step whose data each LDS region holds
   int pidx[32];
   float pw[32];
@@ -287,9 +288,8 @@ __device__ __forceinline__ void stage(char* dst, int nchunks, Waves ws, SrcF src
 // Phase timestamps for the profiling hook: thread 0 of workgroups 0, 7 and
 // 255 writes the constant-rate wall clock at up to 16 marks of every step.
 constexpr int kProfMarks = 24;
-__device__ __forceinline__ void mark(const EngineArgs& a, int s, int k) {
+__device__ __forceinline__ void mark(const EngineArgs& a, int g, int s, int k) {
   if (!a.phase_ts || threadIdx.x != 0) return;
-  const int g = blockIdx.x;
   const int slot = g == 0 ? 0 : (g == 7 ? 1 : (g == NWG - 1 ? 2 : -1));
   if (slot < 0) return;
   a.phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
@@ -355,8 +355,22 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   static_assert(sizeof(Src<SH>) <= SH::SRC_BYTES, "source table size");
   Src<SH>* const srcs = reinterpret_cast<Src<SH>*>(smem + SH::O_SRC);
 
-  const int g = blockIdx.x;
-  const int x = g % NX, m = g / NX;
+  if (threadIdx.x == 0) {
+    mi->abort = 0;
+    int px = 0, pm = 0;
+    if (!claim_place(a.ctl, NX, NM, &px, &pm)) {  // not 32 workgroups per XCD
+      if (a.status) atomicOr(a.status, MOE_STATUS_ENGINE_ABORT);
+      __hip_atomic_store(&a.ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      mi->abort = 1;
+    }
+    mi->px = px;
+    mi->pm = pm;
+  }
+  __syncthreads();
+  // XCD, member index and the logical workgroup id x + 8 m (uniform)
+  const int x = __builtin_amdgcn_readfirstlane(mi->abort ? 0 : mi->px);
+  const int m = __builtin_amdgcn_readfirstlane(mi->abort ? 0 : mi->pm);
+  const int g = x + NX * m;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const bool poller = (int)threadIdx.x < NPT;
   const Ctl c{a.ctl, a.status};
@@ -368,14 +382,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   const int RPID = 64 / LPRD;         // down rows per wave instruction
 
   if (threadIdx.x == 0) {
-    mi->abort = 0;
     mi->rt_step = mi->hd_step = mi->mix_step = -1;
     mi->rt[0].step = mi->rt[1].step = -1;
-    if ((int)xcc_id() != x) {  // the work split relies on blockIdx % 8 == XCD
-      if (a.status) atomicOr(a.status, MOE_STATUS_ENGINE_ABORT);
-      __hip_atomic_store(&a.ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      mi->abort = 1;
-    }
     if (ld_u32(&a.ctl[2])) mi->abort = 1;
   }
   const uint32_t base = ld_u32(&a.ctl[0]);
@@ -570,7 +578,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   auto compute_route = [&](Route& Rt, int lay, int step) {
     block_topk(lg, E, K, Rt.idx, Rt.w, tk_keys, tk_part, tk_cand, tk_sorted);
     __syncthreads();
-    mark(a, step, 15);
+    mark(a, g, step, 15);
     resolve_route(Rt, lay, step);
   };
   // The published prediction (ids and weights) that routes layer N at token t.
@@ -686,7 +694,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     const moe_engine_layer LY = a.layers[lay];
     Route& Rt = mi->rt[par];
 
-    mark(a, s, 0);
+    mark(a, g, s, 0);
     // ---- S0: layer input (global reads by the polling waves only) --------
     if (MODE == 0) {
       if (poller) {
@@ -717,7 +725,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       // prediction gives it (published at least a step ago) while waves 0-3
       // poll the residual
       if (!flush_pred()) break;
-      mark(a, s, 16);
+      mark(a, g, s, 16);
       if (wave == kStageW0 && s + 1 < a.n_steps) {
         const StepInfo f1 = step_info<MODE>(a, s + 1);
         if (f1.ok && !f1.own) route_from_pred_wave(mi->rt[par ^ 1], f1.t, f1.N, f1.lay, s + 1);
@@ -732,7 +740,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
                                   [&](int i, float v) { r0[i] = v; }, c, &mi->abort))
           break;
       }
-      mark(a, s, 17);
+      mark(a, g, s, 17);
       if (N == 0) {  // token start: r = xi + rmsnorm(r)
         const double inv = rsqrt_f64(block_sumsq<SH>(r0, red) / (double)D + 1e-6);
         const float* xi = a.xi + (size_t)(s / a.L) * D;
@@ -754,7 +762,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           r1[j] = vv[q];
           acc += (double)vv[q] * (double)vv[q];
         }
-        mark(a, s, 18);
+        mark(a, g, s, 18);
         rmsnorm_regs_to_x<SH>(vv, acc, xq, xh, red);
       }
     }
@@ -762,7 +770,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     if (g == 0 && a.x_rec && poller)
       for (int j = threadIdx.x; j < D; j += NPT) a.x_rec[(size_t)s * D + j] = xh[j];
 
-    mark(a, s, 1);
+    mark(a, g, s, 1);
     // ---- S1: routing ----------------------------------------------------
     if (f.own) {
       uint64_t* lr = X + a.xo_logr + (size_t)par * a.xs_logr;
@@ -775,22 +783,22 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         if (lane == 0 && e < E) st_tag(lr + e, tag, v);
       }
       if (!flush_pred()) break;
-      mark(a, s, 12);
+      mark(a, g, s, 12);
       if (!poll_all<SH::MAXI_E>(E, tag, [&](int i) { return lr + i; },
                                 [&](int i, float v) { lg[i] = v; }, c, &mi->abort))
         break;
-      mark(a, s, 10);
+      mark(a, g, s, 10);
       compute_route(Rt, lay, s);
     } else if (Rt.step != s) {  // not routed ahead (first step of a launch)
       if (!route_from_pred(Rt, t, N, lay, s)) break;
     }
-    mark(a, s, 11);
+    mark(a, g, s, 11);
     if (g == 0 && threadIdx.x < K) {
       if (a.idx_rec) a.idx_rec[(size_t)s * K + threadIdx.x] = Rt.idx[threadIdx.x];
       if (a.w_rec) a.w_rec[(size_t)s * K + threadIdx.x] = Rt.w[threadIdx.x];
     }
 
-    mark(a, s, 2);
+    mark(a, g, s, 2);
     // ---- S2: expert weights of this step, then compute ------------------
     // Gate/up rows (and head rows, unless staged ahead) by waves 0-3, needed
     // at once; down rows by waves 4-7, needed from S3 on.
@@ -803,7 +811,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       __syncthreads();
     }
 
-    mark(a, s, 3);
+    mark(a, g, s, 3);
     // LoRA-A rows first, so that their exchange overlaps the gate/up rows
     {
       uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
@@ -888,7 +896,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     }
     __syncthreads();
 
-    mark(a, s, 4);
+    mark(a, g, s, 4);
     // ---- ahead: the next step's router / head rows and mixing data --------
     // (expert weights are staged in their own step: staging them here delays
     // the exchanges queued behind the copies)
@@ -911,7 +919,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       }
     }
 
-    mark(a, s, 13);
+    mark(a, g, s, 13);
     // ---- S3: a-vectors of the XCD -> h of this workgroup's rows ---------
     {
       uint64_t* AV = X + a.xo_av + (size_t)par * a.xs_av + (size_t)x * SH::NSEGX * 2 * R;
@@ -919,7 +927,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
               nseg * 2 * R, tag, [&](int i) { return AV + i; }, [&](int i, float v) { av[i] = v; }, c,
               &mi->abort))
         break;
-      mark(a, s, 19);
+      mark(a, g, s, 19);
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
       // 16 lanes per row: the LoRA-B terms of gate and up, then a DPP sum
       static_assert(SH::RMX * 16 <= NT, "one 16-lane group per gate/up row");
@@ -947,7 +955,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
       }
       __syncthreads();
-      mark(a, s, 20);
+      mark(a, g, s, 20);
       // partial a_d[q][kk] over this workgroup's rows of segment q -> ADP
       uint64_t* ADP = X + a.xo_adp + (size_t)par * a.xs_adp +
                       ((size_t)x * NM + m) * SH::NSEGX * R;
@@ -976,7 +984,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       }
     }
 
-    mark(a, s, 5);
+    mark(a, g, s, 5);
     // ---- S4: h of the XCD -> down rows -> tagged partial of the output ---
     {
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
@@ -999,7 +1007,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
         __syncthreads();
       }
-      mark(a, s, 6);
+      mark(a, g, s, 6);
       // down matvec: lane -> 32-column chunk ch (fixed), RPID rows per wave instruction
       const int ch = lane % LPRD, sub = lane / LPRD;
       const bool active = sub < RPID;
@@ -1020,7 +1028,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
           hsum += (v4.x + v4.y) + (v4.z + v4.w);
         }
       }
-      mark(a, s, 21);
+      mark(a, g, s, 21);
       for (int rg = wave; rg * RPID < SH::DR; rg += NWV) {
         const int jj = rg * RPID + sub;
         if (active && jj < SH::DR) {
@@ -1033,7 +1041,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
       }
       __syncthreads();
-      mark(a, s, 22);
+      mark(a, g, s, 22);
       uint64_t* PART = X + a.xo_part + (size_t)par * a.xs_part + (size_t)x * D;
       // 8 threads per row: chunk partials and LoRA-B terms, then a DPP sum
       for (int b0 = 0; b0 < SH::DR * 8; b0 += NT) {
@@ -1056,9 +1064,9 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     }
     __syncthreads();
 
-    mark(a, s, 7);
+    mark(a, g, s, 7);
 
-    mark(a, s, 14);
+    mark(a, g, s, 14);
     // ---- S5: reduce the 8 XCD partials of this workgroup's rows ---------
     {
       if (has_head && g == s % NWG && (MODE == 1 || a.pidx_rec || a.pw_rec)) {
@@ -1078,7 +1086,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
               SH::RR * NX, tag, [&](int i) { return PART + (size_t)(i % NX) * D + g * SH::RR + i / NX; },
               [&](int i, float v) { yl[i] = v; }, c, &mi->abort))
         break;
-      mark(a, s, 8);
+      mark(a, g, s, 8);
       if ((int)threadIdx.x < SH::RR) {
         const int jr = threadIdx.x, j = g * SH::RR + jr;
         float y = 0.f;
@@ -1093,7 +1101,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         }
       }
       __syncthreads();
-      mark(a, s, 9);
+      mark(a, g, s, 9);
     }
   }
 
@@ -1106,6 +1114,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   if (threadIdx.x == 0) {
     const uint32_t old = atomicAdd(&a.ctl[1], 1u);
     if (old == NWG - 1) {
+      release_places(a.ctl, NX);
       __hip_atomic_store(&a.ctl[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&a.ctl[0], base + (uint32_t)a.n_steps, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);

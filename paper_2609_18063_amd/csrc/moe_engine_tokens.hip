@@ -142,6 +142,7 @@ struct TShape {
 
 struct Misc {
   int abort;
+  int x, m;  // this workgroup's XCD and member index
   int pidx[32];
   float pw[32];
 };
@@ -151,8 +152,17 @@ struct Ctl {
   uint32_t* status;
 };
 
-__device__ __forceinline__ void raise_abort(const Ctl& c) {
+// Abort: status bit and the sticky abort word; the first abort also leaves
+// its cause in control words 4..7 (reason: 1 the workgroups do not spread 32
+// per XCD, 2 wait time limit; blockIdx << 16 | wait site; then two details).
+__device__ __forceinline__ void raise_abort(const Ctl& c, uint32_t reason = 2, uint32_t site = 0,
+                                            uint32_t d0 = 0, uint32_t d1 = 0) {
   if (c.status) atomicOr(c.status, MOE_STATUS_ENGINE_ABORT);
+  if (atomicCAS(&c.ctl[4], 0u, reason) == 0u) {
+    __hip_atomic_store(&c.ctl[5], ((uint32_t)blockIdx.x << 16) | site, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&c.ctl[6], d0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&c.ctl[7], d1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   __hip_atomic_store(&c.ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -162,7 +172,7 @@ __device__ __forceinline__ void raise_abort(const Ctl& c) {
 // or another workgroup raised the abort word.
 template <int MAXI, typename AddrF, typename StoreF>
 __device__ bool poll_all(int tid, int count, uint32_t tag, AddrF addr, StoreF store, const Ctl& c,
-                         int* sh_abort) {
+                         int* sh_abort, uint32_t site = 0) {
   constexpr int G = 4;
   long spin = 0;
   bool fail = false;
@@ -185,7 +195,7 @@ __device__ bool poll_all(int tid, int count, uint32_t tag, AddrF addr, StoreF st
         }
       if (!pending) break;
       if (++spin > kSpinMax) {
-        raise_abort(c);
+        raise_abort(c, 2, site, tag, (uint32_t)(tid + q0 * NT));
         fail = true;
       } else if ((spin & 63) == 0 && ld_u32(&c.ctl[2])) {
         fail = true;
@@ -199,35 +209,6 @@ __device__ bool poll_all(int tid, int count, uint32_t tag, AddrF addr, StoreF st
   const bool ok = *sh_abort == 0;
   __syncthreads();
   return ok;
-}
-
-// The same by one wave: lane l polls items l + 64 q. No barrier; false on a
-// time limit or an abort (the caller raises sh_abort for its workgroup).
-template <typename AddrF, typename StoreF>
-__device__ bool wave_poll(int count, uint32_t tag, AddrF addr, StoreF store, const Ctl& c) {
-  const int lane = threadIdx.x & 63;
-  long spin = 0;
-  for (int i0 = 0; i0 < count; i0 += 64) {
-    const int i = i0 + lane;
-    bool done = i >= count;
-    while (!__all(done)) {
-      if (!done) {
-        const uint64_t v = ld_tag(addr(i));
-        if ((uint32_t)(v >> 32) == tag) {
-          store(i, __uint_as_float((uint32_t)v));
-          done = true;
-        }
-      }
-      if (__all(done)) break;
-      if (++spin > kSpinMax) {
-        if (lane == 0) raise_abort(c);
-        return false;
-      }
-      if ((spin & 63) == 0 && ld_u32(&c.ctl[2])) return false;
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  return true;
 }
 
 // fp16 row (global, D halves) held as this lane's D/512 16-byte chunks
@@ -332,9 +313,8 @@ __device__ double block_sum_f64(double v, double* red) {
 // Phase timestamps for the profiling hook: thread 0 of members 0, 1 and 31 of
 // XCD 0 writes the constant-rate wall clock at the marks of its steps.
 constexpr int kProfMarks = 24;
-__device__ __forceinline__ void mark(const EngineArgs& a, int s, int k) {
+__device__ __forceinline__ void mark(const EngineArgs& a, int g, int s, int k) {
   if (!a.phase_ts || threadIdx.x != 0) return;
-  const int g = blockIdx.x;
   const int slot = g == 0 ? 0 : (g == NX ? 1 : (g == NWG - NX ? 2 : -1));
   if (slot < 0) return;
   a.phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
@@ -373,9 +353,22 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   char* const bund_lds = smem + SH::O_SB;
   const bool stage_bund = a.n_slots <= SH::SLX;  // else the bundles are read from the table
 
-  const int g = blockIdx.x;
-  const int x = g % NX, m = g / NX;
   const int tid0 = threadIdx.x;
+  if (tid0 == 0) {
+    mi->abort = 0;
+    int px = 0, pm = 0;
+    if (!eng::claim_place(a.ctl, NX, NM, &px, &pm)) {
+      raise_abort(Ctl{a.ctl, a.status}, 1, 0, eng::xcc_id(), (uint32_t)pm);
+      mi->abort = 1;
+    }
+    mi->x = px;
+    mi->m = pm;
+    if (ld_u32(&a.ctl[2])) mi->abort = 1;
+  }
+  __syncthreads();
+  // XCD and member index (uniform)
+  const int x = __builtin_amdgcn_readfirstlane(mi->abort ? 0 : mi->x);
+  const int m = __builtin_amdgcn_readfirstlane(mi->abort ? 0 : mi->m);
   const int wave = __builtin_amdgcn_readfirstlane(tid0 >> 6), lane0 = tid0 & 63;
   const Ctl c{a.ctl, a.status};
   const int K = a.K, E = a.E, n_list = K + a.S;
@@ -398,16 +391,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   uint64_t* const HV = a.xw + a.xo_hv + (size_t)x * a.xs_hv;
   uint64_t* const ADP = a.xw + a.xo_adp + (size_t)x * a.xs_adp;
 
-  if (tid0 == 0) {
-    mi->abort = 0;
-    if ((int)eng::xcc_id() != x) {  // the work split relies on blockIdx % 8 == XCD
-      raise_abort(c);
-      mi->abort = 1;
-    }
-    if (ld_u32(&a.ctl[2])) mi->abort = 1;
-  }
   const uint32_t base = ld_u32(&a.ctl[0]);
-  __syncthreads();
 
   // ---- a step's inputs, fetched a step ahead --------------------------------
   // step_layer early, the layer's pointers later, the draws and the router
@@ -476,7 +460,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     const uint32_t tag1 = base + (uint32_t)s1 + 1u;
     uint64_t* const LG = LG0 + (size_t)((s1 / NX) & 1) * a.xs_logr;
     return poll_all<SH::MAXI_L>(tid, E, tag1, [&](int i) { return LG + i; }, [&](int i, float v) { lg[i] = v; },
-                                c, &mi->abort);
+                                c, &mi->abort, 1);
   };
   // select: softmax-top-k of lg (every thread, two barriers) into
   // routes[parity]; then wave 0 resolves the slots and bundles (staged slot
@@ -535,7 +519,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     }
     if (m == 0 && head1 && (a.pidx_rec || a.pw_rec)) {  // the head's prediction, recorded
       if (!poll_all<SH::MAXI_L>(tid, E, tag1, [&](int i) { return LH + i; }, [&](int i, float v) { lh[i] = v; },
-                                c, &mi->abort))
+                                c, &mi->abort, 4))
         return false;
       eng::block_topk(lh, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_cand, tk_sorted);
       if (tid < K) {
@@ -642,7 +626,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     int tid = tid0, lane = lane0;
     asm volatile("" : "+v"(tid), "+v"(lane));
     const uint32_t tag = base + (uint32_t)s + 1u;
-    mark(a, s, 0);
+    mark(a, x + NX * m, s, 0);
     if (!cur_ok) {  // the same for every member of the XCD
       if (m == 0 && tid == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
       break;
@@ -665,11 +649,11 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     const uint8_t* const* const dn_q = dn_q2 + par * 2 * SH::NDX;
     const uint8_t* const* const dn_s = dn_q + SH::NDX;
     if (next_ok) stage_slots(lay1, lane);
-    mark(a, s, 10);
+    mark(a, x + NX * m, s, 10);
     // ---- the next step's routing, first half: its x and router rows -----------
     // (into the other parity's x buffer; the fetched inputs die here)
     if (next_ok) route_publish(s1, tid, lane);
-    mark(a, s, 11);
+    mark(a, x + NX * m, s, 11);
 
     // ---- LoRA-A rows of the step: row ar = m + 32 qa of the list's
     // (position, projection, rank) rows, published first ----------------------
@@ -689,7 +673,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       }
       if (lane == 0) st_tag(AV + ar, tag, v);
     }
-    mark(a, s, 1);
+    mark(a, x + NX * m, s, 1);
 
     // ---- LoRA-B rows of gate and up (thread t < RP: local row t), loaded
     // before the gate/up rows so that they arrive during the streaming
@@ -819,7 +803,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         if (b + 1 < SH::NBAT) gu_compute(b + 1, qB, sB);
       }
     }
-    mark(a, s, 2);
+    mark(a, x + NX * m, s, 2);
 
     // ---- the next step's routing, second half: its logits (published by every
     // member at the start of this step) -> top-k, slots, bundles; then its
@@ -831,14 +815,14 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     __syncthreads();
     if (mi->abort) break;
     if (next_ok) fill_tables(routes[par ^ 1], par ^ 1, tid);
-    mark(a, s, 3);
+    mark(a, x + NX * m, s, 3);
 
     // ---- LoRA-A products of the segments -> h of this workgroup's rows ---------
     {
       if (!poll_all<SH::MAXI_A>(tid, nseg * 2 * R, tag, [&](int i) { return AV + (size_t)k0 * 2 * R + i; },
-                                [&](int i, float v) { av[i] = v; }, c, &mi->abort))
+                                [&](int i, float v) { av[i] = v; }, c, &mi->abort, 2))
         break;
-      mark(a, s, 4);
+      mark(a, x + NX * m, s, 4);
       if (tid < RP) {
         const int q = kt - k0;
         float sg = 0.f, su = 0.f;
@@ -878,7 +862,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         if (sub == 0) st_tag(ADP + ((size_t)m * 2 + qd) * R + kkd, tag, acc);
       }
     }
-    mark(a, s, 5);
+    mark(a, x + NX * m, s, 5);
 
     // ---- down rows of this workgroup over every expert of the step -------------
     {
@@ -927,7 +911,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       }
       // the next step's LoRA-A rows (the current step's were read at its start)
       if (next_ok) stage_arows(routes[par ^ 1], lane);
-      mark(a, s, 6);
+      mark(a, x + NX * m, s, 6);
       // h of the step and the A_down partials of the XCD
       if (!poll_all<SH::MAXI_H>(
               tid, NHS + NM * 2 * R, tag,
@@ -936,9 +920,9 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
                 if (i < NHS) hx[(i >> 5) * 36 + (i & 31)] = v;
                 else adp[i - NHS] = v;
               },
-              c, &mi->abort))
+              c, &mi->abort, 3))
         break;
-      mark(a, s, 7);
+      mark(a, x + NX * m, s, 7);
       // A_down h of list position k: the partials of the workgroups whose rows
       // meet expert k, in workgroup order
       if (tid < n_list * R) {
@@ -1000,7 +984,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       dn_compute(0, dqA, dsA);
       dn_compute(NDH, dqB, dsB);
       __syncthreads();
-      mark(a, s, 8);
+      mark(a, x + NX * m, s, 8);
       // the inputs of the step after next arrive while y is summed
       fetch_rows(s2);
       // y = sum over list positions of the weighted down rows and LoRA terms
@@ -1031,7 +1015,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         if (part == 0) a.y[(size_t)s * D + (size_t)m * SH::DR + jo] = acc;
       }
       __syncthreads();
-      mark(a, s, 9);
+      mark(a, x + NX * m, s, 9);
     }
     cur_ok = next_ok;
     if (has_next && !next_ok) {  // the next step's layer is outside the table
@@ -1045,6 +1029,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   if (tid0 == 0) {
     const uint32_t old = atomicAdd(&a.ctl[1], 1u);
     if (old == NWG - 1) {
+      eng::release_places(a.ctl, NX);
       __hip_atomic_store(&a.ctl[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&a.ctl[0], base + (uint32_t)a.n_steps, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }

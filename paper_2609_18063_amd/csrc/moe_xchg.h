@@ -29,6 +29,27 @@ __device__ __forceinline__ unsigned xcc_id() {
   return v;
 }
 
+// The workgroup's place in a launch of nx * nm workgroups, one per CU: its
+// XCD from the hardware register and its member index = its arrival order
+// among the workgroups of that XCD (per-XCD counters ctl[8 + x]; the last
+// workgroup to finish the launch clears them with release_places). Each XCD
+// holds exactly nm of them, but which blockIdx lands on which XCD depends on
+// the dispatcher's state (its round robin need not start at XCD 0). Thread 0
+// calls it; false if the counts do not fit.
+constexpr int kPlaceWord = 8;
+__device__ __forceinline__ bool claim_place(uint32_t* ctl, int nx, int nm, int* x_out, int* m_out) {
+  const unsigned x = xcc_id();
+  if ((int)x >= nx) return false;
+  const uint32_t m = atomicAdd(&ctl[kPlaceWord + x], 1u);
+  *x_out = (int)x;
+  *m_out = (int)m;
+  return (int)m < nm;
+}
+__device__ __forceinline__ void release_places(uint32_t* ctl, int nx) {
+  for (int i = 0; i < nx; ++i)
+    __hip_atomic_store(&ctl[kPlaceWord + i], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ float silu(float z) { return z / (1.f + expf(-z)); }
 
 // fp64 sum over the wave (DPP on the two 32-bit halves of each step's operand)

@@ -60,13 +60,15 @@ def _run(dl, xi, torch, fn="engine_tokens", ws=None, table=None, steps=None):
     getattr(B, fn)(dl.spec, table or dl.table, arr, steps, xi_t, out["y"], ws, idx=out["idx"],
                    w=out["w"], pidx=out["pidx"], pw=out["pw"], status=out["status"])
     torch.cuda.synchronize()
-    return {k: v.cpu().numpy() for k, v in out.items()}, ws
+    res = {k: v.cpu().numpy() for k, v in out.items()}
+    res["ctl"] = ws[:32].view(torch.int32).cpu().numpy()   # control words (abort cause in 4..7)
+    return res, ws
 
 
 def _check(dl, xi, out, what, tokens=None):
     wl = dl.wl
     stats = {}
-    assert int(out["status"][0]) == 0, out["status"]
+    assert int(out["status"][0]) == 0, (out["status"], "control words", out["ctl"][:8].tolist())
     for t in (range(xi.shape[0]) if tokens is None else tokens):
         ref = oracle_token(dl, xi[t])
         exact = check_routing(out["idx"][t], out["w"][t], ref["logits"], wl.K, what, stats)

@@ -167,13 +167,13 @@ __device__ __forceinline__ void raise_abort(const Ctl& c, uint32_t reason = 2, u
 }
 
 // Every thread polls items tid + q NT (q < MAXI) of `count` tagged words until
-// each carries `tag`, storing the values; two barriers. Items are polled four
-// at a time (fewer registers held across the wait). False if a wait ran out
-// or another workgroup raised the abort word.
-template <int MAXI, typename AddrF, typename StoreF>
+// each carries `tag`, storing the values; two barriers. Items are polled G at
+// a time (G < MAXI holds fewer registers across the wait, at one memory round
+// trip per group). False if a wait ran out or another workgroup raised the
+// abort word.
+template <int MAXI, int G = 4, typename AddrF, typename StoreF>
 __device__ bool poll_all(int tid, int count, uint32_t tag, AddrF addr, StoreF store, const Ctl& c,
                          int* sh_abort, uint32_t site = 0) {
-  constexpr int G = 4;
   long spin = 0;
   bool fail = false;
 #pragma unroll
@@ -913,7 +913,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       if (next_ok) stage_arows(routes[par ^ 1], lane);
       mark(a, x + NX * m, s, 6);
       // h of the step and the A_down partials of the XCD
-      if (!poll_all<SH::MAXI_H>(
+      if (!poll_all<SH::MAXI_H, (SH::MAXI_H + 1) / 2>(
               tid, NHS + NM * 2 * R, tag,
               [&](int i) { return i < NHS ? HV + i : ADP + (i - NHS); },
               [&](int i, float v) {

@@ -284,10 +284,10 @@ int moe_engine_layers(const moe_layer_spec* spec, const moe_slot_table* table,
 
 /*
  * The same independent single-token steps and outputs as moe_engine_layers,
- * scheduled for throughput: each XCD (32 of the 256 workgroups) runs its own
- * steps s = x, x + 8, x + 16, ..., so eight steps are in flight at once and
- * the waits of one (exchanges, top-k, slot lookups) overlap the weight
- * streaming of the others. Every step is still one token through one layer
+ * scheduled for throughput: the 256 workgroups form 16 teams of 16 (two per
+ * XCD); team t runs its own steps s = t, t + 16, t + 32, ..., so sixteen
+ * steps are in flight at once and the waits of one (exchanges, top-k, slot
+ * lookups) overlap the weight streaming of the others. Every step is still one token through one layer
  * and reads its weights for that token alone; a step takes longer than under
  * moe_engine_layers, the sequence of steps less time. Results equal the
  * oracle's to the same tolerance as moe_engine_layers' (fp32 sums in another

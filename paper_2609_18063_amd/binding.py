@@ -453,7 +453,7 @@ def engine_tokens_supported(spec):
 
 def engine_tokens(spec, table, layer_arr, step_layer, xi, y, workspace, idx=None, w=None,
                   pidx=None, pw=None, status=None, stream=None):
-    """moe_engine_tokens: the steps of engine_layers, one per XCD in flight."""
+    """moe_engine_tokens: the steps of engine_layers, one per team of 16 workgroups in flight."""
     n = step_layer.numel()
     _check(lib().moe_engine_tokens(ctypes.byref(spec), table.handle, _ptr(layer_arr),
                                    _ptr(step_layer), n, _ptr(xi), _ptr(y), _ptr(idx), _ptr(w),

@@ -7,7 +7,7 @@ namespace moe {
 
 struct EngineArgs {
   int mode;          // 0: independent single-token steps; 1: decode chain;
-                     // 2: independent steps, one per XCD in flight
+                     // 2: independent steps, one per team in flight
   int n_steps;
   int L;             // chain: layers per token
   int first_token;   // chain: token index of the first step
@@ -42,8 +42,9 @@ size_t engine_workspace_words(int E, int d, int L, EngineArgs* a);
 hipError_t launch_engine(EngineArgs& a, int d, int I, int r, hipStream_t st);
 
 // Throughput schedule of independent steps (moe_engine_tokens.hip): one step
-// per XCD in flight. Uses the exchange offsets xo/xs of logr (router logits),
-// loghm (head logits), av, hv and adp, each strided per XCD.
+// per team of 16 workgroups in flight (16 teams). Uses the exchange offsets
+// xo/xs of logr (router logits), loghm (head logits), av, hv and adp, each
+// strided per team.
 bool engine_tokens_supported(int d, int I, int r, int K, int S, int E);
 size_t engine_tokens_workspace_words(int E, int d, int I, int r, int n_list, EngineArgs* a);
 hipError_t launch_engine_tokens(EngineArgs& a, int d, int I, int r, hipStream_t st);

@@ -1,35 +1,39 @@
 // Throughput schedule of independent single-token layer steps for gfx950.
 //
-// One cooperative launch of 256 workgroups (one per CU). XCD x runs the steps
-// s = x, x + 8, x + 16, ... on its own 32 workgroups, so eight steps are in
-// flight at once: while one XCD waits on an exchange, a top-k or a slot
-// lookup, the other seven stream weights. Each step is still one token
-// through one layer, and every weight byte a step reads serves that token
-// only. Exchanges never leave the XCD.
+// One cooperative launch of 256 workgroups (one per CU), split into 16 teams
+// of 16 workgroups, two teams per XCD. Team t runs the steps s = t, t + 16,
+// t + 32, ... so sixteen steps are in flight at once: while one team waits on
+// an exchange, a top-k or a slot lookup, the others stream weights. Each step
+// is still one token through one layer, and every weight byte a step reads
+// serves that token only. Exchanges never leave the XCD.
 //
-// Work split of one step on XCD x, member m (workgroup g = x + 8 m):
-//   routing  member m computes router and head rows e = m + 32 q (one per
-//            wave); the XCD exchanges the logits; every member runs the
+// Work split of one step on team t, member m (NM = 16 members):
+//   routing  member m computes router and head rows e = m + NM (w + 8 q) on
+//            wave w; the team exchanges the logits; every member runs the
 //            softmax-top-k (Appendix A) and resolves the K + S bundles
 //            through the slot table.
 //   gate/up  the K + S experts' intermediate rows lie end to end (n_list I
 //            row pairs); member m owns rows [m RP, (m + 1) RP), RP =
-//            n_list I / 32, at most two experts (segments). It streams their
-//            gate and up rows through registers, plus one of every 32 LoRA-A
+//            n_list I / NM, at most two experts (segments). It streams their
+//            gate and up rows through registers, plus one of every NM LoRA-A
 //            rows of the step (published first, so that their exchange
 //            overlaps the streaming).
 //   h        with the LoRA-A products of its segments: h = silu(g) u for its
 //            rows (Sec. 3.1 Math contract; unmerged LoRA, Sec. 3.3),
 //            published, and its partial A_down h per segment.
-//   down     member m owns output rows [m d/32, (m + 1) d/32) over all
-//            n_list I columns. Its down rows are loaded before it polls h;
-//            it then writes its rows of y = sum_k w_k y_k + y_shared
+//   down     member m owns output rows [m d/NM, (m + 1) d/NM) over all
+//            n_list I columns. Its first down rows are loaded before it polls
+//            h; it then writes its rows of y = sum_k w_k y_k + y_shared
 //            directly, so no partial sums cross workgroups.
+//
+// The streaming loops are runtime loops over batches of four wave
+// instructions held in three register buffers (two batches in flight while
+// one is computed), so the code of a step stays small.
 //
 // Exchange words are {tag, fp32} (moe_xchg.h): the tag is the step's index
 // on a device counter that persists across launches. Every exchange area is
 // used once per step and is rewritten only after every member has read it
-// (each rewrite of step s + 8 depends on an exchange that every member joins
+// (each rewrite of step s + 16 depends on an exchange that every member joins
 // after finishing step s), so no area is double-buffered.
 #include <hip/hip_runtime.h>
 
@@ -44,7 +48,10 @@ using eng::ld_tag;
 using eng::ld_u32;
 using eng::st_tag;
 
-constexpr int NX = 8, NM = 32, NWG = NX * NM, NT = 512, NWV = NT / 64;
+constexpr int NX = 8, NPX = 32, NWG = NX * NPX, NT = 512, NWV = NT / 64;  // XCDs, workgroups per XCD
+// A team is NM workgroups of one XCD that run one step at a time; NTM teams
+// (TPX per XCD) keep NTM steps in flight.
+constexpr int NM = 16, NTM = NWG / NM, TPX = NPX / NM;
 
 typedef _Float16 hv2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -95,7 +102,9 @@ struct TShape {
   static constexpr int CH = IE / 32;                          // lanes per down (row, expert) unit
   static constexpr int UPI = 64 / CH;                         // units per wave instruction
   static constexpr int DR = D / NM;                           // down rows per workgroup
-  static constexpr int NDW = (NLX * DR / UPI + NWV - 1) / NWV; // most down instructions per wave
+  static constexpr int NDH = DR / UPI < 4 ? DR / UPI : 4;     // down instructions per batch (one expert)
+  static constexpr int DRP = (DR * 8 + NT - 1) / NT;          // output-sum passes (eight lanes per row)
+  static constexpr int NRW = (EX + NM * NWV - 1) / (NM * NWV); // router (and head) rows per wave
   static constexpr int NAX = (NLX * 2 * R + NM - 1) / NM;     // most LoRA-A rows per workgroup
   static constexpr int NPA = (RPX + 15) / 16;                 // rows per lane of an A_down term
   static constexpr int NEF = (NLX + 7) / 8;                   // experts per lane of the output sum
@@ -105,10 +114,10 @@ struct TShape {
   static constexpr int MAXI_A = (2 * 2 * R + NT - 1) / NT;    // polled LoRA-A products
   static_assert(D % 512 == 0 && IE % 64 == 0 && D % NM == 0, "shape");
   static_assert(RPX <= IE, "a workgroup's rows span at most two experts");
-  static_assert(DR % UPI == 0, "a down instruction stays inside one expert");
+  static_assert(DR % (UPI * NDH) == 0, "a down batch stays inside one expert");
   static_assert(2 * R * 16 <= NT && R % 8 == 0, "one 16-lane group per A_down term");
-  static_assert(DR * 8 <= NT, "eight lanes per output row");
-  static_assert(EX <= 256 && (EX + NM - 1) / NM <= NWV, "one router row per wave");
+  static_assert(DR * 8 <= NT || DR * 8 % NT == 0, "eight lanes per output row");
+  static_assert(EX <= 256 && NRW <= 2, "at most two router rows per wave");
   static_assert(LPR != 64 || NB % 4 == 0, "whole-wave rows are summed four at a time");
   // LDS layout (bytes)
   static constexpr int NBAT = (NGW + NB - 1) / NB;            // gate/up batches per wave
@@ -131,8 +140,9 @@ struct TShape {
   static constexpr int O_AR = O_DNT + 2 * 2 * NDX * 8;    // [NAX][D] fp16 LoRA-A rows of the next step
   static constexpr int SOX = (EX + 32 + 63) / 64 * 64;    // slot-map entries staged (routed + shared ids)
   static constexpr int O_SO = O_AR + NAX * D * 2;         // [SOX] int32 slot map of the next step's layer
-  static constexpr int SLX = 320;                          // most slots per layer whose bundles are staged
   static constexpr int O_SB = O_SO + SOX * 4;             // [SLX] bundles of the next step's layer
+  // most slots per layer whose bundles are staged (none when they do not fit)
+  static constexpr int SLX = O_SB + 320 * 96 + NWV * 8 + 1024 <= 160 * 1024 ? 320 : 0;
   static constexpr int O_RED = O_SB + SLX * 96;           // [NWV] fp64
   static constexpr int O_MISC = O_RED + NWV * 8;          // Misc
   static constexpr int LDS_USED = O_MISC + 1024;
@@ -315,7 +325,7 @@ __device__ double block_sum_f64(double v, double* red) {
 constexpr int kProfMarks = 24;
 __device__ __forceinline__ void mark(const EngineArgs& a, int g, int s, int k) {
   if (!a.phase_ts || threadIdx.x != 0) return;
-  const int slot = g == 0 ? 0 : (g == NX ? 1 : (g == NWG - NX ? 2 : -1));
+  const int slot = g == 0 ? 0 : (g == NTM ? 1 : (g == NWG - NTM ? 2 : -1));
   if (slot < 0) return;
   a.phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
 }
@@ -357,19 +367,20 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   if (tid0 == 0) {
     mi->abort = 0;
     int px = 0, pm = 0;
-    if (!eng::claim_place(a.ctl, NX, NM, &px, &pm)) {
+    if (!eng::claim_place(a.ctl, NX, NPX, &px, &pm)) {
       raise_abort(Ctl{a.ctl, a.status}, 1, 0, eng::xcc_id(), (uint32_t)pm);
       mi->abort = 1;
     }
-    mi->x = px;
-    mi->m = pm;
+    mi->x = px + NX * (pm / NM);  // team
+    mi->m = pm % NM;             // member of the team
     if (ld_u32(&a.ctl[2])) mi->abort = 1;
   }
   __syncthreads();
   // XCD and member index (uniform)
   const int x = __builtin_amdgcn_readfirstlane(mi->abort ? 0 : mi->x);
   const int m = __builtin_amdgcn_readfirstlane(mi->abort ? 0 : mi->m);
-  const int wave = __builtin_amdgcn_readfirstlane(tid0 >> 6), lane0 = tid0 & 63;
+  int wave = __builtin_amdgcn_readfirstlane(tid0 >> 6);  // passed through an empty asm each step
+  const int lane0 = tid0 & 63;
   const Ctl c{a.ctl, a.status};
   const int K = a.K, E = a.E, n_list = K + a.S;
   const int RP = n_list * IE / NM;           // row pairs of this workgroup
@@ -380,7 +391,6 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   const int NG = 2 * RP / SH::RPI;           // gate/up wave instructions
   const int DI = SH::DR / SH::UPI;           // down instructions per expert
   const int NDI = n_list * DI;               // down instructions
-  const int ndw = (NDI + NWV - 1) / NWV;     // per wave, contiguous
   const int NA = n_list * 2 * R;             // LoRA-A rows of a step
   const int NHS = n_list * IE;               // h entries of a step
 
@@ -395,15 +405,19 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
 
   // ---- a step's inputs, fetched a step ahead --------------------------------
   // step_layer early, the layer's pointers later, the draws and the router
-  // and head rows at the end of the step before: each load is consumed long
-  // after it is issued, so no wait lands in the middle of a step.
+  // rows at the end of the step before: each load is consumed long after it
+  // is issued, so no wait lands in the middle of a step. The head rows are
+  // loaded when the step's routing starts and consumed after the LoRA-A
+  // products.
   constexpr int XPT = D / NT;
   float xin[XPT];
-  U4 rrow[D / 512], hrow[D / 512];
-  const int e_row = m + NM * wave;  // this wave's router and head row
+  U4 rrow[SH::NRW][D / 512];
+  typedef U4 HRows[SH::NRW][D / 512];
+  // this wave's router and head rows e = m + NM (wave + NWV q)
+  auto e_row = [&](int q) { return m + NM * (wave + NWV * q); };
   int lay_f = -1, lay_n = -1;       // the layer of the fetched inputs; of the next fetch
   bool head_f = false;
-  const __half *rt_n = nullptr, *hd_n = nullptr;
+  const __half *rt_n = nullptr, *hd_n = nullptr, *hd_f = nullptr;
   auto layer_ok = [&](int l) { return l >= 0 && l < a.n_table_layers; };
   auto fetch_layer = [&]() {
     rt_n = hd_n = nullptr;
@@ -419,19 +433,30 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     for (int q = 0; q < XPT; ++q) xin[q] = a.xi[(size_t)s1 * D + tid0 + q * NT];
     lay_f = lay_n;
     head_f = layer_ok(lay_f) && hd_n != nullptr;
-    const bool rows = layer_ok(lay_f) && e_row < E;
-    const __half* rsrc = rows ? rt_n + (size_t)e_row * D : reinterpret_cast<const __half*>(a.xi);
-    const __half* hsrc = rows && head_f ? hd_n + (size_t)e_row * D : rsrc;
-    row_load<D>(rrow, rsrc, lane0);
-    row_load<D>(hrow, hsrc, lane0);
+    hd_f = hd_n;
+#pragma unroll
+    for (int q = 0; q < SH::NRW; ++q) {
+      const bool rows = layer_ok(lay_f) && e_row(q) < E;
+      const __half* rsrc = rows ? rt_n + (size_t)e_row(q) * D : reinterpret_cast<const __half*>(a.xi);
+      row_load<D>(rrow[q], rsrc, lane0);
+    }
   };
 
   // ---- routing of step s1, in two halves -----------------------------------
+  // the head rows of the fetched step (on = it is routed here); every
+  // register of hr is written on every path
+  auto head_load = [&](bool on, HRows& hr, int lane) {
+#pragma unroll
+    for (int q = 0; q < SH::NRW; ++q) {
+      const bool rows = on && head_f && e_row(q) < E;
+      row_load<D>(hr[q], rows ? hd_f + (size_t)e_row(q) * D : reinterpret_cast<const __half*>(a.xi), lane);
+    }
+  };
   // publish: x = fp16(rmsnorm(xi)) (single rounding from fp64) and this
-  // workgroup's router and head logits. Uses the fetched inputs.
+  // workgroup's router logits. Uses the fetched inputs.
   auto route_publish = [&](int s1, int tid, int lane) {
     const uint32_t tag1 = base + (uint32_t)s1 + 1u;
-    const int par1 = (s1 / NX) & 1;
+    const int par1 = (s1 / NTM) & 1;
     __half* const xh = xh2 + par1 * D;
     __half* const xq = xq2 + par1 * D;
     double acc = 0.0;
@@ -446,19 +471,33 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       xq[eng::pair_pos(j)] = h;
     }
     __syncthreads();
-    if (e_row < E) {
-      const float v = row_dot<D>(rrow, xh, lane);
-      if (lane == 0) st_tag(LG0 + (size_t)par1 * a.xs_logr + e_row, tag1, v);
-      if (head_f) {
-        const float vh = row_dot<D>(hrow, xh, lane);
-        if (lane == 0) st_tag(LH0 + (size_t)par1 * a.xs_logr + e_row, tag1, vh);
-      }
+#pragma unroll
+    for (int q = 0; q < SH::NRW; ++q) {
+      const int e = e_row(q);
+      if (e >= E) continue;
+      const float v = row_dot<D>(rrow[q], xh, lane);
+      if (lane == 0) st_tag(LG0 + (size_t)par1 * a.xs_logr + e, tag1, v);
+    }
+  };
+  // the head logits of step s1 (after route_publish, whose barrier made x
+  // visible)
+  auto head_publish = [&](int s1, const HRows& hr, int lane) {
+    if (!head_f) return;
+    const uint32_t tag1 = base + (uint32_t)s1 + 1u;
+    const int par1 = (s1 / NTM) & 1;
+    const __half* const xh = xh2 + par1 * D;
+#pragma unroll
+    for (int q = 0; q < SH::NRW; ++q) {
+      const int e = e_row(q);
+      if (e >= E) continue;
+      const float vh = row_dot<D>(hr[q], xh, lane);
+      if (lane == 0) st_tag(LH0 + (size_t)par1 * a.xs_logr + e, tag1, vh);
     }
   };
   // poll: the step's router logits into lg (every thread). False on abort.
   auto route_poll = [&](int s1, int tid) -> bool {
     const uint32_t tag1 = base + (uint32_t)s1 + 1u;
-    uint64_t* const LG = LG0 + (size_t)((s1 / NX) & 1) * a.xs_logr;
+    uint64_t* const LG = LG0 + (size_t)((s1 / NTM) & 1) * a.xs_logr;
     return poll_all<SH::MAXI_L>(tid, E, tag1, [&](int i) { return LG + i; }, [&](int i, float v) { lg[i] = v; },
                                 c, &mi->abort, 1);
   };
@@ -470,7 +509,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
   // on abort. The caller's next barrier publishes routes[parity].
   auto route_select = [&](int s1, int lay1, bool head1, int tid, int lane) -> bool {
     const uint32_t tag1 = base + (uint32_t)s1 + 1u;
-    const int par1 = (s1 / NX) & 1;
+    const int par1 = (s1 / NTM) & 1;
     uint64_t* const LH = LH0 + (size_t)par1 * a.xs_logr;
     Route<NLX>& rt = routes[par1];
     eng::block_topk(lg, E, K, rt.idx, rt.w, tk_keys, tk_part, tk_cand, tk_sorted);
@@ -549,7 +588,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       }
     }
   };
-  // This wave's LoRA-A rows of a resolved step (rows ar = m + 32 qa, qa =
+  // This wave's LoRA-A rows of a resolved step (rows ar = m + NM qa, qa =
   // wave, wave + 8, ...), staged into arow[qa]; the wave reads them after its
   // own dma_wait.
   auto stage_arows = [&](const Route<NLX>& r1, int lane) {
@@ -592,7 +631,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     }
   };
 
-  // ---- first step of this XCD: routed before the loop ------------------------
+  // ---- first step of this team: routed before the loop -----------------------
   int lay = -1;      // layer of the current step
   bool cur_ok = false;
   if (x < a.n_steps && !mi->abort) {
@@ -603,61 +642,164 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     cur_ok = layer_ok(lay);
     if (cur_ok) {
       const bool head0 = head_f;
-      route_publish(x, tid0, lane0);
-      lay_n = a.step_layer[x + NX < a.n_steps ? x + NX : x];
+      {
+        HRows hr;
+        head_load(true, hr, lane0);
+        route_publish(x, tid0, lane0);
+        head_publish(x, hr, lane0);
+      }
+      lay_n = a.step_layer[x + NTM < a.n_steps ? x + NTM : x];
       fetch_layer();
       stage_slots(lay, lane0);
       eng::dma_wait();
       if (route_poll(x, tid0) && route_select(x, lay, head0, tid0, lane0)) {
         __syncthreads();
         if (!mi->abort) {
-          fill_tables(routes[(x / NX) & 1], (x / NX) & 1, tid0);
-          stage_arows(routes[(x / NX) & 1], lane0);
-          fetch_rows(x + NX < a.n_steps ? x + NX : x);
+          fill_tables(routes[(x / NTM) & 1], (x / NTM) & 1, tid0);
+          stage_arows(routes[(x / NTM) & 1], lane0);
+          fetch_rows(x + NTM < a.n_steps ? x + NTM : x);
         }
       }
     }
   }
 
-  for (int s = x; s < a.n_steps && !mi->abort; s += NX) {
+  for (int s = x; s < a.n_steps && !mi->abort; s += NTM) {
     // The thread's index passes through an empty asm each step, so that the
     // compiler recomputes the addresses derived from it inside the step
     // rather than keeping all of them in registers across the loop.
     int tid = tid0, lane = lane0;
-    asm volatile("" : "+v"(tid), "+v"(lane));
+    asm volatile("" : "+v"(tid), "+v"(lane), "+s"(wave));
     const uint32_t tag = base + (uint32_t)s + 1u;
-    mark(a, x + NX * m, s, 0);
-    if (!cur_ok) {  // the same for every member of the XCD
+    mark(a, x + NTM * m, s, 0);
+    if (!cur_ok) {  // the same for every member of the team
       if (m == 0 && tid == 0 && a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
       break;
     }
-    const int par = (s / NX) & 1;
+    const int par = (s / NTM) & 1;
     const Route<NLX>& rt = routes[par];
     const __half* const xh = xh2 + par * D;
     const __half* const xq = xq2 + par * D;
-    // the next step of this XCD, routed during this one (its inputs are in
+    // the next step of this team, routed during this one (its inputs are in
     // xin / rrow / hrow, its layer in lay_f)
-    const int s1 = s + NX;
+    const int s1 = s + NTM;
     const bool has_next = s1 < a.n_steps;
     const int lay1 = lay_f;
     const bool next_ok = has_next && layer_ok(lay1);
     const bool head1 = head_f;
-    const int s2 = s1 + NX < a.n_steps ? s1 + NX : (has_next ? s1 : s);
+    const int s2 = s1 + NTM < a.n_steps ? s1 + NTM : (has_next ? s1 : s);
     lay_n = a.step_layer[s2];
     const uint8_t* const* const gu_q = gu_q2 + par * 4 * SH::RPX;
     const uint8_t* const* const gu_s = gu_q + 2 * SH::RPX;
     const uint8_t* const* const dn_q = dn_q2 + par * 2 * SH::NDX;
     const uint8_t* const* const dn_s = dn_q + SH::NDX;
-    if (next_ok) stage_slots(lay1, lane);
-    mark(a, x + NX * m, s, 10);
-    // ---- the next step's routing, first half: its x and router rows -----------
-    // (into the other parity's x buffer; the fetched inputs die here)
-    if (next_ok) route_publish(s1, tid, lane);
-    mark(a, x + NX * m, s, 11);
-
-    // ---- LoRA-A rows of the step: row ar = m + 32 qa of the list's
-    // (position, projection, rank) rows, published first ----------------------
+    // ---- gate/up rows (raw int4 matvecs), set up and first two batches issued
     eng::dma_wait();  // this wave's LoRA-A rows, staged during the previous step
+    // Item t < RP is the gate row of local row t, item RP + t its up row.
+    // Codes become fp16 pairs q 2^-24 (exact subnormals) under one mask and
+    // meet x in its pair order in v_dot2_f32_f16; 2^24 goes into the scale.
+    // Batches of NB wave instructions in three register buffers: two batches
+    // are in flight while one is computed. The first two are issued at the
+    // start of the step, ahead of the routing work.
+    const int c0 = lane % SH::LPR, gsub = SH::RPI == 1 ? 0 : lane / SH::LPR;
+    hv2 xp[SH::CPL][16];
+    float xs[SH::CPL];
+    const hv2 one2 = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+    for (int cc = 0; cc < SH::CPL; ++cc) {
+      const int ch = c0 + SH::LPR * cc;
+      const U4* src = reinterpret_cast<const U4*>(xq + ch * 32);
+      float sacc = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const U4 v = src[i];
+        xp[cc][4 * i + 0] = __builtin_bit_cast(hv2, v.x);
+        xp[cc][4 * i + 1] = __builtin_bit_cast(hv2, v.y);
+        xp[cc][4 * i + 2] = __builtin_bit_cast(hv2, v.z);
+        xp[cc][4 * i + 3] = __builtin_bit_cast(hv2, v.w);
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sacc = __builtin_amdgcn_fdot2(xp[cc][i], one2, sacc, false);
+      xs[cc] = sacc;
+    }
+    typedef U4 QB[SH::NB][SH::CPL];
+    typedef uint32_t SB[SH::NB][SH::CPL];
+    // rows come from the step's address table (the compiler keeps no
+    // per-row address in registers across the batches)
+    const int nbat = ((NG + NWV - 1) / NWV + SH::NB - 1) / SH::NB;  // batches per wave (most)
+    // (loads past the last batch read the first bytes of the draws, which
+    // the caches hold: a load skipped on some paths would keep its registers
+    // live across the whole step)
+    const uint8_t* const hot = reinterpret_cast<const uint8_t*>(a.xi);
+    auto gu_load = [&](int b, QB& qv, SB& szw) {
+      const uint8_t* pq[SH::NB];
+      const uint8_t* ps[SH::NB];
+#pragma unroll
+      for (int j = 0; j < SH::NB; ++j) {
+        int n = wave + NWV * (b * SH::NB + j);  // wave-uniform
+        const bool in = b < nbat;
+        if (n >= NG) n = NG - 1;                // loaded again, not stored
+        const int t = n * SH::RPI + gsub;
+        pq[j] = in ? gu_q[t] : hot;
+        ps[j] = in ? gu_s[t] : hot;
+      }
+#pragma unroll
+      for (int j = 0; j < SH::NB; ++j) {
+#pragma unroll
+        for (int cc = 0; cc < SH::CPL; ++cc) {
+          const int ch = c0 + SH::LPR * cc;
+          qv[j][cc] = ldw16(pq[j] + ch * 16);
+          szw[j][cc] = ldw4(ps[j] + (ch >> 1) * 4);
+        }
+      }
+    };
+    auto gu_row = [&](const U4 (&qv)[SH::CPL], const uint32_t (&szw)[SH::CPL]) {
+      float acc = 0.f;
+#pragma unroll
+      for (int cc = 0; cc < SH::CPL; ++cc) {
+        const float2 sz = h2f2(szw[cc]);
+        acc += (sz.x * 16777216.f) * dot32_codes(qv[cc], xp[cc]) + sz.y * xs[cc];
+      }
+      return acc;
+    };
+    auto gu_compute = [&](int b, const QB& qv, const SB& szw) {
+      if constexpr (SH::LPR == 64) {  // one row per instruction: sum four rows at once
+#pragma unroll
+        for (int j = 0; j < SH::NB; j += 4) {
+          const int n0 = wave + NWV * (b * SH::NB + j);
+          if (n0 >= NG) continue;
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = n0 + NWV * r < NG ? gu_row(qv[j + r], szw[j + r]) : 0.f;
+          const float tot = rows4_sum(v[0], v[1], v[2], v[3], lane);
+          const int nr = n0 + NWV * (lane & 3);
+          if (lane < 4 && nr < NG) gxu[nr] = tot;
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < SH::NB; ++j) {
+          const int n = wave + NWV * (b * SH::NB + j);
+          if (n >= NG) continue;
+          const float acc = group_sum(gu_row(qv[j], szw[j]), SH::LPR);
+          if (c0 == 0) gxu[n * SH::RPI + gsub] = acc;
+        }
+      }
+    };
+    QB q0, q1, q2;
+    SB z0, z1, z2;
+    gu_load(0, q0, z0);
+    gu_load(1, q1, z1);
+    if (next_ok) stage_slots(lay1, lane);
+    mark(a, x + NTM * m, s, 10);
+    // ---- the next step's routing, first half: its x and router rows -----------
+    // (into the other parity's x buffer; the fetched inputs die here); the
+    // head rows are loaded meanwhile and dotted after the LoRA-A products
+    HRows hr;
+    head_load(next_ok, hr, lane);
+    if (next_ok) route_publish(s1, tid, lane);
+    mark(a, x + NTM * m, s, 11);
+
+    // ---- LoRA-A rows of the step: row ar = m + NM qa of the list's
+    // (position, projection, rank) rows, published first ----------------------
     for (int qa = wave; qa < SH::NAX; qa += NWV) {
       const int ar = m + NM * qa;
       if (ar >= NA) break;
@@ -673,7 +815,8 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       }
       if (lane == 0) st_tag(AV + ar, tag, v);
     }
-    mark(a, x + NX * m, s, 1);
+    if (next_ok) head_publish(s1, hr, lane);
+    mark(a, x + NTM * m, s, 1);
 
     // ---- LoRA-B rows of gate and up (thread t < RP: local row t), loaded
     // before the gate/up rows so that they arrive during the streaming
@@ -708,106 +851,21 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
             ldg2(reinterpret_cast<const __half*>(rt.bd[kd].down.lora_a) + (size_t)kkd * IE + row0 + p - kd * IE)));
     }
 
-    // ---- gate/up rows (raw int4 matvecs) ------------------------------------
-    // Item t < RP is the gate row of local row t, item RP + t its up row.
-    // Codes become fp16 pairs q 2^-24 (exact subnormals) under one mask and
-    // meet x in its pair order in v_dot2_f32_f16; 2^24 goes into the scale.
-    // Two batches of loads in flight per wave (double-buffered registers).
-    {
-      const int c0 = lane % SH::LPR, sub = SH::RPI == 1 ? 0 : lane / SH::LPR;
-      hv2 xp[SH::CPL][16];
-      float xs[SH::CPL];
-      const hv2 one2 = {(_Float16)1.0f, (_Float16)1.0f};
-#pragma unroll
-      for (int cc = 0; cc < SH::CPL; ++cc) {
-        const int ch = c0 + SH::LPR * cc;
-        const U4* src = reinterpret_cast<const U4*>(xq + ch * 32);
-        float sacc = 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const U4 v = src[i];
-          xp[cc][4 * i + 0] = __builtin_bit_cast(hv2, v.x);
-          xp[cc][4 * i + 1] = __builtin_bit_cast(hv2, v.y);
-          xp[cc][4 * i + 2] = __builtin_bit_cast(hv2, v.z);
-          xp[cc][4 * i + 3] = __builtin_bit_cast(hv2, v.w);
-        }
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sacc = __builtin_amdgcn_fdot2(xp[cc][i], one2, sacc, false);
-        xs[cc] = sacc;
-      }
-      typedef U4 QB[SH::NB][SH::CPL];
-      typedef uint32_t SB[SH::NB][SH::CPL];
-      // rows come from the step's address table (the compiler keeps no
-      // per-row address in registers across the batches)
-      auto gu_load = [&](int b, QB& qv, SB& szw) {
-        const uint8_t* pq[SH::NB];
-        const uint8_t* ps[SH::NB];
-#pragma unroll
-        for (int j = 0; j < SH::NB; ++j) {
-          int n = wave + NWV * (b * SH::NB + j);  // wave-uniform
-          if (n >= NG) n = NG - 1;                // loaded again, not stored
-          const int t = n * SH::RPI + sub;
-          pq[j] = gu_q[t];
-          ps[j] = gu_s[t];
-        }
-#pragma unroll
-        for (int j = 0; j < SH::NB; ++j) {
-#pragma unroll
-          for (int cc = 0; cc < SH::CPL; ++cc) {
-            const int ch = c0 + SH::LPR * cc;
-            qv[j][cc] = ldw16(pq[j] + ch * 16);
-            szw[j][cc] = ldw4(ps[j] + (ch >> 1) * 4);
-          }
-        }
-      };
-      auto gu_row = [&](const U4 (&qv)[SH::CPL], const uint32_t (&szw)[SH::CPL]) {
-        float acc = 0.f;
-#pragma unroll
-        for (int cc = 0; cc < SH::CPL; ++cc) {
-          const float2 sz = h2f2(szw[cc]);
-          acc += (sz.x * 16777216.f) * dot32_codes(qv[cc], xp[cc]) + sz.y * xs[cc];
-        }
-        return acc;
-      };
-      auto gu_compute = [&](int b, const QB& qv, const SB& szw) {
-        if constexpr (SH::LPR == 64) {  // one row per instruction: sum four rows at once
-#pragma unroll
-          for (int j = 0; j < SH::NB; j += 4) {
-            const int n0 = wave + NWV * (b * SH::NB + j);
-            if (n0 >= NG) continue;
-            float v[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = n0 + NWV * r < NG ? gu_row(qv[j + r], szw[j + r]) : 0.f;
-            const float tot = rows4_sum(v[0], v[1], v[2], v[3], lane);
-            const int nr = n0 + NWV * (lane & 3);
-            if (lane < 4 && nr < NG) gxu[nr] = tot;
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < SH::NB; ++j) {
-            const int n = wave + NWV * (b * SH::NB + j);
-            if (n >= NG) continue;
-            const float acc = group_sum(gu_row(qv[j], szw[j]), SH::LPR);
-            if (c0 == 0) gxu[n * SH::RPI + sub] = acc;
-          }
-        }
-      };
-      QB qA, qB;
-      SB sA, sB;
-      gu_load(0, qA, sA);
-#pragma unroll
-      for (int b = 0; b < SH::NBAT; b += 2) {
-        if (b + 1 < SH::NBAT) gu_load(b + 1, qB, sB);
-        gu_compute(b, qA, sA);
-        if (b + 2 < SH::NBAT) gu_load(b + 2, qA, sA);
-        if (b + 1 < SH::NBAT) gu_compute(b + 1, qB, sB);
-      }
+    // ---- gate/up rows: the batch loop ----------------------------------------
+    for (int b = 0; b < nbat; b += 3) {
+      gu_load(b + 2, q2, z2);
+      gu_compute(b, q0, z0);
+      gu_load(b + 3, q0, z0);
+      gu_compute(b + 1, q1, z1);
+      gu_load(b + 4, q1, z1);
+      gu_compute(b + 2, q2, z2);
     }
-    mark(a, x + NX * m, s, 2);
+    mark(a, x + NTM * m, s, 2);
 
     // ---- the next step's routing, second half: its logits (published by every
     // member at the start of this step) -> top-k, slots, bundles; then its
     // address tables ------------------------------------------------------------
+    eng::dma_wait();  // this wave's copies of the slot map and bundles
     if (next_ok) {
       if (!route_poll(s1, tid)) break;
       if (!route_select(s1, lay1, head1, tid, lane)) break;
@@ -815,14 +873,14 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
     __syncthreads();
     if (mi->abort) break;
     if (next_ok) fill_tables(routes[par ^ 1], par ^ 1, tid);
-    mark(a, x + NX * m, s, 3);
+    mark(a, x + NTM * m, s, 3);
 
     // ---- LoRA-A products of the segments -> h of this workgroup's rows ---------
     {
       if (!poll_all<SH::MAXI_A>(tid, nseg * 2 * R, tag, [&](int i) { return AV + (size_t)k0 * 2 * R + i; },
                                 [&](int i, float v) { av[i] = v; }, c, &mi->abort, 2))
         break;
-      mark(a, x + NX * m, s, 4);
+      mark(a, x + NTM * m, s, 4);
       if (tid < RP) {
         const int q = kt - k0;
         float sg = 0.f, su = 0.f;
@@ -862,27 +920,31 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         if (sub == 0) st_tag(ADP + ((size_t)m * 2 + qd) * R + kkd, tag, acc);
       }
     }
-    mark(a, x + NX * m, s, 5);
+    mark(a, x + NTM * m, s, 5);
 
     // ---- down rows of this workgroup over every expert of the step -------------
     {
-      // this wave's instructions n = wave ndw + j: list position n / DI, rows
-      // (n % DI) UPI + lane / CH, 32-column chunk lane % CH
+      // Batches of NDH consecutive instructions n, all of one list position
+      // k = n / DI (rows (n % DI) UPI + lane / CH, 32-column chunk lane % CH);
+      // wave w takes batches [w nbw, (w + 1) nbw). Three register buffers:
+      // the first two batches are loaded before the waits of this phase, each
+      // later one while the batch two before it is computed.
       const int cl = lane % SH::CH, su = lane / SH::CH;
-      // two halves: the first is loaded before the waits of this phase, the
-      // second after them, while the first is computed
-      constexpr int NDH = (SH::NDW + 1) / 2;
+      constexpr int NDH = SH::NDH;
+      const int nbt = NDI / NDH;                  // batches of the step
+      const int nbw = (nbt + NWV - 1) / NWV;      // per wave (most)
+      const int nbe = max(0, min(nbw, nbt - wave * nbw));  // this wave's
       typedef U4 DQ[NDH];
       typedef uint32_t DS[NDH];
-      auto dn_load = [&](int j0, DQ& dq, DS& dsz) {
+      auto dn_load = [&](int i, DQ& dq, DS& dsz) {  // past the end: the draws' first bytes
+        const bool in = i < nbe;
+        const int n0 = min(wave * nbw + min(i, nbe - 1), nbt - 1) * NDH;
         const uint8_t* pq[NDH];
         const uint8_t* ps[NDH];
 #pragma unroll
         for (int jh = 0; jh < NDH; ++jh) {
-          int n = wave * ndw + j0 + jh;  // wave-uniform
-          if (n >= NDI) n = NDI - 1;     // loaded again, not used
-          pq[jh] = dn_q[n];
-          ps[jh] = dn_s[n];
+          pq[jh] = in ? dn_q[n0 + jh] : hot;
+          ps[jh] = in ? dn_s[n0 + jh] : hot;
         }
 #pragma unroll
         for (int jh = 0; jh < NDH; ++jh) {
@@ -890,29 +952,38 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
           dsz[jh] = ldw4(ps[jh] + su * (IE / 16) + (cl >> 1) * 4);
         }
       };
-      DQ dqA, dqB;
-      DS dsA, dsB;
-      dn_load(0, dqA, dsA);
+      DQ dq0, dq1, dq2;
+      DS ds0, ds1, ds2;
+      dn_load(0, dq0, ds0);
+      dn_load(1, dq1, ds1);
       if (next_ok) fetch_layer();
-      // LoRA-B rows of down for the output sum: lane (j, part) = (tid / 8, tid % 8)
+      // LoRA-B rows of down for the output sum: lane (j, part) = (tid / 8 +
+      // NT / 8 p, tid % 8) in pass p; loaded after the waits of this phase
       constexpr int BV = R / 8;
-      const int jo = tid >> 3, part = tid & 7;
-      U4 bd[SH::NEF][BV];
+      const int part = tid & 7;
+      auto jo_of = [&](int p) { return (tid >> 3) + (NT / 8) * p; };
+      U4 bd[SH::DRP][SH::NEF][BV];
+      auto bd_load = [&]() {
 #pragma unroll
-      for (int i = 0; i < SH::NEF; ++i) {
-        const int k = part + 8 * i;
+        for (int p = 0; p < SH::DRP; ++p) {
+          const int jo = jo_of(p);
 #pragma unroll
-        for (int v = 0; v < BV; ++v) {
-          bd[i][v] = U4{0u, 0u, 0u, 0u};
-          if (jo < SH::DR && k < n_list && rt.ld[k])
-            bd[i][v] = ldw16(reinterpret_cast<const __half*>(rt.bd[k].down.lora_b) +
-                             ((size_t)m * SH::DR + jo) * R + 8 * v);
+          for (int i = 0; i < SH::NEF; ++i) {
+            const int k = part + 8 * i;
+#pragma unroll
+            for (int v = 0; v < BV; ++v) {
+              bd[p][i][v] = U4{0u, 0u, 0u, 0u};
+              if (jo < SH::DR && k < n_list && rt.ld[k])
+                bd[p][i][v] = ldw16(reinterpret_cast<const __half*>(rt.bd[k].down.lora_b) +
+                                    ((size_t)m * SH::DR + jo) * R + 8 * v);
+            }
+          }
         }
-      }
+      };
       // the next step's LoRA-A rows (the current step's were read at its start)
       if (next_ok) stage_arows(routes[par ^ 1], lane);
-      mark(a, x + NX * m, s, 6);
-      // h of the step and the A_down partials of the XCD
+      mark(a, x + NTM * m, s, 6);
+      // h of the step and the A_down partials of the team
       if (!poll_all<SH::MAXI_H, (SH::MAXI_H + 1) / 2>(
               tid, NHS + NM * 2 * R, tag,
               [&](int i) { return i < NHS ? HV + i : ADP + (i - NHS); },
@@ -922,7 +993,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
               },
               c, &mi->abort, 3))
         break;
-      mark(a, x + NX * m, s, 7);
+      mark(a, x + NTM * m, s, 7);
       // A_down h of list position k: the partials of the workgroups whose rows
       // meet expert k, in workgroup order
       if (tid < n_list * R) {
@@ -935,60 +1006,70 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         }
         adv[tid] = acc;
       }
-      dn_load(NDH, dqB, dsB);
-      // down dot products: reload the h chunk when the expert changes. The
-      // lane's 32 h values (fp32) become two fp16 terms each, hi = fp16(h)
-      // and lo = fp16(h - hi), in pair order, so the codes meet them in
-      // v_dot2_f32_f16; hi + lo carries h to about 2^-22 (|h| < 65504).
+      bd_load();
+      // down dot products: h of the batch's expert is reloaded when the
+      // expert changes. The lane's 32 h values (fp32) become two fp16 terms
+      // each, hi = fp16(h) and lo = fp16(h - hi), in pair order, so the codes
+      // meet them in v_dot2_f32_f16; hi + lo carries h to about 2^-22
+      // (|h| < 65504).
       hv2 hh[16], hlo[16];
       float hsum = 0.f;
       int kc = -1;
-      auto dn_compute = [&](int j0, const DQ& dq, const DS& dsz) {
+      auto dn_compute = [&](int i, const DQ& dq, const DS& dsz) {
+        if (i >= nbe) return;
+        const int n0 = (wave * nbw + i) * NDH;
+        const int k = n0 / DI;
+        if (k != kc) {
+          kc = k;
+          const float4* hp = reinterpret_cast<const float4*>(hx + ((k * IE) / 32 + cl) * 36);
+          float hv[32];
+          hsum = 0.f;
 #pragma unroll
-        for (int jh = 0; jh < NDH; ++jh) {
-          const int j = j0 + jh;
-          const int n = wave * ndw + j;
-          if (j >= SH::NDW || j >= ndw || n >= NDI) continue;
-          const int k = n / DI, jj = (n % DI) * SH::UPI + su;
-          if (k != kc) {
-            kc = k;
-            const float4* hp = reinterpret_cast<const float4*>(hx + ((k * IE) / 32 + cl) * 36);
-            float hv[32];
-            hsum = 0.f;
+          for (int e4 = 0; e4 < 8; ++e4) {
+            const float4 v4 = hp[e4];
+            hv[4 * e4] = v4.x;
+            hv[4 * e4 + 1] = v4.y;
+            hv[4 * e4 + 2] = v4.z;
+            hv[4 * e4 + 3] = v4.w;
+            hsum += (v4.x + v4.y) + (v4.z + v4.w);
+          }
 #pragma unroll
-            for (int e4 = 0; e4 < 8; ++e4) {
-              const float4 v4 = hp[e4];
-              hv[4 * e4] = v4.x;
-              hv[4 * e4 + 1] = v4.y;
-              hv[4 * e4 + 2] = v4.z;
-              hv[4 * e4 + 3] = v4.w;
-              hsum += (v4.x + v4.y) + (v4.z + v4.w);
-            }
+          for (int q4 = 0; q4 < 4; ++q4) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-#pragma unroll
-              for (int mm = 0; mm < 4; ++mm) {
-                const float a0 = hv[8 * i + mm], a1 = hv[8 * i + mm + 4];
-                const _Float16 h0 = (_Float16)a0, h1 = (_Float16)a1;
-                hh[4 * i + mm] = hv2{h0, h1};
-                hlo[4 * i + mm] = hv2{(_Float16)(a0 - (float)h0), (_Float16)(a1 - (float)h1)};
-              }
+            for (int mm = 0; mm < 4; ++mm) {
+              const float a0 = hv[8 * q4 + mm], a1 = hv[8 * q4 + mm + 4];
+              const _Float16 h0 = (_Float16)a0, h1 = (_Float16)a1;
+              hh[4 * q4 + mm] = hv2{h0, h1};
+              hlo[4 * q4 + mm] = hv2{(_Float16)(a0 - (float)h0), (_Float16)(a1 - (float)h1)};
             }
           }
+        }
+#pragma unroll
+        for (int jh = 0; jh < NDH; ++jh) {
+          const int jj = ((n0 + jh) % DI) * SH::UPI + su;
           const float2 sz = h2f2(dsz[jh]);
           float v = (sz.x * 16777216.f) * dot32_codes2(dq[jh], hh, hlo) + sz.y * hsum;
           v = group_sum(v, SH::CH);
           if (cl == 0) yp[jj * NLX + k] = rt.wl[k] * v;
         }
       };
-      dn_compute(0, dqA, dsA);
-      dn_compute(NDH, dqB, dsB);
+      for (int i = 0; i < nbw; i += 3) {
+        dn_load(i + 2, dq2, ds2);
+        dn_compute(i, dq0, ds0);
+        dn_load(i + 3, dq0, ds0);
+        dn_compute(i + 1, dq1, ds1);
+        dn_load(i + 4, dq1, ds1);
+        dn_compute(i + 2, dq2, ds2);
+      }
       __syncthreads();
-      mark(a, x + NX * m, s, 8);
+      mark(a, x + NTM * m, s, 8);
       // the inputs of the step after next arrive while y is summed
       fetch_rows(s2);
       // y = sum over list positions of the weighted down rows and LoRA terms
-      if (jo < SH::DR) {
+#pragma unroll
+      for (int p = 0; p < SH::DRP; ++p) {
+        const int jo = jo_of(p);
+        if (jo >= SH::DR) continue;
         float acc = 0.f;
 #pragma unroll
         for (int i = 0; i < SH::NEF; ++i) {
@@ -1000,7 +1081,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
             float t = 0.f;
 #pragma unroll
             for (int v = 0; v < BV; ++v) {
-              const uint32_t wb[4] = {bd[i][v].x, bd[i][v].y, bd[i][v].z, bd[i][v].w};
+              const uint32_t wb[4] = {bd[p][i][v].x, bd[p][i][v].y, bd[p][i][v].z, bd[p][i][v].w};
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
                 const float2 fb = h2f2(wb[q]);
@@ -1015,7 +1096,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         if (part == 0) a.y[(size_t)s * D + (size_t)m * SH::DR + jo] = acc;
       }
       __syncthreads();
-      mark(a, x + NX * m, s, 9);
+      mark(a, x + NTM * m, s, 9);
     }
     cur_ok = next_ok;
     if (has_next && !next_ok) {  // the next step's layer is outside the table
@@ -1078,14 +1159,14 @@ size_t engine_tokens_workspace_words(int E, int d, int I, int r, int n_list, Eng
   };
   const size_t rr = (size_t)(r > 0 ? r : 1);
   a->xs_logr = (size_t)(E + 31) / 32 * 32;  // one parity of one XCD
-  a->xo_logr = take(tok::NX * 2 * a->xs_logr);
-  a->xo_loghm = take(tok::NX * 2 * a->xs_logr);
+  a->xo_logr = take(tok::NTM * 2 * a->xs_logr);
+  a->xo_loghm = take(tok::NTM * 2 * a->xs_logr);
   a->xs_av = (size_t)n_list * 2 * rr;
-  a->xo_av = take(tok::NX * a->xs_av);
+  a->xo_av = take(tok::NTM * a->xs_av);
   a->xs_hv = (size_t)n_list * I;
-  a->xo_hv = take(tok::NX * a->xs_hv);
+  a->xo_hv = take(tok::NTM * a->xs_hv);
   a->xs_adp = (size_t)tok::NM * 2 * rr;
-  a->xo_adp = take(tok::NX * a->xs_adp);
+  a->xo_adp = take(tok::NTM * a->xs_adp);
   return off;
 }
 

@@ -1,11 +1,12 @@
 """GPU parity of the throughput schedule of the decode engine
-(moe_engine_tokens: one independent single-token step per XCD in flight)
+(moe_engine_tokens: one independent single-token step per team of 16
+workgroups in flight, 16 at once)
 against the CPU oracle, token by token.
 
 Also checked: routing and predictions bit-identical to the latency schedule
 (moe_engine_layers, same router arithmetic), outputs within the layer bar of
 it, repeated launches on one workspace bit-identical, step counts that leave
-XCDs idle, a workspace shared with the other schedule, and the status word
+teams idle, a workspace shared with the other schedule, and the status word
 for a non-resident expert and a bad layer index.
 """
 
@@ -16,6 +17,8 @@ import synth
 from tests.gpu_harness import TOL_REL_INF, DeviceLayer, check_routing, oracle_token, rel_inf
 
 pytestmark = pytest.mark.gpu
+
+TEAMS = 16   # steps in flight: team t runs the steps t, t + 16, ...
 
 
 @pytest.fixture(scope="module")
@@ -89,16 +92,16 @@ def test_tokens_supported(torch_cuda):
 
 
 def test_tokens_tiny_all_steps(tiny, torch_cuda):
-    xi = synth.token_draws(tiny.wl, 0, 27)   # every XCD three or four steps
+    xi = synth.token_draws(tiny.wl, 0, 40)   # every team two or three steps
     out, _ = _run(tiny, xi, torch_cuda)
     stats = _check(tiny, xi, out, "tokens tiny")
     print("tokens tiny:", stats)
-    assert stats["tokens"] >= 24
+    assert stats["tokens"] >= 36
 
 
-@pytest.mark.parametrize("T", [1, 3, 9])
-def test_tokens_tiny_idle_xcds(tiny, torch_cuda, T):
-    """Fewer steps than XCDs (and one step past a multiple of 8)."""
+@pytest.mark.parametrize("T", [1, 3, 9, 17])
+def test_tokens_tiny_idle_teams(tiny, torch_cuda, T):
+    """Fewer steps than teams (and one step past a multiple of the team count)."""
     xi = synth.token_draws(tiny.wl, 40 + T, T)
     out, _ = _run(tiny, xi, torch_cuda)
     _check(tiny, xi, out, "tokens tiny T=%d" % T)
@@ -149,9 +152,9 @@ def test_tokens_status_slot_miss_and_bad_layer(tiny, torch_cuda):
     out2, _ = _run(tiny, xi, torch, steps=steps)
     assert int(out2["status"][0]) & B.MOE_STATUS_BAD_INDEX
     assert not (int(out2["status"][0]) & B.MOE_STATUS_ENGINE_ABORT)
-    # the XCDs that never met the bad step finished their steps
+    # the teams that never met the bad step finished their steps
     for t in range(16):
-        if t % 8 != 5:
+        if t % TEAMS != 5:
             ref = oracle_token(tiny, xi[t])
             if out2["idx"][t].tolist() == out["idx"][t].tolist() and t in others:
                 assert rel_inf(out2["y"][t], ref["y"]) <= TOL_REL_INF

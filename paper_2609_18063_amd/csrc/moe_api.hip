@@ -57,7 +57,7 @@ WsLayout ws_layout(const moe_layer_spec* s, int T) {
   w.g_h = take((size_t)T * n * s->d_expert * sizeof(__half));
   w.g_xp = take((size_t)T * s->d_model * sizeof(__half));
   w.g_ax = take((size_t)T * n * 2 * 16 * sizeof(float));
-  w.g_adp = take((size_t)T * n * (s->d_expert / 128 > 0 ? s->d_expert / 128 : 1) * 16 * sizeof(float));
+  w.g_adp = take((size_t)T * n * (s->d_expert / moe::kGroupSlab > 0 ? s->d_expert / moe::kGroupSlab : 1) * 16 * sizeof(float));
   w.total = off;
   return w;
 }

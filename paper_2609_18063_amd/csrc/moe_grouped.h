@@ -10,6 +10,7 @@ namespace moe {
 constexpr int kGroupRows = 64;   // permuted rows per tile (4 MFMA row blocks of 16)
 constexpr int kGroupMaxR = 16;   // LoRA rank the grouped path supports
 constexpr int kGroupMaxG = 2048; // experts + shared experts the permutation handles
+constexpr int kGroupSlab = 64;   // columns of one partial A_d h (one gate/up workgroup)
 
 // One tile of the grouped GEMMs: rows [row0, row0 + nrows) of the permuted
 // list, all routed to group g (expert id g < E, shared expert E + s), whose
@@ -34,7 +35,7 @@ struct GroupedArgs {
   __half* h;                    // [T * n_list][I], by permuted position, pair order
   __half* xp;                   // [T][d]: x in pair order
   float* ax;                    // [T * n_list][2][16]: A_g x, A_u x by permuted position
-  float* adp;                   // [T * n_list][I / 128][16]: A_d h over 128-column slabs
+  float* adp;                   // [T * n_list][I / kGroupSlab][16]: A_d h over column slabs
   float* y_experts;             // [T][n_list][d]
 };
 

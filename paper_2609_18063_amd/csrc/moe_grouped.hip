@@ -9,17 +9,23 @@
 //             permuted list of y_experts rows (token t, list position k).
 //   prep      x in pair order (below), and per tile A_g x and A_u x (the
 //             LoRA-A products, once per tile instead of once per column slab).
-//   gate/up   per tile x 128 columns: G = X W_g^T, U = X W_u^T over the tile's
-//             rows with v_mfma_f32_16x16x32_f16; int4 codes and the activation
-//             rows stream into LDS through global_load_lds (four 128-k chunks
-//             in flight), the codes are dequantized to fp16 in registers
-//             (w = s q + z, one rounding); the LoRA delta is one MFMA step with
-//             K = the rank (B rows against lora_scale * A x); epilogue
-//             h = silu(g) u stored fp16 in pair order, and the slab's partial
-//             A_d h.
-//   down      per tile x 256 columns: Y = H W_d^T the same way, LoRA-B of down
+//   gate/up   per tile x 64 columns: G = X W_g^T, U = X W_u^T over the tile's
+//             rows with v_mfma_f32_16x16x32_f16 (four waves the gate rows,
+//             four the up rows of the same columns); int4 codes and the
+//             activation rows stream into LDS through global_load_lds in
+//             128-k chunks of whole row segments (a ring of two to four
+//             chunks, by the tile's row count), the (s, z) rows once per
+//             tile; codes are dequantized to fp16 in registers (w = s q + z,
+//             one rounding); the LoRA delta is one MFMA step with K = the
+//             rank (B rows against lora_scale * A x); epilogue h = silu(g) u
+//             stored fp16 in pair order, and the slab's partial A_d h.
+//   down      per tile x 128 columns: Y = H W_d^T the same way, LoRA-B of down
 //             against lora_scale * (the sum of the slab partials of A_d h);
 //             fp32 rows go straight to y_experts.
+//
+// A GEMM workgroup uses under half of the CU's LDS, so two share a CU: the
+// loads that start and end a tile (tile record, bundle, LoRA rows) of one
+// overlap the streaming of the other.
 //
 // Pair order: inside each 8-element piece the elements run [0,4,1,5,2,6,3,7],
 // the order in which the packed nibbles of one code dword come out of a
@@ -37,18 +43,26 @@ typedef _Float16 h2v __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGK = 128;                        // k per staged chunk
-constexpr int kNBuf = 4;                        // ring slots (chunks) per workgroup
 constexpr int kGT = 512;                        // threads of a GEMM workgroup (8 waves)
 constexpr int kGW = kGT / 64;
-constexpr int kXSlot = kGroupRows * kGK * 2;    // one chunk of 64 activation rows (16 KB)
-constexpr int kWBlk = 1024 + 256;               // one column block of one wave: codes + (s, z)
-constexpr int kNBlk = 2;                        // column blocks of 16 per wave
-constexpr int kWSlot = kGW * kNBlk * kWBlk;     // one chunk of all waves' weights
-constexpr int kRingBytes = kNBuf * (kXSlot + kWSlot);
-constexpr int kGateCols = kGW * 16;             // gate/up columns per workgroup (each of g, u)
-constexpr int kDownCols = kGW * kNBlk * 16;     // down columns per workgroup
-constexpr int kSlab = 128;                      // columns per A_d h partial (= kGateCols)
-static_assert(kGateCols == kSlab, "one A_d h partial per gate/up workgroup");
+constexpr int kCodeRow = kGK / 2;               // code bytes of one weight row in a chunk
+constexpr int kActRow = kGK * 2;                // activation bytes of one row in a chunk
+constexpr int kGateCols = kGroupSlab;           // gate (and up) columns per gate/up workgroup
+constexpr int kGateRows = 2 * kGateCols;        // its weight rows: one 16-row block per wave
+constexpr int kDownCols = 128;                  // down columns per down workgroup: one block per wave
+// Ring of chunk slots (the slot count follows the tile's row blocks). With the
+// (s, z) rows and the static arrays a workgroup stays under half the LDS, so
+// two workgroups share a CU and one's latencies hide behind the other's
+// streaming.
+constexpr int kRingBytes = 56 * 1024;
+static_assert(kGateRows == 16 * kGW && kDownCols == 16 * kGW, "one row block per wave");
+// (s, z) rows of the workgroup's weight rows, staged once per tile: Kdim / 16
+// bytes per row
+inline int gate_sz_bytes(int d) { return kGateRows * (d / 16); }
+inline int down_sz_bytes(int I) { return kDownCols * (I / 16); }
+constexpr int kGateStatic = 2 * kGroupRows * 16 * 2 + kGroupRows * 4;  // la, rsrc
+constexpr int kDownStatic = kGroupRows * 16 * 2 + kGroupRows * 4;      // la, ydst
+constexpr int kLdsMax = 80 * 1024;              // per workgroup: two per CU
 
 __device__ __forceinline__ h2v as_h2(uint32_t u) { return __builtin_bit_cast(h2v, u); }
 __device__ __forceinline__ h8 as_h8(U4 u) { return __builtin_bit_cast(h8, u); }
@@ -158,78 +172,100 @@ __device__ __forceinline__ void vm_wait(int n) {
 }
 
 // ---- one tile's k loop --------------------------------------------------------
-// acc[blk][m] += X[rows of block m] . W[16 columns of block blk]^T over Kdim.
-// Ring slot c % kNBuf holds chunk c: the tile's activation rows (srows of
-// them, 16-byte pieces XOR-swizzled by row so that the 16 rows an MFMA
-// operand reads sit on different banks) and every wave's codes and (s, z).
-// xsrc(row, k): global address of 8 activations (pair order) of row `row` at
-// k; qsrc(blk, k): this lane's 16 bytes of codes (32 inputs from k);
-// ssrc(blk, k): its (s, z) word.
-template <typename XSrc, typename QSrc, typename SSrc>
-__device__ __forceinline__ void tile_gemm(char* ring, int Kdim, int mb, XSrc xsrc, QSrc qsrc,
-                                          SSrc ssrc, f4 (*acc)[4]) {
+// acc[0][m] += X[rows of block m] . W[16 rows of this wave's block]^T over
+// Kdim for the MB 16-row blocks of the tile (MB a compile-time count) and
+// NROWS = 128 weight rows (one block of 16 per wave). Chunk c (k in
+// [c kGK, (c+1) kGK)) of every weight row and activation row is staged into a
+// ring slot with global_load_lds, each instruction copying whole row segments
+// (16 rows x 64 bytes of codes, 4 rows x 256 bytes of activations). In LDS
+// the 16-byte pieces of a row are XOR-swizzled by the row, so that the 16
+// rows an MFMA operand reads sit on different banks. MFMA instruction j of a
+// chunk takes, in lane (col, kq), the k values kq 32 + 8 j .. + 7 (one dword
+// of codes; the same k order in both operands, so any order is fine); a lane
+// uses one (s, z) group per chunk. The (s, z) rows of the whole k range are
+// staged before chunk 0.
+// wrow(row) / srow(row): the global code and (s, z) row of weight row `row`;
+// xsrc(row, k): global address of 8 activations (pair order) of activation
+// row `row` at k.
+template <int MB, int NROWS, typename WRow, typename SRow, typename XSrc>
+__device__ __forceinline__ void tile_gemm_mb(char* ring, char* szl, int Kdim, WRow wrow, SRow srow,
+                                             XSrc xsrc, f4 (*acc)[4]) {
+  static_assert(NROWS == 16 * kGW, "one block per wave");
+  constexpr int CODE_B = NROWS * kCodeRow;                     // codes of a slot
+  constexpr int SLOT = CODE_B + MB * 16 * kActRow;
+  constexpr int NBUF = kRingBytes / SLOT < 6 ? kRingBytes / SLOT : 6;
+  static_assert(NBUF >= 2, "two slots at least");
+  constexpr int CODE_I = CODE_B / 1024 / kGW;                  // code copies per wave per chunk
+  constexpr int XI = MB * 16 * kActRow / 1024;                 // activation copies per chunk
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int col = lane & 15, kq = lane >> 4;
+  const int my_x = (XI - wave + kGW - 1) / kGW;                // this wave's activation copies
+  const int per = CODE_I + my_x;                               // this wave's copies per chunk
   const int nch = Kdim / kGK;
-  const int nxi = 4 * mb;                                  // activation copies per chunk
-  const int my_x = (nxi - wave + kGW - 1) / kGW;           // this wave's share of them
-  const int per_chunk = my_x + 2 * kNBlk;                  // this wave's copies per chunk
-  auto xslot = [&](int c) { return ring + (c % kNBuf) * kXSlot; };
-  auto wslot = [&](int c) {
-    return ring + kNBuf * kXSlot + ((c % kNBuf) * kGW + wave) * kNBlk * kWBlk;
-  };
+  const int szr = Kdim / 16;                                   // (s, z) bytes per row
+  auto slot = [&](int c) { return ring + (c % NBUF) * SLOT; };
   auto issue = [&](int c) {
-    const int k0 = c * kGK;
-    char* xs = xslot(c);
-    for (int b = wave; b < nxi; b += kGW) {  // 64 pieces: rows 4b .. 4b+3
-      const int p = b * 64 + lane, row = p >> 4, phys = p & 15;
-      dma16(xsrc(row, k0 + 8 * (phys ^ (row & 15))), xs + b * 1024);
-    }
-    char* ws = wslot(c);
+    char* sl = slot(c);
 #pragma unroll
-    for (int blk = 0; blk < kNBlk; ++blk) {
-      dma16(qsrc(blk, k0 + kq * 32), ws + blk * kWBlk);
-      dma4(ssrc(blk, k0 + kq * 32), ws + blk * kWBlk + 1024);
+    for (int i = 0; i < CODE_I; ++i) {  // rows 16b .. 16b+15, 64 bytes each
+      const int b = wave * CODE_I + i;
+      const int row = 16 * b + (lane >> 2), phys = lane & 3;
+      const int piece = phys ^ ((row >> 2) & 3);
+      dma16(wrow(row) + c * kCodeRow + piece * 16, sl + b * 1024);
+    }
+    for (int b = wave; b < XI; b += kGW) {  // activation rows 4b .. 4b+3, 256 bytes each
+      const int row = 4 * b + (lane >> 4), phys = lane & 15;
+      const int piece = phys ^ (row & 15);
+      dma16(xsrc(row, c * kGK + piece * 8), sl + CODE_B + b * 1024);
     }
   };
   vm_drain();
-  for (int c = 0; c < nch && c < kNBuf - 1; ++c) issue(c);
+  for (int b = wave; b * 1024 < NROWS * szr; b += kGW) {  // (s, z) rows, natural layout
+    const int o = b * 1024 + lane * 16;
+    dma16(srow(o / szr) + o % szr, szl + b * 1024);
+  }
+  const int pre = nch < NBUF ? nch : NBUF;
+  for (int c = 0; c < pre; ++c) issue(c);
+  const int row = wave * 16 + col;                             // this lane's weight row
+  const int sw = (row >> 2) & 3;
   for (int c = 0; c < nch; ++c) {
-    const int ahead = min(nch - 1 - c, kNBuf - 2);  // chunks issued after c
-    vm_wait(ahead * per_chunk);
+    // chunks issued after chunk c: all of the first NBUF at c = 0, then one
+    // per chunk (into the slot of chunk c - 1)
+    const int ahead = c == 0 ? pre - 1 : min(nch - 1 - c, NBUF - 2);
+    vm_wait(ahead * per);
     __syncthreads();  // chunk c is in LDS for every wave; chunk c - 1 is consumed
-    if (c + kNBuf - 1 < nch) issue(c + kNBuf - 1);  // into the slot of chunk c - 1
-    const char* xs = xslot(c);
-    const char* ws = wslot(c);
-    U4 q[kNBlk];
-    h2v s2[kNBlk], z2[kNBlk];
+    if (c > 0 && c + NBUF - 1 < nch) issue(c + NBUF - 1);
+    const char* sl = slot(c);
+    const U4 q = *reinterpret_cast<const U4*>(sl + row * kCodeRow + (kq ^ sw) * 16);
+    const uint32_t szw = *reinterpret_cast<const uint32_t*>(szl + row * szr + (2 * c + (kq >> 1)) * 4);
+    h8 af[4][MB];
 #pragma unroll
-    for (int blk = 0; blk < kNBlk; ++blk) {
-      q[blk] = *reinterpret_cast<const U4*>(ws + blk * kWBlk + lane * 16);
-      const h2v sz = as_h2(*reinterpret_cast<const uint32_t*>(ws + blk * kWBlk + 1024 + lane * 4));
-      s2[blk] = h2v{sz[0], sz[0]};
-      z2[blk] = h2v{sz[1], sz[1]};
-    }
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+        af[j][m] = *reinterpret_cast<const h8*>(sl + CODE_B + (16 * m + col) * kActRow + ((kq * 4 + j) ^ col) * 16);
+    const h2v sz = as_h2(szw);
+    const h2v s2 = h2v{sz[0], sz[0]}, z2 = h2v{sz[1], sz[1]};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      h8 af[4];
+      const uint32_t word = j == 0 ? q.x : j == 1 ? q.y : j == 2 ? q.z : q.w;
+      const h8 w = dequant8(word, s2, z2);
 #pragma unroll
-      for (int m = 0; m < 4; ++m)
-        if (m < mb) {
-          const int row = 16 * m + col;
-          af[m] = *reinterpret_cast<const h8*>(xs + row * 256 + (((kq * 4 + j) ^ col) * 16));
-        }
-#pragma unroll
-      for (int blk = 0; blk < kNBlk; ++blk) {
-        const uint32_t word = j == 0 ? q[blk].x : j == 1 ? q[blk].y : j == 2 ? q[blk].z : q[blk].w;
-        const h8 w = dequant8(word, s2[blk], z2[blk]);
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-          if (m < mb) acc[blk][m] = mfma(af[m], w, acc[blk][m]);
-      }
+      for (int m = 0; m < MB; ++m) acc[0][m] = mfma(af[j][m], w, acc[0][m]);
     }
   }
   __syncthreads();  // the ring is free again
+}
+// mb (1 .. 4) is the same for every thread of the workgroup
+template <int NROWS, typename WRow, typename SRow, typename XSrc>
+__device__ __forceinline__ void tile_gemm(char* ring, char* szl, int Kdim, int mb, WRow wrow, SRow srow,
+                                          XSrc xsrc, f4 (*acc)[4]) {
+  switch (mb) {
+    case 1: tile_gemm_mb<1, NROWS>(ring, szl, Kdim, wrow, srow, xsrc, acc); break;
+    case 2: tile_gemm_mb<2, NROWS>(ring, szl, Kdim, wrow, srow, xsrc, acc); break;
+    case 3: tile_gemm_mb<3, NROWS>(ring, szl, Kdim, wrow, srow, xsrc, acc); break;
+    default: tile_gemm_mb<4, NROWS>(ring, szl, Kdim, wrow, srow, xsrc, acc); break;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -342,14 +378,21 @@ __global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb
       xrow[m] = t >= 0 ? reinterpret_cast<const _Float16*>(a.x) + (size_t)t * d : nullptr;
     }
     const int kbeg = quarter * (d / 4), kend = kbeg + d / 4;
-    for (int k = kbeg + kq * 8; k < kend; k += 32) {
-      const h8 b = arow ? as_h8(ld16(arow + k)) : h8{};
+    for (int k0 = kbeg + kq * 8; k0 < kend; k0 += 128) {  // four k steps: all loads, then the MFMAs
+      h8 b[4], av[4][4];
 #pragma unroll
-      for (int m = 0; m < 4; ++m)
-        if (m < mb) {
-          const h8 av = xrow[m] ? as_h8(ld16(xrow[m] + k)) : h8{};
-          acc[m] = mfma(av, b, acc[m]);
-        }
+      for (int u = 0; u < 4; ++u) {
+        const int k = k0 + 32 * u;
+        const bool in = k < kend;
+        b[u] = arow && in ? as_h8(ld16(arow + k)) : h8{};
+#pragma unroll
+        for (int m = 0; m < 4; ++m) av[u][m] = m < mb && xrow[m] && in ? as_h8(ld16(xrow[m] + k)) : h8{};
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+          if (m < mb) acc[m] = mfma(av[u][m], b[u], acc[m]);
     }
   }
   // C layout: lane (col, kq) holds rows 4 kq + e of block m, rank col
@@ -366,16 +409,23 @@ __global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb
 }
 
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(kGT) grouped_gateup_kernel(GroupedArgs a) {
+// gate/up: workgroup (tile, y) takes the gate and up rows of columns
+// [64 y, 64 y + 64): wave w < 4 the gate rows of columns 64 y + 16 w + col,
+// wave w + 4 the up rows of the same columns.
+__global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
   extern __shared__ __attribute__((aligned(16))) char ring[];
   __shared__ __attribute__((aligned(16))) _Float16 la[2][kGroupRows][16];
   __shared__ int rsrc[kGroupRows];
-  // after the k loop the ring holds h of the tile and the A_d rows
-  _Float16(*hs)[kGateCols] = reinterpret_cast<_Float16(*)[kGateCols]>(ring);
-  _Float16(*ads)[kGateCols] = reinterpret_cast<_Float16(*)[kGateCols]>(ring + kGroupRows * kGateCols * 2);
-  static_assert((kGroupRows + 16) * kGateCols * 2 <= kRingBytes, "h and A_d rows fit in the ring");
-  if ((int)blockIdx.x >= *a.n_tiles) return;
+  char* const szl = ring + kRingBytes;
+  // after the k loop the ring holds the up accumulators, h of the tile and
+  // the A_d rows
+  float* const uacc = reinterpret_cast<float*>(ring);  // [4 waves][4 m][4 e][64 lanes]
+  _Float16(*hs)[kGateCols] = reinterpret_cast<_Float16(*)[kGateCols]>(ring + 16384);
+  _Float16(*ads)[kGateCols] = reinterpret_cast<_Float16(*)[kGateCols]>(ring + 16384 + kGroupRows * kGateCols * 2);
+  static_assert(16384 + (kGroupRows + 16) * kGateCols * 2 <= kRingBytes, "epilogue fits in the ring");
+  // (the record is read beside the count; one past the count is never used)
   const GroupTile tl = a.tiles[blockIdx.x];
+  if ((int)blockIdx.x >= *a.n_tiles) return;
   if (tl.slot < 0) return;  // not resident: the down kernel writes zero rows
   const moe_bundle* bd = a.bundles + tl.slot;
   const int tid = threadIdx.x;
@@ -384,73 +434,96 @@ __global__ void __launch_bounds__(kGT) grouped_gateup_kernel(GroupedArgs a) {
   const int d = a.d, I = a.I, r = a.r;
   const int mb = (tl.nrows + 15) >> 4;
   const int c0 = blockIdx.y * kGateCols;        // first column of this workgroup
-  const int i = c0 + wave * 16 + col;           // this lane's gate/up column
+  const int cc = wave >> 2, wb = wave & 3;      // projection (0 gate, 1 up), column block
+  const int i = c0 + wb * 16 + col;             // this lane's gate/up column
   if (tid < kGroupRows) rsrc[tid] = tid < tl.nrows ? a.perm[tl.row0 + tid] / a.n_list : -1;
   const bool lg = r > 0 && bd->gate.lora_a && bd->gate.lora_b;
   const bool lu = r > 0 && bd->up.lora_a && bd->up.lora_b;
   const bool ld = r > 0 && bd->down.lora_a && bd->down.lora_b;
   // lora_scale * (A x) of the tile's rows, fp16 (rank past r: zero)
   for (int p = tid; p < 2 * kGroupRows * 16; p += kGT) {
-    const int cc = p / (kGroupRows * 16), row = (p >> 4) % kGroupRows, k = p & 15;
+    const int pc = p / (kGroupRows * 16), row = (p >> 4) % kGroupRows, k = p & 15;
     float v = 0.f;
-    if (row < tl.nrows && k < r && (cc == 0 ? lg : lu))
-      v = a.lora_scale * a.ax[((size_t)(tl.row0 + row) * 2 + cc) * 16 + k];
-    la[cc][row][k] = (_Float16)v;
+    if (row < tl.nrows && k < r && (pc == 0 ? lg : lu))
+      v = a.lora_scale * a.ax[((size_t)(tl.row0 + row) * 2 + pc) * 16 + k];
+    la[pc][row][k] = (_Float16)v;
   }
   __syncthreads();
 
-  const uint8_t* qb[2] = {static_cast<const uint8_t*>(bd->gate.q) + (size_t)i * (d / 2),
-                          static_cast<const uint8_t*>(bd->up.q) + (size_t)i * (d / 2)};
-  const uint8_t* sb[2] = {static_cast<const uint8_t*>(bd->gate.sz) + (size_t)i * (d / 16),
-                          static_cast<const uint8_t*>(bd->up.sz) + (size_t)i * (d / 16)};
+  // weight row w_row (0 .. 127): projection w_row / 64, column c0 + w_row % 64
+  auto wrow = [&](int w_row) -> const uint8_t* {
+    const moe_proj& pj = w_row < kGateCols ? bd->gate : bd->up;
+    return static_cast<const uint8_t*>(pj.q) + (size_t)(c0 + (w_row % kGateCols)) * (d / 2);
+  };
+  auto srow = [&](int w_row) -> const uint8_t* {
+    const moe_proj& pj = w_row < kGateCols ? bd->gate : bd->up;
+    return static_cast<const uint8_t*>(pj.sz) + (size_t)(c0 + (w_row % kGateCols)) * (d / 16);
+  };
   const char* xbase = reinterpret_cast<const char*>(a.xp);
   auto xsrc = [&](int row, int k) -> const void* {
     const int t = rsrc[row < tl.nrows ? row : 0];
     return xbase + ((size_t)t * d + k) * 2;
   };
-  auto qsrc = [&](int blk, int k) -> const void* { return qb[blk] + k / 2; };
-  auto ssrc = [&](int blk, int k) -> const void* { return sb[blk] + (k / 64) * 4; };
 
-  f4 acc[2][4];
+  // the epilogue's LoRA-B operand and A_d rows, requested before the k loop
+  const bool lw = cc == 0 ? lg : lu;
+  const h8 bop = lw ? lora_b_operand(static_cast<const __half*>(cc == 0 ? bd->gate.lora_b : bd->up.lora_b), i,
+                                     r, kq)
+                    : h8{};
+  static_assert(16 * kGateCols == 2 * kGT, "two A_d values per thread");
+  _Float16 adv[2];
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    acc[0][m] = f4{0.f, 0.f, 0.f, 0.f};
-    acc[1][m] = acc[0][m];
+  for (int q = 0; q < 2; ++q) {
+    const int p = tid + q * kGT, k = p / kGateCols, c = p % kGateCols;
+    adv[q] = (ld && k < r) ? reinterpret_cast<const _Float16*>(bd->down.lora_a)[(size_t)k * I + c0 + c]
+                           : (_Float16)0.f;
   }
-  tile_gemm(ring, d, mb, xsrc, qsrc, ssrc, acc);
-
-  // LoRA delta: one MFMA step of K = rank against lora_scale * (A x)
+  f4 acc[1][4];
 #pragma unroll
-  for (int cc = 0; cc < 2; ++cc) {
-    if (!(cc == 0 ? lg : lu)) continue;
-    const h8 bop = lora_b_operand(static_cast<const __half*>(cc == 0 ? bd->gate.lora_b : bd->up.lora_b),
-                                  i, r, kq);
+  for (int m = 0; m < 4; ++m) acc[0][m] = f4{0.f, 0.f, 0.f, 0.f};
+  tile_gemm<kGateRows>(ring, szl, d, mb, wrow, srow, xsrc, acc);
+
+  // LoRA delta of this wave's projection: one MFMA step of K = rank against
+  // lora_scale * (A x)
+  if (lw) {
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       if (m >= mb) continue;
       h8 aop = {};
       if (kq < 2) aop = *reinterpret_cast<const h8*>(&la[cc][16 * m + col][kq * 8]);
-      acc[cc][m] = mfma(aop, bop, acc[cc][m]);
+      acc[0][m] = mfma(aop, bop, acc[0][m]);
     }
   }
-  // A_d rows restricted to this workgroup's columns (the ring is free now)
-  for (int p = tid; p < 16 * kGateCols; p += kGT) {
-    const int k = p / kGateCols, cc = p % kGateCols;
-    ads[k][cc] = (ld && k < r) ? reinterpret_cast<const _Float16*>(bd->down.lora_a)[(size_t)k * I + c0 + cc]
-                               : (_Float16)0.f;
+  // the up waves hand their sums to the gate waves of the same columns (same
+  // lane); A_d rows restricted to this workgroup's columns
+  if (cc == 1) {
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      if (m >= mb) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) uacc[((wb * 4 + m) * 4 + e) * 64 + lane] = acc[0][m][e];
+    }
   }
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int p = tid + q * kGT;
+    ads[p / kGateCols][p % kGateCols] = adv[q];
+  }
+  __syncthreads();
   // h = silu(g) u, fp16: to HBM in pair order, and to LDS for A_d h
-  const int ip = (i & ~7) | pair_slot(i & 7);
+  if (cc == 0) {
+    const int ip = (i & ~7) | pair_slot(i & 7);
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    if (m >= mb) continue;
+    for (int m = 0; m < 4; ++m) {
+      if (m >= mb) continue;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int row = 16 * m + 4 * kq + e;
-      const float g = acc[0][m][e], u = acc[1][m][e];
-      const __half h = __float2half(g / (1.0f + expf(-g)) * u);
-      if (row < tl.nrows) a.h[(size_t)(tl.row0 + row) * I + ip] = h;
-      hs[row][wave * 16 + col] = h;
+      for (int e = 0; e < 4; ++e) {
+        const int row = 16 * m + 4 * kq + e;
+        const float g = acc[0][m][e], u = uacc[((wb * 4 + m) * 4 + e) * 64 + lane];
+        const __half h = __float2half(g / (1.0f + expf(-g)) * u);
+        if (row < tl.nrows) a.h[(size_t)(tl.row0 + row) * I + ip] = h;
+        hs[row][wb * 16 + col] = h;
+      }
     }
   }
   __syncthreads();
@@ -459,24 +532,24 @@ __global__ void __launch_bounds__(kGT) grouped_gateup_kernel(GroupedArgs a) {
     for (int p = tid; p < tl.nrows * 16; p += kGT) {
       const int row = p >> 4, k = p & 15;
       float s = 0.f;
-      for (int cc = 0; cc < kGateCols; ++cc) s = fmaf((float)ads[k][cc], (float)hs[row][cc], s);
-      a.adp[((size_t)(tl.row0 + row) * (I / kSlab) + blockIdx.y) * 16 + k] = s;
+      for (int c = 0; c < kGateCols; ++c) s = fmaf((float)ads[k][c], (float)hs[row][c], s);
+      a.adp[((size_t)(tl.row0 + row) * (I / kGroupSlab) + blockIdx.y) * 16 + k] = s;
     }
   }
 }
 
-__global__ void __launch_bounds__(kGT) grouped_down_kernel(GroupedArgs a) {
+__global__ void __launch_bounds__(kGT, 4) grouped_down_kernel(GroupedArgs a) {
   extern __shared__ __attribute__((aligned(16))) char ring[];
   __shared__ __attribute__((aligned(16))) _Float16 la[kGroupRows][16];
   __shared__ int ydst[kGroupRows];
+  const GroupTile tl = a.tiles[blockIdx.x];  // (read beside the count, as in gate/up)
   if ((int)blockIdx.x >= *a.n_tiles) return;
-  const GroupTile tl = a.tiles[blockIdx.x];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int col = lane & 15, kq = lane >> 4;
   const int d = a.d, I = a.I, r = a.r;
   const int mb = (tl.nrows + 15) >> 4;
-  const int n0 = blockIdx.y * kDownCols + wave * 32 + col;  // columns n0 and n0 + 16 of this lane
+  const int n0 = blockIdx.y * kDownCols + wave * 16 + col;  // this lane's output column
   if (tid < kGroupRows) ydst[tid] = tid < tl.nrows ? a.perm[tl.row0 + tid] : -1;
   __syncthreads();
   if (tl.slot < 0) {  // not resident: the pair contributes zeros (the miss is reported)
@@ -493,42 +566,39 @@ __global__ void __launch_bounds__(kGT) grouped_down_kernel(GroupedArgs a) {
     const int row = p >> 4, k = p & 15;
     float v = 0.f;
     if (ld && row < tl.nrows && k < r) {
-      const float* q = a.adp + (size_t)(tl.row0 + row) * (I / kSlab) * 16 + k;
-      for (int sl = 0; sl < I / kSlab; ++sl) v += q[sl * 16];
+      const float* q = a.adp + (size_t)(tl.row0 + row) * (I / kGroupSlab) * 16 + k;
+      for (int sl = 0; sl < I / kGroupSlab; ++sl) v += q[sl * 16];
       v *= a.lora_scale;
     }
     la[row][k] = (_Float16)v;
   }
-  const uint8_t* qb[2] = {static_cast<const uint8_t*>(bd->down.q) + (size_t)n0 * (I / 2),
-                          static_cast<const uint8_t*>(bd->down.q) + (size_t)(n0 + 16) * (I / 2)};
-  const uint8_t* sb[2] = {static_cast<const uint8_t*>(bd->down.sz) + (size_t)n0 * (I / 16),
-                          static_cast<const uint8_t*>(bd->down.sz) + (size_t)(n0 + 16) * (I / 16)};
+  // weight row w_row (0 .. 255): output column blockIdx.y * 256 + w_row
+  const size_t nbase = (size_t)blockIdx.y * kDownCols;
+  auto wrow = [&](int w_row) -> const uint8_t* {
+    return static_cast<const uint8_t*>(bd->down.q) + (nbase + w_row) * (I / 2);
+  };
+  auto srow = [&](int w_row) -> const uint8_t* {
+    return static_cast<const uint8_t*>(bd->down.sz) + (nbase + w_row) * (I / 16);
+  };
   const char* hbase = reinterpret_cast<const char*>(a.h);
   auto xsrc = [&](int row, int k) -> const void* {
     return hbase + ((size_t)(tl.row0 + (row < tl.nrows ? row : 0)) * I + k) * 2;
   };
-  auto qsrc = [&](int blk, int k) -> const void* { return qb[blk] + k / 2; };
-  auto ssrc = [&](int blk, int k) -> const void* { return sb[blk] + (k / 64) * 4; };
 
-  f4 acc[2][4];
+  // the epilogue's LoRA-B operand, requested before the k loop
+  const h8 bop = ld ? lora_b_operand(static_cast<const __half*>(bd->down.lora_b), n0, r, kq) : h8{};
+  f4 acc[1][4];
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    acc[0][m] = f4{0.f, 0.f, 0.f, 0.f};
-    acc[1][m] = acc[0][m];
-  }
-  tile_gemm(ring, I, mb, xsrc, qsrc, ssrc, acc);  // its barriers also publish la
+  for (int m = 0; m < 4; ++m) acc[0][m] = f4{0.f, 0.f, 0.f, 0.f};
+  tile_gemm<kDownCols>(ring, ring + kRingBytes, I, mb, wrow, srow, xsrc, acc);  // its barriers also publish la
 
   if (ld) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const h8 bop = lora_b_operand(static_cast<const __half*>(bd->down.lora_b), n0 + 16 * c, r, kq);
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        if (m >= mb) continue;
-        h8 aop = {};
-        if (kq < 2) aop = *reinterpret_cast<const h8*>(&la[16 * m + col][kq * 8]);
-        acc[c][m] = mfma(aop, bop, acc[c][m]);
-      }
+    for (int m = 0; m < 4; ++m) {
+      if (m >= mb) continue;
+      h8 aop = {};
+      if (kq < 2) aop = *reinterpret_cast<const h8*>(&la[16 * m + col][kq * 8]);
+      acc[0][m] = mfma(aop, bop, acc[0][m]);
     }
   }
 #pragma unroll
@@ -540,7 +610,6 @@ __global__ void __launch_bounds__(kGT) grouped_down_kernel(GroupedArgs a) {
       if (row < tl.nrows) {
         float* y = a.y_experts + (size_t)ydst[row] * d;
         y[n0] = acc[0][m][e];
-        y[n0 + 16] = acc[1][m][e];
       }
     }
   }
@@ -550,20 +619,23 @@ __global__ void __launch_bounds__(kGT) grouped_down_kernel(GroupedArgs a) {
 
 bool grouped_shape_supported(int d, int I, int r, int groups) {
   return d % kDownCols == 0 && I % kGateCols == 0 && d % kGK == 0 && I % kGK == 0 && r >= 0 &&
-         r <= kGroupMaxR && groups <= kGroupMaxG;
+         r <= kGroupMaxR && groups <= kGroupMaxG &&
+         kRingBytes + gate_sz_bytes(d) + kGateStatic <= kLdsMax &&
+         kRingBytes + down_sz_bytes(I) + kDownStatic <= kLdsMax;
 }
 
 hipError_t launch_grouped_ffn(const GroupedArgs& a, hipStream_t st) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)grouped_gateup_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kRingBytes);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax - kGateStatic);
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)grouped_down_kernel,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, kRingBytes);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax - kDownStatic);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
+  const int lds_gu = kRingBytes + gate_sz_bytes(a.d), lds_dn = kRingBytes + down_sz_bytes(a.I);
   hipLaunchKernelGGL(grouped_permute_kernel, dim3(1), dim3(1024), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -571,12 +643,10 @@ hipError_t launch_grouped_ffn(const GroupedArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(grouped_prep_kernel, dim3(xb + a.max_tiles), dim3(kGT), 0, st, a, xb);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(grouped_gateup_kernel, dim3(a.max_tiles, a.I / kGateCols), dim3(kGT), kRingBytes,
-                     st, a);
+  hipLaunchKernelGGL(grouped_gateup_kernel, dim3(a.max_tiles, a.I / kGateCols), dim3(kGT), lds_gu, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(grouped_down_kernel, dim3(a.max_tiles, a.d / kDownCols), dim3(kGT), kRingBytes,
-                     st, a);
+  hipLaunchKernelGGL(grouped_down_kernel, dim3(a.max_tiles, a.d / kDownCols), dim3(kGT), lds_dn, st, a);
   return hipGetLastError();
 }
 

@@ -11,6 +11,7 @@
 // rows with fully coalesced 16-byte loads.  A lane's chunks are the same for
 // every row it visits, so the 32*CPL activations it needs stay in registers.
 #include "moe_kernels.h"
+#include "moe_xchg.h"
 
 namespace moe {
 
@@ -92,6 +93,23 @@ __global__ void __launch_bounds__(256) route_kernel(const __half* __restrict__ x
   if (wave == 0) wave_topk<true>(lt, E, K, idx + (size_t)t * K, wout + (size_t)t * K, tk_scratch);
   if (threadIdx.x == 0)
     __hip_atomic_store(&counters[t], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The same selection and weights by one 512-thread workgroup per token
+// (E <= 256, K <= 32): two-stage ranking of the keys (moe_xchg.h), a few
+// barriers instead of one wave's 32 ballot rounds.
+__global__ void __launch_bounds__(512) topk_block_kernel(const float* __restrict__ logits, int E, int K,
+                                                         int32_t* __restrict__ idx,
+                                                         float* __restrict__ w) {
+  __shared__ float lg[256];
+  __shared__ uint64_t keys[256];
+  __shared__ int part[256];
+  __shared__ uint64_t cand[128];
+  __shared__ uint64_t sorted[32];
+  const int t = blockIdx.x;
+  if ((int)threadIdx.x < E) lg[threadIdx.x] = logits[(size_t)t * E + threadIdx.x];
+  __syncthreads();
+  eng::block_topk(lg, E, K, idx + (size_t)t * K, w + (size_t)t * K, keys, part, cand, sorted);
 }
 
 __global__ void __launch_bounds__(64) topk_kernel(const float* __restrict__ logits, int E, int K,
@@ -465,7 +483,10 @@ hipError_t launch_route(const __half* x, const __half* W, int T, int E, int d, i
 
 hipError_t launch_topk(const float* logits, int T, int E, int K, int32_t* idx, float* w,
                        hipStream_t st) {
-  hipLaunchKernelGGL(topk_kernel, dim3(T), dim3(64), 0, st, logits, E, K, idx, w);
+  if (E <= 256 && K <= 32)
+    hipLaunchKernelGGL(topk_block_kernel, dim3(T), dim3(512), 0, st, logits, E, K, idx, w);
+  else
+    hipLaunchKernelGGL(topk_kernel, dim3(T), dim3(64), 0, st, logits, E, K, idx, w);
   return hipGetLastError();
 }
 

@@ -258,28 +258,6 @@ __device__ __forceinline__ float dot32_codes(const U4& q, const hv2 (&xp)[16]) {
   }
   return fmaf(d1, 0.0625f, d0);
 }
-// The same against fp32 activations given as two fp16 terms each (hi + lo,
-// pair order), both terms of a pair meeting the same masked codes.
-__device__ __forceinline__ float dot32_codes2(const U4& q, const hv2 (&hh)[16], const hv2 (&hl)[16]) {
-  const uint32_t wd[4] = {q.x, q.y, q.z, q.w};
-  float d0 = 0.f, d1 = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t w = wd[i], w8 = wd[i] >> 8;
-    const hv2 p0 = __builtin_bit_cast(hv2, w & 0x000F000Fu), p1 = __builtin_bit_cast(hv2, w & 0x00F000F0u);
-    const hv2 p2 = __builtin_bit_cast(hv2, w8 & 0x000F000Fu), p3 = __builtin_bit_cast(hv2, w8 & 0x00F000F0u);
-    d0 = __builtin_amdgcn_fdot2(p0, hh[4 * i + 0], d0, false);
-    d0 = __builtin_amdgcn_fdot2(p0, hl[4 * i + 0], d0, false);
-    d1 = __builtin_amdgcn_fdot2(p1, hh[4 * i + 1], d1, false);
-    d1 = __builtin_amdgcn_fdot2(p1, hl[4 * i + 1], d1, false);
-    d0 = __builtin_amdgcn_fdot2(p2, hh[4 * i + 2], d0, false);
-    d0 = __builtin_amdgcn_fdot2(p2, hl[4 * i + 2], d0, false);
-    d1 = __builtin_amdgcn_fdot2(p3, hh[4 * i + 3], d1, false);
-    d1 = __builtin_amdgcn_fdot2(p3, hl[4 * i + 3], d1, false);
-  }
-  return fmaf(d1, 0.0625f, d0);
-}
-
 // Sums over the wave of four values per lane at once: lane l returns the
 // total of value (l & 3). Two exchange stages leave each lane one value
 // summed over its lane pair and quad; rotations within the 16-lane row and
@@ -1008,11 +986,11 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
       }
       bd_load();
       // down dot products: h of the batch's expert is reloaded when the
-      // expert changes. The lane's 32 h values (fp32) become two fp16 terms
-      // each, hi = fp16(h) and lo = fp16(h - hi), in pair order, so the codes
-      // meet them in v_dot2_f32_f16; hi + lo carries h to about 2^-22
-      // (|h| < 65504).
-      hv2 hh[16], hlo[16];
+      // expert changes. The lane's 32 h values (fp32) are rounded once to
+      // fp16 (|h| < 65504), in pair order, so the codes meet them in
+      // v_dot2_f32_f16 with fp32 accumulation; the zero-point term takes the
+      // fp32 sum of h.
+      hv2 hh[16];
       float hsum = 0.f;
       int kc = -1;
       auto dn_compute = [&](int i, const DQ& dq, const DS& dsz) {
@@ -1038,9 +1016,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
 #pragma unroll
             for (int mm = 0; mm < 4; ++mm) {
               const float a0 = hv[8 * q4 + mm], a1 = hv[8 * q4 + mm + 4];
-              const _Float16 h0 = (_Float16)a0, h1 = (_Float16)a1;
-              hh[4 * q4 + mm] = hv2{h0, h1};
-              hlo[4 * q4 + mm] = hv2{(_Float16)(a0 - (float)h0), (_Float16)(a1 - (float)h1)};
+              hh[4 * q4 + mm] = hv2{(_Float16)a0, (_Float16)a1};
             }
           }
         }
@@ -1048,7 +1024,7 @@ __global__ void __launch_bounds__(NT) tokens_kernel(EngineArgs a) {
         for (int jh = 0; jh < NDH; ++jh) {
           const int jj = ((n0 + jh) % DI) * SH::UPI + su;
           const float2 sz = h2f2(dsz[jh]);
-          float v = (sz.x * 16777216.f) * dot32_codes2(dq[jh], hh, hlo) + sz.y * hsum;
+          float v = (sz.x * 16777216.f) * dot32_codes(dq[jh], hh) + sz.y * hsum;
           v = group_sum(v, SH::CH);
           if (cl == 0) yp[jj * NLX + k] = rt.wl[k] * v;
         }

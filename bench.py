@@ -246,6 +246,45 @@ def per_call_path(B, torch, spec, table, layers, tokens, n_steps, wl, hip):
     return ms / n_steps, gu
 
 
+def head_mlp_path(B, torch, wl, n_heads=96, hidden=512, calls=192):
+    """Full prerouter head (moe_preroute_mlp: fc1 -> erf-GELU -> fc2 + the
+    linear residual path on x ++ two routed-set one-hots) at batch 1, one call
+    per decode step, replayed from a HIP graph, rotating over ``n_heads``
+    seeded heads (about 3.4 MB each, more in all than the last-level cache).
+    Algorithmic bytes per call: fc1's x columns, the 2K one-hot rows it
+    gathers, b1, fc2, b2, the residual path, x, the logits."""
+    import synth
+    spec = B.spec_from_workload(wl)
+    d, E, K = wl.d, wl.E, wl.K
+    heads, keep = [], []
+    for n in range(n_heads):
+        h = synth.prerouter_mlp(wl, n, hidden)
+        dev = [torch.from_numpy(np.ascontiguousarray(a)).cuda()
+               for a in (h["w1"][:, :d], h["w1"][:, d:].T, h["w2"], h["b1"], h["b2"], h["wl"])]
+        keep.append(dev)
+        heads.append(B.head_mlp(hidden, dev[0], dev[1], dev[2], b1=dev[3], b2=dev[4], w_l=dev[5]))
+    x = torch.from_numpy(np.stack([synth.token_draws(wl, 0, 1)[0].astype(np.float16)])).cuda()
+    g = np.random.default_rng(7)
+    rt = torch.from_numpy(g.choice(E, (1, K), replace=False).astype(np.int32)).cuda()
+    rtm1 = torch.from_numpy(g.choice(E, (1, K), replace=False).astype(np.int32)).cuda()
+    idx = torch.empty(1, K, dtype=torch.int32, device="cuda")
+    w = torch.empty(1, K, dtype=torch.float32, device="cuda")
+    ws = torch.zeros(B.preroute_mlp_workspace_bytes(spec, hidden, 1), dtype=torch.uint8, device="cuda")
+    B.preroute_mlp(spec, heads[0], x, rt, rtm1, idx, w, ws)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        for j in range(calls):
+            B.preroute_mlp(spec, heads[j % n_heads], x, rt, rtm1, idx, w, ws)
+    graph.replay()
+    graph.replay()
+    ms = time_launch(torch, graph.replay) / calls
+    nbytes = (hidden * d + 2 * K * hidden + hidden + E * hidden + E + E * d + d) * 2 + E * 4
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    log("prerouter MLP head, batch 1: %.2f us per call, %.1f GB/s" % (ms * 1e3, gbs))
+    return {"us_per_call": round(ms * 1e3, 3), "bytes_per_call": nbytes, "GB_s": round(gbs, 1),
+            "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "hidden": hidden, "heads": n_heads}
+
+
 def batched_path(B, torch, spec, table, wl, L, Ts=(64, 512), reps=20):
     """Batched decode / prefill on the 35B-class layer (tokens grouped by
     expert, MFMA contractions): Zipf(1.1) routing through softmax-top-k on
@@ -479,6 +518,7 @@ def main():
     log("per-call path: %.2f us/step; its gate/up kernel %.2f us" % (pc_us * 1e3, gu_ms * 1e3))
 
     batched = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
+    head_mlp = head_mlp_path(B, torch, wl)
 
     tier_res = None if args.no_tier else tier_path(B, torch, T=args.tier_tokens)
 
@@ -517,6 +557,7 @@ def main():
             "GB_s": round(chain_gbs, 1),
         },
         "batched": batched,
+        "prerouter_mlp_head": head_mlp,
         "host_tier": tier_res,
         "per_call_path": {"us_per_step": round(pc_us * 1e3, 3),
                           "gateup_kernel_us": round(gu_ms * 1e3, 3)},

@@ -170,6 +170,43 @@ int moe_preroute(const moe_layer_spec* next, const void* x_f16, const void* w_he
                  size_t workspace_bytes, void* stream);
 
 /*
+ * Full prerouter head (Sec. 3.2, Head): fc1 -> erf-GELU -> fc2 plus a linear
+ * residual path on the hidden state. The input feature of token t is
+ *   f = [x_t (d), onehot(routed_t[t]) (E), onehot(routed_tm1[t]) (E)],
+ * the experts this layer routed to at this token and at the previous one.
+ *   hidden = fp16(gelu(W1 f + b1)),  gelu(z) = z (1 + erf(z / sqrt 2)) / 2
+ *   l      = W2 hidden + b2 + W_l x_t          (fp32)
+ * then the softmax-top-k of moe_route on l. The result is layer N+1's
+ * routing at token t+1 (Prediction-as-routing). `next` describes layer N+1;
+ * this layer's expert count and K are taken to be next's.
+ * Layout (all fp16, device, 16-byte aligned):
+ *   w1_x [H][d]   the columns of W1 that multiply x
+ *   w1_r [2E][H]  the columns of W1 that multiply the one-hots, transposed:
+ *                 row e for expert e at this token, row E + e at the previous
+ *   b1 [H] (or NULL: zero), w2 [E][H], b2 [E] (or NULL), w_l [E][d] (or NULL)
+ * H = `hidden`, a multiple of 8; d and E multiples of 8.
+ * routed_t: device int32 [T][K]; routed_tm1: device int32 [T][K] or NULL (no
+ * previous token: a zero one-hot). Ids outside [0, E) contribute nothing.
+ * logits_opt: device fp32 [T][E] or NULL; pred_idx [T][K], pred_w [T][K].
+ * workspace: moe_preroute_mlp_workspace_bytes(next, hidden, T) bytes of
+ * device memory (no initial contents needed).
+ */
+typedef struct moe_head_mlp {
+  int32_t hidden;
+  const void* w1_x;
+  const void* w1_r;
+  const void* b1;
+  const void* w2;
+  const void* b2;
+  const void* w_l;
+} moe_head_mlp;
+size_t moe_preroute_mlp_workspace_bytes(const moe_layer_spec* next, int hidden, int T);
+int moe_preroute_mlp(const moe_layer_spec* next, const moe_head_mlp* head, const void* x_f16, int T,
+                     const int32_t* routed_t, const int32_t* routed_tm1, float* logits_opt,
+                     int32_t* pred_idx, float* pred_w, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+/*
  * Experts (Sec. 3.1, Math contract; Sec. 3.3): for every token t and every
  * list position k in [0, K+S):
  *   e = idx[t][k] for k < K, else E + (k - K)

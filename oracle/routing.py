@@ -27,6 +27,22 @@ Readings (the paper is silent on these):
 * Sigmoid-group bias: an optional per-expert vector added to the sigmoid
   before selection (zero when absent); group membership is contiguous
   (group ``i`` holds experts ``i*E/n .. (i+1)*E/n - 1``).
+
+The full prerouter head follows §3.2 (Head): per layer
+``fc1 -> erf-GELU -> fc2`` plus a linear residual path ``l`` on the hidden
+state; the input feature is the hidden state concatenated with two top-k
+one-hots, the experts this layer routed to at this token and those at the
+previous token (``d + 2E`` features).  Readings for the head:
+
+* Feature order: ``[x (d), onehot(routed at t) (E), onehot(routed at t-1) (E)]``;
+  at the first token the previous-token one-hot is all zero.
+* Both linear layers carry optional fp16 biases (zero when absent); ``l``
+  acts on ``x`` alone (``W_l [E, d]``, the shape of the next layer's router,
+  from which it is warm-started; absent means zero).
+* Precision (the heads are fp16): fc1's pre-activation and GELU are exact
+  (float64), the hidden activation is rounded once to fp16 (it is fc2's fp16
+  input), and ``fc2(hidden) + b2 + l(x)`` is exact and rounded once to fp32.
+* GELU is the erf form ``z * Phi(z) = z (1 + erf(z / sqrt 2)) / 2``.
 """
 
 import numpy as np
@@ -90,6 +106,57 @@ def preroute(w_head16, x16, k):
     *next* token (§3.2, Motivation and Prediction-as-routing).
     """
     return route(w_head16, x16, k)
+
+
+def gelu_erf(z):
+    """erf-GELU ``z Phi(z)`` in float64 (§3.2, Head)."""
+    from scipy.special import erf
+    z = np.asarray(z, dtype=np.float64)
+    return 0.5 * z * (1.0 + erf(z / np.sqrt(2.0)))
+
+
+def prerouter_feature(x16, routed_t, routed_tm1, n_experts):
+    """The head's input: ``x`` followed by the one-hots of the set routed at
+    this token and at the previous one (``None`` at the first token), as
+    float64 ``[d + 2E]``."""
+    x = np.asarray(x16, dtype=np.float16).astype(np.float64)
+    oh = np.zeros(2 * n_experts, dtype=np.float64)
+    oh[np.asarray(routed_t, dtype=np.int64)] = 1.0
+    if routed_tm1 is not None:
+        oh[n_experts + np.asarray(routed_tm1, dtype=np.int64)] = 1.0
+    return np.concatenate([x, oh])
+
+
+def prerouter_mlp_logits(head, x16, routed_t, routed_tm1):
+    """Full prerouter head logits, fp32 ``[E]``.
+
+    ``head``: dict with ``w1`` fp16 ``[H, d + 2E]``, ``w2`` fp16 ``[E, H]``,
+    and optional ``b1`` fp16 ``[H]``, ``b2`` fp16 ``[E]``, ``wl`` fp16
+    ``[E, d]`` (None or absent: zero).
+    """
+    w1 = np.asarray(head["w1"], dtype=np.float16).astype(np.float64)
+    w2 = np.asarray(head["w2"], dtype=np.float16).astype(np.float64)
+    n_e = w2.shape[0]
+    f = prerouter_feature(x16, routed_t, routed_tm1, n_e)
+    pre = w1 @ f
+    if head.get("b1") is not None:
+        pre = pre + np.asarray(head["b1"], dtype=np.float16).astype(np.float64)
+    hid = gelu_erf(pre).astype(np.float16).astype(np.float64)
+    out = w2 @ hid
+    if head.get("b2") is not None:
+        out = out + np.asarray(head["b2"], dtype=np.float16).astype(np.float64)
+    if head.get("wl") is not None:
+        wl = np.asarray(head["wl"], dtype=np.float16).astype(np.float64)
+        out = out + wl @ np.asarray(x16, dtype=np.float16).astype(np.float64)
+    return out.astype(np.float32)
+
+
+def preroute_mlp(head, x16, routed_t, routed_tm1, k):
+    """Full prerouter head + softmax-top-k: the next layer's routing at the
+    next token (§3.2, Head and Prediction-as-routing)."""
+    l = prerouter_mlp_logits(head, x16, routed_t, routed_tm1)
+    inds, w = softmax_topk(l, k)
+    return l, inds, w
 
 
 def near_tie_gap(l, k):

@@ -41,6 +41,11 @@ class MoeEngineLayer(ctypes.Structure):
                 ("mix_perm", c_void_p)]
 
 
+class MoeHeadMlp(ctypes.Structure):
+    _fields_ = [("hidden", c_int32), ("w1_x", c_void_p), ("w1_r", c_void_p), ("b1", c_void_p),
+                ("w2", c_void_p), ("b2", c_void_p), ("w_l", c_void_p)]
+
+
 class MoeBundleLayout(ctypes.Structure):
     _fields_ = [("gate", ctypes.c_int64 * 4), ("up", ctypes.c_int64 * 4),
                 ("down", ctypes.c_int64 * 4)]
@@ -75,6 +80,10 @@ SIGNATURES = {
                           c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "moe_preroute": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
                              c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "moe_preroute_mlp_workspace_bytes": (c_size_t, [ctypes.POINTER(MoeLayerSpec), c_int, c_int]),
+    "moe_preroute_mlp": (c_int, [ctypes.POINTER(MoeLayerSpec), ctypes.POINTER(MoeHeadMlp), c_void_p,
+                                 c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                 c_size_t, c_void_p]),
     "moe_expert_ffn_int4_lora": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p,
                                          c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                          c_void_p]),
@@ -357,6 +366,27 @@ def preroute(spec_next, x, w_head, pred_idx, pred_w, workspace, logits=None, str
                               _ptr(pred_idx), _ptr(pred_w), _ptr(workspace),
                               workspace.numel() * workspace.element_size(), _stream(stream)),
            "moe_preroute")
+
+
+def head_mlp(hidden, w1_x, w1_r, w2, b1=None, b2=None, w_l=None):
+    """moe_head_mlp of device fp16 tensors (layouts as in include/moe_api.h)."""
+    def p(t):
+        return None if t is None else t.data_ptr()
+    return MoeHeadMlp(hidden, p(w1_x), p(w1_r), p(b1), p(w2), p(b2), p(w_l))
+
+
+def preroute_mlp_workspace_bytes(spec_next, hidden, T):
+    return lib().moe_preroute_mlp_workspace_bytes(ctypes.byref(spec_next), hidden, T)
+
+
+def preroute_mlp(spec_next, head, x, routed_t, routed_tm1, pred_idx, pred_w, workspace, logits=None,
+                 stream=None):
+    """Full prerouter head (moe_preroute_mlp); ``head`` from ``head_mlp``."""
+    T = x.shape[0]
+    _check(lib().moe_preroute_mlp(ctypes.byref(spec_next), ctypes.byref(head), _ptr(x), T, _ptr(routed_t),
+                                  _ptr(routed_tm1), _ptr(logits), _ptr(pred_idx), _ptr(pred_w),
+                                  _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                  _stream(stream)), "moe_preroute_mlp")
 
 
 def expert_ffn(spec, table, layer, x, idx, y_experts, status, workspace, stream=None):

@@ -260,6 +260,52 @@ int moe_preroute(const moe_layer_spec* next, const void* x_f16, const void* w_he
                       workspace_bytes, stream);
 }
 
+size_t moe_preroute_mlp_workspace_bytes(const moe_layer_spec* next, int hidden, int T) {
+  if (moe_spec_check(next) != MOE_OK || hidden <= 0 || T < 0) return 0;
+  const size_t t = (size_t)(T < 1 ? 1 : T);
+  return (t * hidden * 2 + 255) / 256 * 256 + t * next->n_experts * 4;
+}
+
+int moe_preroute_mlp(const moe_layer_spec* next, const moe_head_mlp* head, const void* x_f16, int T,
+                     const int32_t* routed_t, const int32_t* routed_tm1, float* logits_opt,
+                     int32_t* pred_idx, float* pred_w, void* ws, size_t ws_bytes, void* stream) {
+  int rc = moe_spec_check(next);
+  if (rc != MOE_OK) return rc;
+  if (!head || T < 0) return MOE_EINVAL;
+  const int H = head->hidden, d = next->d_model, E = next->n_experts, K = next->top_k;
+  if (H <= 0 || H % 8 || d % 8 || E % 8 || K > 32) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!x_f16 || !head->w1_x || !head->w1_r || !head->w2 || !routed_t || !pred_idx || !pred_w || !ws)
+    return MOE_EINVAL;
+  if (!aligned16(x_f16) || !aligned16(head->w1_x) || !aligned16(head->w1_r) || !aligned16(head->w2) ||
+      (head->b1 && !aligned16(head->b1)) || (head->b2 && !aligned16(head->b2)) ||
+      (head->w_l && !aligned16(head->w_l)) || !aligned4(routed_t) || (routed_tm1 && !aligned4(routed_tm1)) ||
+      !aligned4(pred_idx) || !aligned4(pred_w) || !aligned16(ws) || (logits_opt && !aligned16(logits_opt)))
+    return MOE_EALIGN;
+  if (ws_bytes < moe_preroute_mlp_workspace_bytes(next, H, T)) return MOE_ENOMEM;
+  moe::HeadMlpArgs a{};
+  a.T = T;
+  a.d = d;
+  a.E = E;
+  a.K = K;
+  a.H = H;
+  a.x = static_cast<const __half*>(x_f16);
+  a.w1x = static_cast<const __half*>(head->w1_x);
+  a.w1r = static_cast<const __half*>(head->w1_r);
+  a.b1 = static_cast<const __half*>(head->b1);
+  a.w2 = static_cast<const __half*>(head->w2);
+  a.b2 = static_cast<const __half*>(head->b2);
+  a.wl = static_cast<const __half*>(head->w_l);
+  a.routed_t = routed_t;
+  a.routed_tm1 = routed_tm1;
+  a.hidden = static_cast<__half*>(ws);
+  a.logits = logits_opt ? logits_opt
+                        : reinterpret_cast<float*>(static_cast<char*>(ws) + ((size_t)T * H * 2 + 255) / 256 * 256);
+  a.idx = pred_idx;
+  a.w = pred_w;
+  return from_hip(moe::launch_head_mlp(a, static_cast<hipStream_t>(stream)));
+}
+
 int moe_expert_ffn_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, int layer,
                              const void* x_f16, int T, const int32_t* idx, float* y_experts,
                              uint32_t* status_dev, void* ws, size_t ws_bytes, void* stream) {

@@ -50,8 +50,9 @@ using eng::st_tag;
 
 constexpr int NX = 8, NPX = 32, NWG = NX * NPX, NT = 512, NWV = NT / 64;  // XCDs, workgroups per XCD
 // A team is NM workgroups of one XCD that run one step at a time; NTM teams
-// (TPX per XCD) keep NTM steps in flight.
-constexpr int NM = 16, NTM = NWG / NM, TPX = NPX / NM;
+// (NPX / NM per XCD) keep NTM steps in flight.
+constexpr int NM = 16, NTM = NWG / NM;
+static_assert(NPX % NM == 0, "whole teams per XCD");
 
 typedef _Float16 hv2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));

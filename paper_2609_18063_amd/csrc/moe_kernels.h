@@ -30,6 +30,26 @@ hipError_t launch_route(const __half* x, const __half* W, int T, int E, int d, i
                         hipStream_t st);
 hipError_t launch_topk(const float* logits, int T, int E, int K, int32_t* idx, float* w,
                        hipStream_t st);
+
+// Full prerouter head (moe_head.hip): fc1 + erf-GELU into `hidden`, fc2 + b2 +
+// the residual path into `logits`, then softmax-top-k into idx / w.
+struct HeadMlpArgs {
+  int T, d, E, K, H;
+  const __half* x;                // [T][d]
+  const __half* w1x;              // [H][d]
+  const __half* w1r;              // [2E][H]
+  const __half* b1;               // [H] or null
+  const __half* w2;               // [E][H]
+  const __half* b2;               // [E] or null
+  const __half* wl;               // [E][d] or null
+  const int32_t* routed_t;        // [T][K]
+  const int32_t* routed_tm1;      // [T][K] or null
+  __half* hidden;                 // [T][H]
+  float* logits;                  // [T][E]
+  int32_t* idx;                   // [T][K]
+  float* w;                       // [T][K]
+};
+hipError_t launch_head_mlp(const HeadMlpArgs& a, hipStream_t st);
 // prof_start / prof_stop: if non-null, the gate/up kernel is launched with
 // hipExtLaunchKernelGGL and records them around its execution.
 hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st, hipEvent_t prof_start,

@@ -33,7 +33,7 @@ import numpy as np
 __all__ = [
     "WORKLOADS", "Workload", "rng", "int4_projection", "fp32_weights",
     "lora_pair", "bundle", "router_weights", "token_draws", "zipf_logits",
-    "mixing", "ar1_token_draws",
+    "mixing", "ar1_token_draws", "prerouter_mlp",
 ]
 
 
@@ -115,6 +115,18 @@ def bundle(wl, layer, expert, lora=True, lora_on=("gate", "up", "down")):
 def router_weights(wl, layer, kind):
     """fp16 ``[E, d]``; ``kind`` 0 = the layer's router, 1 = its prerouter head."""
     return rng(wl.wid, layer, _ROUTER_ID, kind).normal(0.0, 0.02, size=(wl.E, wl.d)).astype(np.float16)
+
+
+def prerouter_mlp(wl, layer, hidden=512):
+    """Full prerouter head of ``layer`` (fp16, N(0, 0.02) entries): ``w1``
+    ``[hidden, d + 2E]``, ``b1 [hidden]``, ``w2 [E, hidden]``, ``b2 [E]``, and
+    the residual path ``wl`` drawn as the next layer's router."""
+    g = rng(wl.wid, layer, _ROUTER_ID, 2)
+    w1 = g.normal(0.0, 0.02, size=(hidden, wl.d + 2 * wl.E)).astype(np.float16)
+    b1 = g.normal(0.0, 0.02, size=hidden).astype(np.float16)
+    w2 = g.normal(0.0, 0.02, size=(wl.E, hidden)).astype(np.float16)
+    b2 = g.normal(0.0, 0.02, size=wl.E).astype(np.float16)
+    return {"w1": w1, "b1": b1, "w2": w2, "b2": b2, "wl": router_weights(wl, layer + 1, 0)}
 
 
 def token_draws(wl, t0, count, stream=0):

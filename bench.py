@@ -285,6 +285,46 @@ def head_mlp_path(B, torch, wl, n_heads=96, hidden=512, calls=192):
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "hidden": hidden, "heads": n_heads}
 
 
+def sigmoid_group_path(B, torch, calls=192):
+    """Sigmoid-group routing (App. A; 8 groups, 4 survive, scale 2.5) at the
+    8B tier's shape (d 4096, E 64, K 4): moe_route at batch 1 (router logits
+    and the selection, one call per decode step, 24 routers rotating, from a
+    HIP graph) and the selection alone on 64 tokens' logits."""
+    import synth
+    wl = synth.WORKLOADS["tier8b"]
+    spec = B.make_spec(wl.d, wl.E, wl.K, wl.S, wl.I, wl.r, wl.lora_scale, sigmoid_group=(8, 4, 2.5))
+    routers = [torch.from_numpy(synth.router_weights(wl, n, 0)).cuda() for n in range(24)]
+    x = torch.from_numpy(np.stack([synth.token_draws(wl, 0, 1)[0].astype(np.float16)])).cuda()
+    idx = torch.empty(1, wl.K, dtype=torch.int32, device="cuda")
+    w = torch.empty(1, wl.K, dtype=torch.float32, device="cuda")
+    ws = torch.zeros(B.workspace_bytes(spec, 1), dtype=torch.uint8, device="cuda")
+    B.route(spec, x, routers[0], idx, w, ws)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        for j in range(calls):
+            B.route(spec, x, routers[j % len(routers)], idx, w, ws)
+    graph.replay()
+    ms = time_launch(torch, graph.replay) / calls
+    nbytes = wl.E * wl.d * 2 + wl.d * 2 + wl.E * 4 + wl.K * 8
+    T = 64
+    lg = torch.from_numpy(synth.zipf_logits(wl, T, seed=3)).cuda()
+    idx64 = torch.empty(T, wl.K, dtype=torch.int32, device="cuda")
+    w64 = torch.empty(T, wl.K, dtype=torch.float32, device="cuda")
+    B.topk(spec, lg, idx64, w64)
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=torch.cuda.Stream()):
+        for _ in range(calls):
+            B.topk(spec, lg, idx64, w64)
+    g2.replay()
+    ms_sel = time_launch(torch, g2.replay) / calls
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    log("sigmoid-group routing (8B tier shape): route %.2f us per call (%.1f GB/s); selection of %d "
+        "tokens %.2f us" % (ms * 1e3, gbs, T, ms_sel * 1e3))
+    return {"route_us_per_call": round(ms * 1e3, 3), "route_bytes": nbytes, "route_GB_s": round(gbs, 1),
+            "select_T64_us": round(ms_sel * 1e3, 3), "groups": "8 of which 4 survive, scale 2.5",
+            "shape": "d 4096, E 64, K 4"}
+
+
 def batched_path(B, torch, spec, table, wl, L, Ts=(64, 512), reps=20):
     """Batched decode / prefill on the 35B-class layer (tokens grouped by
     expert, MFMA contractions): Zipf(1.1) routing through softmax-top-k on
@@ -519,6 +559,7 @@ def main():
 
     batched = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
     head_mlp = head_mlp_path(B, torch, wl)
+    sigmoid_group = sigmoid_group_path(B, torch)
 
     tier_res = None if args.no_tier else tier_path(B, torch, T=args.tier_tokens)
 
@@ -558,6 +599,7 @@ def main():
         },
         "batched": batched,
         "prerouter_mlp_head": head_mlp,
+        "sigmoid_group_routing": sigmoid_group,
         "host_tier": tier_res,
         "per_call_path": {"us_per_step": round(pc_us * 1e3, 3),
                           "gateup_kernel_us": round(gu_ms * 1e3, 3)},

@@ -56,6 +56,9 @@ extern "C" {
 
 /* ---- layer description (the MoESpec of Sec. 3) --------------------------- */
 #define MOE_ROUTING_SOFTMAX_TOPK 0   /* App. A, Softmax-topk                    */
+#define MOE_ROUTING_SIGMOID_GROUP 1  /* App. A, Sigmoid-group (moe_topk, moe_route,
+                                        moe_preroute, moe_preroute_mlp; the
+                                        decode engines take softmax-topk only)  */
 
 typedef struct moe_layer_spec {
   int32_t d_model;     /* hidden size d; multiple of 64, <= 8192             */
@@ -67,7 +70,11 @@ typedef struct moe_layer_spec {
   int32_t lora_rank;   /* r; 0 (no adapters) or 1..64                        */
   float   lora_scale;  /* alpha / r, the LoRA delta multiplier (Sec. 3.3)    */
   int32_t routing;     /* MOE_ROUTING_*                                      */
-  int32_t reserved[7]; /* must be zero                                       */
+  int32_t n_groups;    /* sigmoid-group: groups n, E % n == 0, E <= 256; else 0 */
+  int32_t top_groups;  /* sigmoid-group: surviving groups G, 1..n, K <= G E / n;
+                          else 0                                             */
+  float   route_scale; /* sigmoid-group: weight scale s > 0; else 0           */
+  int32_t reserved[4]; /* must be zero                                       */
 } moe_layer_spec;
 
 /*
@@ -253,11 +260,23 @@ int moe_combine_add(const moe_layer_spec* spec, const float* y_experts, const fl
                     float* y_inout, void* stream);
 
 /*
- * Softmax-top-k on given logits (App. A): logits device fp32 [T][E] ->
- * idx [T][K], w [T][K]. Same selection and weights as moe_route.
+ * Top-k on given logits (App. A), by spec->routing: logits device fp32
+ * [T][E] -> idx [T][K], w [T][K]. Same selection and weights as moe_route.
+ * Softmax-topk: the K largest logits (descending, ties to the lower id),
+ * w = softmax over the selected set. Sigmoid-group: sigma = sigmoid(l); a
+ * group's score is the sum of its two largest sigma (groups are contiguous
+ * runs of E / n ids); the G best groups survive (ties to the lower group);
+ * the K largest sigma among the survivors are selected (descending, ties to
+ * the lower id) and w = s sigma / (sum of the selected sigma + 1e-20).
  */
 int moe_topk(const moe_layer_spec* spec, const float* logits, int T, int32_t* idx, float* w,
              void* stream);
+
+/* Sigmoid-group top-k with a selection bias (App. A: selection uses the
+ * biased score sigma + bias, the weights the raw sigma): bias device fp32 [E]
+ * or NULL. MOE_EINVAL unless spec->routing is MOE_ROUTING_SIGMOID_GROUP. */
+int moe_topk_biased(const moe_layer_spec* spec, const float* logits, const float* bias, int T,
+                    int32_t* idx, float* w, void* stream);
 
 /* ---- decode-chain stand-in for attention ---------------------------------
  * The paper's decoder runs attention before each MoE layer, and the head of

@@ -19,13 +19,15 @@ c_int, c_int32, c_float, c_void_p, c_size_t = (ctypes.c_int, ctypes.c_int32, cty
 
 MOE_OK, MOE_EINVAL, MOE_EALIGN, MOE_ENOTRESIDENT, MOE_EHIP, MOE_ENOMEM = 0, -1, -2, -3, -4, -5
 MOE_STATUS_SLOT_MISS, MOE_STATUS_BAD_INDEX = 1, 2
+MOE_ROUTING_SOFTMAX_TOPK, MOE_ROUTING_SIGMOID_GROUP = 0, 1
 
 
 class MoeLayerSpec(ctypes.Structure):
     _fields_ = [("d_model", c_int32), ("n_experts", c_int32), ("top_k", c_int32),
                 ("n_shared", c_int32), ("d_expert", c_int32), ("group_size", c_int32),
                 ("lora_rank", c_int32), ("lora_scale", c_float), ("routing", c_int32),
-                ("reserved", c_int32 * 7)]
+                ("n_groups", c_int32), ("top_groups", c_int32), ("route_scale", c_float),
+                ("reserved", c_int32 * 4)]
 
 
 class MoeProj(ctypes.Structure):
@@ -94,6 +96,8 @@ SIGNATURES = {
                             c_void_p]),
     "moe_topk": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p, c_void_p,
                          c_void_p]),
+    "moe_topk_biased": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
+                                c_void_p, c_void_p]),
     "moe_profile_arm": (c_int, [c_int, c_void_p, c_void_p]),
     "moe_slot_policy_create": (c_int, [c_int, c_int, c_int, ctypes.POINTER(c_void_p)]),
     "moe_slot_policy_destroy": (c_int, [c_void_p]),
@@ -164,11 +168,16 @@ def _stream(stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def make_spec(d, n_experts, top_k, n_shared, d_expert, lora_rank, lora_scale, group_size=64):
+def make_spec(d, n_experts, top_k, n_shared, d_expert, lora_rank, lora_scale, group_size=64,
+              sigmoid_group=None):
+    """``sigmoid_group``: None (softmax-topk) or (n_groups, top_groups, scale)."""
     s = MoeLayerSpec()
     s.d_model, s.n_experts, s.top_k, s.n_shared = d, n_experts, top_k, n_shared
     s.d_expert, s.group_size, s.lora_rank, s.lora_scale = d_expert, group_size, lora_rank, lora_scale
-    s.routing = 0
+    s.routing = MOE_ROUTING_SOFTMAX_TOPK
+    if sigmoid_group is not None:
+        s.routing = MOE_ROUTING_SIGMOID_GROUP
+        s.n_groups, s.top_groups, s.route_scale = sigmoid_group
     return s
 
 
@@ -418,6 +427,13 @@ def topk(spec, logits, idx, w, stream=None):
     T = logits.shape[0]
     _check(lib().moe_topk(ctypes.byref(spec), _ptr(logits), T, _ptr(idx), _ptr(w), _stream(stream)),
            "moe_topk")
+
+
+def topk_biased(spec, logits, bias, idx, w, stream=None):
+    """Sigmoid-group top-k with a selection bias (fp32 [E] device tensor or None)."""
+    T = logits.shape[0]
+    _check(lib().moe_topk_biased(ctypes.byref(spec), _ptr(logits), _ptr(bias), T, _ptr(idx), _ptr(w),
+                                 _stream(stream)), "moe_topk_biased")
 
 
 def profile_arm(which, start_event, stop_event):

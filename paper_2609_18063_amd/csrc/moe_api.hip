@@ -90,8 +90,17 @@ int moe_spec_check(const moe_layer_spec* s) {
   if (s->group_size != 64) return MOE_EINVAL;
   if (s->lora_rank < 0 || s->lora_rank > 64) return MOE_EINVAL;
   if (!(s->lora_scale == s->lora_scale)) return MOE_EINVAL;
-  if (s->routing != MOE_ROUTING_SOFTMAX_TOPK) return MOE_EINVAL;
-  for (int i = 0; i < 7; ++i)
+  if (s->routing == MOE_ROUTING_SOFTMAX_TOPK) {
+    if (s->n_groups != 0 || s->top_groups != 0 || s->route_scale != 0.f) return MOE_EINVAL;
+  } else if (s->routing == MOE_ROUTING_SIGMOID_GROUP) {
+    const int n = s->n_groups, E = s->n_experts;
+    if (n < 1 || E > 256 || E % n) return MOE_EINVAL;
+    if (s->top_groups < 1 || s->top_groups > n || s->top_k > s->top_groups * (E / n)) return MOE_EINVAL;
+    if (!(s->route_scale > 0.f) || s->route_scale > 1e30f) return MOE_EINVAL;
+  } else {
+    return MOE_EINVAL;
+  }
+  for (int i = 0; i < 4; ++i)
     if (s->reserved[i] != 0) return MOE_EINVAL;
   return MOE_OK;
 }
@@ -240,10 +249,15 @@ static int route_common(const moe_layer_spec* s, const void* x, const void* W, i
   const WsLayout L = ws_layout(s, T);
   if (ws_bytes < L.total) return MOE_ENOMEM;
   float* logits = logits_opt ? logits_opt : at<float>(ws, L.logits);
-  return from_hip(moe::launch_route(static_cast<const __half*>(x), static_cast<const __half*>(W),
-                                    T, s->n_experts, s->d_model, s->top_k, logits, idx, w,
-                                    at<uint32_t>(ws, L.counters),
-                                    static_cast<hipStream_t>(stream)));
+  const bool sg = s->routing == MOE_ROUTING_SIGMOID_GROUP;
+  hipError_t e = moe::launch_route(static_cast<const __half*>(x), static_cast<const __half*>(W), T,
+                                   s->n_experts, s->d_model, s->top_k, logits, sg ? nullptr : idx, w,
+                                   at<uint32_t>(ws, L.counters), static_cast<hipStream_t>(stream));
+  if (e == hipSuccess && sg)
+    e = moe::launch_topk_sigmoid_group(logits, nullptr, T, s->n_experts, s->top_k, s->n_groups,
+                                       s->top_groups, s->route_scale, idx, w,
+                                       static_cast<hipStream_t>(stream));
+  return from_hip(e);
 }
 
 int moe_route(const moe_layer_spec* spec, const void* x_f16, const void* w_router_f16, int T,
@@ -303,6 +317,9 @@ int moe_preroute_mlp(const moe_layer_spec* next, const moe_head_mlp* head, const
                         : reinterpret_cast<float*>(static_cast<char*>(ws) + ((size_t)T * H * 2 + 255) / 256 * 256);
   a.idx = pred_idx;
   a.w = pred_w;
+  a.n_groups = next->routing == MOE_ROUTING_SIGMOID_GROUP ? next->n_groups : 0;
+  a.top_groups = next->top_groups;
+  a.route_scale = next->route_scale;
   return from_hip(moe::launch_head_mlp(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -443,14 +460,31 @@ int moe_topk(const moe_layer_spec* s, const float* logits, int T, int32_t* idx, 
   if (T == 0) return MOE_OK;
   if (!logits || !idx || !w) return MOE_EINVAL;
   if (!aligned16(logits) || !aligned4(idx) || !aligned4(w)) return MOE_EALIGN;
+  if (s->routing == MOE_ROUTING_SIGMOID_GROUP)
+    return from_hip(moe::launch_topk_sigmoid_group(logits, nullptr, T, s->n_experts, s->top_k, s->n_groups,
+                                                   s->top_groups, s->route_scale, idx, w,
+                                                   static_cast<hipStream_t>(stream)));
   return from_hip(moe::launch_topk(logits, T, s->n_experts, s->top_k, idx, w,
                                    static_cast<hipStream_t>(stream)));
+}
+
+int moe_topk_biased(const moe_layer_spec* s, const float* logits, const float* bias, int T, int32_t* idx,
+                    float* w, void* stream) {
+  int rc = moe_spec_check(s);
+  if (rc != MOE_OK) return rc;
+  if (s->routing != MOE_ROUTING_SIGMOID_GROUP || T < 0) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (!logits || !idx || !w) return MOE_EINVAL;
+  if (!aligned16(logits) || !aligned4(idx) || !aligned4(w) || (bias && !aligned4(bias))) return MOE_EALIGN;
+  return from_hip(moe::launch_topk_sigmoid_group(logits, bias, T, s->n_experts, s->top_k, s->n_groups,
+                                                 s->top_groups, s->route_scale, idx, w,
+                                                 static_cast<hipStream_t>(stream)));
 }
 
 // ---- persistent decode engine ----------------------------------------------
 
 int moe_engine_supported(const moe_layer_spec* s) {
-  if (moe_spec_check(s) != MOE_OK) return MOE_EINVAL;
+  if (moe_spec_check(s) != MOE_OK || s->routing != MOE_ROUTING_SOFTMAX_TOPK) return MOE_EINVAL;
   if (!moe::engine_shape_supported(s->d_model, s->d_expert, s->lora_rank, s->top_k, s->n_shared,
                                    s->n_experts))
     return MOE_EINVAL;
@@ -481,7 +515,7 @@ size_t moe_engine_workspace_bytes(const moe_layer_spec* s, int n_layers) {
 }
 
 int moe_engine_tokens_supported(const moe_layer_spec* s) {
-  if (moe_spec_check(s) != MOE_OK) return MOE_EINVAL;
+  if (moe_spec_check(s) != MOE_OK || s->routing != MOE_ROUTING_SOFTMAX_TOPK) return MOE_EINVAL;
   if (!moe::engine_tokens_supported(s->d_model, s->d_expert, s->lora_rank, s->top_k, s->n_shared,
                                     s->n_experts))
     return MOE_EINVAL;

@@ -93,6 +93,9 @@ hipError_t launch_head_mlp(const HeadMlpArgs& a, hipStream_t st) {
                      a.E, a.w2, a.b2, a.wl, a.logits);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.n_groups > 0)
+    return launch_topk_sigmoid_group(a.logits, nullptr, a.T, a.E, a.K, a.n_groups, a.top_groups,
+                                     a.route_scale, a.idx, a.w, st);
   return launch_topk(a.logits, a.T, a.E, a.K, a.idx, a.w, st);
 }
 

@@ -30,6 +30,10 @@ hipError_t launch_route(const __half* x, const __half* W, int T, int E, int d, i
                         hipStream_t st);
 hipError_t launch_topk(const float* logits, int T, int E, int K, int32_t* idx, float* w,
                        hipStream_t st);
+// Sigmoid-group top-k (App. A), E <= 256; bias [E] or null.
+hipError_t launch_topk_sigmoid_group(const float* logits, const float* bias, int T, int E, int K,
+                                     int n_groups, int top_groups, float scale, int32_t* idx, float* w,
+                                     hipStream_t st);
 
 // Full prerouter head (moe_head.hip): fc1 + erf-GELU into `hidden`, fc2 + b2 +
 // the residual path into `logits`, then softmax-top-k into idx / w.
@@ -48,6 +52,8 @@ struct HeadMlpArgs {
   float* logits;                  // [T][E]
   int32_t* idx;                   // [T][K]
   float* w;                       // [T][K]
+  int n_groups, top_groups;       // sigmoid-group selection when n_groups > 0
+  float route_scale;
 };
 hipError_t launch_head_mlp(const HeadMlpArgs& a, hipStream_t st);
 // prof_start / prof_stop: if non-null, the gate/up kernel is launched with

@@ -41,9 +41,9 @@ __global__ void __launch_bounds__(256) rmsnorm_f16_kernel(const float* __restric
     x[(size_t)t * d + j] = __half(static_cast<_Float16>((double)row[j] * r));
 }
 
-// Router / prerouter logits for one token per grid row, then top-k by the
-// last workgroup of that token to finish (a counter in the workspace, left
-// at zero afterwards).
+// Router / prerouter logits for one token per grid row, then (if idx is
+// given) softmax-top-k by the last workgroup of that token to finish (a
+// counter in the workspace, left at zero afterwards).
 template <int RPW>
 __global__ void __launch_bounds__(256) route_kernel(const __half* __restrict__ x,
                                                     const __half* __restrict__ W, int E, int d,
@@ -90,7 +90,7 @@ __global__ void __launch_bounds__(256) route_kernel(const __half* __restrict__ x
   __syncthreads();
   if (!last) return;
   __threadfence();
-  if (wave == 0) wave_topk<true>(lt, E, K, idx + (size_t)t * K, wout + (size_t)t * K, tk_scratch);
+  if (wave == 0 && idx) wave_topk<true>(lt, E, K, idx + (size_t)t * K, wout + (size_t)t * K, tk_scratch);
   if (threadIdx.x == 0)
     __hip_atomic_store(&counters[t], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -110,6 +110,69 @@ __global__ void __launch_bounds__(512) topk_block_kernel(const float* __restrict
   if ((int)threadIdx.x < E) lg[threadIdx.x] = logits[(size_t)t * E + threadIdx.x];
   __syncthreads();
   eng::block_topk(lg, E, K, idx + (size_t)t * K, w + (size_t)t * K, keys, part, cand, sorted);
+}
+
+// Sigmoid-group selection (App. A), one 512-thread workgroup per token
+// (E <= 256): sigma = sigmoid(l) in fp32, the selection score sigma + bias;
+// a group's score is the sum of its two largest selection scores (its one
+// score if it has one member); the top_groups best groups survive (ties to
+// the lower group); the K largest surviving scores are selected with the
+// engines' two-stage ranking (descending, ties to the lower id); the weights
+// use the raw sigma: w = scale sigma / (sum of the selected sigma + 1e-20).
+__global__ void __launch_bounds__(512) topk_sigmoid_group_kernel(const float* __restrict__ logits,
+                                                                 const float* __restrict__ bias, int E,
+                                                                 int K, int n_groups, int top_groups,
+                                                                 float scale, int32_t* __restrict__ idx,
+                                                                 float* __restrict__ w) {
+  __shared__ float sig[256], sel[256], masked[256], gsc[256];
+  __shared__ int keep[256];
+  __shared__ int32_t tidx[32];
+  __shared__ float tw[32];
+  __shared__ uint64_t keys[256];
+  __shared__ int part[256];
+  __shared__ uint64_t cand[128];
+  __shared__ uint64_t sorted[32];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  if (tid < E) {
+    const float s = 1.0f / (1.0f + expf(-logits[(size_t)t * E + tid]));
+    sig[tid] = s;
+    sel[tid] = bias ? s + bias[tid] : s;
+  }
+  __syncthreads();
+  const int per = E / n_groups;
+  if (tid < n_groups) {
+    float m1 = -INFINITY, m2 = -INFINITY;
+    for (int j = 0; j < per; ++j) {
+      const float v = sel[tid * per + j];
+      if (v > m1) {
+        m2 = m1;
+        m1 = v;
+      } else if (v > m2) {
+        m2 = v;
+      }
+    }
+    gsc[tid] = per >= 2 ? m1 + m2 : m1;
+  }
+  __syncthreads();
+  if (tid < n_groups) {
+    const float me = gsc[tid];
+    int rank = 0;
+    for (int g = 0; g < n_groups; ++g) rank += (gsc[g] > me) || (gsc[g] == me && g < tid);
+    keep[tid] = rank < top_groups;
+  }
+  __syncthreads();
+  if (tid < E) masked[tid] = keep[tid / per] ? sel[tid] : -INFINITY;
+  __syncthreads();
+  eng::block_topk(masked, E, K, tidx, tw, keys, part, cand, sorted);
+  __syncthreads();
+  if (tid < 64) {
+    const float s = tid < K ? sig[tidx[tid]] : 0.f;
+    const float sum = wave_sum(s);
+    if (tid < K) {
+      idx[(size_t)t * K + tid] = tidx[tid];
+      w[(size_t)t * K + tid] = scale * s / (sum + 1e-20f);
+    }
+  }
 }
 
 __global__ void __launch_bounds__(64) topk_kernel(const float* __restrict__ logits, int E, int K,
@@ -478,6 +541,15 @@ hipError_t launch_route(const __half* x, const __half* W, int T, int E, int d, i
   dim3 grid((E + rows_per_wg - 1) / rows_per_wg, T);
   hipLaunchKernelGGL(route_kernel<RPW>, grid, dim3(256), (size_t)d * 2, st, x, W, E, d, K, logits,
                      idx, w, counters);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_sigmoid_group(const float* logits, const float* bias, int T, int E, int K,
+                                     int n_groups, int top_groups, float scale, int32_t* idx, float* w,
+                                     hipStream_t st) {
+  if (E > 256 || K > 32 || n_groups < 1 || E % n_groups) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(topk_sigmoid_group_kernel, dim3(T), dim3(512), 0, st, logits, bias, E, K, n_groups,
+                     top_groups, scale, idx, w);
   return hipGetLastError();
 }
 

@@ -74,6 +74,27 @@ def test_spec_check_rejects_k_above_e_and_reserved(B):
     assert B.spec_check(spec) == B.MOE_EINVAL
 
 
+def test_spec_check_sigmoid_group(B):
+    """Sigmoid-group routing (App. A): n groups dividing E (E <= 256), 1 <= G <= n,
+    K <= G E / n, scale > 0; the group fields must be zero under softmax-topk."""
+    ok = B.make_spec(4096, 128, 8, 0, 1024, 16, 2.0, sigmoid_group=(8, 4, 2.5))
+    assert B.spec_check(ok) == 0
+    for groups in [(7, 4, 2.5), (8, 0, 2.5), (8, 9, 2.5), (8, 4, 0.0), (8, 4, -1.0), (8, 4, float("nan"))]:
+        assert B.spec_check(B.make_spec(4096, 128, 8, 0, 1024, 16, 2.0, sigmoid_group=groups)) == B.MOE_EINVAL
+    # K above the survivors' experts: 1 group of 16 ids survives, K = 17 > 16
+    assert B.spec_check(B.make_spec(4096, 128, 17, 0, 1024, 16, 2.0, sigmoid_group=(8, 1, 1.0))) == B.MOE_EINVAL
+    assert B.spec_check(B.make_spec(4096, 512, 8, 0, 1024, 16, 2.0, sigmoid_group=(8, 4, 1.0))) == B.MOE_EINVAL
+    soft = B.make_spec(4096, 128, 8, 0, 1024, 16, 2.0)
+    soft.n_groups = 8
+    assert B.spec_check(soft) == B.MOE_EINVAL
+    # the biased top-k exists only for sigmoid-group specs
+    L = B.lib()
+    ws = ctypes.c_void_p(0x100000)
+    sp = B.spec_from_workload(synth.WORKLOADS["tiny"])
+    assert L.moe_topk_biased(ctypes.byref(sp), ws, ws, 1, ws, ws, None) == B.MOE_EINVAL
+    assert L.moe_topk_biased(ctypes.byref(ok), None, None, 0, None, None, None) == B.MOE_OK
+
+
 def _fake_bundle(B, base):
     p = B.MoeProj(base, base + 0x1000, base + 0x2000, base + 0x3000)
     return B.MoeBundle(p, p, p)

@@ -285,6 +285,69 @@ def head_mlp_path(B, torch, wl, n_heads=96, hidden=512, calls=192):
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "hidden": hidden, "heads": n_heads}
 
 
+def merge_retention_path(B, torch, wl, T=8):
+    """The merged alternative of Sec. 3.3 on one expert of ``wl``: the adapter
+    folded into the int4 weights on the device (moe_merge_requantize), then the
+    unmerged (U), merged (M) and base (B) experts on T tokens through
+    moe_expert_ffn_int4_lora. Weight-level retention from the kernel's per-group
+    sums; output-level retention 1 - ||U - M|| / ||U - B|| from the outputs.
+    Two adapter sizes: delta entries of std 1e-3 (the paper's figure) and the
+    configuration's (A ~ N(0, 1/r), B ~ N(0, 0.01), scale 2). The merge kernel
+    is timed over the expert's three projections."""
+    import synth
+    out = {}
+    dims = {"gate": (wl.I, wl.d), "up": (wl.I, wl.d), "down": (wl.d, wl.I)}
+    spec = B.make_spec(wl.d, 8, 3, 0, wl.I, wl.r, wl.lora_scale)
+    xi = torch.from_numpy(synth.token_draws(wl, 0, T)).cuda()
+    x = torch.empty(T, wl.d, dtype=torch.float16, device="cuda")
+    B.rmsnorm_f16(xi, x)
+    idx = torch.tensor([[0, 1, 2]] * T, dtype=torch.int32, device="cuda")
+    ye = torch.empty(T, 3, wl.d, dtype=torch.float32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.zeros(B.workspace_bytes(spec, T), dtype=torch.uint8, device="cuda")
+    for label, b_std in (("delta_std_1e-3", 1e-3 / (wl.lora_scale * np.sqrt(wl.r) * wl.a_std)),
+                         ("configuration", None)):
+        bundle = synth.bundle(wl, 0, 7, b_std=b_std)
+        keep, U, M, Bs, merges, weight = [], {}, {}, {}, [], {}
+        for p, (o, i) in dims.items():
+            U[p], k1 = B.upload_projection(bundle[p], bundle["lora"][p], "cuda")
+            Bs[p], k2 = B.upload_projection(bundle[p], None, "cuda")
+            q_out = torch.empty(o, i // 2, dtype=torch.uint8, device="cuda")
+            sz_out = torch.empty(o, i // 64, 2, dtype=torch.float16, device="cuda")
+            stats = torch.empty(o, i // 64, 2, dtype=torch.float64, device="cuda")
+            merges.append((U[p], o, i, q_out, sz_out, stats))
+            M[p] = B.MoeProj(q_out.data_ptr(), sz_out.data_ptr(), None, None)
+            keep += [k1, k2, q_out, sz_out, stats]
+
+        def merge_all():
+            for pj, o, i, q_out, sz_out, stats in merges:
+                B.merge_requantize(pj, o, i, wl.r, wl.lora_scale, q_out, sz_out, stats)
+        merge_all()
+        ms = time_launch(torch, merge_all)
+        for (pj, o, i, q_out, sz_out, stats), p in zip(merges, dims):
+            tot = stats.sum(dim=(0, 1))
+            weight[p] = round(float(tot[0] / tot[1]), 4)
+        table = B.SlotTable(1, 8, 8)
+        for e, pj in enumerate((U, M, Bs)):
+            table.bind(0, e, e, B.MoeBundle(pj["gate"], pj["up"], pj["down"]), keep=keep)
+        table.sync()
+        B.expert_ffn(spec, table, 0, x, idx, ye, status, ws)
+        torch.cuda.synchronize()
+        y = ye.double()
+        n1 = torch.linalg.norm(y[:, 0] - y[:, 1]).item()
+        n2 = torch.linalg.norm(y[:, 0] - y[:, 2]).item()
+        table.close()
+        nbytes = sum(o * i // 2 + o * i // 16 + wl.r * (o + i) * 2 + o * i // 2 + o * i // 16
+                     for o, i in dims.values())
+        out[label] = {"weight_retention": weight, "output_retention": round(1.0 - n1 / n2, 4),
+                      "merge_us_per_expert": round(ms * 1e3, 2),
+                      "merge_GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+        log("merged adapter (%s): weight retention %s, output retention %.4f; merge %.1f us per expert"
+            % (label, weight, 1.0 - n1 / n2, ms * 1e3))
+    out["tokens"] = T
+    return out
+
+
 def sigmoid_group_path(B, torch, calls=192):
     """Sigmoid-group routing (App. A; 8 groups, 4 survive, scale 2.5) at the
     8B tier's shape (d 4096, E 64, K 4): moe_route at batch 1 (router logits
@@ -560,6 +623,7 @@ def main():
     batched = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
     head_mlp = head_mlp_path(B, torch, wl)
     sigmoid_group = sigmoid_group_path(B, torch)
+    merge_retention = merge_retention_path(B, torch, wl)
 
     tier_res = None if args.no_tier else tier_path(B, torch, T=args.tier_tokens)
 
@@ -600,6 +664,7 @@ def main():
         "batched": batched,
         "prerouter_mlp_head": head_mlp,
         "sigmoid_group_routing": sigmoid_group,
+        "merge_vs_unmerged": merge_retention,
         "host_tier": tier_res,
         "per_call_path": {"us_per_step": round(pc_us * 1e3, 3),
                           "gateup_kernel_us": round(gu_ms * 1e3, 3)},

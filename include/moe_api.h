@@ -447,6 +447,35 @@ int moe_stager_use(moe_stager* s, int layer, const int32_t* experts, int n, void
 int moe_stager_release(moe_stager* s, int layer);
 int moe_stager_stats_get(const moe_stager* s, moe_stager_stats* out);
 
+/* ---- an adapter merged into the int4 weights (Sec. 3.3, Recovery LoRA:
+ *      the merged alternative, kept to measure what merging loses) -------- */
+
+/*
+ * Fold the adapter of `src` into its weights and re-quantize to int4 g64,
+ * the alternative to the unmerged delta that Sec. 3.3 rejects because most
+ * of a small delta falls below the group step. Per 64-input group:
+ *   w = s q + z and delta = lora_scale * (B A)[o][i] in float64,
+ *   m = fp32(w + delta) (one rounding), lo / hi = the group's min / max of m,
+ *   s' = fp16((hi - lo) / 15), z' = fp16(lo),
+ *   q' = clamp(rint((m - z') / s'), 0, 15) in fp32 (0 when s' == 0);
+ * the same quantizer as the format's (Sec. 2, Quantization).
+ *   src       device projection [out_dim x in_dim] (moe_proj layout); with
+ *             lora_a or lora_b NULL, delta = 0 (a plain re-quantization)
+ *   rank      r of src's adapter (1..64), ignored without an adapter
+ *   q_out     device uint8 [out_dim][in_dim/2], sz_out device fp16 pairs
+ *             [out_dim][in_dim/64][2] (the moe_proj layout), caller-owned;
+ *             must not overlap src
+ *   stats     device double [out_dim][in_dim/64][2] or NULL: per group the sums
+ *             of actual * delta and of delta^2, actual = (s' q' + z') - w; their
+ *             totals give the weight-level retention sum(actual delta) / sum(delta^2)
+ * Asynchronous on `stream`; nothing is allocated. MOE_EINVAL: NULL src, src->q,
+ * src->sz, q_out or sz_out, out_dim < 1, in_dim < 64, in_dim % 64 != 0, or an
+ * adapter with rank outside 1..64; MOE_EALIGN: sz, sz_out, lora_a, lora_b not
+ * 2-byte aligned or stats not 8-byte aligned.
+ */
+int moe_merge_requantize(const moe_proj* src, int out_dim, int in_dim, int rank, float lora_scale,
+                         void* q_out, void* sz_out, double* stats, void* stream);
+
 /* ---- profiling (not part of the hot path) ------------------------------- */
 #define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */
 #define MOE_PROF_ENGINE_PHASES 1 /* the next decode-engine launch writes, for

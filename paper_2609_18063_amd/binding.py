@@ -99,6 +99,8 @@ SIGNATURES = {
     "moe_topk_biased": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_void_p,
                                 c_void_p, c_void_p]),
     "moe_profile_arm": (c_int, [c_int, c_void_p, c_void_p]),
+    "moe_merge_requantize": (c_int, [ctypes.POINTER(MoeProj), c_int, c_int, c_int, ctypes.c_float,
+                                     c_void_p, c_void_p, c_void_p, c_void_p]),
     "moe_slot_policy_create": (c_int, [c_int, c_int, c_int, ctypes.POINTER(c_void_p)]),
     "moe_slot_policy_destroy": (c_int, [c_void_p]),
     "moe_slot_policy_stage": (c_int, [c_void_p, c_int, c_void_p, c_int, c_void_p]),
@@ -434,6 +436,16 @@ def topk_biased(spec, logits, bias, idx, w, stream=None):
     T = logits.shape[0]
     _check(lib().moe_topk_biased(ctypes.byref(spec), _ptr(logits), _ptr(bias), T, _ptr(idx), _ptr(w),
                                  _stream(stream)), "moe_topk_biased")
+
+
+def merge_requantize(proj, out_dim, in_dim, rank, lora_scale, q_out, sz_out, stats=None,
+                     stream=None):
+    """moe_merge_requantize: ``proj`` a MoeProj of device pointers; ``q_out``
+    uint8 ``[out, in/2]``, ``sz_out`` fp16 ``[out, in/64, 2]``, ``stats``
+    float64 ``[out, in/64, 2]`` or None (device tensors)."""
+    _check(lib().moe_merge_requantize(ctypes.byref(proj), out_dim, in_dim, rank, lora_scale,
+                                      _ptr(q_out), _ptr(sz_out), _ptr(stats), _stream(stream)),
+           "moe_merge_requantize")
 
 
 def profile_arm(which, start_event, stop_event):

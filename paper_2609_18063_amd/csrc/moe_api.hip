@@ -426,6 +426,25 @@ static int combine_common(const moe_layer_spec* s, const float* y_experts, const
                                       accumulate, static_cast<hipStream_t>(stream)));
 }
 
+int moe_merge_requantize(const moe_proj* src, int out_dim, int in_dim, int rank, float lora_scale,
+                         void* q_out, void* sz_out, double* stats, void* stream) {
+  if (!src || !src->q || !src->sz || !q_out || !sz_out) return MOE_EINVAL;
+  if (out_dim < 1 || in_dim < 64 || in_dim % 64) return MOE_EINVAL;
+  const bool adapter = src->lora_a && src->lora_b;
+  if (adapter && (rank < 1 || rank > 64)) return MOE_EINVAL;
+  if ((long long)out_dim * (in_dim / 64) > (1ll << 31) - 4) return MOE_EINVAL;
+  auto a2 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 1) == 0; };
+  if (!a2(src->sz) || !a2(sz_out) || (adapter && (!a2(src->lora_a) || !a2(src->lora_b))) ||
+      (stats && (reinterpret_cast<uintptr_t>(stats) & 7)))
+    return MOE_EALIGN;
+  return from_hip(moe::launch_merge_requantize(
+      static_cast<const uint8_t*>(src->q), static_cast<const __half*>(src->sz),
+      adapter ? static_cast<const __half*>(src->lora_a) : nullptr,
+      adapter ? static_cast<const __half*>(src->lora_b) : nullptr, out_dim, in_dim,
+      adapter ? rank : 0, lora_scale, static_cast<uint8_t*>(q_out), static_cast<__half*>(sz_out),
+      stats, static_cast<hipStream_t>(stream)));
+}
+
 int moe_combine(const moe_layer_spec* s, const float* y_experts, const float* w, int T, float* y,
                 void* stream) {
   return combine_common(s, y_experts, w, T, y, 0, stream);

@@ -56,6 +56,11 @@ struct HeadMlpArgs {
   float route_scale;
 };
 hipError_t launch_head_mlp(const HeadMlpArgs& a, hipStream_t st);
+// Adapter merged into one int4 g64 projection and re-quantized (moe_merge.hip).
+hipError_t launch_merge_requantize(const uint8_t* q, const __half* sz, const __half* A,
+                                   const __half* B, int out_dim, int in_dim, int rank,
+                                   float lora_scale, uint8_t* q_out, __half* sz_out, double* stats,
+                                   hipStream_t st);
 // prof_start / prof_stop: if non-null, the gate/up kernel is launched with
 // hipExtLaunchKernelGGL and records them around its execution.
 hipError_t launch_ffn(const FfnArgs& a, int T, hipStream_t st, hipEvent_t prof_start,

@@ -96,8 +96,10 @@ def lora_pair(key_a, key_b, out_dim, in_dim, r, a_std, b_std):
     return a, b
 
 
-def bundle(wl, layer, expert, lora=True, lora_on=("gate", "up", "down")):
-    """Expert ``expert`` of ``layer`` (ids ``E .. E+S-1`` are the shared experts)."""
+def bundle(wl, layer, expert, lora=True, lora_on=("gate", "up", "down"), b_std=None):
+    """Expert ``expert`` of ``layer`` (ids ``E .. E+S-1`` are the shared experts).
+    ``b_std`` overrides the workload's std of the LoRA ``B`` entries: the
+    delta ``scale * B A`` then has entries of std ``scale * b_std * sqrt(r) * a_std``."""
     dims = {"gate": (wl.I, wl.d), "up": (wl.I, wl.d), "down": (wl.d, wl.I)}
     out = {"lora": {}}
     for p, (o, i) in dims.items():
@@ -106,7 +108,7 @@ def bundle(wl, layer, expert, lora=True, lora_on=("gate", "up", "down")):
         if lora and p in lora_on:
             out["lora"][p] = lora_pair((wl.wid, layer, expert, _T_A[p]),
                                        (wl.wid, layer, expert, _T_B[p]),
-                                       o, i, wl.r, wl.a_std, wl.b_std)
+                                       o, i, wl.r, wl.a_std, wl.b_std if b_std is None else b_std)
         else:
             out["lora"][p] = None
     return out

@@ -180,3 +180,26 @@ def test_library_fails_loudly_when_missing(tmp_path, monkeypatch):
     monkeypatch.setattr(binding, "_lib", None)
     with pytest.raises(ImportError):
         binding.lib()
+
+
+def test_merge_requantize_argument_checks(B):
+    """moe_merge_requantize rejects bad shapes and alignments before any
+    device work (the pointers below are never dereferenced)."""
+    lib = B.lib()
+    ok = B.MoeProj(0x10000, 0x20000, None, None)
+    ad = B.MoeProj(0x10000, 0x20000, 0x30000, 0x40000)
+
+    def call(p, out_dim, in_dim, rank=0, q_out=0x50000, sz_out=0x60000, stats=None):
+        return lib.moe_merge_requantize(None if p is None else ctypes.byref(p), out_dim, in_dim, rank,
+                                        2.0, q_out, sz_out, stats, None)
+
+    assert call(None, 4, 64) == B.MOE_EINVAL
+    assert call(ok, 0, 64) == B.MOE_EINVAL
+    assert call(ok, 4, 32) == B.MOE_EINVAL
+    assert call(ok, 4, 96) == B.MOE_EINVAL
+    assert call(ok, 4, 64, q_out=None) == B.MOE_EINVAL
+    assert call(ad, 4, 64, rank=0) == B.MOE_EINVAL
+    assert call(ad, 4, 64, rank=65) == B.MOE_EINVAL
+    assert call(B.MoeProj(0x10000, 0x20001, None, None), 4, 64) == B.MOE_EALIGN
+    assert call(ok, 4, 64, sz_out=0x60001) == B.MOE_EALIGN
+    assert call(ok, 4, 64, stats=0x70004) == B.MOE_EALIGN

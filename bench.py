@@ -436,6 +436,63 @@ def batched_path(B, torch, spec, table, wl, L, Ts=(64, 512), reps=20):
     return res
 
 
+def file_tier_runs(torch, tier, spec, layers, xi, pool, L, n_slots, wl, T=16):
+    """The same staged chain with the bundles in a file (the SSD tier of
+    Sec. 3.1): first with the file's pages in the page cache (warm), then
+    after dropping them (cold). Per run: tokens/s, misses, the host read
+    rate into the pinned bounce buffers, and a least-squares fit of the host
+    time of a stage call, a + b * copies (the paper models a layer's load as
+    a fixed cost plus a cost per cold expert)."""
+    import shutil
+    import tempfile
+    d = os.environ.get("MOE_TIER_FILE_DIR", tempfile.gettempdir())
+    need = L * pool.n_ids * pool.stride
+    free = shutil.disk_usage(d).free
+    if free < 2 * need:
+        log("file tier skipped: %.1f GB free in %s, %.1f GB needed" % (free / 1e9, d, need / 1e9))
+        return {"skipped": "%.1f GB free in %s" % (free / 1e9, d)}
+    t0 = time.time()
+    fpool = tier.FilePool(os.path.join(d, "moe_tier8b_%d.bin" % os.getpid()), L, pool.n_ids,
+                          lambda n, e: synth_bundle(wl, n, e), replicate=True, n_bounce=4, n_io=8)
+    log("8B tier file: %.1f GB written in %.1fs" % (need / 1e9, time.time() - t0))
+    out = {"file_GB": round(need / 1e9, 2), "tokens": T, "n_bounce": fpool.n_bounce,
+           "io_threads": fpool.n_io}
+    try:
+        for label in ("warm", "cold"):
+            if label == "cold":
+                fpool.drop_page_cache()
+            ch = tier.TieredChain(spec, layers, fpool, n_slots)
+            torch.cuda.synchronize()
+            w0 = time.perf_counter()
+            ch.run(xi[:T])
+            wall = time.perf_counter() - w0
+            assert int(ch.status.item()) == 0
+            st, io = ch.stager.stats(), ch.stager.io_stats()
+            pts = np.array([(c, t) for c, t in ch.stage_host_s if c > 0], dtype=np.float64)
+            fit = None
+            if len(pts) >= 3 and np.ptp(pts[:, 0]) > 0:
+                b, a = np.polyfit(pts[:, 0], pts[:, 1] * 1e3, 1)
+                fit = {"ms_fixed": round(float(a), 3), "ms_per_copy": round(float(b), 3)}
+            ch.close()
+            out[label] = {
+                "tokens_per_s": round(T / wall, 2),
+                "misses_per_token": round(st["copies"] / T, 2),
+                "read_GB_s": round(io["read_bytes"] / max(io["read_ns"], 1), 2),
+                "read_ms_per_token": round(io["read_ns"] * 1e-6 / T, 3),
+                "stage_host_fit": fit,
+            }
+            log("8B tier from a file (%s page cache): %.1f tok/s, %.2f misses/token, read %.2f GB/s, "
+                "stage fit %s" % (label, T / wall, st["copies"] / T, out[label]["read_GB_s"], fit))
+    finally:
+        fpool.remove()
+    return out
+
+
+def synth_bundle(wl, n, e):
+    import synth
+    return synth.bundle(wl, n, e)
+
+
 def tier_path(B, torch, T=64, L=24, rho=0.5):
     """The 8B tier with host-tier staging: 24 layers whose 64 experts per
     layer live in pinned host memory, 3 x top-4 device slots per layer; the
@@ -473,6 +530,7 @@ def tier_path(B, torch, T=64, L=24, rho=0.5):
     st = ch.stager.stats()
     copy_s = ch.copy_ms * 1e-3
     ch.close()
+    file_res = file_tier_runs(torch, tier, spec, layers, xi, pool, L, n_slots, wl)
     # the same chain, every expert resident: compute only
     table, keep = tier.resident_table(spec, pool, layers)
     dc = C.DeviceChain(spec, table, layers)
@@ -507,6 +565,7 @@ def tier_path(B, torch, T=64, L=24, rho=0.5):
         "overlap": None if overlap is None else round(overlap, 3),
         "adjacent_set_overlap": round(tier.set_overlap(ch.log, L), 3),
     }
+    res["file_tier"] = file_res
     log("8B tier staged: %.1f tok/s, %.2f misses/token, H2D %.1f GB/s, compute-only %.3f ms/token, "
         "overlap %s" % (res["tokens_per_s"], res["misses_per_token"], res["h2d_GB_s"] or 0,
                         res["compute_only_ms_per_token"], res["overlap"]))

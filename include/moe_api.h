@@ -430,6 +430,23 @@ typedef struct moe_stager moe_stager;
 int moe_stager_create(moe_slot_table* table, const moe_bundle_layout* layout, size_t bundle_bytes,
                       const void* const* host_bundles, void* slot_pool, size_t slot_stride,
                       moe_stager** out);
+/*
+ * The same stager with the bundles in a file instead of pinned memory (the
+ * SSD tier of Sec. 3.1, SSD streaming: per-layer stacked weights read through
+ * the OS page cache). The file at `path` holds [n_layers][n_ids] records of
+ * file_stride bytes (>= bundle_bytes); record (layer, e) is the packed bundle
+ * of expert e, in the same layout as a pinned host bundle. It is mapped
+ * read-only for the stager's lifetime and must not change meanwhile. Each copy
+ * reads its record into one of n_bounce (1..16) pinned bounce buffers, split
+ * over n_io (1..16) host threads inside moe_stager_stage (page faults read the
+ * file, or hit the page cache), then enqueues the host -> slot copy; a bounce
+ * buffer is reused after the copy from it has completed. MOE_EINVAL: a bad
+ * argument, a file that cannot be opened or is shorter than n_layers * n_ids *
+ * file_stride; MOE_ENOMEM: the mapping or the bounce buffers failed.
+ */
+int moe_stager_create_file(moe_slot_table* table, const moe_bundle_layout* layout,
+                           size_t bundle_bytes, const char* path, size_t file_stride, int n_bounce,
+                           int n_io, void* slot_pool, size_t slot_stride, moe_stager** out);
 int moe_stager_destroy(moe_stager* s);
 /* Stages a set (policy stage), rewrites the layer's slot-table rows on the
  * device and copies each missing bundle host -> slot, all enqueued on
@@ -446,6 +463,9 @@ int moe_stager_use(moe_stager* s, int layer, const int32_t* experts, int n, void
  * knows it, e.g. from an event recorded after them): unpin that set. */
 int moe_stager_release(moe_stager* s, int layer);
 int moe_stager_stats_get(const moe_stager* s, moe_stager_stats* out);
+/* File tier: host time spent reading records into bounce buffers (ns) and the
+ * bytes read; both 0 for a pinned-memory stager. */
+int moe_stager_io_stats(const moe_stager* s, int64_t* read_ns, int64_t* read_bytes);
 
 /* ---- an adapter merged into the int4 weights (Sec. 3.3, Recovery LoRA:
  *      the merged alternative, kept to measure what merging loses) -------- */

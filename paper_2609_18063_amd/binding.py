@@ -110,6 +110,11 @@ SIGNATURES = {
     "moe_stager_create": (c_int, [c_void_p, ctypes.POINTER(MoeBundleLayout), c_size_t, c_void_p,
                                   c_void_p, c_size_t, ctypes.POINTER(c_void_p)]),
     "moe_stager_destroy": (c_int, [c_void_p]),
+    "moe_stager_create_file": (c_int, [c_void_p, ctypes.POINTER(MoeBundleLayout), c_size_t,
+                                       ctypes.c_char_p, c_size_t, c_int, c_int, c_void_p, c_size_t,
+                                       ctypes.POINTER(c_void_p)]),
+    "moe_stager_io_stats": (c_int, [c_void_p, ctypes.POINTER(ctypes.c_int64),
+                                    ctypes.POINTER(ctypes.c_int64)]),
     "moe_stager_stage": (c_int, [c_void_p, c_int, c_void_p, c_int, c_void_p, c_void_p]),
     "moe_stager_use": (c_int, [c_void_p, c_int, c_void_p, c_int, c_void_p, c_void_p]),
     "moe_stager_release": (c_int, [c_void_p, c_int]),
@@ -284,14 +289,29 @@ class SlotPolicy:
 class Stager:
     """The slot policy driving a slot table: pinned host bundles -> device slots."""
 
-    def __init__(self, table, layout, bundle_bytes, host_ptrs, slot_pool, slot_stride):
+    def __init__(self, table, layout, bundle_bytes, host_ptrs, slot_pool, slot_stride, file=None):
+        """``file``: None (bundles at ``host_ptrs`` in pinned memory) or
+        ``(path, file_stride, n_bounce, n_io)`` for the file tier."""
         h = c_void_p()
-        ptrs = (c_void_p * len(host_ptrs))(*host_ptrs)
-        _check(lib().moe_stager_create(table.handle, ctypes.byref(layout), bundle_bytes, ptrs,
-                                       _ptr(slot_pool), slot_stride, ctypes.byref(h)),
-               "moe_stager_create")
+        if file is None:
+            ptrs = (c_void_p * len(host_ptrs))(*host_ptrs)
+            _check(lib().moe_stager_create(table.handle, ctypes.byref(layout), bundle_bytes, ptrs,
+                                           _ptr(slot_pool), slot_stride, ctypes.byref(h)),
+                   "moe_stager_create")
+        else:
+            path, file_stride, n_bounce, n_io = file
+            _check(lib().moe_stager_create_file(table.handle, ctypes.byref(layout), bundle_bytes,
+                                                str(path).encode(), file_stride, n_bounce, n_io,
+                                                _ptr(slot_pool), slot_stride, ctypes.byref(h)),
+                   "moe_stager_create_file")
         self.handle = h
         self.table, self.pool = table, slot_pool
+
+    def io_stats(self):
+        ns, nb = ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().moe_stager_io_stats(self.handle, ctypes.byref(ns), ctypes.byref(nb)),
+               "moe_stager_io_stats")
+        return {"read_ns": ns.value, "read_bytes": nb.value}
 
     def stage(self, layer, experts, copy_stream):
         e = _i32(experts)

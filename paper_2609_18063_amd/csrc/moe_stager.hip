@@ -14,6 +14,15 @@
 //                     hipMemcpyAsync on a copy stream; an event per staged
 //                     set lets the compute stream wait for exactly its copies.
 //
+// File tier (Sec. 3.1, SSD streaming; the paper maps per-layer stacked
+// weight files and reads experts through the OS page cache): with
+// moe_stager_create_file the bundles live in one file, [L][n_ids] records of
+// file_stride bytes, mapped read-only. A copy reads the record from the
+// mapping into one of a ring of pinned bounce buffers (page faults read the
+// file, or hit the page cache), split over a few host threads, then
+// hipMemcpyAsync moves it to the slot; a bounce buffer is reused only after
+// the event recorded behind its copy.
+//
 // Policy (the paper leaves it open; the reading is stated once here and in
 // the header): every layer keeps a FIFO of staged-but-unused sets and a FIFO
 // of sets in use.  Staging a set walks it in routing order; a resident expert
@@ -24,10 +33,17 @@
 // it).  A clock that advances on every copy and every use orders "last use".
 #include <hip/hip_runtime.h>
 
+#include <fcntl.h>
+#include <sys/mman.h>
+#include <sys/stat.h>
+#include <unistd.h>
+
 #include <algorithm>
+#include <chrono>
 #include <cstring>
 #include <deque>
 #include <new>
+#include <thread>
 #include <vector>
 
 #include "moe_table.h"
@@ -189,6 +205,15 @@ struct moe_stager {
   std::vector<std::deque<hipEvent_t>> set_ev;
   std::deque<hipEvent_t> free_ev;
   moe_stager_stats stats{};
+  // file tier (map == nullptr: pinned host bundles)
+  int fd = -1;
+  const char* map = nullptr;
+  size_t map_bytes = 0, file_stride = 0, bounce_stride = 0;
+  char* bounce = nullptr;
+  int n_bounce = 0, bounce_next = 0, n_io = 1;
+  std::vector<hipEvent_t> bounce_ev;
+  std::vector<char> bounce_used;
+  int64_t read_ns = 0, read_bytes = 0;
 };
 
 namespace {
@@ -256,24 +281,25 @@ int push_rows(moe_stager* s, int layer, hipStream_t st) {
 
 }  // namespace
 
-int moe_stager_create(moe_slot_table* table, const moe_bundle_layout* layout, size_t bundle_bytes,
-                      const void* const* host_bundles, void* slot_pool, size_t slot_stride,
-                      moe_stager** out) {
-  if (!table || !layout || !host_bundles || !slot_pool || !out || bundle_bytes == 0 ||
+namespace {
+
+// Everything but the bundle source: host_bundles is null for the file tier.
+int create_common(moe_slot_table* table, const moe_bundle_layout* layout, size_t bundle_bytes,
+                  const void* const* host_bundles, void* slot_pool, size_t slot_stride,
+                  moe_stager** out) {
+  if (!table || !layout || !slot_pool || !out || bundle_bytes == 0 ||
       slot_stride < bundle_bytes || (slot_stride & 255) != 0 || !table->dev)
     return MOE_EINVAL;
   if (!layout_ok(layout, bundle_bytes)) return MOE_EINVAL;
   if ((reinterpret_cast<uintptr_t>(slot_pool) & 255) != 0) return MOE_EALIGN;
   const size_t nh = (size_t)table->n_layers * table->n_ids;
-  for (size_t i = 0; i < nh; ++i)
-    if (!host_bundles[i]) return MOE_EINVAL;
   moe_stager* s = new (std::nothrow) moe_stager;
   if (!s) return MOE_ENOMEM;
   s->table = table;
   s->layout = *layout;
   s->bundle_bytes = bundle_bytes;
   s->slot_stride = slot_stride;
-  s->host.assign(host_bundles, host_bundles + nh);
+  if (host_bundles) s->host.assign(host_bundles, host_bundles + nh);
   s->pool = static_cast<char*>(slot_pool);
   s->set_ev.resize(table->n_layers);
   int rc = moe_slot_policy_create(table->n_layers, table->n_ids, table->n_slots, &s->policy);
@@ -303,6 +329,92 @@ int moe_stager_create(moe_slot_table* table, const moe_bundle_layout* layout, si
   return MOE_OK;
 }
 
+// Copy one record of the mapped file into a bounce buffer over n threads.
+void read_record(const char* src, char* dst, size_t n, int threads) {
+  if (threads <= 1 || n < ((size_t)1 << 20)) {
+    std::memcpy(dst, src, n);
+    return;
+  }
+  const size_t part = (n / threads + 4095) / 4096 * 4096;
+  std::vector<std::thread> th;
+  for (int k = 1; k < threads; ++k) {
+    const size_t o = part * k;
+    if (o >= n) break;
+    th.emplace_back([=] { std::memcpy(dst + o, src + o, std::min(part, n - o)); });
+  }
+  std::memcpy(dst, src, std::min(part, n));
+  for (auto& x : th) x.join();
+}
+
+}  // namespace
+
+int moe_stager_create(moe_slot_table* table, const moe_bundle_layout* layout, size_t bundle_bytes,
+                      const void* const* host_bundles, void* slot_pool, size_t slot_stride,
+                      moe_stager** out) {
+  if (!table || !host_bundles) return MOE_EINVAL;
+  const size_t nh = (size_t)table->n_layers * table->n_ids;
+  for (size_t i = 0; i < nh; ++i)
+    if (!host_bundles[i]) return MOE_EINVAL;
+  return create_common(table, layout, bundle_bytes, host_bundles, slot_pool, slot_stride, out);
+}
+
+int moe_stager_create_file(moe_slot_table* table, const moe_bundle_layout* layout,
+                           size_t bundle_bytes, const char* path, size_t file_stride, int n_bounce,
+                           int n_io, void* slot_pool, size_t slot_stride, moe_stager** out) {
+  if (!table || !path || !out || file_stride < bundle_bytes || n_bounce < 1 || n_bounce > 16 ||
+      n_io < 1 || n_io > 16)
+    return MOE_EINVAL;
+  const int fd = open(path, O_RDONLY | O_CLOEXEC);
+  if (fd < 0) return MOE_EINVAL;
+  struct stat st;
+  const size_t need = (size_t)table->n_layers * table->n_ids * file_stride;
+  if (fstat(fd, &st) != 0 || (size_t)st.st_size < need) {
+    close(fd);
+    return MOE_EINVAL;
+  }
+  void* m = mmap(nullptr, need, PROT_READ, MAP_SHARED, fd, 0);
+  if (m == MAP_FAILED) {
+    close(fd);
+    return MOE_ENOMEM;
+  }
+  moe_stager* s = nullptr;
+  int rc = create_common(table, layout, bundle_bytes, nullptr, slot_pool, slot_stride, &s);
+  if (rc != MOE_OK) {
+    munmap(m, need);
+    close(fd);
+    return rc;
+  }
+  s->fd = fd;
+  s->map = static_cast<const char*>(m);
+  s->map_bytes = need;
+  s->file_stride = file_stride;
+  s->n_bounce = n_bounce;
+  s->n_io = n_io;
+  s->bounce_stride = (bundle_bytes + 4095) / 4096 * 4096;
+  if (hipHostMalloc(reinterpret_cast<void**>(&s->bounce), s->bounce_stride * n_bounce,
+                    hipHostMallocDefault) != hipSuccess) {
+    s->bounce = nullptr;
+    moe_stager_destroy(s);
+    return MOE_ENOMEM;
+  }
+  s->bounce_ev.assign(n_bounce, nullptr);
+  s->bounce_used.assign(n_bounce, 0);
+  for (auto& e : s->bounce_ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+      moe_stager_destroy(s);
+      return MOE_EHIP;
+    }
+  *out = s;
+  return MOE_OK;
+}
+
+int moe_stager_io_stats(const moe_stager* s, int64_t* read_ns, int64_t* read_bytes) {
+  if (!s || !read_ns || !read_bytes) return MOE_EINVAL;
+  *read_ns = s->read_ns;
+  *read_bytes = s->read_bytes;
+  return MOE_OK;
+}
+
 int moe_stager_destroy(moe_stager* s) {
   if (!s) return MOE_OK;
   for (auto& q : s->set_ev)
@@ -315,6 +427,14 @@ int moe_stager_destroy(moe_stager* s) {
       (void)hipEventDestroy(e);
     }
   if (s->ring) (void)hipHostFree(s->ring);
+  for (hipEvent_t e : s->bounce_ev)
+    if (e) {
+      (void)hipEventSynchronize(e);
+      (void)hipEventDestroy(e);
+    }
+  if (s->bounce) (void)hipHostFree(s->bounce);
+  if (s->map) munmap(const_cast<char*>(s->map), s->map_bytes);
+  if (s->fd >= 0) close(s->fd);
   moe_slot_policy_destroy(s->policy);
   delete s;
   return MOE_OK;
@@ -346,8 +466,33 @@ int moe_stager_stage(moe_stager* s, int layer, const int32_t* experts, int n, vo
   for (int i = 0; i < nc && rc == MOE_OK; ++i) {
     const int e = cp[2 * i], slot = cp[2 * i + 1];
     char* dst = s->pool + ((size_t)layer * t->n_slots + slot) * s->slot_stride;
-    if (hipMemcpyAsync(dst, s->host[(size_t)layer * t->n_ids + e], s->bundle_bytes,
-                       hipMemcpyHostToDevice, st) != hipSuccess)
+    const void* src = nullptr;
+    if (s->map) {  // file tier: record -> bounce buffer (host threads) -> slot
+      const int b = s->bounce_next;
+      s->bounce_next = (b + 1) % s->n_bounce;
+      if (s->bounce_used[b] && hipEventSynchronize(s->bounce_ev[b]) != hipSuccess) {
+        rc = MOE_EHIP;
+        break;
+      }
+      char* bb = s->bounce + (size_t)b * s->bounce_stride;
+      const auto t0 = std::chrono::steady_clock::now();
+      read_record(s->map + ((size_t)layer * t->n_ids + e) * s->file_stride, bb, s->bundle_bytes,
+                  s->n_io);
+      s->read_ns += std::chrono::duration_cast<std::chrono::nanoseconds>(
+                        std::chrono::steady_clock::now() - t0)
+                        .count();
+      s->read_bytes += (int64_t)s->bundle_bytes;
+      src = bb;
+      if (hipMemcpyAsync(dst, src, s->bundle_bytes, hipMemcpyHostToDevice, st) != hipSuccess ||
+          hipEventRecord(s->bounce_ev[b], st) != hipSuccess) {
+        rc = MOE_EHIP;
+        break;
+      }
+      s->bounce_used[b] = 1;
+      continue;
+    }
+    src = s->host[(size_t)layer * t->n_ids + e];
+    if (hipMemcpyAsync(dst, src, s->bundle_bytes, hipMemcpyHostToDevice, st) != hipSuccess)
       rc = MOE_EHIP;
   }
   if (rc == MOE_OK && ev && hipEventRecord(ev, st) != hipSuccess) rc = MOE_EHIP;

@@ -15,7 +15,14 @@ Motivation and Prediction-as-routing; §3.1, staged executor):
 Everything on the device is the library's: the per-call kernels for the
 layer, and the library's stager (policy, slot-table rows, hipMemcpyAsync).
 This module only orders the calls and moves the K routing ids to the host.
+
+With a :class:`FilePool` the bundles live in a file instead (the SSD tier of
+§3.1, SSD streaming): the library maps it and reads each missing record
+through a pinned bounce buffer, so the page cache (warm) or the disk (cold)
+sits in front of the PCIe copy.
 """
+
+import os
 
 import time
 
@@ -70,6 +77,60 @@ class HostPool:
         return self.buf[o:o + self.bundle_bytes]
 
 
+class FilePool:
+    """The bundles of every layer in one file, ``[n_layers][n_ids]`` records
+    of ``stride`` bytes (the layout of :class:`HostPool`), read by the
+    library's file-tier stager through ``n_bounce`` pinned bounce buffers
+    and ``n_io`` host threads."""
+
+    def __init__(self, path, n_layers, n_ids, bundle_fn, replicate=False, n_bounce=4, n_io=4):
+        first, self.layout = bundle_layout(bundle_fn(0, 0))
+        self.bundle_bytes = first.nbytes
+        self.stride = (first.nbytes + 255) // 256 * 256
+        self.n_layers, self.n_ids = n_layers, n_ids
+        self.path, self.n_bounce, self.n_io = str(path), n_bounce, n_io
+        pad = bytes(self.stride - first.nbytes)
+        with open(self.path, "wb") as f:
+            block = None
+            for n in range(n_layers):
+                if replicate and block is not None:
+                    f.write(block)
+                    continue
+                parts = []
+                for e in range(n_ids):
+                    b = first if (n, e) == (0, 0) else bundle_layout(bundle_fn(n, e))[0]
+                    parts.append(b.tobytes() + pad)
+                blk = b"".join(parts)
+                if replicate:
+                    block = blk
+                f.write(blk)
+
+    def stager_file(self):
+        return (self.path, self.stride, self.n_bounce, self.n_io)
+
+    def bytes_of(self, layer, expert):
+        o = (layer * self.n_ids + expert) * self.stride
+        with open(self.path, "rb") as f:
+            f.seek(o)
+            data = f.read(self.bundle_bytes)
+        return torch.frombuffer(bytearray(data), dtype=torch.uint8)
+
+    def drop_page_cache(self):
+        """Ask the kernel to drop the file's clean pages (a cold read next)."""
+        fd = os.open(self.path, os.O_RDONLY)
+        try:
+            os.fsync(fd)
+            os.posix_fadvise(fd, 0, 0, os.POSIX_FADV_DONTNEED)
+        finally:
+            os.close(fd)
+
+    def remove(self):
+        try:
+            os.remove(self.path)
+        except FileNotFoundError:
+            pass
+
+
 class TieredChain:
     """Decode chain of ``len(layers)`` layers whose experts are staged from
     ``pool`` into ``n_slots`` device slots per layer.
@@ -88,8 +149,12 @@ class TieredChain:
         self.table = B.SlotTable(self.L, n_ids, n_slots)
         self.table.sync()
         self.slots = torch.empty(self.L * n_slots * pool.stride, dtype=torch.uint8, device=dev)
-        self.stager = B.Stager(self.table, pool.layout, pool.bundle_bytes, pool.ptrs(), self.slots,
-                               pool.stride)
+        if isinstance(pool, FilePool):
+            self.stager = B.Stager(self.table, pool.layout, pool.bundle_bytes, None, self.slots,
+                                   pool.stride, file=pool.stager_file())
+        else:
+            self.stager = B.Stager(self.table, pool.layout, pool.bundle_bytes, pool.ptrs(), self.slots,
+                                   pool.stride)
         self.copy_stream = torch.cuda.Stream()      # default priority
         self.ws = torch.zeros(B.workspace_bytes(spec, 1), dtype=torch.uint8, device=dev)
         self.r = torch.zeros(1, d, dtype=torch.float32, device=dev)
@@ -108,6 +173,7 @@ class TieredChain:
         self.queued = None      # (t + 1, n + 1, event) prediction read back, not yet staged
         self.used_layers = []   # layers of the sets used and not yet released, in use order
         self.copy_ms = 0.0
+        self.stage_host_s = []  # (copies, host seconds) of every stage call
         self.copy_events = []
         self.stall_s = 0.0
         self.log = []           # (t, n, "demand" | "predicted", set, copies)
@@ -124,7 +190,9 @@ class TieredChain:
         start = torch.cuda.Event(enable_timing=True)
         stop = torch.cuda.Event(enable_timing=True)
         start.record(self.copy_stream)
+        h0 = time.perf_counter()
         copies = self.stager.stage(n, s, self.copy_stream)
+        self.stage_host_s.append((len(copies), time.perf_counter() - h0))
         stop.record(self.copy_stream)
         if copies:
             self.copy_events.append((start, stop))

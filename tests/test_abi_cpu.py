@@ -203,3 +203,37 @@ def test_merge_requantize_argument_checks(B):
     assert call(B.MoeProj(0x10000, 0x20001, None, None), 4, 64) == B.MOE_EALIGN
     assert call(ok, 4, 64, sz_out=0x60001) == B.MOE_EALIGN
     assert call(ok, 4, 64, stats=0x70004) == B.MOE_EALIGN
+
+
+def test_stager_file_argument_checks(B):
+    """moe_stager_create_file rejects bad arguments before touching the file
+    or the device."""
+    lib = B.lib()
+    h = ctypes.c_void_p()
+    lay = B.MoeBundleLayout()
+    for args in ((None, 4096, b"/nonexistent", 4096, 2, 2),      # no table
+                 (0x1000, 4096, None, 4096, 2, 2),              # no path
+                 (0x1000, 4096, b"/nonexistent", 1024, 2, 2),   # stride < bundle
+                 (0x1000, 4096, b"/nonexistent", 4096, 0, 2),   # no bounce buffer
+                 (0x1000, 4096, b"/nonexistent", 4096, 2, 17)):  # too many threads
+        table, nbytes, path, stride, nb, nio = args
+        assert lib.moe_stager_create_file(table, ctypes.byref(lay), nbytes, path, stride, nb, nio,
+                                          0x100000, 4096, ctypes.byref(h)) == B.MOE_EINVAL
+    assert lib.moe_stager_io_stats(None, None, None) == B.MOE_EINVAL
+
+
+def test_file_pool_records(tmp_path):
+    """The file tier's records are the packed bundles, at stride offsets."""
+    from paper_2609_18063_amd import tier
+    wl = synth.WORKLOADS["tiny"]
+    fp = tier.FilePool(tmp_path / "pool.bin", 2, 3, lambda n, e: synth.bundle(wl, n, e), n_bounce=2)
+    assert os.path.getsize(fp.path) == 2 * 3 * fp.stride and fp.stride % 256 == 0
+    for n in range(2):
+        for e in range(3):
+            ref = tier.bundle_layout(synth.bundle(wl, n, e))[0]
+            assert np.array_equal(fp.bytes_of(n, e).numpy(), ref)
+    rp = tier.FilePool(tmp_path / "rep.bin", 3, 2, lambda n, e: synth.bundle(wl, n, e), replicate=True)
+    assert np.array_equal(rp.bytes_of(2, 1).numpy(), rp.bytes_of(0, 1).numpy())
+    fp.drop_page_cache()
+    fp.remove()
+    assert not os.path.exists(fp.path)

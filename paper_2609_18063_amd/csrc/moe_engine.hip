@@ -165,6 +165,7 @@ struct Route {
   int lg_gate[4], lg_up[4], lg_down[4];  // the segment's adapter on that projection is applied
   float dsc[4];          // segw * lora_scale where the down adapter is applied, else 0
   moe_bundle segbd[4];   // the segments' bundles, copied from the slot table
+  int src_ok;            // the staging source table of this routing is filled
 };
 
 // Source addresses of one step's staged weights for this workgroup,
@@ -286,10 +287,10 @@ __device__ __forceinline__ void stage(char* dst, int nchunks, Waves ws, SrcF src
 }
 
 // Phase timestamps for the profiling hook: thread 0 of workgroups 0, 7 and
-// 255 writes the constant-rate wall clock at up to 16 marks of every step.
+// 255 writes the constant-rate wall clock at up to 24 marks of every step (mark 23 by the first thread of wave 4).
 constexpr int kProfMarks = 24;
-__device__ __forceinline__ void mark(const EngineArgs& a, int g, int s, int k) {
-  if (!a.phase_ts || threadIdx.x != 0) return;
+__device__ __forceinline__ void mark(const EngineArgs& a, int g, int s, int k, int tid = 0) {
+  if (!a.phase_ts || threadIdx.x != tid) return;
   const int slot = g == 0 ? 0 : (g == 7 ? 1 : (g == NWG - 1 ? 2 : -1));
   if (slot < 0) return;
   a.phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
@@ -384,6 +385,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   if (threadIdx.x == 0) {
     mi->rt_step = mi->hd_step = mi->mix_step = -1;
     mi->rt[0].step = mi->rt[1].step = -1;
+    mi->rt[0].src_ok = mi->rt[1].src_ok = 1;
     if (ld_u32(&a.ctl[2])) mi->abort = 1;
   }
   const uint32_t base = ld_u32(&a.ctl[0]);
@@ -412,10 +414,14 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   // the source table that goes with routing Rt (one per step parity)
   auto src_of = [&](const Route& Rt) -> Src<SH>& { return srcs[&Rt == &mi->rt[0] ? 0 : 1]; };
   // Source table entries k = tid, tid + nthr, ... of a resolved routing Rt.
-  auto fill_src = [&](const Route& Rt, int tid, int nthr) {
+  // (entries part * ... of one kind only when part >= 0: 0 gate/up rows, 1 LoRA-A
+  // rows, 2 down column chunks; a wave then runs one branch)
+  auto fill_src = [&](const Route& Rt, int tid, int nthr, int part = -1) {
     Src<SH>& S = src_of(Rt);
     const int nrow = 2 * RM, nar = SH::NAX, ncol = GX / 32;
-    for (int k = tid; k < nrow + nar + ncol; k += nthr) {
+    const int k0 = part <= 0 ? 0 : (part == 1 ? nrow : nrow + nar);
+    const int k1 = part < 0 ? nrow + nar + ncol : (part == 0 ? nrow : (part == 1 ? nrow + nar : nrow + nar + ncol));
+    for (int k = k0 + tid; k < k1; k += nthr) {
       if (k < nrow) {  // gate / up row k
         const int lr = m * RM + (k < RM ? k : k - RM);
         const int q = row_seg(lr);
@@ -565,7 +571,10 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       const int k = mi->seg[q].k;
       resolve_seg(Rt, lay, q, k < K ? Rt.idx[k] : E + (k - K), k < K ? Rt.w[k] : 1.f);
     }
-    if (threadIdx.x == 0) Rt.step = step;
+    if (threadIdx.x == 0) {
+      Rt.step = step;
+      Rt.src_ok = 1;
+    }
     __syncthreads();
     fill_src(Rt, threadIdx.x, NT);
     __syncthreads();
@@ -602,14 +611,17 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   // u of the prediction (ids, then weights), lanes q < nseg resolve segment q.
   // The caller's next barrier hands Rt to the workgroup. On a timeout or an
   // abort it raises the abort flag the next poll_all reports.
-  auto route_from_pred_wave = [&](Route& Rt, int t, int N, int lay, int step) {
+  // `have`: lane u's word `pre` was loaded a step earlier (used if its tag is
+  // already the expected one, else the word is polled as usual).
+  auto route_from_pred_wave = [&](Route& Rt, int t, int N, int lay, int step, bool have,
+                                  uint64_t pre) {
     const uint64_t* pw = pred_of(t, N);
     uint64_t v = 0;
     bool ok = true;
     if (lane < 2 * K) {
       long spin = 0;
-      for (;;) {
-        v = ld_tag(pw + lane);
+      for (bool first = true;; first = false) {
+        v = (first && have) ? pre : ld_tag(pw + lane);
         if ((uint32_t)(v >> 32) == (uint32_t)t + 1u) break;
         if (++spin > kSpinMax) {
           if (c.status) atomicOr(c.status, MOE_STATUS_ENGINE_ABORT);
@@ -636,9 +648,12 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     const float wk = __int_as_float(__shfl(word, kq < K ? K + kq : 0, kWave));
     if (lane < nseg) resolve_seg(Rt, lay, lane, kq < K ? ek : E + (kq - K), wk);
     // the segments written by other lanes of this wave are read next
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    fill_src(Rt, lane, kWave);
-    if (lane == 0) Rt.step = step;
+    // the source table is filled later (src_ok = 0): by this wave while the
+    // polling waves wait in S4, else when the step starts staging
+    if (lane == 0) {
+      Rt.src_ok = 0;
+      Rt.step = step;
+    }
   };
   // the head logits that route layer N at token t (written at token t - 1)
   auto logh_of = [&](int t, int N) {
@@ -681,6 +696,10 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     __syncthreads();
     return true;
   };
+  // Wave 4 (chain): the prediction words of step s + 2, loaded during step s so
+  // that routing step s + 1 ahead starts from them (pf_step: the step they are for).
+  uint64_t pf_word = 0;
+  int pf_step = -1;
   for (int s = 0; s < a.n_steps && !mi->abort; ++s) {
     const uint32_t tag = base + (uint32_t)s + 1u;
     const int par = s & 1;
@@ -728,7 +747,17 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       mark(a, g, s, 16);
       if (wave == kStageW0 && s + 1 < a.n_steps) {
         const StepInfo f1 = step_info<MODE>(a, s + 1);
-        if (f1.ok && !f1.own) route_from_pred_wave(mi->rt[par ^ 1], f1.t, f1.N, f1.lay, s + 1);
+        if (f1.ok && !f1.own)
+          route_from_pred_wave(mi->rt[par ^ 1], f1.t, f1.N, f1.lay, s + 1, pf_step == s + 1, pf_word);
+        pf_step = -1;
+        if (s + 2 < a.n_steps) {  // published at least a token ago: in flight until the next step
+          const StepInfo f2 = step_info<MODE>(a, s + 2);
+          if (f2.ok && !f2.own) {
+            if (lane < 2 * K) pf_word = ld_tag(pred_of(f2.t, f2.N) + lane);
+            pf_step = s + 2;
+          }
+        }
+        mark(a, g, s, 23, kStageW0 * 64);
       }
       if (s == 0) {
         if (poller)
@@ -803,6 +832,10 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     // Gate/up rows (and head rows, unless staged ahead) by waves 0-3, needed
     // at once; down rows by waves 4-7, needed from S3 on.
     {
+      if (!Rt.src_ok) {  // routed ahead by one wave: this step's source table
+        fill_src(Rt, threadIdx.x, NT);
+        __syncthreads();
+      }
       dma_wait();  // nothing outstanding here: keeps the copy loops free of waits
       stage_gu(Rt, kPollW);
       if (has_head && mi->hd_step != s) stage_rows(SH::O_HD, LY.head, kPollW);
@@ -988,9 +1021,18 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     // ---- S4: h of the XCD -> down rows -> tagged partial of the output ---
     {
       uint64_t* HV = X + a.xo_hv + (size_t)par * a.xs_hv + (size_t)x * SH::GXX;
+      if (MODE == 1 && wave >= kStageW0 && wave < kStageW0 + 3) {
+        // the next step's source table (LDS only) while waves 0-3 poll: one
+        // kind of entry per wave; marked filled after the poll's barriers
+        Route& Rn = mi->rt[par ^ 1];
+        if (Rn.step == s + 1 && !Rn.src_ok)
+          fill_src(Rn, lane, kWave, wave - kStageW0);
+      }
       if (!poll_all<(SH::GXX + NPT - 1) / NPT>(GX, tag, [&](int i) { return HV + i; },
                                               [&](int i, float v) { hx[hx_pos(i)] = v; }, c, &mi->abort))
         break;
+      // every wave has passed the poll's barriers: the three parts are written
+      if (MODE == 1 && threadIdx.x == 0 && mi->rt[par ^ 1].step == s + 1) mi->rt[par ^ 1].src_ok = 1;
       // a_d[q][kk] = sum of the 32 members' partials
       {
         uint64_t* ADP = X + a.xo_adp + (size_t)par * a.xs_adp + (size_t)x * NM * SH::NSEGX * R;

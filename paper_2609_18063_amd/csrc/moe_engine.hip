@@ -546,10 +546,11 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   // wave 0); one barrier.
   // Segment q of routing Rt: expert e (routed: id idx[k]; shared: E + k - K)
   // with weight wk, resolved to its slot and bundle.
-  auto resolve_seg = [&](Route& Rt, int lay, int q, int e, float wk) {
+  // slot_pre >= -1: the slot, looked up earlier (-2: look it up now)
+  auto resolve_seg = [&](Route& Rt, int lay, int q, int e, float wk, int slot_pre = -2) {
     const int k = mi->seg[q].k;
     const bool bad = k < K && (e < 0 || e >= E);
-    const int slot = bad ? -1 : a.slot_of[(size_t)lay * a.n_ids + e];
+    const int slot = bad ? -1 : (slot_pre >= -1 ? slot_pre : a.slot_of[(size_t)lay * a.n_ids + e]);
     Rt.segok[q] = slot >= 0;
     moe_bundle b{};
     if (slot >= 0) b = a.bundles[(size_t)lay * a.n_slots + slot];
@@ -614,7 +615,7 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   // `have`: lane u's word `pre` was loaded a step earlier (used if its tag is
   // already the expected one, else the word is polled as usual).
   auto route_from_pred_wave = [&](Route& Rt, int t, int N, int lay, int step, bool have,
-                                  uint64_t pre) {
+                                  uint64_t pre, bool have_slot, int pre_slot) {
     const uint64_t* pw = pred_of(t, N);
     uint64_t v = 0;
     bool ok = true;
@@ -646,7 +647,10 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     const int kq = lane < nseg ? mi->seg[lane].k : 0;
     const int ek = __shfl(word, kq < K ? kq : 0, kWave);
     const float wk = __int_as_float(__shfl(word, kq < K ? K + kq : 0, kWave));
-    if (lane < nseg) resolve_seg(Rt, lay, lane, kq < K ? ek : E + (kq - K), wk);
+    // the slots looked up from the same words a step earlier, if the words
+    // used are those (their tag was already right then)
+    const bool use_slot = have_slot && have && (uint32_t)(pre >> 32) == (uint32_t)t + 1u;
+    if (lane < nseg) resolve_seg(Rt, lay, lane, kq < K ? ek : E + (kq - K), wk, use_slot ? pre_slot : -2);
     // the segments written by other lanes of this wave are read next
     // the source table is filled later (src_ok = 0): by this wave while the
     // polling waves wait in S4, else when the step starts staging
@@ -700,6 +704,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
   // that routing step s + 1 ahead starts from them (pf_step: the step they are for).
   uint64_t pf_word = 0;
   int pf_step = -1;
+  // ... and the slots of that step's segments, looked up during step s's S4
+  int pf_slot = -1, pf_slot_step = -1;
   for (int s = 0; s < a.n_steps && !mi->abort; ++s) {
     const uint32_t tag = base + (uint32_t)s + 1u;
     const int par = s & 1;
@@ -748,7 +754,9 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
       if (wave == kStageW0 && s + 1 < a.n_steps) {
         const StepInfo f1 = step_info<MODE>(a, s + 1);
         if (f1.ok && !f1.own)
-          route_from_pred_wave(mi->rt[par ^ 1], f1.t, f1.N, f1.lay, s + 1, pf_step == s + 1, pf_word);
+          route_from_pred_wave(mi->rt[par ^ 1], f1.t, f1.N, f1.lay, s + 1, pf_step == s + 1, pf_word,
+                               pf_slot_step == s + 1, pf_slot);
+        pf_slot_step = -1;
         pf_step = -1;
         if (s + 2 < a.n_steps) {  // published at least a token ago: in flight until the next step
           const StepInfo f2 = step_info<MODE>(a, s + 2);
@@ -1027,6 +1035,16 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
         Route& Rn = mi->rt[par ^ 1];
         if (Rn.step == s + 1 && !Rn.src_ok)
           fill_src(Rn, lane, kWave, wave - kStageW0);
+        if (wave == kStageW0 && pf_step == s + 2) {  // the slots of step s + 2's segments
+          const StepInfo f2 = step_info<MODE>(a, s + 2);
+          const bool tag_ok = (uint32_t)(pf_word >> 32) == (uint32_t)f2.t + 1u;
+          const int kq = lane < nseg ? mi->seg[lane].k : 0;
+          const int ek = __shfl((int)(uint32_t)pf_word, kq < K ? kq : 0, kWave);
+          const int e = kq < K ? ek : E + (kq - K);
+          pf_slot = -1;
+          if (lane < nseg && e >= 0 && e < a.n_ids) pf_slot = a.slot_of[(size_t)f2.lay * a.n_ids + e];
+          pf_slot_step = __all(lane >= 2 * K || tag_ok) ? s + 2 : -1;
+        }
       }
       if (!poll_all<(SH::GXX + NPT - 1) / NPT>(GX, tag, [&](int i) { return HV + i; },
                                               [&](int i, float v) { hx[hx_pos(i)] = v; }, c, &mi->abort))

@@ -367,12 +367,15 @@ int moe_engine_tokens(const moe_layer_spec* spec, const moe_slot_table* table,
  * at token t >= 1 routes by the prediction that the head of layer N-1 made at
  * token t-1. The predictions persist in the workspace between calls.
  * Optional records (device, [n_tokens*n_layers] rows in token-major order):
- * x_rec fp16 [.][d], idx_rec / w_rec / pidx_rec / pw_rec [.][K], y_rec fp32 [.][d].
+ * x_rec fp16 [.][d] (the layer input), r_rec fp32 [.][d] (the residual after
+ * the mixing, before the layer output is added), idx_rec / w_rec (the
+ * routing used) and pidx_rec / pw_rec (the head's prediction) [.][K],
+ * y_rec fp32 [.][d] (the layer output).
  */
 int moe_engine_chain(const moe_layer_spec* spec, const moe_slot_table* table,
                      const moe_engine_layer* layers, int n_layers, int first_token, int n_tokens,
-                     const float* xi, float* r_state, void* x_rec, int32_t* idx_rec, float* w_rec,
-                     int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status,
+                     const float* xi, float* r_state, void* x_rec, float* r_rec, int32_t* idx_rec,
+                     float* w_rec, int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status,
                      void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- host-tier staging -----------------------------------------------------

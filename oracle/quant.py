@@ -79,10 +79,12 @@ def dequantize_g64(q, s, z):
     """Reconstruct ``w_hat = s * q + z`` (float64, exact) for every weight."""
     q = np.asarray(q, dtype=np.float64)
     rows, cols = q.shape
-    s64 = np.repeat(np.asarray(s, dtype=np.float64), GROUP, axis=1)
-    z64 = np.repeat(np.asarray(z, dtype=np.float64), GROUP, axis=1)
-    assert s64.shape == (rows, cols)
-    return s64 * q + z64
+    s64 = np.asarray(s, dtype=np.float64)
+    z64 = np.asarray(z, dtype=np.float64)
+    assert s64.shape == (rows, cols // GROUP) and z64.shape == s64.shape
+    # group g of a row holds inputs 64 g .. 64 g + 63
+    w = s64[:, :, None] * q.reshape(rows, cols // GROUP, GROUP) + z64[:, :, None]
+    return w.reshape(rows, cols)
 
 
 def projection_bytes(out_dim, in_dim):

@@ -134,7 +134,8 @@ SIGNATURES = {
                                   c_void_p, c_void_p, c_size_t, c_void_p]),
     "moe_engine_chain": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_int,
                                  c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
-                                 c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                 c_void_p]),
 }
 
 MOE_PROF_FFN_MAIN = 0
@@ -542,11 +543,12 @@ def engine_tokens(spec, table, layer_arr, step_layer, xi, y, workspace, idx=None
 
 def engine_chain(spec, table, layer_arr, n_layers, first_token, xi, r_state, workspace,
                  x_rec=None, idx=None, w=None, pidx=None, pw=None, y_rec=None, status=None,
-                 stream=None):
+                 stream=None, r_rec=None):
     n_tokens = xi.shape[0]
     _check(lib().moe_engine_chain(ctypes.byref(spec), table.handle, _ptr(layer_arr), n_layers,
                                   first_token, n_tokens, _ptr(xi), _ptr(r_state), _ptr(x_rec),
-                                  _ptr(idx), _ptr(w), _ptr(pidx), _ptr(pw), _ptr(y_rec),
+                                  _ptr(r_rec), _ptr(idx), _ptr(w), _ptr(pidx), _ptr(pw),
+                                  _ptr(y_rec),
                                   _ptr(status), _ptr(workspace),
                                   workspace.numel() * workspace.element_size(), _stream(stream)),
            "moe_engine_chain")

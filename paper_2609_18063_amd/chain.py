@@ -54,6 +54,8 @@ class DeviceChain:
         B.chain_token_start(self.xi, self.r)
         for n, lay in enumerate(self.layers):
             B.chain_mix_rmsnorm(lay["mix_d"], lay["mix_perm"], self.r, self.x)
+            if record is not None:
+                record["r"][t, n].copy_(self.r[0])
             if self.uses_prediction(t, n):
                 idx, w = self.pred_idx[t % 2, n], self.pred_w[t % 2, n]
             else:
@@ -67,6 +69,7 @@ class DeviceChain:
             B.expert_ffn(s, self.table, n, self.x, idx, ye, self.status, self.ws)
             B.combine_add(s, ye, w, self.r)
             if record is not None:
+                record["r_post"][t, n].copy_(self.r[0])
                 record["x"][t, n].copy_(self.x[0])
                 record["idx"][t, n].copy_(idx[0])
                 record["w"][t, n].copy_(w[0])
@@ -85,6 +88,8 @@ class DeviceChain:
         dev = "cuda"
         return {
             "x": torch.zeros(T, L, d, dtype=torch.float16, device=dev),
+            "r": torch.zeros(T, L, d, dtype=torch.float32, device=dev),
+            "r_post": torch.zeros(T, L, d, dtype=torch.float32, device=dev),
             "idx": torch.zeros(T, L, K, dtype=torch.int32, device=dev),
             "w": torch.zeros(T, L, K, dtype=torch.float32, device=dev),
             "pidx": torch.full((T, L, K), -1, dtype=torch.int32, device=dev),

@@ -554,6 +554,7 @@ static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n
   if (n_table_layers > t->n_layers || t->n_ids < s->n_experts + s->n_shared) return MOE_EINVAL;
   if (!aligned16(ws) || !aligned16(a.xi) || (a.y && !aligned16(a.y)) ||
       (a.r_state && !aligned16(a.r_state)) || (a.x_rec && !aligned16(a.x_rec)) ||
+      (a.r_rec && !aligned4(a.r_rec)) ||
       (a.idx_rec && !aligned4(a.idx_rec)) || (a.w_rec && !aligned4(a.w_rec)) ||
       (a.pidx_rec && !aligned4(a.pidx_rec)) || (a.pw_rec && !aligned4(a.pw_rec)) ||
       (a.status && !aligned4(a.status)))
@@ -621,9 +622,9 @@ int moe_engine_tokens(const moe_layer_spec* s, const moe_slot_table* t,
 
 int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,
                      const moe_engine_layer* layers, int n_layers, int first_token, int n_tokens,
-                     const float* xi, float* r_state, void* x_rec, int32_t* idx_rec, float* w_rec,
-                     int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status, void* ws,
-                     size_t ws_bytes, void* stream) {
+                     const float* xi, float* r_state, void* x_rec, float* r_rec, int32_t* idx_rec,
+                     float* w_rec, int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status,
+                     void* ws, size_t ws_bytes, void* stream) {
   if (n_layers < 1 || n_tokens < 0 || first_token < 0 || !r_state) return MOE_EINVAL;
   if ((long long)n_tokens * n_layers > (1LL << 30)) return MOE_EINVAL;
   if (n_tokens == 0) return MOE_OK;
@@ -638,6 +639,7 @@ int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,
   a.xi = xi;
   a.r_state = r_state;
   a.x_rec = static_cast<__half*>(x_rec);
+  a.r_rec = r_rec;
   a.idx_rec = idx_rec;
   a.w_rec = w_rec;
   a.pidx_rec = pidx_rec;

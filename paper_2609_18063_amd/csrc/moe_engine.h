@@ -23,6 +23,7 @@ struct EngineArgs {
   float* y;                      // mode 0: [n_steps][d] output; mode 1: optional record
   float* r_state;                // mode 1: [d] residual, in/out
   __half* x_rec;                 // optional [n_steps][d]
+  float* r_rec;                  // optional [n_steps][d]: chain residual after the mixing
   int32_t* idx_rec;              // optional [n_steps][K]
   float* w_rec;
   int32_t* pidx_rec;

@@ -806,6 +806,8 @@ __global__ void __launch_bounds__(NT) engine_kernel(EngineArgs a) {
     __syncthreads();
     if (g == 0 && a.x_rec && poller)
       for (int j = threadIdx.x; j < D; j += NPT) a.x_rec[(size_t)s * D + j] = xh[j];
+    if (MODE == 1 && g == 1 && a.r_rec && poller)
+      for (int j = threadIdx.x; j < D; j += NPT) a.r_rec[(size_t)s * D + j] = r1[j];
 
     mark(a, g, s, 1);
     // ---- S1: routing ----------------------------------------------------

@@ -165,3 +165,87 @@ def test_zipf_logits_popularity_is_skewed():
     idx = np.argsort(-logits, axis=1, kind="stable")[:, :wl.K]
     counts = np.bincount(idx.ravel(), minlength=wl.E)
     assert counts.max() > 300 and (counts > 0).sum() > 150
+
+
+# ---- the attention stand-in of the chain, pinned by hand-derived values ----
+
+def _golden_standin():
+    import json
+    import os
+    return json.load(open(os.path.join(os.path.dirname(__file__), "golden", "chain_standin.json")))
+
+
+def test_standin_mix_hand_case():
+    g = _golden_standin()["mix"]
+    got = stack.mix(np.array(g["r"], np.float32), np.array(g["mix_d"], np.float16),
+                    np.array(g["mix_perm"], np.int32))
+    assert got.dtype == np.float32
+    assert got.tolist() == g["value"]
+
+
+def test_standin_layer_input_hand_case():
+    g = _golden_standin()["layer_input"]
+    got = routing.rms_norm_f16(np.array(g["r"], np.float32))
+    assert got.dtype == np.float16
+    assert got.astype(np.float64).tolist() == g["value"]
+
+
+def test_standin_token_start_hand_case():
+    g = _golden_standin()["token_start"]
+    xi = np.array(g["xi"], np.float32)
+    got = stack.token_start(xi, np.array(g["r_prev"], np.float32))
+    assert got.dtype == np.float32
+    assert got.astype(np.float64).tolist() == g["value"]
+    assert np.array_equal(stack.token_start(xi, None), xi)
+
+
+def test_standin_residual_add():
+    r = np.array([1.0, 2.0 ** 24, -3.0, 0.5], np.float32)
+    y = np.array([0.25, 1.0, 3.0, -0.5], np.float64)
+    # fp32 sums: 1.25 exact; 2^24 + 1 rounds to even (2^24); -3 + 3 = 0; 0
+    assert stack.add_output(r, y).tolist() == [1.25, 2.0 ** 24, 0.0, 0.0]
+
+
+def test_chain_records_follow_the_standin():
+    """Every record of the chain is tied to its neighbours by the pinned
+    stand-in steps: x_N is the layer input of the mixed residual, the next
+    layer's mixed residual is mix(r + y_N), and a token starts from the
+    previous token's last residual."""
+    wl = synth.WORKLOADS["tiny"]
+    nl = 3
+    layers = _stack_layers(wl, nl)
+    xi = synth.token_draws(wl, 0, 3)
+    out = stack.decode_chain(xi, layers, wl.K, wl.lora_scale)
+    r_prev = None
+    for t, recs in enumerate(out):
+        r = stack.token_start(xi[t], r_prev)
+        for n, rec in enumerate(recs):
+            r = stack.mix(r, layers[n]["mix_d"], layers[n]["mix_perm"])
+            assert rec["r_mixed"].dtype == np.float32
+            assert np.array_equal(rec["r_mixed"], r), (t, n)
+            assert np.array_equal(rec["x16"], routing.rms_norm_f16(r)), (t, n)
+            r = stack.add_output(r, rec["y"])
+        r_prev = r
+
+
+def test_standin_pins_catch_planted_mistakes():
+    """Plausible mistakes in the stand-in, planted in copies of its steps,
+    each miss a hand-derived value."""
+    g = _golden_standin()
+    m = g["mix"]
+    r, d, p = (np.array(m["r"], np.float32), np.array(m["mix_d"], np.float16),
+               np.array(m["mix_perm"], np.int64))
+    r64, d64 = r.astype(np.float64), d.astype(np.float64)
+    inv = np.argsort(p)
+    swapped = (r64 + d64 * r64[inv]).astype(np.float32)          # permutation the other way
+    wrong_side = (r64[p] + d64 * r64).astype(np.float32)         # scale on the wrong operand
+    no_skip = (d64 * r64[p]).astype(np.float32)                  # residual term dropped
+    for bad in (swapped, wrong_side, no_skip):
+        assert bad.tolist() != m["value"]
+    ts = g["token_start"]
+    xi, rp = np.array(ts["xi"], np.float64), np.array(ts["r_prev"], np.float64)
+    dropped = xi.astype(np.float32)                              # previous token ignored
+    unnormed = (xi + rp).astype(np.float32)                      # normalization dropped
+    meannorm = (xi + rp / np.sqrt(np.mean(rp) + 1e-6)).astype(np.float32)  # mean instead of mean square
+    for bad in (dropped, unnormed, meannorm):
+        assert bad.astype(np.float64).tolist() != ts["value"]

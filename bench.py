@@ -1,14 +1,20 @@
-"""Benchmark: decode steps of the 35B-class int4 MoE layer at batch 1.
+"""Benchmark: batch-1 decode of the 40-layer stack of the 35B-class int4 MoE layer.
 
-A step is the whole hot path on one token: layer input (RMSNorm -> fp16),
-router + softmax-top-k, prerouter prediction for the next layer, the 8
-routed + 1 shared int4 group-64 SwiGLU experts with the unmerged LoRA delta,
-and the combine.  Steps rotate over 40 resident layers (40 x ~520 MB), so
-weights come from HBM and not from the 256 MB last-level cache.  The K timed
-steps run in one launch of the persistent decode engine, with the inputs
-already resident in HBM.  Also measured: tokens/s of the 40-layer stack
-(autoregressive, prediction-as-routing) and the per-call path.  Prints one
-JSON line.
+A step is one token through all 40 layers, the whole decode hot path: layer
+input (residual mixing in place of attention, RMSNorm -> fp16), routing by
+the layer's own router (layer 0, and every layer of the first token) or by
+the prediction its head made one token earlier (prediction-as-routing), the
+8 routed + 1 shared int4 group-64 SwiGLU experts with the unmerged LoRA
+delta, the combine, and the head's prediction for the next layer.  The 40
+layers are resident in HBM (40 x ~520 MB), so weights come from HBM and not
+from the 256 MB last-level cache.  The K timed tokens run in one launch of
+the persistent decode engine, with the inputs already resident in HBM; the
+headline ``value`` is the layer steps' algorithmic bytes over that launch's
+GPU time.  Also measured: independent single-token layer steps (one at a
+time, and 16 in flight), the per-call path, the batched / prefill path, the
+full prerouter head, sigmoid-group routing, the merged alternative, the 8B
+host tier, and the float64 oracle on this machine's cores.  Prints one JSON
+line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -32,11 +38,11 @@ METRIC = "int4 MoE layer achieved HBM GB/s (% peak) at batch 1; tokens/s, 40-lay
 
 
 # The dominant kernel of the timed step and the sources its counters depend on.
-ENGINE_SOURCES = ("paper_2609_18063_amd/csrc/moe_engine_tokens.hip",
+ENGINE_SOURCES = ("paper_2609_18063_amd/csrc/moe_engine.hip",
                   "paper_2609_18063_amd/csrc/moe_engine.h",
                   "paper_2609_18063_amd/csrc/moe_xchg.h",
                   "paper_2609_18063_amd/csrc/moe_device.h")
-TRAFFIC_PROFILE = "profiles/moe35b_tokens_hbm_traffic.md"
+TRAFFIC_PROFILE = "profiles/moe35b_chain_hbm_traffic.md"
 
 
 def sources_sha256():
@@ -163,38 +169,139 @@ def step(B, spec, table, lay, i, xi_row, bufs):
     B.combine(spec, bufs["ye"], bufs["w"], bufs["y"])
 
 
-def cpu_baseline(wl, budget_s=15.0):
-    """The oracle as it stands, on a bounded sample of the same workload."""
-    import synth
-    from oracle import expert as o_expert, routing as o_routing
+def chain_bytes(wl, L, T, first_token=0):
+    """Algorithmic bytes of T tokens of the L-layer decode chain: per layer
+    step the selected experts + shared expert with their LoRA, the layer's
+    head (not at the last layer), the layer's router where it routes itself
+    (layer 0, and every layer of token 0), and the residual read and written
+    (fp32 [d] each)."""
+    nb = layer_bytes(wl)
+    mat = wl.E * wl.d * 2
+    total = 0
+    for t in range(first_token, first_token + T):
+        own = L if t == 0 else 1
+        total += L * nb["ffn"] + (L - 1) * mat + own * mat + L * 2 * wl.d * 4
+    return total
+
+
+def cpu_model():
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
-    router = synth.router_weights(wl, 0, 0)
-    head = synth.router_weights(wl, 0, 1)
-    shared = [synth.bundle(wl, 0, wl.E + s) for s in range(wl.S)]
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def _oracle_runs(wl, L, budget_s):
+    """Time the float64 oracle on bounded samples of the four workloads (the
+    bundles are generated outside the timed regions).  Returns per-workload
+    seconds per unit."""
+    import synth
+    from oracle import batched as o_batched, expert as o_expert, routing as o_routing
+    from oracle import stack as o_stack
     cache = {}
-    done, spent = 0, 0.0
-    while spent < budget_s and done < 200:
+
+    def bundle(w, n, e):
+        key = (w.name, n, e)
+        if key not in cache:
+            cache[key] = synth.bundle(w, n, e)
+        return cache[key]
+
+    out = {}
+    # 35B-class layer, independent tokens (the bench's stack uses layer 0's experts everywhere)
+    router, head = synth.router_weights(wl, 0, 0), synth.router_weights(wl, 0, 1)
+    shared = [bundle(wl, 0, wl.E + s) for s in range(wl.S)]
+    spent, done = 0.0, 0
+    while spent < budget_s and done < 100:
         xi = synth.token_draws(wl, done, 1)[0]
         x16 = o_routing.rms_norm_f16(xi)
-        _, inds, _ = o_routing.route(router, x16, wl.K)
-        for e in inds:                      # inputs are prepared outside the timed region
-            if int(e) not in cache:
-                cache[int(e)] = synth.bundle(wl, 0, int(e))
+        for e in o_routing.route(router, x16, wl.K)[1]:
+            bundle(wl, 0, int(e))
         t0 = time.perf_counter()
-        o_routing.rms_norm_f16(xi)
-        o_expert.moe_layer(x16, wl.K, lambda e: cache[e], shared, wl.lora_scale,
+        x16 = o_routing.rms_norm_f16(xi)
+        o_expert.moe_layer(x16, wl.K, lambda e: bundle(wl, 0, e), shared, wl.lora_scale,
                            w_router16=router, w_head16=head)
         spent += time.perf_counter() - t0
         done += 1
-    per_tok = spent / done
-    return {"value": round(layer_bytes(wl)["step"] / per_tok / 1e9, 4), "unit": "GB/s",
-            "cores": int(threads), "kind": "oracle",
-            "sample": "%d tokens of the 35B-class layer (float64 oracle, %.2f s/token)"
-                      % (done, per_tok)}
+    out["layer"] = {"s_per_token": spent / done, "tokens": done}
+    # 40-layer chain: the first tokens through the first layers, extrapolated to 40 layers
+    n_lay = 4
+    layers = []
+    for n in range(n_lay):
+        d, perm = synth.mixing(wl, n)
+        layers.append({"router": synth.router_weights(wl, n, 0), "head": synth.router_weights(wl, n, 1),
+                       "mix_d": d, "mix_perm": perm, "routed": (lambda e: bundle(wl, 0, e)),
+                       "shared": shared})
+    xi = synth.token_draws(wl, 0, 2, stream=1)
+    o_stack.decode_chain(xi, layers, wl.K, wl.lora_scale)        # bundles into the cache
+    t0 = time.perf_counter()
+    o_stack.decode_chain(xi, layers, wl.K, wl.lora_scale)
+    per_layer = (time.perf_counter() - t0) / (2 * n_lay)
+    out["chain"] = {"s_per_layer_step": per_layer, "s_per_token": per_layer * L,
+                    "sample": "2 tokens x %d layers, extrapolated to %d layers" % (n_lay, L)}
+    # batched T = 64 (Zipf routing), a sample of its tokens, extrapolated
+    T = 64
+    logits = synth.zipf_logits(wl, T, seed=T)
+    x = o_routing.rms_norm_f16(synth.token_draws(wl, 300 + T, T))
+    sample = list(range(0, T, 8))
+    for t in sample:
+        for e in o_routing.softmax_topk(logits[t], wl.K)[0]:
+            bundle(wl, 0, int(e))
+    t0 = time.perf_counter()
+    o_batched.batched_layer(x, logits, wl.K, lambda e: bundle(wl, 0, e), shared, wl.lora_scale,
+                            tokens=sample)
+    per_tok = (time.perf_counter() - t0) / len(sample)
+    out["batched_T64"] = {"s_per_batch": per_tok * T, "sample": "%d of the %d tokens" % (len(sample), T)}
+    # 8B-tier layer, compute only (the oracle does not model the copies)
+    w8 = synth.WORKLOADS["tier8b"]
+    r8, h8 = synth.router_weights(w8, 0, 0), synth.router_weights(w8, 0, 1)
+    xs = [o_routing.rms_norm_f16(v) for v in synth.token_draws(w8, 0, 2)]
+    for x16 in xs:
+        for e in o_routing.route(r8, x16, w8.K)[1]:
+            bundle(w8, 0, int(e))
+    t0 = time.perf_counter()
+    for x16 in xs:
+        o_expert.moe_layer(x16, w8.K, lambda e: bundle(w8, 0, e), [], w8.lora_scale,
+                           w_router16=r8, w_head16=h8)
+    out["tier8b_layer"] = {"s_per_token_layer": (time.perf_counter() - t0) / len(xs),
+                           "sample": "2 tokens through one layer (compute only)"}
+    return out
+
+
+def cpu_baseline(wl, L, budget_s=4.0):
+    """The oracle as it stands, timed on this machine's cores: once with one
+    BLAS thread and once with every core of the affinity mask, each on
+    bounded samples of the same workloads.  ``value`` is the chain's layer
+    step on all cores, in the headline's unit."""
+    from threadpoolctl import threadpool_limits
+    cores = len(os.sched_getaffinity(0))
+    runs = {}
+    for name, n in (("one_thread", 1), ("all_cores", cores)):
+        with threadpool_limits(limits=n):
+            runs[name] = _oracle_runs(wl, L, budget_s)
+    nb = layer_bytes(wl)
+    chain_layer = nb["ffn"] + wl.E * wl.d * 2 + 2 * wl.d * 4
+    res = {}
+    for name, r in runs.items():
+        res[name] = {
+            "layer_GB_s": round(nb["step"] / r["layer"]["s_per_token"] / 1e9, 4),
+            "layer_ms_per_token": round(r["layer"]["s_per_token"] * 1e3, 2),
+            "chain_GB_s": round(chain_layer / r["chain"]["s_per_layer_step"] / 1e9, 4),
+            "chain_tokens_per_s": round(1.0 / r["chain"]["s_per_token"], 4),
+            "batched_T64_ms_per_batch": round(r["batched_T64"]["s_per_batch"] * 1e3, 1),
+            "tier8b_ms_per_token_layer": round(r["tier8b_layer"]["s_per_token_layer"] * 1e3, 2),
+        }
+    a = runs["all_cores"]
+    return {"value": res["all_cores"]["chain_GB_s"], "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": "float64 oracle; value: the 40-layer chain's layer step (%s); also the "
+                      "35B-class layer on %d tokens, batched T=64 (%s), the 8B-tier layer (%s)"
+                      % (a["chain"]["sample"], a["layer"]["tokens"], a["batched_T64"]["sample"],
+                         a["tier8b_layer"]["sample"]),
+            "cpu_model": cpu_model(), "runs": res}
 
 
 def time_launch(torch, fn):
@@ -573,22 +680,34 @@ def tier_path(B, torch, T=64, L=24, rho=0.5):
     return res
 
 
+def chain_launch(B, spec, table, arr, L, tokens, r_state, ws, status):
+    """One engine launch of the decode chain over ``tokens`` from token 0."""
+    r_state.zero_()
+    B.engine_chain(spec, table, arr, L, 0, tokens, r_state, ws, status=status)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    # untimed; about 15 ms of the same work, so that the timed launch meets the
-    # clocks of sustained decoding rather than those of an idle GPU
-    ap.add_argument("--warmup", type=int, default=4000)
+    ap.add_argument("--steps", type=int, default=256,
+                    help="timed steps: tokens of the 40-layer stack, one launch")
+    ap.add_argument("--warmup", type=int, default=16, help="untimed tokens before the timed launch")
+    # untimed as well: about this much chain work first, so that the timed launch
+    # meets the clocks of sustained decoding rather than those of an idle GPU
+    ap.add_argument("--clock-warmup-ms", type=float, default=40.0)
     ap.add_argument("--layers", type=int, default=40)
-    ap.add_argument("--stack-tokens", type=int, default=256)
+    ap.add_argument("--indep-steps", type=int, default=2000,
+                    help="independent single-token steps per launch of the latency and "
+                         "throughput schedules")
     ap.add_argument("--per-call-steps", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
     ap.add_argument("--no-tier", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the headline chain and the two independent-step schedules")
     ap.add_argument("--tier-tokens", type=int, default=64)
-    ap.add_argument("--only-engine", action="store_true",
-                    help="time the engine launch only (for counter runs)")
+    ap.add_argument("--only-chain", action="store_true",
+                    help="time the headline chain launch only (for counter runs)")
     ap.add_argument("--only-batched", action="store_true",
                     help="time the batched / prefill path only (for kernel traces)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -613,136 +732,145 @@ def main():
     table, layers = build_stack(wl, L, torch)
     arr = B.engine_layer_array(layers)
     hip = Hip()
-
-    if args.only_batched:
-        print(json.dumps({"batched": batched_path(B, torch, spec, table, wl, L)}), flush=True)
-        return
-
-    # ---- single-token layer steps (the layer metric): one engine launch ----
-    # Throughput schedule (the measured step): each XCD runs its own steps.
-    tokens = torch.from_numpy(synth.token_draws(wl, 0, K + W)).cuda()
-    step_layer = (torch.arange(K + W, dtype=torch.int32, device="cuda") % L).contiguous()
-    y = torch.empty(K + W, wl.d, dtype=torch.float32, device="cuda")
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
-    ws = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
-    assert B.engine_tokens_supported(spec), "the throughput schedule does not support this shape"
-    if W:
-        B.engine_tokens(spec, table, arr, step_layer[K:], tokens[K:], y[K:], ws, status=status)
-    ms_total = time_launch(torch, lambda: B.engine_tokens(spec, table, arr, step_layer[:K],
-                                                          tokens[:K], y[:K], ws, status=status))
-    assert int(status.item()) == 0, "engine status %d" % int(status.item())
-    ms_step = ms_total / K
-    gbs = nb["step"] * K / (ms_total * 1e-3) / 1e9
-    log("engine (16 steps in flight), %d single-token steps in one launch: %.3f ms, "
-        "%.2f us/step, %.1f GB/s" % (K, ms_total, ms_step * 1e3, gbs))
+    try:
+        if args.only_batched:
+            print(json.dumps({"batched": batched_path(B, torch, spec, table, wl, L)}), flush=True)
+            return
 
-    if args.copy_calibration:
-        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)                      # reads 1 GiB, writes 1 GiB
-        torch.cuda.synchronize()
-        del src, dst
-    if args.only_engine:
-        print(json.dumps({"engine_us_per_step": round(ms_step * 1e3, 3), "GB_s": round(gbs, 2)}),
-              flush=True)
-        return
+        # ---- the headline: batch-1 decode of the 40-layer stack --------------
+        # (a step = one token through all layers: input norm, routing by the own
+        # router or by the prediction of the previous token, experts with LoRA,
+        # combine, head prediction, residual mixing), one launch of the chain.
+        ws_c = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+        r_state = torch.zeros(wl.d, dtype=torch.float32, device="cuda")
+        warm_tok = torch.from_numpy(synth.token_draws(wl, 0, 64, stream=2)).cuda()
+        t_end = time.perf_counter() + args.clock_warmup_ms * 1e-3
+        while time.perf_counter() < t_end:
+            chain_launch(B, spec, table, arr, L, warm_tok, r_state, ws_c, status)
+            torch.cuda.synchronize()
+        stack_tok = torch.from_numpy(synth.token_draws(wl, 0, K + W, stream=1)).cuda()
+        if W:
+            chain_launch(B, spec, table, arr, L, stack_tok[K:], r_state, ws_c, status)
+        ms_chain = time_launch(torch, lambda: chain_launch(B, spec, table, arr, L, stack_tok[:K],
+                                                           r_state, ws_c, status))
+        assert int(status.item()) == 0, "engine status %d" % int(status.item())
+        c_bytes = chain_bytes(wl, L, K)
+        chain_gbs = c_bytes / (ms_chain * 1e-3) / 1e9
+        tok_s = K / (ms_chain * 1e-3)
+        us_layer = ms_chain * 1e3 / (K * L)
+        log("decode chain, %d layers: %d tokens in %.3f ms -> %.1f tok/s, %.2f us per layer step, "
+            "%.1f GB/s (%.1f%% of HBM)" % (L, K, ms_chain, tok_s, us_layer, chain_gbs,
+                                           100 * chain_gbs / PEAK_HBM_GBS))
+        if args.copy_calibration:
+            src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+            dst = torch.empty_like(src)
+            dst.copy_(src)                      # reads 1 GiB, writes 1 GiB
+            torch.cuda.synchronize()
+            del src, dst
+        if args.only_chain:
+            print(json.dumps({"chain_ms": round(ms_chain, 4), "us_per_layer_step": round(us_layer, 3),
+                              "GB_s": round(chain_gbs, 2)}), flush=True)
+            return
 
-    # Latency schedule: every step on the whole chip, one after another.
-    if W:
-        B.engine_layers(spec, table, arr, step_layer[K:], tokens[K:], y[K:], ws, status=status)
-    ms_lat = time_launch(torch, lambda: B.engine_layers(spec, table, arr, step_layer[:K],
-                                                        tokens[:K], y[:K], ws, status=status))
-    assert int(status.item()) == 0, "engine status %d" % int(status.item())
-    lat_gbs = nb["step"] * K / (ms_lat * 1e-3) / 1e9
-    log("engine (one step at a time on the whole chip): %.2f us/step, %.1f GB/s"
-        % (ms_lat / K * 1e3, lat_gbs))
+        # ---- independent single-token steps: latency and throughput schedules --
+        N = args.indep_steps
+        tokens = torch.from_numpy(synth.token_draws(wl, 0, 2 * N)).cuda()
+        step_layer = (torch.arange(2 * N, dtype=torch.int32, device="cuda") % L).contiguous()
+        y = torch.empty(2 * N, wl.d, dtype=torch.float32, device="cuda")
+        ws = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+        B.engine_layers(spec, table, arr, step_layer[N:], tokens[N:], y[N:], ws, status=status)
+        ms_lat = time_launch(torch, lambda: B.engine_layers(spec, table, arr, step_layer[:N],
+                                                            tokens[:N], y[:N], ws, status=status))
+        assert int(status.item()) == 0, "engine status %d" % int(status.item())
+        lat_gbs = nb["step"] * N / (ms_lat * 1e-3) / 1e9
+        log("independent steps, one at a time on the whole chip: %.2f us/step, %.1f GB/s"
+            % (ms_lat / N * 1e3, lat_gbs))
+        assert B.engine_tokens_supported(spec), "the throughput schedule does not support this shape"
+        B.engine_tokens(spec, table, arr, step_layer[N:], tokens[N:], y[N:], ws, status=status)
+        ms_tok = time_launch(torch, lambda: B.engine_tokens(spec, table, arr, step_layer[:N],
+                                                            tokens[:N], y[:N], ws, status=status))
+        assert int(status.item()) == 0, "engine status %d" % int(status.item())
+        tok_gbs = nb["step"] * N / (ms_tok * 1e-3) / 1e9
+        log("independent steps, 16 in flight (one per team of 16 workgroups): %.2f us/step, "
+            "%.1f GB/s" % (ms_tok / N * 1e3, tok_gbs))
 
-    # ---- 40-layer stack, autoregressive decode (prediction-as-routing) ----
-    T = args.stack_tokens
-    ws2 = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
-    r_state = torch.zeros(wl.d, dtype=torch.float32, device="cuda")
-    stack_tok = torch.from_numpy(synth.token_draws(wl, 0, T + 16, stream=1)).cuda()
-    B.engine_chain(spec, table, arr, L, 0, stack_tok[T:], r_state, ws2, status=status)
-    r_state.zero_()
-    ws2.zero_()
-    ms_chain = time_launch(torch, lambda: B.engine_chain(spec, table, arr, L, 0, stack_tok[:T],
-                                                         r_state, ws2, status=status))
-    assert int(status.item()) == 0, "engine status %d" % int(status.item())
-    tok_s = T / (ms_chain * 1e-3)
-    # per token (t >= 1): 40 x the nine bundles, plus 39 heads and the layer-0 router
-    chain_bytes = T * L * (nb["ffn"] + nb["route"] // 2)
-    chain_gbs = chain_bytes / (ms_chain * 1e-3) / 1e9
-    log("engine, %d-layer stack: %d tokens in %.3f ms -> %.1f tok/s, %.1f GB/s"
-        % (L, T, ms_chain, tok_s, chain_gbs))
+        extras = {}
+        if not args.no_extras:
+            pc_us, gu_ms = per_call_path(B, torch, spec, table, layers, tokens, args.per_call_steps,
+                                         wl, hip)
+            log("per-call path: %.2f us/step; its gate/up kernel %.2f us" % (pc_us * 1e3, gu_ms * 1e3))
+            extras["per_call_path"] = {"us_per_step": round(pc_us * 1e3, 3),
+                                       "gateup_kernel_us": round(gu_ms * 1e3, 3)}
+            extras["batched"] = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
+            extras["prerouter_mlp_head"] = head_mlp_path(B, torch, wl)
+            extras["sigmoid_group_routing"] = sigmoid_group_path(B, torch)
+            extras["merge_vs_unmerged"] = merge_retention_path(B, torch, wl)
+            extras["host_tier"] = None if args.no_tier else tier_path(B, torch, T=args.tier_tokens)
 
-    # ---- the per-call path, for comparison ----
-    pc_us, gu_ms = per_call_path(B, torch, spec, table, layers, tokens, args.per_call_steps, wl, hip)
-    log("per-call path: %.2f us/step; its gate/up kernel %.2f us" % (pc_us * 1e3, gu_ms * 1e3))
-
-    batched = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
-    head_mlp = head_mlp_path(B, torch, wl)
-    sigmoid_group = sigmoid_group_path(B, torch)
-    merge_retention = merge_retention_path(B, torch, wl)
-
-    tier_res = None if args.no_tier else tier_path(B, torch, T=args.tier_tokens)
-
-    cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
-    out = {
-        "metric": METRIC,
-        "value": round(gbs, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": W,
-        "ms_per_step": round(ms_step, 6),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic (seeded int4 g64 experts, fp16 LoRA / router / head, N(0,1) tokens)",
-        "config": {
-            "workload": "moe35b decode layer at batch 1: d 2048, 256 experts top-8 + 1 shared, "
-                        "I 512, int4 g64 + fp16 (s,z), LoRA r16 on gate/up/down, router + "
-                        "prerouter fp16 [256x2048]; single-token steps rotating over %d resident "
-                        "layers" % L,
-            "tokens": K,
-            "bytes_per_step": nb["step"],
-        },
-        "pct_peak_hbm": round(100.0 * gbs / PEAK_HBM_GBS, 2),
-        "schedule": "one single-token step per team of 16 workgroups in flight (16 at once); "
-                    "each step reads its weights for its own token",
-        "latency_schedule": {"us_per_step": round(ms_lat / K * 1e3, 3), "GB_s": round(lat_gbs, 1),
-                             "frac_hbm": round(lat_gbs / PEAK_HBM_GBS, 4)},
-        "stack": {
-            "workload": "%d-layer stack of the moe35b layer, %d autoregressive tokens, "
-                        "prediction-as-routing" % (L, T),
-            "tokens_per_s": round(tok_s, 1),
-            "ms_per_token": round(ms_chain / T, 5),
-            "GB_s": round(chain_gbs, 1),
-        },
-        "batched": batched,
-        "prerouter_mlp_head": head_mlp,
-        "sigmoid_group_routing": sigmoid_group,
-        "merge_vs_unmerged": merge_retention,
-        "host_tier": tier_res,
-        "per_call_path": {"us_per_step": round(pc_us * 1e3, 3),
-                          "gateup_kernel_us": round(gu_ms * 1e3, 3)},
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "tokens_kernel (persistent; %d single-token layer steps per launch, 16 "
-                      "in flight)" % K,
-            "achieved": round(gbs, 2),
-            "peak": PEAK_HBM_GBS,
+        cpu = None if args.no_cpu_baseline else cpu_baseline(wl, L)
+        out = {
+            "metric": METRIC,
+            "value": round(chain_gbs, 2),
             "unit": "GB/s",
-            "frac": round(gbs / PEAK_HBM_GBS, 4),
-            "traffic": measured_traffic(K),
-            "traffic_source": TRAFFIC_PROFILE,
-            "bytes_per_launch": nb["step"] * K,
-            "mean_launch_us": round(ms_total * 1e3, 3),
-        },
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(out), flush=True)
+            "n_gpus": 1,
+            "steps": K,
+            "warmup": W,
+            "ms_per_step": round(ms_chain / K, 6),
+            "higher_is_better": True,
+            "scaling": "weak",
+            "vs_baseline": None,
+            "dtype": "int4/f16->f32",
+            "dtype_detail": "int4 g64 weights with fp16 (scale, zero); fp16 x; fp32 h; the int4 "
+                            "codes meet fp16 activations in v_dot2_f32_f16; fp32 accumulate",
+            "data": "synthetic (seeded int4 g64 experts, fp16 LoRA / router / head / mixing, "
+                    "N(0,1) token draws)",
+            "config": {
+                "workload": "moe35b 40-layer stack, batch-1 autoregressive decode: d 2048, 256 "
+                            "experts top-8 + 1 shared, I 512, int4 g64 + fp16 (s,z), LoRA r16 on "
+                            "gate/up/down, router + prerouter head fp16 [256x2048] per layer, "
+                            "prediction-as-routing, residual mixing in place of attention; "
+                            "one step = one token through all %d layers" % L,
+                "layers": L,
+                "tokens": K,
+                "bytes_per_launch": c_bytes,
+            },
+            "tokens_per_s": round(tok_s, 1),
+            "us_per_layer_step": round(us_layer, 3),
+            "pct_peak_hbm": round(100.0 * chain_gbs / PEAK_HBM_GBS, 2),
+            "roofline": {
+                "bound": "hbm",
+                "kernel": "engine_kernel, decode chain (one cooperative launch of %d tokens x %d "
+                          "layers)" % (K, L),
+                "achieved": round(chain_gbs, 2),
+                "peak": PEAK_HBM_GBS,
+                "unit": "GB/s",
+                "frac": round(chain_gbs / PEAK_HBM_GBS, 4),
+                "traffic": measured_traffic(K),
+                "traffic_source": TRAFFIC_PROFILE,
+                "bytes_per_launch": c_bytes,
+                "mean_launch_us": round(ms_chain * 1e3, 3),
+            },
+            "latency_schedule": {
+                "what": "independent single-token steps of the 35B-class layer, one at a time on "
+                        "the whole chip, own routing every step, rotating over %d layers" % L,
+                "us_per_step": round(ms_lat / N * 1e3, 3), "GB_s": round(lat_gbs, 1),
+                "frac_hbm": round(lat_gbs / PEAK_HBM_GBS, 4), "steps": N},
+            "concurrent_independent_steps": {
+                "what": "the same steps with 16 in flight (one per team of 16 workgroups); "
+                        "not a batch-1 figure: a decode chain cannot overlap its tokens",
+                "us_per_step": round(ms_tok / N * 1e3, 3), "GB_s": round(tok_gbs, 1),
+                "frac_hbm": round(tok_gbs / PEAK_HBM_GBS, 4), "steps": N},
+            "cpu_baseline": cpu,
+        }
+        out.update(extras)
+        print(json.dumps(out), flush=True)
+    finally:
+        # every library object released here, in order, while the runtime is up
+        torch.cuda.synchronize()
+        table.close()
+        del layers, arr
+        torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

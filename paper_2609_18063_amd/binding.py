@@ -7,6 +7,7 @@ missing, loading fails with ``ImportError``: there is no fallback path.
 """
 
 import ctypes
+import sys
 import os
 
 import numpy as np
@@ -234,7 +235,10 @@ class SlotTable:
             _check(lib().moe_slot_table_destroy(self.handle), "moe_slot_table_destroy")
             self.handle = None
 
-    def __del__(self):
+    def __del__(self, _finalizing=sys.is_finalizing):
+        # no runtime calls while the interpreter shuts down: close() explicitly
+        if _finalizing():
+            return
         try:
             self.close()
         except Exception:
@@ -280,7 +284,10 @@ class SlotPolicy:
             lib().moe_slot_policy_destroy(self.handle)
             self.handle = None
 
-    def __del__(self):
+    def __del__(self, _finalizing=sys.is_finalizing):
+        # no runtime calls while the interpreter shuts down: close() explicitly
+        if _finalizing():
+            return
         try:
             self.close()
         except Exception:
@@ -342,7 +349,10 @@ class Stager:
             lib().moe_stager_destroy(self.handle)
             self.handle = None
 
-    def __del__(self):
+    def __del__(self, _finalizing=sys.is_finalizing):
+        # no runtime calls while the interpreter shuts down: close() explicitly
+        if _finalizing():
+            return
         try:
             self.close()
         except Exception:

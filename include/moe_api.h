@@ -229,6 +229,25 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* spec, const moe_slot_table* t
                              void* stream);
 
 /*
+ * The same computation as moe_expert_ffn_int4_lora (same kernels, same
+ * results bit for bit), for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation. There is no workspace argument: the intermediate values live in
+ * a static device array of MOE_NOALLOC_SCRATCH_BYTES per GPU, which the library
+ * holds until the process ends (its address on each device is looked up once,
+ * at the first call on that device). The call allocates nothing and frees
+ * nothing. A call whose workspace layout (moe_workspace_bytes(spec, T)) exceeds
+ * the array returns MOE_ENOMEM before any work is enqueued. Every call on one
+ * GPU shares that GPU's array: calls that overlap (other streams, other host
+ * threads) race, so order them on one stream. Nothing in the array has to
+ * start at zero: each call writes every value before it reads it.
+ */
+#define MOE_NOALLOC_SCRATCH_BYTES (4u << 20)
+int moe_expert_ffn_int4_lora_noalloc(const moe_layer_spec* spec, const moe_slot_table* table,
+                                     int layer, const void* x_f16, int T, const int32_t* idx,
+                                     float* y_experts, uint32_t* status_dev, void* stream);
+
+/*
  * Batched decode / prefill experts (Sec. 3.1, Executor paths: the whole-layer
  * path serves prefill; Math contract: every path gives the same outputs).
  * Same inputs, outputs and status behaviour as moe_expert_ffn_int4_lora, for

@@ -90,6 +90,9 @@ SIGNATURES = {
     "moe_expert_ffn_int4_lora": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int, c_void_p,
                                          c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                          c_void_p]),
+    "moe_expert_ffn_int4_lora_noalloc": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int,
+                                                 c_void_p, c_int, c_void_p, c_void_p, c_void_p,
+                                                 c_void_p]),
     "moe_expert_ffn_grouped_int4_lora": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_int,
                                                  c_void_p, c_int, c_void_p, c_void_p, c_void_p,
                                                  c_void_p, c_size_t, c_void_p]),
@@ -437,6 +440,18 @@ def expert_ffn(spec, table, layer, x, idx, y_experts, status, workspace, stream=
                                           _ptr(idx), _ptr(y_experts), _ptr(status), _ptr(workspace),
                                           workspace.numel() * workspace.element_size(),
                                           _stream(stream)), "moe_expert_ffn_int4_lora")
+
+
+MOE_NOALLOC_SCRATCH_BYTES = 4 << 20
+
+
+def expert_ffn_noalloc(spec, table, layer, x, idx, y_experts, status, stream=None):
+    """``expert_ffn`` without a workspace: the library's static per-device scratch."""
+    T = x.shape[0]
+    _check(lib().moe_expert_ffn_int4_lora_noalloc(ctypes.byref(spec), table.handle, layer, _ptr(x),
+                                                  T, _ptr(idx), _ptr(y_experts), _ptr(status),
+                                                  _stream(stream)),
+           "moe_expert_ffn_int4_lora_noalloc")
 
 
 def expert_ffn_grouped(spec, table, layer, x, idx, y_experts, status, workspace, stream=None):

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -74,6 +75,29 @@ thread_local void* g_prof_engine_ts = nullptr;
 template <typename T>
 T* at(void* base, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
+// Scratch of moe_expert_ffn_int4_lora_noalloc: one array per device, resident
+// until the process ends. Host code never passes `scratch` itself (on the host
+// it names a stand-in, not device memory): it passes the device address that
+// hipGetSymbolAddress returns for the current device, looked up once per device.
+__device__ __align__(256) char scratch[MOE_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_of_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return MOE_EINVAL;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MOE_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MOE_OK;
 }
 
 }  // namespace
@@ -364,6 +388,21 @@ int moe_expert_ffn_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, i
   ProfArm arm = g_prof_ffn;
   g_prof_ffn = ProfArm{};
   return from_hip(moe::launch_ffn(a, T, static_cast<hipStream_t>(stream), arm.start, arm.stop));
+}
+
+int moe_expert_ffn_int4_lora_noalloc(const moe_layer_spec* s, const moe_slot_table* t, int layer,
+                                     const void* x_f16, int T, const int32_t* idx, float* y_experts,
+                                     uint32_t* status_dev, void* stream) {
+  int rc = moe_spec_check(s);
+  if (rc != MOE_OK) return rc;
+  if (T < 0) return MOE_EINVAL;
+  if (T == 0) return MOE_OK;
+  if (ws_layout(s, T).total > MOE_NOALLOC_SCRATCH_BYTES) return MOE_ENOMEM;
+  void* ws = nullptr;
+  rc = scratch_of_current_device(&ws);
+  if (rc != MOE_OK) return rc;
+  return moe_expert_ffn_int4_lora(s, t, layer, x_f16, T, idx, y_experts, status_dev, ws,
+                                  MOE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int moe_expert_ffn_grouped_int4_lora(const moe_layer_spec* s, const moe_slot_table* t, int layer,

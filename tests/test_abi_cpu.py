@@ -237,3 +237,16 @@ def test_file_pool_records(tmp_path):
     fp.drop_page_cache()
     fp.remove()
     assert not os.path.exists(fp.path)
+
+
+def test_noalloc_ffn_rejects_sizes_beyond_its_scratch(B):
+    """The no-allocation expert entry point refuses, before any runtime call,
+    a token count whose workspace layout exceeds its static scratch."""
+    spec = B.spec_from_workload(synth.WORKLOADS["moe35b"])
+    big = 1
+    while B.workspace_bytes(spec, big) <= B.MOE_NOALLOC_SCRATCH_BYTES:
+        big *= 2
+    assert big > 16              # the scratch holds at least 16 tokens of the 35B-class layer
+    rc = B.lib().moe_expert_ffn_int4_lora_noalloc(ctypes.byref(spec), None, 0, None, big, None,
+                                                  None, None, None)
+    assert rc == B.MOE_ENOMEM

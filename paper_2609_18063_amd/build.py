@@ -8,6 +8,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmoe.so")
 SOURCES = ["moe_api.hip", "moe_kernels.hip", "moe_engine.hip", "moe_engine_tokens.hip",
+           "moe_engine_pipe.hip",
            "moe_grouped.hip", "moe_stager.hip", "moe_head.hip", "moe_merge.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -3,6 +3,7 @@
 // and kernel launches.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -555,8 +556,24 @@ int moe_engine_supported(const moe_layer_spec* s) {
 
 static constexpr size_t kEngineCtlBytes = 256;
 
+// the chain on two alternating halves of the chip (same device rule as moe_engine_supported)
+static int engine_pipe_supported(const moe_layer_spec* s) {
+  if (moe_spec_check(s) != MOE_OK || s->routing != MOE_ROUTING_SOFTMAX_TOPK) return MOE_EINVAL;
+  if (!moe::engine_pipe_supported(s->d_model, s->d_expert, s->lora_rank, s->top_k, s->n_shared,
+                                  s->n_experts))
+    return MOE_EINVAL;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_EHIP;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return MOE_EHIP;
+  return cus == 256 ? MOE_OK : MOE_EINVAL;
+}
+
 // exchange words of the engine's schedule for a.mode (fills a's offsets)
 static size_t engine_words(const moe_layer_spec* s, int n_layers, moe::EngineArgs* a) {
+  if (a->mode == 3)
+    return moe::engine_pipe_workspace_words(s->n_experts, s->d_model, s->d_expert, s->lora_rank,
+                                            s->top_k + s->n_shared, n_layers, a);
   if (a->mode == 2)
     return moe::engine_tokens_workspace_words(s->n_experts, s->d_model, s->d_expert, s->lora_rank,
                                               s->top_k + s->n_shared, a);
@@ -569,7 +586,9 @@ size_t moe_engine_workspace_bytes(const moe_layer_spec* s, int n_layers) {
   const size_t w0 = engine_words(s, n_layers, &a);
   a.mode = 2;
   const size_t w2 = engine_words(s, n_layers, &a);
-  return kEngineCtlBytes + (w0 > w2 ? w0 : w2) * 8;
+  a.mode = 3;
+  const size_t w3 = engine_words(s, n_layers, &a);
+  return kEngineCtlBytes + std::max(w0, std::max(w2, w3)) * 8;
 }
 
 int moe_engine_tokens_supported(const moe_layer_spec* s) {
@@ -586,7 +605,8 @@ int moe_engine_tokens_supported(const moe_layer_spec* s) {
 
 static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n_table_layers,
                          moe::EngineArgs& a, void* ws, size_t ws_bytes, void* stream) {
-  int rc = a.mode == 2 ? moe_engine_tokens_supported(s) : moe_engine_supported(s);
+  int rc = a.mode == 2 ? moe_engine_tokens_supported(s)
+                       : (a.mode == 3 ? engine_pipe_supported(s) : moe_engine_supported(s));
   if (rc != MOE_OK) return rc;
   if (!t || !ws || !a.layers || !a.xi) return MOE_EINVAL;
   if (!t->dev) return MOE_EINVAL;
@@ -617,6 +637,9 @@ static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n
   if (a.mode == 2)
     return from_hip(moe::launch_engine_tokens(a, s->d_model, s->d_expert, s->lora_rank,
                                               static_cast<hipStream_t>(stream)));
+  if (a.mode == 3)
+    return from_hip(moe::launch_engine_pipe(a, s->d_model, s->d_expert, s->lora_rank,
+                                            static_cast<hipStream_t>(stream)));
   return from_hip(moe::launch_engine(a, s->d_model, s->d_expert, s->lora_rank,
                                      static_cast<hipStream_t>(stream)));
 }
@@ -668,7 +691,8 @@ int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,
   if ((long long)n_tokens * n_layers > (1LL << 30)) return MOE_EINVAL;
   if (n_tokens == 0) return MOE_OK;
   moe::EngineArgs a{};
-  a.mode = 1;
+  // the two-half pipeline where the shape allows it, else the whole-chip chain
+  a.mode = engine_pipe_supported(s) == MOE_OK ? 3 : 1;
   a.n_steps = n_tokens * n_layers;
   a.L = n_layers;
   a.first_token = first_token;

@@ -7,7 +7,8 @@ namespace moe {
 
 struct EngineArgs {
   int mode;          // 0: independent single-token steps; 1: decode chain;
-                     // 2: independent steps, one per team in flight
+                     // 2: independent steps, one per team in flight;
+                     // 3: decode chain on two alternating halves of the chip
   int n_steps;
   int L;             // chain: layers per token
   int first_token;   // chain: token index of the first step
@@ -49,5 +50,12 @@ hipError_t launch_engine(EngineArgs& a, int d, int I, int r, hipStream_t st);
 bool engine_tokens_supported(int d, int I, int r, int K, int S, int E);
 size_t engine_tokens_workspace_words(int E, int d, int I, int r, int n_list, EngineArgs* a);
 hipError_t launch_engine_tokens(EngineArgs& a, int d, int I, int r, hipStream_t st);
+
+// Decode chain on two alternating halves of the chip (moe_engine_pipe.hip):
+// one half computes a layer while the other loads its next layer's experts.
+// Uses the offsets xo/xs of logr, av, hv, part, rv, logh and pred.
+bool engine_pipe_supported(int d, int I, int r, int K, int S, int E);
+size_t engine_pipe_workspace_words(int E, int d, int I, int r, int n_list, int L, EngineArgs* a);
+hipError_t launch_engine_pipe(EngineArgs& a, int d, int I, int r, hipStream_t st);
 
 }  // namespace moe

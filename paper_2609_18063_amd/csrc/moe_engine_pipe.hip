@@ -143,23 +143,25 @@ struct PShape {
   static constexpr int RPI = 64 / LPR;                       // gate/up rows per wave instruction
   static constexpr int CPL = D / 32 / LPR;                   // 16-byte code chunks per lane and row
   static constexpr int NGW = (2 * RMX / RPI + NWV - 1) / NWV;  // gate/up instructions per wave
-  static constexpr int DR = D / NM;                          // down rows per workgroup (one per lane)
-  static constexpr int CPRX = GXX / 32;                      // most 32-column chunks per down row
+  static constexpr int GXG = NLX * IE;                       // most rows of a step (h entries)
   static constexpr int NAX = (NSEGX * 2 * R + NM - 1) / NM;  // LoRA-A (gate/up) rows per workgroup
-  static constexpr int NADX = (NSEGX * R + NM - 1) / NM;     // A_down rank rows per workgroup
+  static constexpr int NAP = (NLX * R + NWGG - 1) / NWGG;    // A_down rank rows per workgroup
   static constexpr int HRX = (EX + NWGG - 1) / NWGG;         // router / head rows per workgroup
-  static constexpr int RR = D / NWGG;                        // reducer rows per workgroup
+  static constexpr int RR = D / NWGG;                        // output rows per workgroup
+  // down rows: an instruction covers RPD rows of one expert, CPE lanes (32 columns each) per row
+  static constexpr int CPE = IE / 32;
+  static constexpr int RPD = 64 / CPE < RR ? 64 / CPE : RR;
+  static constexpr int NDW = (NLX * (RR / RPD) + NWV - 1) / NWV;  // down instructions per wave
   static constexpr int MDN = D / NT;                         // residual entries per thread
   static constexpr int MAXI_R = (D + NPT - 1) / NPT;
-  static constexpr int MAXI_H = (GXX / 2 + NPT - 1) / NPT;
+  static constexpr int MAXI_H = (GXG / 2 + NPT - 1) / NPT;
   static constexpr int MAXI_A = (NSEGX * 2 * R + NPT - 1) / NPT;
   static constexpr int MAXI_E = (EX + NPT - 1) / NPT;
-  static constexpr int NRED = RR * NXG + NXG * NSEGX * R;    // words a reducer polls
-  static constexpr int MAXI_P = (NRED + NPT - 1) / NPT;
-  static constexpr int TPR = NT / RR < 64 ? NT / RR : 64;    // reducer threads per row
-  static constexpr int NCW = (CPRX + NWV - 1) / NWV;         // down chunks per wave
-  static_assert(D % NT == 0 && D % NWGG == 0 && IE % 64 == 0 && IE <= 512 && DR <= 64, "shape");
-  static_assert(NAX <= NWV && HRX <= NWV && NADX <= NWV, "rows per wave");
+  static constexpr int MAXI_D = (NLX * R + NPT - 1) / NPT;
+  static constexpr int TPR = NT / RR < 64 ? NT / RR : 64;    // threads per output row (B_down term)
+  static_assert(D % NT == 0 && D % NWGG == 0 && IE % 64 == 0 && IE <= 2048 && CPE <= 64, "shape");
+  static_assert(RR % RPD == 0, "whole down instructions");
+  static_assert(NAX <= NWV && HRX <= NWV && NAP <= NWV, "rows per wave");
   static_assert(RMX * 8 <= NT, "eight threads per gate/up row pair");
   static_assert(EX <= 256 && HRX <= 2 && NLX <= 10, "routing");
   static_assert(TPR >= 8 && (TPR & (TPR - 1)) == 0 && TPR <= 64, "reducer threads");
@@ -170,30 +172,20 @@ struct PShape {
   static constexpr int O_HD = O_RT + kb(HRX * D * 2);          // [HRX][D] head rows
   static constexpr int O_BGU = O_HD + kb(HRX * D * 2);         // [2 RMX][R] fp16 LoRA-B (gate, up)
   static constexpr int O_GS = O_BGU + kb(2 * RMX * R * 2);     // [2 RMX][D / 64] (scale, zero) of gate/up
-  static constexpr int O_AD = O_GS + kb(2 * RMX * (D / 64) * 4);  // [NADX][IE] fp16 A_down rank rows
-  static constexpr int O_BD = O_AD + kb(NADX * IE * 2);        // [RR][NLX][R] fp16 B_down rows
-  // down codes [chunk][row] and their (scale, zero) [group][row]; one spare
-  // entry per chunk / group row keeps the transposing writes free of bank conflicts
-  static constexpr int DQS = DR * 16 + 16;                     // bytes per chunk
-  static constexpr int DSS = DR * 4 + 4;                       // bytes per group
-  static constexpr int NDU = (DR * CPRX + NT - 1) / NT;        // down code pieces per thread
-  static constexpr int NDZ = (DR * CPRX / 2 + NT - 1) / NT;    // down (scale, zero) words per thread
-  static constexpr int O_DQ = O_BD + kb(RR * NLX * R * 2);
-  static constexpr int O_DS = O_DQ + (CPRX * DQS + 15) / 16 * 16;
-  static constexpr int O_XH = O_DS + (CPRX / 2 * DSS + 15) / 16 * 16;  // [D] fp16 x
+  static constexpr int O_AD = O_GS + kb(2 * RMX * (D / 64) * 4);  // [NAP][IE] fp16 A_down rank rows
+  static constexpr int O_BD = O_AD + kb(NAP * IE * 2);         // [RR][NLX][R] fp16 B_down rows
+  static constexpr int O_XH = O_BD + kb(RR * NLX * R * 2);     // [D] fp16 x
   static constexpr int O_XQ = O_XH + D * 2;                    // [D] fp16 x, pair order
   static constexpr int O_R = O_XQ + D * 2;                     // [D] fp32 residual in
   static constexpr int O_R1 = O_R + D * 4;                     // [D] fp32 residual after mixing
-  static constexpr int O_HX = O_R1 + D * 4;                    // [GXX] fp16 h of the XCD
-  static constexpr int O_HQ = O_HX + GXX * 2;                  // [GXX] fp16 the same h, pair order
-  static constexpr int O_HS = O_HQ + GXX * 2;                  // [CPRX] fp32 sums of 32-column chunks of h
-  static constexpr int O_CW = O_HS + CPRX * 4;                 // [CPRX] fp32 combine weight of each chunk
-  static constexpr int O_GXU = O_CW + CPRX * 4;                // [2 RMX] fp32 raw gate, up
+  static constexpr int O_HX = O_R1 + D * 4;                    // [GXG] fp16 h of the step
+  static constexpr int O_HQ = O_HX + GXG * 2;                  // [GXG] fp16 the same h, pair order
+  static constexpr int O_HI = O_HQ + GXG * 2;                  // [RMX] int: segment and adapter flags of a row pair
+  static constexpr int O_GXU = O_HI + RMX * 4;                 // [2 RMX] fp32 raw gate, up
   static constexpr int O_AV = O_GXU + 2 * RMX * 4;             // [NSEGX][2R] fp32 LoRA-A products
-  static constexpr int O_DP = O_AV + NSEGX * 2 * R * 4;        // [NWV][64] fp32 down partials per wave
-  static constexpr int O_AS = O_DP + NWV * 64 * 4;             // [NLX][R] fp32 A_down h per expert
-  static constexpr int O_YL = O_AS + NLX * R * 4;              // [NRED] fp32 reducer inputs
-  static constexpr int O_LG = O_YL + NRED * 4;                 // [256] fp32 logits
+  static constexpr int O_DP = O_AV + NSEGX * 2 * R * 4;        // [NLX][RR] fp32 weighted down rows per expert
+  static constexpr int O_YL = O_DP + NLX * RR * 4;             // [NLX][R] fp32 A_down h per expert
+  static constexpr int O_LG = O_YL + NLX * R * 4;              // [256] fp32 logits
   static constexpr int O_TK = O_LG + 256 * 4;                  // top-k scratch
   static constexpr int TK_BYTES = 256 * 8 + 256 * 4 + 128 * 8 + 32 * 8;
   static constexpr int O_GR = O_TK + TK_BYTES;                 // [NWV][NGW][64] fp32 gate/up lane partials
@@ -229,7 +221,6 @@ struct alignas(16) Route {
 struct Misc {
   Route rt[2];       // by (step >> 1) & 1: the step being computed, the next one of the half
   int nseg, abort, px, pm;
-  int kseg[16][3];   // per list position: reducer-input offsets of its A_down h (-1: none)
   Seg seg[NXG][4];   // segments of the four XCDs of the half
   int nsegx[NXG];
   int pidx[32];
@@ -243,11 +234,10 @@ struct Src {
   const uint8_t* gus[2 * SH::RMX];  // their (scale, zero) rows
   const uint8_t* bgu[2 * SH::RMX];  // their LoRA-B rows
   const uint8_t* ar[SH::NAX];       // LoRA-A rows of gate / up
-  const uint8_t* dq[SH::CPRX];      // down codes of 32-column chunk ch at the workgroup's first row
-  const uint8_t* dsz[SH::CPRX];     // their (scale, zero)
-  const uint8_t* ad[SH::NADX];      // A_down rank rows (segment columns only)
-  int adn[SH::NADX];                // their 16-byte pieces (the segment's columns / 8)
-  const uint8_t* bd[SH::NLX];       // B_down of list position k at the reducer's first row
+  const uint8_t* dq[SH::NLX];       // down codes of list position k at the workgroup's first output row
+  const uint8_t* dz[SH::NLX];       // their (scale, zero)
+  const uint8_t* bd[SH::NLX];       // B_down of list position k at the first output row
+  const uint8_t* ad[SH::NAP];       // A_down rank rows of the workgroup's (expert, rank) pairs
 };
 
 constexpr int kProfMarks = 24;
@@ -285,17 +275,13 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   const uint32_t* gsm = reinterpret_cast<const uint32_t*>(smem + SH::O_GS);
   __half* adm = reinterpret_cast<__half*>(smem + SH::O_AD);
   __half* bdm = reinterpret_cast<__half*>(smem + SH::O_BD);
-  char* dqm = smem + SH::O_DQ;
-  char* dsm = smem + SH::O_DS;
   __half* xh = reinterpret_cast<__half*>(smem + SH::O_XH);
   __half* xq = reinterpret_cast<__half*>(smem + SH::O_XQ);
   float* rr0 = reinterpret_cast<float*>(smem + SH::O_R);
   float* rr1 = reinterpret_cast<float*>(smem + SH::O_R1);
   __half* hx = reinterpret_cast<__half*>(smem + SH::O_HX);
   __half* hq = reinterpret_cast<__half*>(smem + SH::O_HQ);
-  float* hsum = reinterpret_cast<float*>(smem + SH::O_HS);
-  float* cwl = reinterpret_cast<float*>(smem + SH::O_CW);
-  float* adsum = reinterpret_cast<float*>(smem + SH::O_AS);
+  int* hinfo = reinterpret_cast<int*>(smem + SH::O_HI);
   float* gxu = reinterpret_cast<float*>(smem + SH::O_GXU);
   float* av = reinterpret_cast<float*>(smem + SH::O_AV);
   float* dp = reinterpret_cast<float*>(smem + SH::O_DP);
@@ -336,7 +322,7 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   const int GX = n_list * IE / NXG;
   const int RM = GX / NM;
   const int NGI = 2 * RM / SH::RPI;   // gate/up instructions of the workgroup
-  const int CPR = GX / 32;
+  const int NDI = n_list * (SH::RR / SH::RPD);  // down instructions of the workgroup
   const uint32_t base = ld_u32(&apx->ctl[0]);
 
   if (tx < NXG) {  // segments of XCD tx of the half
@@ -351,15 +337,6 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
       col += len;
     }
     mi->nsegx[xx] = n;
-  }
-  __syncthreads();
-  if ((int)tx < n_list) {  // where the reducer finds A_down h of list position k
-    const int k = tx;
-    int n = 0;
-    for (int xx = 0; xx < NXG; ++xx)
-      for (int q = 0; q < mi->nsegx[xx]; ++q)
-        if (mi->seg[xx][q].k == k && n < 3) mi->kseg[k][n++] = SH::RR * NXG + (xx * SH::NSEGX + q) * R;
-    for (; n < 3; ++n) mi->kseg[k][n] = -1;
   }
   __syncthreads();
   const int nseg = __builtin_amdgcn_readfirstlane(mi->nsegx[xg]);
@@ -436,8 +413,13 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   // Source table of routing Rt (every thread; LDS only); the caller's barrier follows.
   const uint8_t* const dummy = reinterpret_cast<const uint8_t*>(apx->xi);
   auto fill_src = [&](const Route& Rt) {
-    const int nrow = 2 * RM, ncol = CPR;
-    const int n_all = nrow + SH::NAX + ncol + SH::NADX + SH::NLX;
+    if (tx < RM) {  // row pair tx: segment (bits 0-7), resolved (8), gate (9) and up (10) adapters
+      const int q = row_seg(m * RM + tx), kl = sg[q].k;
+      const int ok = Rt.ok[kl] ? 1 : 0;
+      hinfo[tx] = q | (ok << 8) | ((ok && Rt.lg[kl]) << 9) | ((ok && Rt.lu[kl]) << 10);
+    }
+    const int nrow = 2 * RM;
+    const int n_all = nrow + SH::NAX + SH::NLX + SH::NAP;
     for (int k = tx; k < n_all; k += NT) {
       if (k < nrow) {
         const int lr = m * RM + (k < RM ? k : k - RM);
@@ -470,47 +452,37 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
         continue;
       }
       kk -= SH::NAX;
-      if (kk < ncol) {  // down chunk kk: the XCD's columns [32 kk, 32 kk + 32)
-        const int col = kk * 32, q = row_seg(col), kl = sg[q].k;
-        const uint8_t *p = dummy, *ps = dummy;
-        if (Rt.ok[kl]) {
-          const int ec = sg[q].i0 + (col - sg[q].col0);
-          p = reinterpret_cast<const uint8_t*>(Rt.b(kl).down.q) + (size_t)(m * SH::DR) * (IE / 2) + ec / 2;
-          ps = reinterpret_cast<const uint8_t*>(Rt.b(kl).down.sz) + (size_t)(m * SH::DR) * (IE / 16) +
-               (ec / 64) * 4;
+      if (kk < SH::NLX) {  // list position kk: down rows, their scales and B_down at the first output row
+        const size_t j0 = (size_t)gw * SH::RR;
+        const uint8_t *p = dummy, *pz = dummy, *pb = dummy;
+        if (kk < n_list && Rt.ok[kk]) {
+          const moe_proj& dn = Rt.b(kk).down;
+          p = reinterpret_cast<const uint8_t*>(dn.q) + j0 * (IE / 2);
+          pz = reinterpret_cast<const uint8_t*>(dn.sz) + j0 * (IE / 16);
+          if (Rt.ld[kk]) pb = reinterpret_cast<const uint8_t*>(dn.lora_b) + j0 * R * 2;
         }
         S->dq[kk] = p;
-        S->dsz[kk] = ps;
+        S->dz[kk] = pz;
+        S->bd[kk] = pb;
         continue;
       }
-      kk -= ncol;
-      if (kk < SH::NADX) {  // A_down rank row of pair m + NM kk of the XCD's (segment, rank) pairs
-        const int pr = m + NM * kk;
+      kk -= SH::NLX;
+      {  // A_down rank row of pair gw + NWGG kk of the step's (expert, rank) pairs
+        const int pr = gw + NWGG * kk;
         const uint8_t* p = dummy;
-        int n8 = 1;
-        if (pr < nseg * R) {
-          const int q = pr / R, rr = pr % R, kl = sg[q].k;
-          if (Rt.ok[kl] && Rt.ld[kl]) {
-            p = reinterpret_cast<const uint8_t*>(Rt.b(kl).down.lora_a) + ((size_t)rr * IE + sg[q].i0) * 2;
-            n8 = sg[q].len / 8;
-          }
+        if (pr < n_list * R) {
+          const int k = pr / R, rr = pr % R;
+          if (Rt.ok[k] && Rt.ld[k]) p = reinterpret_cast<const uint8_t*>(Rt.b(k).down.lora_a) + (size_t)rr * IE * 2;
         }
         S->ad[kk] = p;
-        S->adn[kk] = n8;
-        continue;
-      }
-      kk -= SH::NADX;
-      {  // B_down of list position kk at this reducer's first row
-        const uint8_t* p = dummy;
-        if (kk < n_list && Rt.ok[kk] && Rt.ld[kk])
-          p = reinterpret_cast<const uint8_t*>(Rt.b(kk).down.lora_b) + (size_t)(gw * SH::RR) * R * 2;
-        S->bd[kk] = p;
       }
     }
   };
 
   // ---- weights held in registers between the staging and the step ----------
   U4 gq[SH::NGW][SH::CPL];
+  U4 dq[SH::NDW];        // down codes: instruction j of this wave, this lane's row and chunk
+  uint32_t dz[SH::NDW];  // their (scale, zero)
   __half mixd[SH::MDN];  // mixing scales
   int mixp[SH::MDN];     // mixing permutation
 #pragma unroll
@@ -518,15 +490,19 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
 #pragma unroll
     for (int cc = 0; cc < SH::CPL; ++cc) gq[j][cc] = U4{0, 0, 0, 0};
 #pragma unroll
+  for (int j = 0; j < SH::NDW; ++j) {
+    dq[j] = U4{0, 0, 0, 0};
+    dz[j] = 0;
+  }
+#pragma unroll
   for (int q = 0; q < SH::MDN; ++q) {
     mixd[q] = __ushort_as_half(0);
     mixp[q] = 0;
   }
 
-  // Expert weights of the routing whose source table is filled: gate/up codes
-  // into registers, the rest into LDS. Every wave issues its loads; the down
-  // codes and scales are then written to LDS transposed (chunk-major), which
-  // waits for them.
+  // Expert weights of the routing whose source table is filled: gate/up and
+  // down codes into registers, the rest into LDS. Every wave issues its
+  // loads; nothing waits here.
   auto stage_experts = [&]() {
 #pragma unroll
     for (int j = 0; j < SH::NGW; ++j) {
@@ -540,25 +516,16 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
         }
       }
     }
-    // down codes and scales: read row by row (consecutive threads, consecutive
-    // pieces of a row), written transposed to LDS once they arrive (below)
-    U4 dv[SH::NDU];
-    uint32_t zv[SH::NDZ];
-    const int ndu = SH::DR * CPR, ndz = SH::DR * (CPR / 2);
+    // down rows: instruction di = j NWV + wave covers rows of expert di / (RR / RPD);
+    // lane: row rg RPD + lane / CPE, 32-column chunk lane % CPE
 #pragma unroll
-    for (int q = 0; q < SH::NDU; ++q) {
-      const int u = q * NT + (int)tx;
-      if (u < ndu) {
-        const int row = u / CPR, c = u - row * CPR;
-        dv[q] = ldw16(S->dq[c] + (size_t)row * (IE / 2));
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < SH::NDZ; ++q) {
-      const int u = q * NT + (int)tx;
-      if (u < ndz) {
-        const int row = u / (CPR / 2), g = u - row * (CPR / 2);
-        zv[q] = ldw4(S->dsz[2 * g] + (size_t)row * (IE / 16));
+    for (int j = 0; j < SH::NDW; ++j) {
+      const int di = j * NWV + wave;
+      if (di < NDI && lane < SH::RPD * SH::CPE) {
+        const int k = di / (SH::RR / SH::RPD), rg = di % (SH::RR / SH::RPD);
+        const int row = rg * SH::RPD + lane / SH::CPE, c = lane % SH::CPE;
+        dq[j] = ldw16(S->dq[k] + (size_t)row * (IE / 2) + c * 16);
+        dz[j] = ldw4(S->dz[k] + (size_t)row * (IE / 16) + (c >> 1) * 4);
       }
     }
     constexpr int GSP = D / 64 * 4 / 16;  // 16-byte pieces of a gate/up (scale, zero) row
@@ -575,10 +542,9 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
       const int i = b * 64 + lane, ii = i < SH::NAX * (D / 8) ? i : 0;
       dma16(S->ar[ii / (D / 8)] + (ii % (D / 8)) * 16, arow + b * 512);
     }
-    for (int b = wave; b * 64 < SH::NADX * (IE / 8); b += NWV) {  // [NADX][IE] A_down rank rows
-      const int i = b * 64 + lane, ii = i < SH::NADX * (IE / 8) ? i : 0;
-      const int row = ii / (IE / 8), pc = ii % (IE / 8);  // pieces past the segment re-read piece 0
-      dma16(S->ad[row] + (pc < S->adn[row] ? pc : 0) * 16, adm + b * 512);
+    for (int b = wave; b * 64 < SH::NAP * (IE / 8); b += NWV) {  // [NAP][IE] A_down rank rows
+      const int i = b * 64 + lane, ii = i < SH::NAP * (IE / 8) ? i : 0;
+      dma16(S->ad[ii / (IE / 8)] + (ii % (IE / 8)) * 16, adm + b * 512);
     }
     {  // [RR][NLX][R] B_down rows of the reducer: piece i = (jr NLX + k) BCH + c
       constexpr int nbd = SH::RR * SH::NLX * BCH;
@@ -586,22 +552,6 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
         const int i = b * 64 + lane, ii = i < nbd ? i : 0;
         const int c = ii % BCH, jk = ii / BCH, k = jk % SH::NLX, jr = jk / SH::NLX;
         dma16(S->bd[k] + (size_t)jr * R * 2 + c * 16, bdm + b * 512);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < SH::NDU; ++q) {
-      const int u = q * NT + (int)tx;
-      if (u < ndu) {
-        const int row = u / CPR, c = u - row * CPR;
-        *reinterpret_cast<U4*>(dqm + c * SH::DQS + row * 16) = dv[q];
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < SH::NDZ; ++q) {
-      const int u = q * NT + (int)tx;
-      if (u < ndz) {
-        const int row = u / (CPR / 2), g = u - row * (CPR / 2);
-        *reinterpret_cast<uint32_t*>(dsm + g * SH::DSS + row * 4) = zv[q];
       }
     }
   };
@@ -693,6 +643,18 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
       __syncthreads();
     } else {
       uint64_t* rv = X + apx->xo_rv + (size_t)((s - 1) & 1) * apx->xs_rv;
+      // The half usually arrives here well before the other half's output:
+      // one thread first watches one word of it (lightly), so that 128
+      // workgroups do not poll the whole vector while the other half's
+      // exchanges are in flight; then every word is polled.
+      if (tx == 0) {
+        long spin = 0;
+        while ((uint32_t)(ld_tag(rv + gw * SH::RR) >> 32) != tag - 1u && ++spin < kSpinMax) {
+          if ((spin & 63) == 0 && ld_u32(&apx->ctl[2])) break;
+          __builtin_amdgcn_s_sleep(8);
+        }
+      }
+      __syncthreads();
       if (!poll_all<SH::MAXI_R>(D, tag - 1u, [&](int i) { return rv + i; },
                                 [&](int i, uint32_t v) { rr0[i] = __uint_as_float(v); }, apx->ctl, apx->status,
                                 &mi->abort))
@@ -795,7 +757,6 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
       if (apx->idx_rec) apx->idx_rec[(size_t)s * K + tx] = Rt.idx[tx];
       if (apx->w_rec) apx->w_rec[(size_t)s * K + tx] = Rt.w[tx];
     }
-    if ((int)tx < CPR) cwl[tx] = Rt.wl[sg[row_seg(tx * 32)].k];
     mark(s, 3);
 
     // ---- S2: LoRA-A rows of gate/up (published first), head rows ---------------
@@ -948,18 +909,19 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
                               &mi->abort))
       break;
     mark(s, 5);
-    uint64_t* HV = X + apx->xo_hv + ((size_t)grp * NXG + xg) * apx->xs_hv;
+    uint64_t* HV = X + apx->xo_hv + (size_t)grp * apx->xs_hv;  // h of the step's rows, in pairs
     {
       const int i = tx >> 3, kl8 = tx & 7;
       float hv = 0.f;
       if (i < RM) {
-        const int lr = m * RM + i;
-        const int q = row_seg(lr), kl = sg[q].k;
-        const bool ok = Rt.ok[kl], lgg = ok && Rt.lg[kl], lgu = ok && Rt.lu[kl];
+        const int info = hinfo[i];
+        const int q = info & 0xff;
+        const bool ok = (info >> 8) & 1, lgg = (info >> 9) & 1, lgu = (info >> 10) & 1;
         float sgt = 0.f, sut = 0.f;
+#pragma unroll
         for (int kk = kl8; kk < R; kk += 8) {
-          if (lgg) sgt = fmaf(__half2float(bgu[(size_t)i * R + kk]), av[q * 2 * R + kk], sgt);
-          if (lgu) sut = fmaf(__half2float(bgu[(size_t)(RM + i) * R + kk]), av[q * 2 * R + R + kk], sut);
+          sgt = fmaf(__half2float(bgu[(size_t)i * R + kk]), av[q * 2 * R + kk], sgt);
+          sut = fmaf(__half2float(bgu[(size_t)(RM + i) * R + kk]), av[q * 2 * R + R + kk], sut);
         }
         sgt = group_sum(sgt, 8);
         sut = group_sum(sut, 8);
@@ -969,14 +931,15 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
           hv = silu(gg) * uu;
         }
       }
-      // rows 2i' and 2i' + 1 share a word; the odd row's value is 8 lanes up
-      const float hn = __shfl_down(hv, 8, 64);
+      // rows 2i' and 2i' + 1 share a word; the odd row's value is 8 lanes up (same 16-lane row)
+      const float hn = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(hv), 0x108, 0xf, 0xf, true));
       if (i < RM && kl8 == 0 && (i & 1) == 0) {
         const uint32_t w = (uint32_t)__half_as_ushort(__float2half_rn(hv)) |
                            ((uint32_t)__half_as_ushort(__float2half_rn(hn)) << 16);
-        st_word(HV + (m * RM + i) / 2, tag, w);
+        st_word(HV + (xg * GX + m * RM + i) / 2, tag, w);
       }
     }
+    mark(s, 13);
     // ahead wave: the next step's routing words and slots
     int pf_slot = -1;
     bool pf_ok = false;
@@ -994,8 +957,8 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
       }
     }
 
-    // ---- S5: h of the XCD -> A_down h of this workgroup's pairs ---------------
-    if (!poll_all<SH::MAXI_H>(GX / 2, tag, [&](int i) { return HV + i; },
+    // ---- S5: h of the step (all experts) -> A_down h of this workgroup's pairs ---
+    if (!poll_all<SH::MAXI_H>(n_list * IE / 2, tag, [&](int i) { return HV + i; },
                               [&](int i, uint32_t v) {
                                 reinterpret_cast<uint32_t*>(hx)[i] = v;
                                 reinterpret_cast<uint16_t*>(hq)[pair_pos(2 * i)] = (uint16_t)v;
@@ -1004,14 +967,6 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
                               apx->ctl, apx->status, &mi->abort))
       break;
     mark(s, 6);
-    if ((int)tx < CPR) {  // sums of h over each 32-column chunk (the zero-point term)
-      const uint32_t* hw = reinterpret_cast<const uint32_t*>(hx) + tx * 16;
-      const hv2 one2 = {(_Float16)1.0f, (_Float16)1.0f};
-      float acc = 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, hw[i]), one2, acc, false);
-      hsum[tx] = acc;
-    }
     if (pf_ok) {  // ahead wave: the next step's bundles, in flight during the down rows
       const StepInfo fn = sinfo(sn);
       const int q = lane / 6, c = lane % 6;
@@ -1021,16 +976,16 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
         src = reinterpret_cast<const char*>(apx->bundles + (size_t)fn.N * apx->n_slots + sq) + 16 * c;
       dma16(src, Rn.bd);
     }
-    uint64_t* ADX = X + apx->xo_adp + ((size_t)grp * NXG + xg) * apx->xs_adp;
-    if (wave < SH::NADX) {  // pair m + NM wave: A_down rank row rr of segment q, dot h
-      const int pr = m + NM * wave;
-      if (pr < nseg * R) {
-        const int q = pr / R, kl = sg[q].k;
+    uint64_t* ADX = X + apx->xo_adp + (size_t)grp * apx->xs_adp;  // A_down h, [list position][rank]
+    if (wave < SH::NAP) {  // pair gw + NWGG wave: rank row rr of expert k's A_down, dot its h
+      const int pr = gw + NWGG * wave;
+      if (pr < n_list * R) {
+        const int k = pr / R;
         float acc = 0.f;
-        if (Rt.ok[kl] && Rt.ld[kl]) {
-          for (int c8 = lane; c8 * 8 < sg[q].len; c8 += 64) {
+        if (Rt.ok[k] && Rt.ld[k]) {
+          for (int c8 = lane; c8 * 8 < IE; c8 += 64) {
             const U4 a8 = *reinterpret_cast<const U4*>(adm + (size_t)wave * IE + c8 * 8);
-            const U4 h8 = *reinterpret_cast<const U4*>(hx + sg[q].col0 + c8 * 8);
+            const U4 h8 = *reinterpret_cast<const U4*>(hx + (size_t)k * IE + c8 * 8);
             acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, a8.x), __builtin_bit_cast(hv2, h8.x), acc, false);
             acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, a8.y), __builtin_bit_cast(hv2, h8.y), acc, false);
             acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, a8.z), __builtin_bit_cast(hv2, h8.z), acc, false);
@@ -1041,124 +996,79 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
         if (lane == 0) st_word(ADX + pr, tag, __float_as_uint(acc));
       }
     }
-
-    __syncthreads();
     mark(s, 12);
-    // ---- S6: down rows of the XCD's columns: lane = row, waves split the chunks --
-    // (the LDS reads of the next chunk are issued before the current chunk's products)
+
+    // ---- S6: this workgroup's output rows over every expert's columns ---------------
+    // (codes in registers; the lane's h chunk read in pair order; CPE lanes per row)
     {
-      const int rl = lane < SH::DR ? lane : 0;
-      U4 cw[SH::NCW];
-      uint32_t szw[SH::NCW];
-      float hsc[SH::NCW], wsc[SH::NCW];
+      const hv2 one2 = {(_Float16)1.0f, (_Float16)1.0f};
+      const int rsub = lane / SH::CPE, c = lane % SH::CPE;
 #pragma unroll
-      for (int i = 0; i < SH::NCW; ++i) {
-        const int c0 = wave + NWV * i;
-        const int c = c0 < CPR ? c0 : 0;
-        cw[i] = *reinterpret_cast<const U4*>(dqm + c * SH::DQS + rl * 16);
-        szw[i] = *reinterpret_cast<const uint32_t*>(dsm + (c >> 1) * SH::DSS + rl * 4);
-        hsc[i] = hsum[c];
-        wsc[i] = c0 < CPR ? cwl[c] : 0.f;
-      }
-      auto load_h = [&](int i, U4 (&hv)[4]) {  // h of the wave's chunk i, pair order (broadcast reads)
-        const int c0 = wave + NWV * i;
-        const U4* hsrc = reinterpret_cast<const U4*>(hq + (c0 < CPR ? c0 : 0) * 32);
+      for (int j = 0; j < SH::NDW; ++j) {
+        const int di = j * NWV + wave;
+        if (di < NDI) {
+          const int k = di / (SH::RR / SH::RPD), rg = di % (SH::RR / SH::RPD);
+          const float wk = Rt.wl[k];  // uniform
+          if (wk != 0.f) {
+            const U4* hsrc = reinterpret_cast<const U4*>(hq + (size_t)k * IE + c * 32);
+            const uint32_t wd[4] = {dq[j].x, dq[j].y, dq[j].z, dq[j].w};
+            float da = 0.f, db = 0.f, hsum = 0.f;
 #pragma unroll
-        for (int g8 = 0; g8 < 4; ++g8) hv[g8] = hsrc[g8];
-      };
-      U4 hcur[4], hnext[4];
-      load_h(0, hcur);
-      float acc = 0.f;
-#pragma unroll
-      for (int i = 0; i < SH::NCW; ++i) {
-        if (i + 1 < SH::NCW) load_h(i + 1, hnext);
-        const uint32_t wd[4] = {cw[i].x, cw[i].y, cw[i].z, cw[i].w};
-        float da = 0.f, db = 0.f;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint32_t w8 = wd[k] >> 8;
-          const U4 hk = hcur[k];
-          da = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, wd[k] & 0x000F000Fu), __builtin_bit_cast(hv2, hk.x),
-                                      da, false);
-          db = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, wd[k] & 0x00F000F0u), __builtin_bit_cast(hv2, hk.y),
-                                      db, false);
-          da = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w8 & 0x000F000Fu), __builtin_bit_cast(hv2, hk.z), da,
-                                      false);
-          db = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w8 & 0x00F000F0u), __builtin_bit_cast(hv2, hk.w), db,
-                                      false);
+            for (int g8 = 0; g8 < 4; ++g8) {
+              const U4 hk = hsrc[g8];
+              const uint32_t w8 = wd[g8] >> 8;
+              da = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, wd[g8] & 0x000F000Fu), __builtin_bit_cast(hv2, hk.x),
+                                          da, false);
+              db = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, wd[g8] & 0x00F000F0u), __builtin_bit_cast(hv2, hk.y),
+                                          db, false);
+              da = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w8 & 0x000F000Fu), __builtin_bit_cast(hv2, hk.z), da,
+                                          false);
+              db = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, w8 & 0x00F000F0u), __builtin_bit_cast(hv2, hk.w), db,
+                                          false);
+              hsum = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, hk.x), one2, hsum, false);
+              hsum = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, hk.y), one2, hsum, false);
+              hsum = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, hk.z), one2, hsum, false);
+              hsum = __builtin_amdgcn_fdot2(__builtin_bit_cast(hv2, hk.w), one2, hsum, false);
+            }
+            const float d = fmaf(db, 0.0625f, da);
+            const float2 sz = h2f2(dz[j]);
+            float v = (sz.x * 16777216.f) * d + sz.y * hsum;
+            v = group_sum(v, SH::CPE);
+            if (c == 0 && rsub < SH::RPD) dp[k * SH::RR + rg * SH::RPD + rsub] = wk * v;
+          } else if (c == 0 && rsub < SH::RPD) {
+            dp[k * SH::RR + rg * SH::RPD + rsub] = 0.f;
+          }
         }
-        const float d = fmaf(db, 0.0625f, da);
-        const float2 sz = h2f2(szw[i]);
-        const float v = (sz.x * 16777216.f) * d + sz.y * hsc[i];
-        acc += wsc[i] != 0.f ? wsc[i] * v : 0.f;
-#pragma unroll
-        for (int g8 = 0; g8 < 4; ++g8) hcur[g8] = hnext[g8];
-        __builtin_amdgcn_sched_barrier(0);
       }
-      dp[wave * 64 + lane] = acc;
     }
-    __syncthreads();
     mark(s, 7);
-    // the XCD's partial of the output rows (one thread per row)
-    uint64_t* PART = X + apx->xo_part + (size_t)grp * NXG * apx->xs_part;
-    if ((int)tx < SH::DR) {
-      const int jj = tx;
-      float acc = 0.f;
-#pragma unroll
-      for (int w = 0; w < NWV; ++w) acc += dp[w * 64 + jj];
-      st_word(PART + (size_t)xg * apx->xs_part + m * SH::DR + jj, tag, __float_as_uint(acc));
-    }
     if (pf_ok) {  // ahead wave: the next step's routing, resolved
       dma_wait();
       route_finish(Rn, pf_slot, sn);
     }
     mark(s, 8);
 
-    // ---- S7: reduce: XCD partials + B_down (A_down h) -> residual ---------------
-    // yl: [RR][NXG] partials, then [NXG][NSEGX][R] A_down h of every XCD's segments
-    if (!poll_all<SH::MAXI_P>(
-            SH::NRED, tag,
-            [&](int i) -> uint64_t* {
-              if (i < SH::RR * NXG) return PART + (size_t)(i % NXG) * apx->xs_part + gw * SH::RR + i / NXG;
-              const int jx = i - SH::RR * NXG, xx = jx / (SH::NSEGX * R), pr = jx % (SH::NSEGX * R);
-              return X + apx->xo_adp + ((size_t)grp * NXG + xx) * apx->xs_adp + pr;
-            },
-            [&](int i, uint32_t v) { yl[i] = __uint_as_float(v); }, apx->ctl, apx->status, &mi->abort, [&](int i) {
-              // A_down h words of absent segments are never written: not polled
-              if (i < SH::RR * NXG) return true;
-              const int jx = i - SH::RR * NXG, xx = jx / (SH::NSEGX * R), pr = jx % (SH::NSEGX * R);
-              return pr < mi->nsegx[xx] * R;
-            }))
+    // ---- S7: A_down h of every expert -> B_down term; rows -> residual ----------
+    if (!poll_all<SH::MAXI_D>(n_list * R, tag, [&](int i) { return ADX + i; },
+                              [&](int i, uint32_t v) { yl[i] = __uint_as_float(v); }, apx->ctl, apx->status,
+                              &mi->abort))
       break;
-    if ((int)tx < n_list * R) {  // A_down h of each expert: its segments' sum
-      const int k = tx / R, rr = tx % R;
-      float v = 0.f;
-#pragma unroll
-      for (int n = 0; n < 3; ++n) {
-        const int o = mi->kseg[k][n];
-        if (o >= 0) v += yl[o + rr];
-      }
-      adsum[tx] = v;
-    }
-    __syncthreads();
+    mark(s, 14);
     if ((int)tx < SH::RR * SH::TPR) {
       const int jr = tx / SH::TPR, sub = tx % SH::TPR;
       const int j = gw * SH::RR + jr;
-      // B_down (A_down h) of every expert with a down adapter
+      // B_down (A_down h) of every expert with a down adapter, and the experts' rows
       float acc = 0.f;
       for (int term = sub; term < n_list * R; term += SH::TPR) {
         const int k = term / R, rr = term % R;
-        acc = fmaf(Rt.dsc[k] * __half2float(bdm[((size_t)jr * SH::NLX + k) * R + rr]), adsum[term], acc);
+        acc = fmaf(Rt.dsc[k] * __half2float(bdm[((size_t)jr * SH::NLX + k) * R + rr]), yl[term], acc);
       }
+      for (int k = sub; k < n_list; k += SH::TPR) acc += dp[k * SH::RR + jr];
       acc = group_sum(acc, SH::TPR);
       if (sub == 0) {
-        float y = 0.f;
-#pragma unroll
-        for (int xx = 0; xx < NXG; ++xx) y += yl[jr * NXG + xx];
-        y += acc;
-        const float rn = rr1[j] + y;
+        const float rn = rr1[j] + acc;
         st_word(X + apx->xo_rv + (size_t)(s & 1) * apx->xs_rv + j, tag, __float_as_uint(rn));
-        if (apx->y) apx->y[(size_t)s * D + j] = y;
+        if (apx->y) apx->y[(size_t)s * D + j] = acc;
         if (s + 1 == apx->n_steps) apx->r_state[j] = rn;
       }
     }
@@ -1256,10 +1166,7 @@ static bool fits(int n_list, int I, int E, int K) {
   const int GX = n_list * I / NXG;
   if (GX % (NM * 2) != 0 || (2 * (GX / NM)) % SH::RPI != 0) return false;
   if (max_segments(n_list, I) > SH::NSEGX) return false;
-  // down chunk pairs share a quantization group: segments start on 64-column boundaries
-  for (int x = 0; x < NXG; ++x)
-    if ((x * GX) % I % 64 != 0) return false;
-  return GX / 32 <= SH::CPRX;
+  return true;
 }
 
 }  // namespace pipe
@@ -1279,17 +1186,14 @@ size_t engine_pipe_workspace_words(int E, int d, int I, int r, int n_list, int L
     return o;
   };
   const int NSEGX = 4;
-  const int GXX = n_list * I / pipe::NXG;
   a->xs_logr = (size_t)(E + 31) / 32 * 32;
   a->xo_logr = take(2 * a->xs_logr);  // by half
   a->xs_av = (size_t)NSEGX * 2 * r;
   a->xo_av = take(2 * pipe::NXG * a->xs_av);  // by half and XCD
-  a->xs_hv = (size_t)(GXX / 2 + 31) / 32 * 32;
-  a->xo_hv = take(2 * pipe::NXG * a->xs_hv);
-  a->xs_adp = (size_t)NSEGX * r;  // A_down h of the XCD's segments
-  a->xo_adp = take(2 * pipe::NXG * a->xs_adp);
-  a->xs_part = (size_t)d;
-  a->xo_part = take(2 * pipe::NXG * a->xs_part);
+  a->xs_hv = (size_t)(n_list * I / 2 + 31) / 32 * 32;  // h of a step, two per word
+  a->xo_hv = take(2 * a->xs_hv);                       // by half
+  a->xs_adp = (size_t)(n_list * r + 31) / 32 * 32;     // A_down h of every expert
+  a->xo_adp = take(2 * a->xs_adp);
   a->xs_rv = (size_t)d;
   a->xo_rv = take(2 * a->xs_rv);  // by step parity
   a->xs_logh_layer = (size_t)(E + 31) / 32 * 32;

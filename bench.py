@@ -38,7 +38,7 @@ METRIC = "int4 MoE layer achieved HBM GB/s (% peak) at batch 1; tokens/s, 40-lay
 
 
 # The dominant kernel of the timed step and the sources its counters depend on.
-ENGINE_SOURCES = ("paper_2609_18063_amd/csrc/moe_engine.hip",
+ENGINE_SOURCES = ("paper_2609_18063_amd/csrc/moe_engine_pipe.hip",
                   "paper_2609_18063_amd/csrc/moe_engine.h",
                   "paper_2609_18063_amd/csrc/moe_xchg.h",
                   "paper_2609_18063_amd/csrc/moe_device.h")
@@ -821,8 +821,10 @@ def main():
             "scaling": "weak",
             "vs_baseline": None,
             "dtype": "int4/f16->f32",
-            "dtype_detail": "int4 g64 weights with fp16 (scale, zero); fp16 x; fp32 h; the int4 "
-                            "codes meet fp16 activations in v_dot2_f32_f16; fp32 accumulate",
+            "dtype_detail": "int4 g64 weights with fp16 (scale, zero); fp16 x; h computed in fp32 "
+                            "and rounded once to fp16 for the down projection (|h| < 65504); "
+                            "the int4 codes meet fp16 activations in v_dot2_f32_f16; fp32 "
+                            "accumulate; fp32 residual, fp64 rmsnorm sums",
             "data": "synthetic (seeded int4 g64 experts, fp16 LoRA / router / head / mixing, "
                     "N(0,1) token draws)",
             "config": {
@@ -840,8 +842,9 @@ def main():
             "pct_peak_hbm": round(100.0 * chain_gbs / PEAK_HBM_GBS, 2),
             "roofline": {
                 "bound": "hbm",
-                "kernel": "engine_kernel, decode chain (one cooperative launch of %d tokens x %d "
-                          "layers)" % (K, L),
+                "kernel": "pipe_kernel, decode chain (one cooperative launch of %d tokens x %d "
+                          "layers; each layer step on one half of the chip while the other half "
+                          "loads the next step's experts)" % (K, L),
                 "achieved": round(chain_gbs, 2),
                 "peak": PEAK_HBM_GBS,
                 "unit": "GB/s",

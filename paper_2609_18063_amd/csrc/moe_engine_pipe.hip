@@ -17,17 +17,17 @@
 //   The K routed + S shared experts' intermediate rows lie end to end
 //   (n_list I rows); XCD xg of the half owns GX = n_list I / 4 of them (at
 //   most NSEGX expert segments). Workgroup m of that XCD holds RM = GX / 32
-//   gate/up row pairs in registers, and the down rows [m D/32, (m+1) D/32)
-//   restricted to the XCD's GX columns in LDS (lane order).
+//   gate/up row pairs in registers.
 //   - LoRA-A rows of gate/up: spread over the XCD's workgroups, exchanged in
-//     the XCD; then h = silu(g) u of the workgroup's rows, exchanged in the
-//     XCD rounded once to fp16 (the precision the down products take it in).
-//   - Down rows of the XCD's columns -> the XCD's partial of the output.
-//     The A_down h terms of the XCD's columns (one rank row of one segment
-//     per wave) are published beside it.
-//   - 128 reducers of D/128 rows each add the four XCD partials and the
-//     down adapter's B_down (A_down h), then publish the residual that the
-//     other half reads to start the next layer.
+//     the XCD; then h = silu(g) u of the workgroup's rows, published to the
+//     whole half rounded once to fp16 (the precision the down products take
+//     it in), two rows per exchange word.
+//   - Down: workgroup gw of the half owns the D/128 output rows
+//     [gw D/128, (gw+1) D/128) over every expert's columns (codes in
+//     registers), so no partial sums cross workgroups. The A_down h dots (one
+//     rank row of one expert per wave) are exchanged across the half; each
+//     workgroup adds B_down (A_down h) to its own rows and publishes its slice
+//     of the residual, which the other half reads to start the next layer.
 //
 // Exchange words are {tag, 32-bit payload} written and polled with
 // agent-scope relaxed atomics; the tag is the step index on a counter that
@@ -164,7 +164,7 @@ struct PShape {
   static_assert(NAX <= NWV && HRX <= NWV && NAP <= NWV, "rows per wave");
   static_assert(RMX * 8 <= NT, "eight threads per gate/up row pair");
   static_assert(EX <= 256 && HRX <= 2 && NLX <= 10, "routing");
-  static_assert(TPR >= 8 && (TPR & (TPR - 1)) == 0 && TPR <= 64, "reducer threads");
+  static_assert(TPR >= 8 && (TPR & (TPR - 1)) == 0 && TPR <= 64, "threads per output row");
   static constexpr int kb(int b) { return (b + 1023) / 1024 * 1024; }
   // LDS layout (bytes); DMA regions padded to whole 1 KiB wave copies
   static constexpr int O_AR = 0;                               // [NAX][D] fp16 LoRA-A rows
@@ -350,6 +350,21 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
     if (!apx->phase_ts || tx != 0) return;
     const int slot = gw == 0 ? 0 : (gw == 7 ? 1 : (gw == NWGG - 1 ? 2 : -1));
     if (slot >= 0) apx->phase_ts[((size_t)s * 3 + slot) * kProfMarks + k] = wall_clock64();
+  };
+  // Before a bulk poll: thread p < 128 spins on one word of producer p (the
+  // last word it writes), so that the whole vector is read about once, after
+  // every producer has stored. A timeout here falls through to the bulk poll,
+  // which reports it.
+  auto watch = [&](auto marker, uint32_t tg) {
+    if ((int)tx < NWGG) {
+      const uint64_t* p = marker((int)tx);
+      long spin = 0;
+      while ((uint32_t)(ld_tag(p) >> 32) != tg && ++spin < kSpinMax) {
+        if ((spin & 63) == 0 && ld_u32(&apx->ctl[2])) break;
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    __syncthreads();
   };
   uint64_t* const X = apx->xw;
   auto pred_of = [&](int t, int N) { return X + apx->xo_pred + ((size_t)(t & 1) * apx->L + N) * apx->xs_pred; };
@@ -546,7 +561,7 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
       const int i = b * 64 + lane, ii = i < SH::NAP * (IE / 8) ? i : 0;
       dma16(S->ad[ii / (IE / 8)] + (ii % (IE / 8)) * 16, adm + b * 512);
     }
-    {  // [RR][NLX][R] B_down rows of the reducer: piece i = (jr NLX + k) BCH + c
+    {  // [RR][NLX][R] B_down rows of the workgroup's output rows: piece i = (jr NLX + k) BCH + c
       constexpr int nbd = SH::RR * SH::NLX * BCH;
       for (int b = wave; b * 64 < nbd; b += NWV) {
         const int i = b * 64 + lane, ii = i < nbd ? i : 0;
@@ -644,17 +659,10 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
     } else {
       uint64_t* rv = X + apx->xo_rv + (size_t)((s - 1) & 1) * apx->xs_rv;
       // The half usually arrives here well before the other half's output:
-      // one thread first watches one word of it (lightly), so that 128
-      // workgroups do not poll the whole vector while the other half's
-      // exchanges are in flight; then every word is polled.
-      if (tx == 0) {
-        long spin = 0;
-        while ((uint32_t)(ld_tag(rv + gw * SH::RR) >> 32) != tag - 1u && ++spin < kSpinMax) {
-          if ((spin & 63) == 0 && ld_u32(&apx->ctl[2])) break;
-          __builtin_amdgcn_s_sleep(8);
-        }
-      }
-      __syncthreads();
+      // it watches one word per producer until all have stored (so that 128
+      // workgroups do not poll the whole vector in repeated rounds while the
+      // other half is still at work), then polls every word.
+      watch([&](int p) { return rv + p * SH::RR + SH::RR - 1; }, tag - 1u);
       if (!poll_all<SH::MAXI_R>(D, tag - 1u, [&](int i) { return rv + i; },
                                 [&](int i, uint32_t v) { rr0[i] = __uint_as_float(v); }, apx->ctl, apx->status,
                                 &mi->abort))

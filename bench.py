@@ -680,6 +680,67 @@ def tier_path(B, torch, T=64, L=24, rho=0.5):
     return res
 
 
+# phase marks of the two-half chain engine, in step order
+PHASE_MARKS = [
+    (0, "step start (own codes staged)"),
+    (1, "residual of the previous layer received"),
+    (2, "mixing + rmsnorm -> x (fp16)"),
+    (3, "routing ready (predicted, resolved ahead)"),
+    (4, "gate/up rows done"),
+    (5, "LoRA-A products of the XCD received"),
+    (13, "h of the workgroup's rows published"),
+    (6, "h of the step received (all experts)"),
+    (12, "A_down h dots published"),
+    (7, "down rows done"),
+    (8, "next step's routing resolved (ahead wave)"),
+    (14, "A_down h dots received"),
+    (9, "residual slice published"),
+    (10, "next step's experts staged"),
+    (11, "head prediction flushed"),
+]
+
+
+def phase_profile(B, torch, spec, table, arr, L, wl, T):
+    """Device wall-clock marks of every step of one chain launch of T tokens
+    (workgroups 0, 7 and 127 of the half that runs the step): median time of
+    each mark after the step's start, over steps with t >= 1 and layer >= 1
+    (routed by the prediction) and over the own-routed layer-0 steps."""
+    import synth
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+    r_state = torch.zeros(wl.d, dtype=torch.float32, device="cuda")
+    tok = torch.from_numpy(synth.token_draws(wl, 0, T, stream=1)).cuda()
+    warm = torch.from_numpy(synth.token_draws(wl, 0, 16, stream=2)).cuda()
+    for _ in range(3):
+        chain_launch(B, spec, table, arr, L, warm, r_state, ws, status)
+    torch.cuda.synchronize()
+    n = T * L
+    ts = torch.zeros(n * 3 * 24, dtype=torch.int64, device="cuda")
+    B.profile_arm(B.MOE_PROF_ENGINE_PHASES, ts.data_ptr(), 0)
+    t0 = time.perf_counter()
+    chain_launch(B, spec, table, arr, L, tok, r_state, ws, status)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3
+    assert int(status.item()) == 0, "engine status %d" % int(status.item())
+    a = ts.cpu().numpy().reshape(n, 3, 24).astype(np.int64)
+    out = {"tokens": T, "layers": L, "launch_wall_ms": round(wall_ms, 3), "unit": "us after the step's start",
+           "clock": "device wall clock, 100 MHz"}
+    for label, sel in (("predicted_steps", lambda s: s // L >= 1 and s % L >= 1),
+                       ("own_routed_layer0_steps", lambda s: s // L >= 1 and s % L == 0)):
+        steps = [s for s in range(n - 1) if sel(s)]
+        rows = []
+        for k, name in PHASE_MARKS:
+            v = a[steps, 0, k]
+            ok = v > 0
+            if ok.sum():
+                rows.append({"mark": k, "what": name,
+                             "us": round(float(np.median((v[ok] - a[steps, 0, 0][ok]) * 0.01)), 2)})
+        nxt = (a[[s + 1 for s in steps], 0, 0] - a[steps, 0, 0]) * 0.01
+        out[label] = {"steps": len(steps), "marks": rows,
+                      "next_step_start_us": round(float(np.median(nxt)), 2)}
+    return out
+
+
 def chain_launch(B, spec, table, arr, L, tokens, r_state, ws, status):
     """One engine launch of the decode chain over ``tokens`` from token 0."""
     r_state.zero_()
@@ -710,6 +771,8 @@ def main():
                     help="time the headline chain launch only (for counter runs)")
     ap.add_argument("--only-batched", action="store_true",
                     help="time the batched / prefill path only (for kernel traces)")
+    ap.add_argument("--phase-profile", type=int, default=0, metavar="T",
+                    help="print the phase marks of one chain launch of T tokens and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain device copy of 1 GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -734,6 +797,10 @@ def main():
     hip = Hip()
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
     try:
+        if args.phase_profile:
+            print(json.dumps({"phase_profile": phase_profile(B, torch, spec, table, arr, L, wl,
+                                                             args.phase_profile)}), flush=True)
+            return
         if args.only_batched:
             print(json.dumps({"batched": batched_path(B, torch, spec, table, wl, L)}), flush=True)
             return

@@ -521,10 +521,13 @@ int moe_merge_requantize(const moe_proj* src, int out_dim, int in_dim, int rank,
 /* ---- profiling (not part of the hot path) ------------------------------- */
 #define MOE_PROF_FFN_MAIN 0  /* the expert kernel that streams the gate/up weights */
 #define MOE_PROF_ENGINE_PHASES 1 /* the next decode-engine launch writes, for
-                                    workgroups 0, 7 and 255, the device wall clock
-                                    (wall_clock64) at 24 marks of every step into
-                                    start_event, read as a device uint64 array
-                                    [n_steps][3][24]; stop_event is unused */
+                                    three workgroups of every step (0, 7 and 255
+                                    of the launch; in the two-half decode chain
+                                    0, 7 and 127 of the half that runs the step),
+                                    the device wall clock (wall_clock64) at 24
+                                    marks of the step into start_event, read as
+                                    a device uint64 array [n_steps][3][24];
+                                    stop_event is unused */
 
 /*
  * Arm per-launch timing. For MOE_PROF_FFN_MAIN, the next launch of that

@@ -366,7 +366,11 @@ int moe_engine_layers(const moe_layer_spec* spec, const moe_slot_table* table,
  * and reads its weights for that token alone; a step takes longer than under
  * moe_engine_layers, the sequence of steps less time. Results equal the
  * oracle's to the same tolerance as moe_engine_layers' (fp32 sums in another
- * order, so not bit-identical to it). Shapes: moe_engine_tokens_supported.
+ * order, so not bit-identical to it). Precision: h = silu(g) u is computed in
+ * fp32 and rounded once to fp16 for the down projection (valid while
+ * |h| < 65504; larger values become infinities), whose int4 codes meet it in
+ * fp16 dot products with fp32 accumulation; moe_engine_layers keeps h in
+ * fp32. Shapes: moe_engine_tokens_supported.
  * Same workspace (moe_engine_workspace_bytes) and ordering rules.
  */
 int moe_engine_tokens_supported(const moe_layer_spec* spec);
@@ -390,6 +394,15 @@ int moe_engine_tokens(const moe_layer_spec* spec, const moe_slot_table* table,
  * the mixing, before the layer output is added), idx_rec / w_rec (the
  * routing used) and pidx_rec / pw_rec (the head's prediction) [.][K],
  * y_rec fp32 [.][d] (the layer output).
+ * Schedule: on a 256-CU device, for the layer shapes the two-half schedule
+ * is compiled for (d 2048 / I 512 / r 16 with K + S <= 9 and E <= 256;
+ * d 512 / I 256 / r 8 with K + S <= 2 and E <= 16; the K + S experts' rows
+ * splitting evenly over its 128 workgroups), layer steps alternate between
+ * two halves of the chip (even and odd XCDs): one half computes a layer
+ * while the other loads the experts of its next layer, known a token ahead
+ * from the prediction. There h = silu(g) u is rounded once to fp16 (valid while
+ * |h| < 65504) for the down projection and the down adapter's A product.
+ * Other shapes run the whole-chip engine of moe_engine_layers (h in fp32).
  */
 int moe_engine_chain(const moe_layer_spec* spec, const moe_slot_table* table,
                      const moe_engine_layer* layers, int n_layers, int first_token, int n_tokens,

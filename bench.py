@@ -399,8 +399,11 @@ def merge_retention_path(B, torch, wl, T=8):
     moe_expert_ffn_int4_lora. Weight-level retention from the kernel's per-group
     sums; output-level retention 1 - ||U - M|| / ||U - B|| from the outputs.
     Two adapter sizes: delta entries of std 1e-3 (the paper's figure) and the
-    configuration's (A ~ N(0, 1/r), B ~ N(0, 0.01), scale 2). The merge kernel
-    is timed over the expert's three projections."""
+    configuration's (A ~ N(0, 1/r), B ~ N(0, 0.01), scale 2); each on weights
+    quantized from fp32 N(0, 0.02) masters (the configuration's recipe, and
+    the weights whose retention is comparable with the paper's) and on the
+    codes drawn directly (uniform codes, the synthetic group step). The merge
+    kernel is timed over the expert's three projections."""
     import synth
     out = {}
     dims = {"gate": (wl.I, wl.d), "up": (wl.I, wl.d), "down": (wl.d, wl.I)}
@@ -412,9 +415,12 @@ def merge_retention_path(B, torch, wl, T=8):
     ye = torch.empty(T, 3, wl.d, dtype=torch.float32, device="cuda")
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
     ws = torch.zeros(B.workspace_bytes(spec, T), dtype=torch.uint8, device="cuda")
-    for label, b_std in (("delta_std_1e-3", 1e-3 / (wl.lora_scale * np.sqrt(wl.r) * wl.a_std)),
-                         ("configuration", None)):
-        bundle = synth.bundle(wl, 0, 7, b_std=b_std)
+    b_small = 1e-3 / (wl.lora_scale * np.sqrt(wl.r) * wl.a_std)
+    for label, b_std, quantized in (("quantized_weights_delta_std_1e-3", b_small, True),
+                                    ("quantized_weights_configuration", None, True),
+                                    ("drawn_codes_delta_std_1e-3", b_small, False),
+                                    ("drawn_codes_configuration", None, False)):
+        bundle = synth.bundle(wl, 0, 7, b_std=b_std, quantized=quantized)
         keep, U, M, Bs, merges, weight = [], {}, {}, {}, [], {}
         for p, (o, i) in dims.items():
             U[p], k1 = B.upload_projection(bundle[p], bundle["lora"][p], "cuda")
@@ -741,6 +747,16 @@ def phase_profile(B, torch, spec, table, arr, L, wl, T):
     return out
 
 
+def copy_calibration(torch):
+    """One plain device copy of 1 GiB (reads 1 GiB, writes 1 GiB): the scale of
+    the HBM byte counters."""
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def chain_launch(B, spec, table, arr, L, tokens, r_state, ws, status):
     """One engine launch of the decode chain over ``tokens`` from token 0."""
     r_state.zero_()
@@ -771,6 +787,8 @@ def main():
                     help="time the headline chain launch only (for counter runs)")
     ap.add_argument("--only-batched", action="store_true",
                     help="time the batched / prefill path only (for kernel traces)")
+    ap.add_argument("--only", choices=("merge", "head", "sigmoid", "tier", "per_call"),
+                    help="run one secondary measurement only and print it")
     ap.add_argument("--phase-profile", type=int, default=0, metavar="T",
                     help="print the phase marks of one chain launch of T tokens and exit")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -802,7 +820,24 @@ def main():
                                                              args.phase_profile)}), flush=True)
             return
         if args.only_batched:
-            print(json.dumps({"batched": batched_path(B, torch, spec, table, wl, L)}), flush=True)
+            res = batched_path(B, torch, spec, table, wl, L)
+            if args.copy_calibration:
+                copy_calibration(torch)
+            print(json.dumps({"batched": res}), flush=True)
+            return
+        if args.only:
+            legs = {"merge": lambda: merge_retention_path(B, torch, wl),
+                    "head": lambda: head_mlp_path(B, torch, wl),
+                    "sigmoid": lambda: sigmoid_group_path(B, torch),
+                    "tier": lambda: tier_path(B, torch, T=args.tier_tokens)}
+            if args.only == "per_call":
+                N = args.per_call_steps
+                tokens = torch.from_numpy(synth.token_draws(wl, 0, 2 * N)).cuda()
+                pc_us, gu_ms = per_call_path(B, torch, spec, table, layers, tokens, N, wl, hip)
+                res = {"us_per_step": round(pc_us * 1e3, 3), "gateup_kernel_us": round(gu_ms * 1e3, 3)}
+            else:
+                res = legs[args.only]()
+            print(json.dumps({args.only: res}), flush=True)
             return
 
         # ---- the headline: batch-1 decode of the 40-layer stack --------------
@@ -830,11 +865,7 @@ def main():
             "%.1f GB/s (%.1f%% of HBM)" % (L, K, ms_chain, tok_s, us_layer, chain_gbs,
                                            100 * chain_gbs / PEAK_HBM_GBS))
         if args.copy_calibration:
-            src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-            dst = torch.empty_like(src)
-            dst.copy_(src)                      # reads 1 GiB, writes 1 GiB
-            torch.cuda.synchronize()
-            del src, dst
+            copy_calibration(torch)
         if args.only_chain:
             print(json.dumps({"chain_ms": round(ms_chain, 4), "us_per_layer_step": round(us_layer, 3),
                               "GB_s": round(chain_gbs, 2)}), flush=True)

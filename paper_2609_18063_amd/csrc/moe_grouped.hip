@@ -412,6 +412,18 @@ __global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb
 // gate/up: workgroup (tile, y) takes the gate and up rows of columns
 // [64 y, 64 y + 64): wave w < 4 the gate rows of columns 64 y + 16 w + col,
 // wave w + 4 the up rows of the same columns.
+// Block b of a GEMM grid -> (token tile, column tile). The dispatcher deals
+// blocks to the 8 XCDs in turn, so blocks b and b + 8 share an XCD: every
+// column tile of token tile x gets a block that is congruent to x mod 8, the
+// ny of them 8 apart. The tile's activations (and its row list) then go
+// through one XCD's L2, fetched once instead of once per column tile. The
+// grid is the tile count rounded up to a multiple of 8, times ny.
+__device__ __forceinline__ void tile_of_block(int b, int ny, int& x, int& y) {
+  const int grp = b / (8 * ny), r = b - grp * 8 * ny;
+  x = grp * 8 + (r & 7);
+  y = r >> 3;
+}
+
 __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
   extern __shared__ __attribute__((aligned(16))) char ring[];
   __shared__ __attribute__((aligned(16))) _Float16 la[2][kGroupRows][16];
@@ -424,8 +436,10 @@ __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
   _Float16(*ads)[kGateCols] = reinterpret_cast<_Float16(*)[kGateCols]>(ring + 16384 + kGroupRows * kGateCols * 2);
   static_assert(16384 + (kGroupRows + 16) * kGateCols * 2 <= kRingBytes, "epilogue fits in the ring");
   // (the record is read beside the count; one past the count is never used)
-  const GroupTile tl = a.tiles[blockIdx.x];
-  if ((int)blockIdx.x >= *a.n_tiles) return;
+  int bx, by;
+  tile_of_block(blockIdx.x, a.I / kGateCols, bx, by);
+  const GroupTile tl = a.tiles[bx < a.max_tiles ? bx : 0];
+  if (bx >= *a.n_tiles) return;
   if (tl.slot < 0) return;  // not resident: the down kernel writes zero rows
   const moe_bundle* bd = a.bundles + tl.slot;
   const int tid = threadIdx.x;
@@ -433,7 +447,7 @@ __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
   const int col = lane & 15, kq = lane >> 4;
   const int d = a.d, I = a.I, r = a.r;
   const int mb = (tl.nrows + 15) >> 4;
-  const int c0 = blockIdx.y * kGateCols;        // first column of this workgroup
+  const int c0 = by * kGateCols;                // first column of this workgroup
   const int cc = wave >> 2, wb = wave & 3;      // projection (0 gate, 1 up), column block
   const int i = c0 + wb * 16 + col;             // this lane's gate/up column
   if (tid < kGroupRows) rsrc[tid] = tid < tl.nrows ? a.perm[tl.row0 + tid] / a.n_list : -1;
@@ -533,7 +547,7 @@ __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
       const int row = p >> 4, k = p & 15;
       float s = 0.f;
       for (int c = 0; c < kGateCols; ++c) s = fmaf((float)ads[k][c], (float)hs[row][c], s);
-      a.adp[((size_t)(tl.row0 + row) * (I / kGroupSlab) + blockIdx.y) * 16 + k] = s;
+      a.adp[((size_t)(tl.row0 + row) * (I / kGroupSlab) + by) * 16 + k] = s;
     }
   }
 }
@@ -542,20 +556,22 @@ __global__ void __launch_bounds__(kGT, 4) grouped_down_kernel(GroupedArgs a) {
   extern __shared__ __attribute__((aligned(16))) char ring[];
   __shared__ __attribute__((aligned(16))) _Float16 la[kGroupRows][16];
   __shared__ int ydst[kGroupRows];
-  const GroupTile tl = a.tiles[blockIdx.x];  // (read beside the count, as in gate/up)
-  if ((int)blockIdx.x >= *a.n_tiles) return;
+  int bx, by;
+  tile_of_block(blockIdx.x, a.d / kDownCols, bx, by);
+  const GroupTile tl = a.tiles[bx < a.max_tiles ? bx : 0];  // (read beside the count, as in gate/up)
+  if (bx >= *a.n_tiles) return;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int col = lane & 15, kq = lane >> 4;
   const int d = a.d, I = a.I, r = a.r;
   const int mb = (tl.nrows + 15) >> 4;
-  const int n0 = blockIdx.y * kDownCols + wave * 16 + col;  // this lane's output column
+  const int n0 = by * kDownCols + wave * 16 + col;  // this lane's output column
   if (tid < kGroupRows) ydst[tid] = tid < tl.nrows ? a.perm[tl.row0 + tid] : -1;
   __syncthreads();
   if (tl.slot < 0) {  // not resident: the pair contributes zeros (the miss is reported)
     for (int p = tid; p < tl.nrows * kDownCols; p += kGT) {
       const int row = p / kDownCols, c = p % kDownCols;
-      a.y_experts[(size_t)ydst[row] * d + blockIdx.y * kDownCols + c] = 0.f;
+      a.y_experts[(size_t)ydst[row] * d + by * kDownCols + c] = 0.f;
     }
     return;
   }
@@ -572,8 +588,8 @@ __global__ void __launch_bounds__(kGT, 4) grouped_down_kernel(GroupedArgs a) {
     }
     la[row][k] = (_Float16)v;
   }
-  // weight row w_row (0 .. 255): output column blockIdx.y * 256 + w_row
-  const size_t nbase = (size_t)blockIdx.y * kDownCols;
+  // weight row w_row (0 .. 255): output column by * 256 + w_row
+  const size_t nbase = (size_t)by * kDownCols;
   auto wrow = [&](int w_row) -> const uint8_t* {
     return static_cast<const uint8_t*>(bd->down.q) + (nbase + w_row) * (I / 2);
   };
@@ -643,10 +659,11 @@ hipError_t launch_grouped_ffn(const GroupedArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(grouped_prep_kernel, dim3(xb + a.max_tiles), dim3(kGT), 0, st, a, xb);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(grouped_gateup_kernel, dim3(a.max_tiles, a.I / kGateCols), dim3(kGT), lds_gu, st, a);
+  const int tiles8 = (a.max_tiles + 7) / 8 * 8;
+  hipLaunchKernelGGL(grouped_gateup_kernel, dim3(tiles8 * (a.I / kGateCols)), dim3(kGT), lds_gu, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(grouped_down_kernel, dim3(a.max_tiles, a.d / kDownCols), dim3(kGT), lds_dn, st, a);
+  hipLaunchKernelGGL(grouped_down_kernel, dim3(tiles8 * (a.d / kDownCols)), dim3(kGT), lds_dn, st, a);
   return hipGetLastError();
 }
 

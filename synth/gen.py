@@ -26,6 +26,13 @@ Value distributions:
 * Token draws ``xi [d]`` ~ N(0, 1), fp32 (the layer input is their RMS
   normalization, computed by the code under test).
 * fp32 master weights N(0, 0.02) for the quantizer test.
+* Optionally (``bundle(..., quantized=True)``), expert weights made as the
+  configurations describe them: fp32 N(0, 0.02) masters quantized int4
+  asymmetric per group of 64 inputs (group minimum and maximum in fp32,
+  fp16 ``s = (hi - lo) / 15`` and ``z = lo``, codes ``rint((w - z) / s)``
+  taken in fp32 and clamped to 0..15, code 0 where ``s`` is 0).  This is
+  the recipe of the input data; the arithmetic under test only reads the
+  codes and (s, z) it produces.
 """
 
 import numpy as np
@@ -33,7 +40,7 @@ import numpy as np
 __all__ = [
     "WORKLOADS", "Workload", "rng", "int4_projection", "fp32_weights",
     "lora_pair", "bundle", "router_weights", "token_draws", "zipf_logits",
-    "mixing", "ar1_token_draws", "prerouter_mlp",
+    "mixing", "ar1_token_draws", "prerouter_mlp", "quantized_projection",
 ]
 
 
@@ -86,6 +93,24 @@ def int4_projection(key_q, key_sz, out_dim, in_dim, w_std=0.02):
     return q, s, z
 
 
+def quantized_projection(key, out_dim, in_dim, std=0.02):
+    """fp32 N(0, std) masters of ``key`` quantized int4 per group of 64 inputs
+    (the input recipe above): packed codes ``[out, in/2]``, fp16 s, z."""
+    w = fp32_weights(key, out_dim, in_dim, std).reshape(out_dim, in_dim // 64, 64)
+    lo = w.min(axis=2)
+    hi = w.max(axis=2)
+    s = ((hi - lo) / np.float32(15.0)).astype(np.float16)
+    z = lo.astype(np.float16)
+    s32 = s.astype(np.float32)[:, :, None]
+    z32 = z.astype(np.float32)[:, :, None]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        c = np.rint((w - z32) / s32)
+    c = np.where(s32 == 0, 0.0, c)
+    q = np.clip(c, 0, 15).astype(np.uint8).reshape(out_dim, in_dim)
+    packed = (q[:, 0::2] | (q[:, 1::2] << 4)).astype(np.uint8)
+    return np.ascontiguousarray(packed), s, z
+
+
 def fp32_weights(key, out_dim, in_dim, std=0.02):
     return rng(*key).normal(0.0, std, size=(out_dim, in_dim)).astype(np.float32)
 
@@ -96,15 +121,20 @@ def lora_pair(key_a, key_b, out_dim, in_dim, r, a_std, b_std):
     return a, b
 
 
-def bundle(wl, layer, expert, lora=True, lora_on=("gate", "up", "down"), b_std=None):
+def bundle(wl, layer, expert, lora=True, lora_on=("gate", "up", "down"), b_std=None, quantized=False):
     """Expert ``expert`` of ``layer`` (ids ``E .. E+S-1`` are the shared experts).
     ``b_std`` overrides the workload's std of the LoRA ``B`` entries: the
-    delta ``scale * B A`` then has entries of std ``scale * b_std * sqrt(r) * a_std``."""
+    delta ``scale * B A`` then has entries of std ``scale * b_std * sqrt(r) * a_std``.
+    ``quantized``: weights quantized from fp32 N(0, w_std) masters instead of
+    drawn directly as codes."""
     dims = {"gate": (wl.I, wl.d), "up": (wl.I, wl.d), "down": (wl.d, wl.I)}
     out = {"lora": {}}
     for p, (o, i) in dims.items():
-        out[p] = int4_projection((wl.wid, layer, expert, _T_Q[p]),
-                                 (wl.wid, layer, expert, _T_SZ[p]), o, i, wl.w_std)
+        if quantized:
+            out[p] = quantized_projection((wl.wid, layer, expert, _T_Q[p], 1), o, i, wl.w_std)
+        else:
+            out[p] = int4_projection((wl.wid, layer, expert, _T_Q[p]),
+                                     (wl.wid, layer, expert, _T_SZ[p]), o, i, wl.w_std)
         if lora and p in lora_on:
             out["lora"][p] = lora_pair((wl.wid, layer, expert, _T_A[p]),
                                        (wl.wid, layer, expert, _T_B[p]),

@@ -125,3 +125,19 @@ def test_dequantize_is_exact():
 def test_quantize_rejects_ragged_groups(shape):
     with pytest.raises(ValueError):
         quant.quantize_g64(np.zeros((shape[0], shape[1] + 1), np.float32))
+
+
+def test_input_recipe_quantizer_matches_the_oracle():
+    """The seeded inputs' quantized weights (synth.quantized_projection, the
+    configuration's recipe) carry exactly the codes, scales and zeros of the
+    oracle's quantizer on the same fp32 masters."""
+    import synth
+    for key, (o, i) in (((3, 1, 4), (16, 128)), ((3, 5, 9), (64, 512)), ((7, 0, 2), (8, 2048))):
+        q, s, z = synth.quantized_projection(key, o, i)
+        qo, so, zo = quant.quantize_g64(synth.fp32_weights(key, o, i))
+        un = np.empty((o, i), dtype=np.uint8)
+        un[:, 0::2] = q & 15
+        un[:, 1::2] = q >> 4
+        assert np.array_equal(un, qo)
+        assert np.array_equal(s.view(np.uint16), so.view(np.uint16))
+        assert np.array_equal(z.view(np.uint16), zo.view(np.uint16))

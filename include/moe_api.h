@@ -471,13 +471,17 @@ int moe_stager_create(moe_slot_table* table, const moe_bundle_layout* layout, si
  * the OS page cache). The file at `path` holds [n_layers][n_ids] records of
  * file_stride bytes (>= bundle_bytes); record (layer, e) is the packed bundle
  * of expert e, in the same layout as a pinned host bundle. It is mapped
- * read-only for the stager's lifetime and must not change meanwhile. Each copy
- * reads its record into one of n_bounce (1..16) pinned bounce buffers, split
- * over n_io (1..16) host threads inside moe_stager_stage (page faults read the
- * file, or hit the page cache), then enqueues the host -> slot copy; a bounce
- * buffer is reused after the copy from it has completed. MOE_EINVAL: a bad
- * argument, a file that cannot be opened or is shorter than n_layers * n_ids *
- * file_stride; MOE_ENOMEM: the mapping or the bounce buffers failed.
+ * read-only for the stager's lifetime and must not change meanwhile. The
+ * stager's own I/O thread takes the staged sets in order: each copy reads its
+ * record into one of n_bounce (1..16) pinned bounce buffers, split over n_io
+ * (1..16) host threads (page faults read the file, or hit the page cache),
+ * then enqueues the host -> slot copy on the set's copy_stream; a bounce
+ * buffer is reused after the copy from it has completed. moe_stager_stage
+ * returns once the set is queued; moe_stager_use blocks the calling thread
+ * until the set's copies are enqueued. The stager uses the device that was
+ * current at creation. MOE_EINVAL: a bad argument, a file that cannot be
+ * opened or is shorter than n_layers * n_ids * file_stride; MOE_ENOMEM: the
+ * mapping, the bounce buffers or the thread failed.
  */
 int moe_stager_create_file(moe_slot_table* table, const moe_bundle_layout* layout,
                            size_t bundle_bytes, const char* path, size_t file_stride, int n_bounce,
@@ -485,9 +489,13 @@ int moe_stager_create_file(moe_slot_table* table, const moe_bundle_layout* layou
 int moe_stager_destroy(moe_stager* s);
 /* Stages a set (policy stage), rewrites the layer's slot-table rows on the
  * device and copies each missing bundle host -> slot, all enqueued on
- * copy_stream. Returns the number of copies (copies as in the policy) or an
- * error. A kernel may read a slot only between the use and the release of a
- * set that holds it, so unpinned slots are free to overwrite. */
+ * copy_stream (for the file tier, the copies by the I/O thread). Returns the
+ * number of copies (copies as in the policy) or an error. A kernel may read a
+ * slot only between the use and the release of a set that holds it, so
+ * unpinned slots are free to overwrite. If a copy cannot be enqueued after the
+ * policy took the set, the slots no longer hold what the table says: the
+ * stager is then failed, and this and every later stage and use return
+ * MOE_EHIP. */
 int moe_stager_stage(moe_stager* s, int layer, const int32_t* experts, int n, void* copy_stream,
                      int32_t* copies);
 /* Uses the oldest staged set of the layer: compute_stream waits for that

@@ -21,7 +21,9 @@
 // mapping into one of a ring of pinned bounce buffers (page faults read the
 // file, or hit the page cache), split over a few host threads, then
 // hipMemcpyAsync moves it to the slot; a bounce buffer is reused only after
-// the event recorded behind its copy.
+// the event recorded behind its copy. The reads run on the stager's I/O
+// thread, in the order the sets were staged, so that staging does not hold up
+// the thread that launches the kernels.
 //
 // Policy (the paper leaves it open; the reading is stated once here and in
 // the header): every layer keeps a FIFO of staged-but-unused sets and a FIFO
@@ -39,9 +41,12 @@
 #include <unistd.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
+#include <condition_variable>
 #include <cstring>
 #include <deque>
+#include <mutex>
 #include <new>
 #include <thread>
 #include <vector>
@@ -213,13 +218,37 @@ struct moe_stager {
   int n_bounce = 0, bounce_next = 0, n_io = 1;
   std::vector<hipEvent_t> bounce_ev;
   std::vector<char> bounce_used;
-  int64_t read_ns = 0, read_bytes = 0;
+  std::atomic<int64_t> read_ns{0}, read_bytes{0};
+  // File tier: one I/O thread takes the staged sets in order, reads their
+  // records and issues their copies, so that stage() returns at once and the
+  // launching thread keeps launching. use() waits (on the host) only until
+  // the set's copies are issued, then makes the compute stream wait for them.
+  struct IoJob {
+    int layer = 0;
+    std::vector<int32_t> cp;  // (expert, slot) pairs
+    hipEvent_t ev = nullptr;  // recorded after the set's copies
+    hipStream_t st = nullptr;
+    uint64_t seq = 0;
+  };
+  std::thread io;
+  std::mutex mu;
+  std::condition_variable cv_job, cv_issued;
+  std::deque<IoJob> jobs;
+  uint64_t next_seq = 0, issued = 0;           // sets with seq < issued are issued
+  bool stop = false;
+  std::vector<std::deque<uint64_t>> set_seq;  // [L] FIFO parallel to set_ev (file tier)
+  int device = 0;
+  // A copy could not be issued after the table and the policy had taken the
+  // set: the slots no longer hold what the table says, so every later stage
+  // and use fails with MOE_EHIP.
+  std::atomic<bool> failed{false};
 };
 
 namespace {
 
 constexpr int kRing = 64;
 constexpr size_t kRetire = 32;
+constexpr uint64_t kNoJob = ~(uint64_t)0;  // a set that needed no copy
 
 hipEvent_t take_event(moe_stager* s) {
   if (s->free_ev.size() > kRetire) {
@@ -302,6 +331,7 @@ int create_common(moe_slot_table* table, const moe_bundle_layout* layout, size_t
   if (host_bundles) s->host.assign(host_bundles, host_bundles + nh);
   s->pool = static_cast<char*>(slot_pool);
   s->set_ev.resize(table->n_layers);
+  s->set_seq.resize(table->n_layers);
   int rc = moe_slot_policy_create(table->n_layers, table->n_ids, table->n_slots, &s->policy);
   if (rc != MOE_OK) {
     delete s;
@@ -344,6 +374,50 @@ void read_record(const char* src, char* dst, size_t n, int threads) {
   }
   std::memcpy(dst, src, std::min(part, n));
   for (auto& x : th) x.join();
+}
+
+// File tier, on the I/O thread: record (layer, e) -> a free bounce buffer ->
+// slot `slot` by hipMemcpyAsync on `st`. False if a HIP call failed.
+bool copy_record(moe_stager* s, int layer, int e, int slot, hipStream_t st) {
+  const moe_slot_table* t = s->table;
+  char* dst = s->pool + ((size_t)layer * t->n_slots + slot) * s->slot_stride;
+  const int b = s->bounce_next;
+  s->bounce_next = (b + 1) % s->n_bounce;
+  if (s->bounce_used[b] && hipEventSynchronize(s->bounce_ev[b]) != hipSuccess) return false;
+  char* bb = s->bounce + (size_t)b * s->bounce_stride;
+  const auto t0 = std::chrono::steady_clock::now();
+  read_record(s->map + ((size_t)layer * t->n_ids + e) * s->file_stride, bb, s->bundle_bytes, s->n_io);
+  s->read_ns += std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0)
+                    .count();
+  s->read_bytes += (int64_t)s->bundle_bytes;
+  if (hipMemcpyAsync(dst, bb, s->bundle_bytes, hipMemcpyHostToDevice, st) != hipSuccess ||
+      hipEventRecord(s->bounce_ev[b], st) != hipSuccess)
+    return false;
+  s->bounce_used[b] = 1;
+  return true;
+}
+
+void io_loop(moe_stager* s) {
+  (void)hipSetDevice(s->device);
+  for (;;) {
+    moe_stager::IoJob j;
+    {
+      std::unique_lock<std::mutex> lk(s->mu);
+      s->cv_job.wait(lk, [&] { return s->stop || !s->jobs.empty(); });
+      if (s->jobs.empty()) return;  // stopped, every queued set issued
+      j = std::move(s->jobs.front());
+      s->jobs.pop_front();
+    }
+    bool ok = !s->failed.load();
+    for (size_t i = 0; ok && 2 * i < j.cp.size(); ++i) ok = copy_record(s, j.layer, j.cp[2 * i], j.cp[2 * i + 1], j.st);
+    if (ok && j.ev && hipEventRecord(j.ev, j.st) != hipSuccess) ok = false;
+    {
+      std::lock_guard<std::mutex> lk(s->mu);
+      if (!ok) s->failed = true;
+      s->issued = j.seq + 1;
+    }
+    s->cv_issued.notify_all();
+  }
 }
 
 }  // namespace
@@ -404,19 +478,37 @@ int moe_stager_create_file(moe_slot_table* table, const moe_bundle_layout* layou
       moe_stager_destroy(s);
       return MOE_EHIP;
     }
+  if (hipGetDevice(&s->device) != hipSuccess) {
+    moe_stager_destroy(s);
+    return MOE_EHIP;
+  }
+  try {
+    s->io = std::thread(io_loop, s);
+  } catch (...) {
+    moe_stager_destroy(s);
+    return MOE_ENOMEM;
+  }
   *out = s;
   return MOE_OK;
 }
 
 int moe_stager_io_stats(const moe_stager* s, int64_t* read_ns, int64_t* read_bytes) {
   if (!s || !read_ns || !read_bytes) return MOE_EINVAL;
-  *read_ns = s->read_ns;
-  *read_bytes = s->read_bytes;
+  *read_ns = s->read_ns.load();
+  *read_bytes = s->read_bytes.load();
   return MOE_OK;
 }
 
 int moe_stager_destroy(moe_stager* s) {
   if (!s) return MOE_OK;
+  if (s->io.joinable()) {  // the I/O thread issues every queued set, then leaves
+    {
+      std::lock_guard<std::mutex> lk(s->mu);
+      s->stop = true;
+    }
+    s->cv_job.notify_all();
+    s->io.join();
+  }
   for (auto& q : s->set_ev)
     for (hipEvent_t e : q)
       if (e) (void)hipEventDestroy(e);  // null: a set that needed no copy
@@ -443,6 +535,7 @@ int moe_stager_destroy(moe_stager* s) {
 int moe_stager_stage(moe_stager* s, int layer, const int32_t* experts, int n, void* copy_stream,
                      int32_t* copies) {
   if (!s) return MOE_EINVAL;
+  if (s->failed) return MOE_EHIP;
   std::vector<int32_t> cp((size_t)2 * (n > 0 ? n : 1));
   const int nc = policy_stage(s->policy, layer, experts, n, cp.data());
   if (nc < 0) return nc;
@@ -460,44 +553,37 @@ int moe_stager_stage(moe_stager* s, int layer, const int32_t* experts, int n, vo
   // A set with no copy needs no wait: each of its experts was copied for an
   // earlier set of the layer, whose use (first, in FIFO order) waits for it.
   hipEvent_t ev = nullptr;
-  if (nc > 0 && !(ev = take_event(s))) return MOE_EHIP;
+  if (nc > 0 && !(ev = take_event(s))) {
+    s->failed = true;  // the policy and the table already hold the set
+    return MOE_EHIP;
+  }
   int rc = MOE_OK;
   if (nc > 0) rc = push_rows(s, layer, st);
-  for (int i = 0; i < nc && rc == MOE_OK; ++i) {
-    const int e = cp[2 * i], slot = cp[2 * i + 1];
-    char* dst = s->pool + ((size_t)layer * t->n_slots + slot) * s->slot_stride;
-    const void* src = nullptr;
-    if (s->map) {  // file tier: record -> bounce buffer (host threads) -> slot
-      const int b = s->bounce_next;
-      s->bounce_next = (b + 1) % s->n_bounce;
-      if (s->bounce_used[b] && hipEventSynchronize(s->bounce_ev[b]) != hipSuccess) {
-        rc = MOE_EHIP;
-        break;
-      }
-      char* bb = s->bounce + (size_t)b * s->bounce_stride;
-      const auto t0 = std::chrono::steady_clock::now();
-      read_record(s->map + ((size_t)layer * t->n_ids + e) * s->file_stride, bb, s->bundle_bytes,
-                  s->n_io);
-      s->read_ns += std::chrono::duration_cast<std::chrono::nanoseconds>(
-                        std::chrono::steady_clock::now() - t0)
-                        .count();
-      s->read_bytes += (int64_t)s->bundle_bytes;
-      src = bb;
-      if (hipMemcpyAsync(dst, src, s->bundle_bytes, hipMemcpyHostToDevice, st) != hipSuccess ||
-          hipEventRecord(s->bounce_ev[b], st) != hipSuccess) {
-        rc = MOE_EHIP;
-        break;
-      }
-      s->bounce_used[b] = 1;
-      continue;
+  if (s->map) {  // file tier: the I/O thread reads the records and issues the copies
+    uint64_t seq = kNoJob;
+    if (rc == MOE_OK && nc > 0) {
+      std::lock_guard<std::mutex> lk(s->mu);
+      seq = s->next_seq++;
+      s->jobs.push_back(moe_stager::IoJob{layer, std::vector<int32_t>(cp.begin(), cp.begin() + 2 * nc), ev, st, seq});
     }
-    src = s->host[(size_t)layer * t->n_ids + e];
-    if (hipMemcpyAsync(dst, src, s->bundle_bytes, hipMemcpyHostToDevice, st) != hipSuccess)
-      rc = MOE_EHIP;
+    if (seq != kNoJob) s->cv_job.notify_one();
+    s->set_ev[layer].push_back(ev);
+    s->set_seq[layer].push_back(seq);
+  } else {
+    for (int i = 0; i < nc && rc == MOE_OK; ++i) {
+      const int e = cp[2 * i], slot = cp[2 * i + 1];
+      char* dst = s->pool + ((size_t)layer * t->n_slots + slot) * s->slot_stride;
+      if (hipMemcpyAsync(dst, s->host[(size_t)layer * t->n_ids + e], s->bundle_bytes, hipMemcpyHostToDevice,
+                         st) != hipSuccess)
+        rc = MOE_EHIP;
+    }
+    if (rc == MOE_OK && ev && hipEventRecord(ev, st) != hipSuccess) rc = MOE_EHIP;
+    s->set_ev[layer].push_back(ev);
   }
-  if (rc == MOE_OK && ev && hipEventRecord(ev, st) != hipSuccess) rc = MOE_EHIP;
-  s->set_ev[layer].push_back(ev);
-  if (rc != MOE_OK) return rc;
+  if (rc != MOE_OK) {
+    s->failed = true;
+    return rc;
+  }
   if (copies) std::memcpy(copies, cp.data(), (size_t)2 * nc * sizeof(int32_t));
   s->stats.stages += 1;
   s->stats.copies += nc;
@@ -508,10 +594,20 @@ int moe_stager_stage(moe_stager* s, int layer, const int32_t* experts, int n, vo
 int moe_stager_use(moe_stager* s, int layer, const int32_t* experts, int n, void* compute_stream,
                    int32_t* slots) {
   if (!s) return MOE_EINVAL;
+  if (s->failed) return MOE_EHIP;
   const int rc = policy_use(s->policy, layer, experts, n, slots);
   if (rc != MOE_OK) return rc;
   hipEvent_t ev = s->set_ev[layer].front();
   s->set_ev[layer].pop_front();
+  if (s->map) {  // the set's copies must have been issued (its event recorded)
+    const uint64_t seq = s->set_seq[layer].front();
+    s->set_seq[layer].pop_front();
+    if (seq != kNoJob) {
+      std::unique_lock<std::mutex> lk(s->mu);
+      s->cv_issued.wait(lk, [&] { return s->issued > seq || s->failed; });
+      if (s->failed) return MOE_EHIP;
+    }
+  }
   hipError_t e = hipSuccess;
   if (ev) {
     e = hipStreamWaitEvent(static_cast<hipStream_t>(compute_stream), ev, 0);

@@ -656,6 +656,53 @@ def synth_bundle(wl, n, e):
     return synth.bundle(wl, n, e)
 
 
+def prefill_whole_layer(torch, tier, spec, routers, pool, wl, T=512):
+    """Prefill of T tokens through the 8B tier's layers on the whole-layer path
+    (§3.1, Executor paths): every expert of layer N+1 (64 bundles, one copy of
+    the layer's packed records) is loaded while layer N computes on the other
+    of two device layer buffers; every layer routes itself (grouped experts,
+    MFMA). Beside it: the same prefill with every layer resident (compute
+    only), the time of the layer copies alone, and their overlap."""
+    import synth
+    xi = torch.from_numpy(synth.token_draws(wl, 900, T)).cuda()
+    ex = tier.WholeLayerPrefill(spec, routers, pool)
+    ex.run(xi)                                   # warm-up
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ex.run(xi)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    assert int(ex.status.item()) == 0
+    # the layer copies alone
+    c0 = time.perf_counter()
+    for n in range(pool.n_layers):
+        ex._load(n, n % 2, ex.copy_stream)
+    ex.copy_stream.synchronize()
+    copy_s = time.perf_counter() - c0
+    ex.close()
+    rs = tier.WholeLayerPrefill(spec, routers, pool, resident=True)
+    rs.run(xi)
+    torch.cuda.synchronize()
+    r0 = time.perf_counter()
+    rs.run(xi)
+    torch.cuda.synchronize()
+    compute_s = time.perf_counter() - r0
+    rs.close()
+    overlap = (copy_s + compute_s - wall) / min(copy_s, compute_s)
+    layer_bytes_ = pool.n_ids * pool.stride
+    out = {"tokens": T, "layers": pool.n_layers, "tokens_per_s": round(T / wall, 1),
+           "ms_per_layer": round(wall * 1e3 / pool.n_layers, 3),
+           "compute_only_tokens_per_s": round(T / compute_s, 1),
+           "copy_only_ms_per_layer": round(copy_s * 1e3 / pool.n_layers, 3),
+           "h2d_GB_s": round(layer_bytes_ * pool.n_layers / copy_s / 1e9, 2),
+           "MB_per_layer_load": round(layer_bytes_ / 1e6, 1), "overlap": round(overlap, 3)}
+    log("8B tier prefill, whole-layer path: %.1f tok/s (%.2f ms per layer; compute only %.1f tok/s; "
+        "layer copies alone %.2f ms per layer, %.1f GB/s); overlap %.3f"
+        % (out["tokens_per_s"], out["ms_per_layer"], out["compute_only_tokens_per_s"],
+           out["copy_only_ms_per_layer"], out["h2d_GB_s"], overlap))
+    return out
+
+
 def tier_path(B, torch, T=64, L=24, rho=0.5):
     """The 8B tier with host-tier staging: 24 layers whose 64 experts per
     layer live in pinned host memory, 3 x top-4 device slots per layer; the
@@ -729,6 +776,24 @@ def tier_path(B, torch, T=64, L=24, rho=0.5):
         "adjacent_set_overlap": round(tier.set_overlap(ch.log, L), 3),
     }
     res["file_tier"] = file_res
+    res["prefill_whole_layer"] = prefill_whole_layer(torch, tier, spec, [l["router"] for l in layers],
+                                                     pool, wl)
+    # slot capacity: the slots of a layer are an LRU cache of its experts (the
+    # paper's "hot" set); more slots per layer, fewer misses
+    sweep = {}
+    for ns in (2 * wl.K, 3 * wl.K, 6 * wl.K, 12 * wl.K):
+        chs = tier.TieredChain(spec, layers, pool, ns)
+        torch.cuda.synchronize()
+        s0 = time.perf_counter()
+        chs.run(xi)
+        ws_ = time.perf_counter() - s0
+        assert int(chs.status.item()) == 0
+        sts = chs.stager.stats()
+        chs.close()
+        sweep[ns] = {"tokens_per_s": round(T / ws_, 1), "misses_per_token": round(sts["copies"] / T, 2)}
+    res["slot_capacity_sweep"] = sweep
+    log("8B tier slot capacity (slots per layer: tok/s, misses/token): %s"
+        % {k: (v["tokens_per_s"], v["misses_per_token"]) for k, v in sweep.items()})
     log("8B tier staged: %.1f tok/s, %.2f misses/token, H2D %.1f GB/s, compute-only %.3f ms/token, "
         "overlap %s" % (res["tokens_per_s"], res["misses_per_token"], res["h2d_GB_s"] or 0,
                         res["compute_only_ms_per_token"], res["overlap"]))

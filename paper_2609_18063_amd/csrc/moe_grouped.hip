@@ -62,7 +62,9 @@ inline int gate_sz_bytes(int d) { return kGateRows * (d / 16); }
 inline int down_sz_bytes(int I) { return kDownCols * (I / 16); }
 constexpr int kGateStatic = 2 * kGroupRows * 16 * 2 + kGroupRows * 4;  // la, rsrc
 constexpr int kDownStatic = kGroupRows * 16 * 2 + kGroupRows * 4;      // la, ydst
-constexpr int kLdsMax = 80 * 1024;              // per workgroup: two per CU
+constexpr int kLdsMax = 160 * 1024;             // LDS of a CU: the most one workgroup may take
+// (a launch asks only for what its shape needs: up to 80 KB, two workgroups
+// share a CU; the d 4096 gate/up rows need more, and run one per CU)
 
 __device__ __forceinline__ h2v as_h2(uint32_t u) { return __builtin_bit_cast(h2v, u); }
 __device__ __forceinline__ h8 as_h8(U4 u) { return __builtin_bit_cast(h8, u); }

@@ -341,3 +341,127 @@ def resident_table(spec, pool, layers):
 
 
 __all__ = ["HostPool", "TieredChain", "bundle_layout", "set_overlap", "resident_table"]
+
+
+class WholeLayerPrefill:
+    """Prefill of T tokens through the layers of ``pool`` on the whole-layer
+    path (§3.1, Executor paths; §3.2, Two consumption profiles): every
+    expert of a layer is loaded in one shot, into one of two device layer
+    buffers, while the previous layer computes on the other.
+
+    Per layer N (a prefill routes every layer by its own router; the
+    residual stream of the T tokens stands in for attention):
+    ``x = fp16(rmsnorm(r))``, ``moe_route``, the grouped experts on table
+    layer N mod 2, ``r += combine`` (``moe_combine_add``); ``r`` starts at
+    the token draws. The loads are single host -> device copies of the
+    layer's packed bundles ([n_ids] records of ``stride`` bytes) from the
+    pinned pool, or, for a :class:`FilePool`, the layer's records read from
+    the file into a pinned staging buffer first (the page cache or the disk
+    in front of the copy); the copy of layer N+1 waits for the compute of
+    layer N-1, which last used its buffer.
+
+    ``resident=True`` binds every layer at once to a device copy of the
+    whole pool instead (the comparison the path must match bit for bit).
+    ``routers``: device fp16 [E, d] per layer."""
+
+    def __init__(self, spec, routers, pool, resident=False):
+        self.spec, self.routers, self.pool = spec, routers, pool
+        self.L, self.n_ids = pool.n_layers, pool.n_ids
+        self.resident = resident
+        self.per_layer = self.n_ids * pool.stride
+        nb = self.L if resident else 2
+        self.table = B.SlotTable(nb, self.n_ids, self.n_ids)
+        self.buf = torch.empty(nb * self.per_layer, dtype=torch.uint8, device="cuda")
+        base = self.buf.data_ptr()
+        lay = pool.layout
+
+        def proj(addr, offs):
+            return B.MoeProj(addr + offs[0], addr + offs[1],
+                             (addr + offs[2]) if offs[2] >= 0 else None,
+                             (addr + offs[3]) if offs[3] >= 0 else None)
+
+        for b in range(nb):
+            for e in range(self.n_ids):
+                a = base + b * self.per_layer + e * pool.stride
+                self.table.bind(b, e, e, B.MoeBundle(proj(a, lay.gate), proj(a, lay.up), proj(a, lay.down)))
+        self.table.sync()
+        self.copy_stream = torch.cuda.Stream()      # default priority
+        self.stage = None
+        if isinstance(pool, FilePool):   # two pinned staging buffers, alternating by layer
+            self.stage = [torch.empty(self.per_layer, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+            self.stage_free = [torch.cuda.Event(), torch.cuda.Event()]
+        if resident:
+            for n in range(self.L):
+                self._load(n, n, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+        self.load_ms = []
+
+    def _load(self, n, b, stream):
+        dst = self.buf[b * self.per_layer:(b + 1) * self.per_layer]
+        if self.stage is None:
+            src = self.pool.buf[n * self.per_layer:(n + 1) * self.per_layer]
+        else:
+            sb = n % 2
+            self.stage_free[sb].synchronize()      # the copy out of this staging buffer is done
+            with open(self.pool.path, "rb", buffering=0) as f:
+                f.seek(n * self.per_layer)
+                mv = memoryview(self.stage[sb].numpy())
+                got = 0
+                while got < self.per_layer:
+                    k = f.readinto(mv[got:])
+                    if not k:
+                        raise IOError("short read of layer %d" % n)
+                    got += k
+            src = self.stage[sb]
+        with torch.cuda.stream(stream):
+            dst.copy_(src, non_blocking=True)
+            if self.stage is not None:
+                self.stage_free[n % 2].record(stream)
+
+    def run(self, xi, record=False):
+        """``xi`` device fp32 [T, d] -> final residual [T, d] (and, with
+        ``record``, the per-layer x, idx, w and residual before each layer)."""
+        spec = self.spec
+        T, d = xi.shape
+        K, n = spec.top_k, spec.top_k + spec.n_shared
+        cur = torch.cuda.current_stream()
+        r = xi.clone()
+        x = torch.empty(T, d, dtype=torch.float16, device="cuda")
+        idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
+        w = torch.empty(T, K, dtype=torch.float32, device="cuda")
+        ye = torch.empty(T, n, d, dtype=torch.float32, device="cuda")
+        ws = torch.zeros(B.workspace_bytes(spec, T), dtype=torch.uint8, device="cuda")
+        self.status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        rec = {"x": [], "idx": [], "w": [], "r": []} if record else None
+        loaded = [torch.cuda.Event(), torch.cuda.Event()]
+        freed = [torch.cuda.Event(), torch.cuda.Event()]
+        if not self.resident:
+            self.copy_stream.wait_stream(cur)
+            self._load(0, 0, self.copy_stream)
+            loaded[0].record(self.copy_stream)
+        for N in range(self.L):
+            b = N if self.resident else N % 2
+            if not self.resident:
+                cur.wait_event(loaded[b])
+            if record:
+                rec["r"].append(r.clone())
+            B.rmsnorm_f16(r, x)
+            B.route(spec, x, self.routers[N], idx, w, ws)
+            B.expert_ffn_grouped(spec, self.table, b, x, idx, ye, self.status, ws)
+            B.combine_add(spec, ye, w, r)
+            if record:
+                rec["x"].append(x.clone())
+                rec["idx"].append(idx.clone())
+                rec["w"].append(w.clone())
+            if not self.resident:
+                freed[b].record(cur)
+                if N + 1 < self.L:   # the next layer's load (host read included) while this one computes
+                    if N >= 1:       # its buffer was last read by layer N - 1
+                        self.copy_stream.wait_event(freed[(N + 1) % 2])
+                    self._load(N + 1, (N + 1) % 2, self.copy_stream)
+                    loaded[(N + 1) % 2].record(self.copy_stream)
+        return r, rec
+
+    def close(self):
+        torch.cuda.synchronize()
+        self.table.close()

@@ -392,6 +392,47 @@ def head_mlp_path(B, torch, wl, n_heads=96, hidden=512, calls=192):
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "hidden": hidden, "heads": n_heads}
 
 
+def head_chain_path(B, torch, wl, table, layers, hidden=512, T=12):
+    """The per-call decode chain over the 40-layer stack (HIP-graph replay of
+    each token) with the predictions made by the linear head (moe_preroute)
+    and by the full head (moe_preroute_mlp fed the routing each layer used at
+    this token and the last, i.e. the chain's own predictions)."""
+    import synth
+    from paper_2609_18063_amd import chain as C
+    spec = B.spec_from_workload(wl)
+    L = len(layers)
+    keep, structs = [], []
+    for n in range(L):
+        if n + 1 == L:
+            structs.append(None)
+            continue
+        h = synth.prerouter_mlp(wl, n, hidden)
+        dev = [torch.from_numpy(np.ascontiguousarray(a)).cuda()
+               for a in (h["w1"][:, :wl.d], h["w1"][:, wl.d:].T, h["w2"], h["b1"], h["b2"], h["wl"])]
+        keep.append(dev)
+        structs.append(B.head_mlp(hidden, dev[0], dev[1], dev[2], b1=dev[3], b2=dev[4], w_l=dev[5]))
+    xi = torch.from_numpy(synth.token_draws(wl, 0, T, stream=3)).cuda()
+    out = {"layers": L, "tokens": T, "hidden": hidden}
+    for label, heads in (("linear_head", None), ("full_head", structs)):
+        dc = C.DeviceChain(spec, table, layers, heads_mlp=heads)
+        dc.capture()
+
+        def replay_all():
+            dc.reset()
+            for t in range(T):
+                dc.xi.copy_(xi[t:t + 1])
+                dc.replay_token(t)
+
+        replay_all()
+        ms = time_launch(torch, replay_all)
+        assert int(dc.status.item()) == 0
+        out[label] = {"ms_per_token": round(ms / T, 3), "tokens_per_s": round(T / (ms * 1e-3), 1)}
+        del dc
+    log("per-call chain, 40 layers: linear head %.3f ms/token, full head %.3f ms/token"
+        % (out["linear_head"]["ms_per_token"], out["full_head"]["ms_per_token"]))
+    return out
+
+
 def merge_retention_path(B, torch, wl, T=8):
     """The merged alternative of Sec. 3.3 on one expert of ``wl``: the adapter
     folded into the int4 weights on the device (moe_merge_requantize), then the
@@ -902,7 +943,7 @@ def main():
                     help="time the headline chain launch only (for counter runs)")
     ap.add_argument("--only-batched", action="store_true",
                     help="time the batched / prefill path only (for kernel traces)")
-    ap.add_argument("--only", choices=("merge", "head", "sigmoid", "tier", "per_call"),
+    ap.add_argument("--only", choices=("merge", "head", "head_chain", "sigmoid", "tier", "per_call"),
                     help="run one secondary measurement only and print it")
     ap.add_argument("--phase-profile", type=int, default=0, metavar="T",
                     help="print the phase marks of one chain launch of T tokens and exit")
@@ -942,6 +983,7 @@ def main():
             return
         if args.only:
             legs = {"merge": lambda: merge_retention_path(B, torch, wl),
+                    "head_chain": lambda: head_chain_path(B, torch, wl, table, layers),
                     "head": lambda: head_mlp_path(B, torch, wl),
                     "sigmoid": lambda: sigmoid_group_path(B, torch),
                     "tier": lambda: tier_path(B, torch, T=args.tier_tokens)}
@@ -1017,6 +1059,7 @@ def main():
                                        "gateup_kernel_us": round(gu_ms * 1e3, 3)}
             extras["batched"] = None if args.no_batched else batched_path(B, torch, spec, table, wl, L)
             extras["prerouter_mlp_head"] = head_mlp_path(B, torch, wl)
+            extras["prerouter_mlp_head"]["chain_per_call"] = head_chain_path(B, torch, wl, table, layers)
             extras["sigmoid_group_routing"] = sigmoid_group_path(B, torch)
             extras["merge_vs_unmerged"] = merge_retention_path(B, torch, wl)
             extras["host_tier"] = None if args.no_tier else tier_path(B, torch, T=args.tier_tokens)

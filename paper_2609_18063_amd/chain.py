@@ -10,6 +10,13 @@ is about to use at token t+1.
 
 The attention that precedes every MoE layer in the paper's decoder is
 replaced by the O(d) residual mixing of ``moe_chain_mix_rmsnorm``.
+
+With ``heads_mlp`` the prediction comes from the full prerouter head
+(``moe_preroute_mlp``, §3.2 Head): its input is layer N's x, the experts layer N
+routed to at this token and those at the previous token. At decode those sets
+are themselves the predictions of the head before (prediction-as-routing), so
+the head sees its own chain's predictions rather than the true routing (the
+paper's feature drift).
 """
 
 import torch
@@ -26,7 +33,7 @@ class DeviceChain:
     bound in ``table`` at table layer ``N``.
     """
 
-    def __init__(self, spec, table, layers, consumers=None):
+    def __init__(self, spec, table, layers, consumers=None, heads_mlp=None):
         self.spec, self.table, self.layers = spec, table, layers
         self.L = len(layers)
         self.consumers = set(range(1, self.L)) if consumers is None else set(consumers)
@@ -44,6 +51,15 @@ class DeviceChain:
         self.ye = torch.empty(1, n, d, dtype=torch.float32, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.graphs = {}
+        # full prerouter heads: per layer a moe_head_mlp struct (binding.head_mlp)
+        # or None (the linear head, moe_preroute); the routing each layer used
+        # at the last two tokens, by token parity, is their one-hot input
+        self.heads_mlp = heads_mlp
+        if heads_mlp is not None:
+            hidden = max(h.hidden for h in heads_mlp if h is not None)
+            self.ws_mlp = torch.zeros(B.preroute_mlp_workspace_bytes(spec, hidden, 1), dtype=torch.uint8,
+                                      device=dev)
+            self.used_idx = torch.full((2, self.L, 1, K), -1, dtype=torch.int32, device=dev)
 
     def uses_prediction(self, t, n):
         return t > 0 and n > 0 and n in self.consumers
@@ -61,7 +77,14 @@ class DeviceChain:
             else:
                 B.route(s, self.x, lay["router"], self.own_idx, self.own_w, self.ws)
                 idx, w = self.own_idx, self.own_w
-            if n + 1 < self.L and lay.get("head") is not None:
+            mlp = self.heads_mlp[n] if self.heads_mlp is not None else None
+            if n + 1 < self.L and mlp is not None:
+                nxt = (t + 1) % 2
+                prev = self.used_idx[(t - 1) % 2, n] if t > 0 else None
+                B.preroute_mlp(s, mlp, self.x, idx, prev, self.pred_idx[nxt, n + 1], self.pred_w[nxt, n + 1],
+                               self.ws_mlp)
+                self.used_idx[t % 2, n].copy_(idx)
+            elif n + 1 < self.L and lay.get("head") is not None:
                 nxt = (t + 1) % 2
                 B.preroute(s, self.x, lay["head"], self.pred_idx[nxt, n + 1], self.pred_w[nxt, n + 1],
                            self.ws)
@@ -73,7 +96,7 @@ class DeviceChain:
                 record["x"][t, n].copy_(self.x[0])
                 record["idx"][t, n].copy_(idx[0])
                 record["w"][t, n].copy_(w[0])
-                if n + 1 < self.L and lay.get("head") is not None:
+                if n + 1 < self.L and (lay.get("head") is not None or mlp is not None):
                     nxt = (t + 1) % 2
                     record["pidx"][t, n].copy_(self.pred_idx[nxt, n + 1, 0])
                     record["pw"][t, n].copy_(self.pred_w[nxt, n + 1, 0])

@@ -104,25 +104,26 @@ def oracle_token(dl, xi_row, routing=None):
     return out
 
 
-def check_routing(got_idx, got_w, ref_logits, k, what, stats):
+def check_routing(got_idx, got_w, ref_logits, k, what, stats, tie=NEAR_TIE, w_rtol=2e-6):
     """Routing parity: bit-exact set and order, except where the oracle's
-    K-th and (K+1)-th logits are within NEAR_TIE (counted); order swaps
-    inside the top-K are allowed only between logits within NEAR_TIE."""
+    K-th and (K+1)-th logits are within ``tie`` (NEAR_TIE unless the logits
+    carry a stated precision of their own; counted); order swaps inside the
+    top-K are allowed only between logits within ``tie``."""
     ref_idx, ref_w = o_routing.softmax_topk(ref_logits, k)
     got_idx = np.asarray(got_idx)
     if got_idx.tolist() == ref_idx.tolist():
-        assert np.allclose(got_w, ref_w, rtol=2e-6, atol=1e-7), (what, got_w, ref_w)
+        assert np.allclose(got_w, ref_w, rtol=w_rtol, atol=1e-7), (what, got_w, ref_w)
         return True
     l = np.asarray(ref_logits, dtype=np.float64)
     # every mismatch must be explained by near-equal logits in the oracle
     order = np.argsort(-l, kind="stable")
     for pos in range(k):
         if got_idx[pos] != ref_idx[pos]:
-            assert abs(l[got_idx[pos]] - l[ref_idx[pos]]) <= NEAR_TIE, (what, pos, got_idx, ref_idx)
+            assert abs(l[got_idx[pos]] - l[ref_idx[pos]]) <= tie, (what, pos, got_idx, ref_idx)
     assert len(set(got_idx.tolist())) == k
     gap = o_routing.near_tie_gap(l, k)
     if set(got_idx.tolist()) != set(ref_idx.tolist()):
-        assert gap <= NEAR_TIE, (what, gap)
+        assert gap <= tie, (what, gap)
         stats["near_tie_set"] = stats.get("near_tie_set", 0) + 1
     else:
         stats["near_tie_order"] = stats.get("near_tie_order", 0) + 1
@@ -182,7 +183,7 @@ def _x_flip_is_tie(r32, j, got16, want16):
     return abs(v - 0.5 * (a + b)) <= 1e-12 * abs(v)
 
 
-def teacher_forced_chain(rec, xi, np_layers, wl, L, y_at=None, what="chain"):
+def teacher_forced_chain(rec, xi, np_layers, wl, L, y_at=None, what="chain", pred_oracle=None):
     """Teacher-forced per-layer parity of a recorded decode chain.
 
     ``rec`` holds host arrays [T, L, ...] of what the device did at every
@@ -202,7 +203,9 @@ def teacher_forced_chain(rec, xi, np_layers, wl, L, y_at=None, what="chain"):
       counted); every other layer uses exactly the prediction the device made
       for it one token earlier;
     * prediction: bit-exact against the oracle's prerouting of ``x``, except
-      at near-ties (counted);
+      at near-ties (counted); ``pred_oracle(t, n, x)``, when given, returns
+      the oracle's prediction logits and the tie and weight tolerances of a
+      head whose logits carry their own stated precision (the full head);
     * output (at the (t, n) where ``y_at(t, n)`` holds, default all): within
       TOL_REL_INF of the oracle layer on ``x`` with the device's routing.
     """
@@ -245,7 +248,12 @@ def teacher_forced_chain(rec, xi, np_layers, wl, L, y_at=None, what="chain"):
                     ("prediction not used as routing", tag)
                 assert np.array_equal(rec["w"][t, n], rec["pw"][t - 1, n - 1]), ("weights", tag)
                 stats["pred_routing"] += 1
-            if n + 1 < L and lay.get("head") is not None:
+            if n + 1 < L and pred_oracle is not None:
+                pl, tie, w_rtol = pred_oracle(t, n, x_got)
+                check_routing(rec["pidx"][t, n], rec["pw"][t, n], pl, K, tag + ("pred",),
+                              stats["prediction_near_ties"], tie=tie, w_rtol=w_rtol)
+                stats["predictions"] += 1
+            elif n + 1 < L and lay.get("head") is not None:
                 pl = o_routing.logits_fp32(lay["head"], x_got)
                 check_routing(rec["pidx"][t, n], rec["pw"][t, n], pl, K, tag + ("pred",),
                               stats["prediction_near_ties"])

@@ -604,7 +604,7 @@ def layer_load_fit(torch, tier, spec, layers, fpool, n_slots, drop, reps=4):
         fpool.drop_page_cache()
     ch = tier.TieredChain(spec, layers, fpool, n_slots)
     K = spec.top_k
-    comp = torch.cuda.Stream()
+    comp = ch.streams.compute
     # never-loaded experts in a seeded random order (consecutive ids would read
     # the file sequentially and let the kernel's readahead serve later loads)
     g = np.random.default_rng(11)

@@ -180,6 +180,24 @@ def _stream(stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+class StreamPair:
+    """Two streams for work that must overlap (copies beside kernels), taken
+    one right after the other from torch's stream pool (default priority).
+    The pool creates its streams together, and HIP maps streams onto a few
+    hardware queues (GPU_MAX_HW_QUEUES) in creation order, so consecutive pool
+    streams sit on different queues; a pool stream paired with the null
+    stream can share its queue and serialize against it. Pool streams live as
+    long as the process, so ``close`` has nothing to free."""
+
+    def __init__(self):
+        import torch
+        self.compute = torch.cuda.Stream()
+        self.copy = torch.cuda.Stream()
+
+    def close(self):
+        pass
+
+
 def make_spec(d, n_experts, top_k, n_shared, d_expert, lora_rank, lora_scale, group_size=64,
               sigmoid_group=None):
     """``sigmoid_group``: None (softmax-topk) or (n_groups, top_groups, scale)."""

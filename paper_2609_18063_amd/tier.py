@@ -155,7 +155,10 @@ class TieredChain:
         else:
             self.stager = B.Stager(self.table, pool.layout, pool.bundle_bytes, pool.ptrs(), self.slots,
                                    pool.stride)
-        self.copy_stream = torch.cuda.Stream()      # default priority
+        # the layers run on `compute`, the staging copies on `copy`: two streams
+        # made back to back, so that they never share a hardware queue
+        self.streams = B.StreamPair()
+        self.copy_stream = self.streams.copy
         self.ws = torch.zeros(B.workspace_bytes(spec, 1), dtype=torch.uint8, device=dev)
         self.r = torch.zeros(1, d, dtype=torch.float32, device=dev)
         self.x = torch.empty(1, d, dtype=torch.float16, device=dev)
@@ -294,8 +297,10 @@ class TieredChain:
         T = xi_tokens.shape[0]
         rec = self.new_record(T) if record else None
         self.r.zero_()
-        for t in range(T):
-            self.run_token(t, xi_tokens[t:t + 1], record=rec)
+        self.streams.compute.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(self.streams.compute):
+            for t in range(T):
+                self.run_token(t, xi_tokens[t:t + 1], record=rec)
         self.finish()
         return rec
 
@@ -306,6 +311,7 @@ class TieredChain:
     def close(self):
         self.stager.close()
         self.table.close()
+        self.streams.close()
 
 
 def set_overlap(log, L):
@@ -385,7 +391,10 @@ class WholeLayerPrefill:
                 a = base + b * self.per_layer + e * pool.stride
                 self.table.bind(b, e, e, B.MoeBundle(proj(a, lay.gate), proj(a, lay.up), proj(a, lay.down)))
         self.table.sync()
-        self.copy_stream = torch.cuda.Stream()      # default priority
+        # the layers run on `compute`, the loads on `copy`: two streams made
+        # back to back, so that they never share a hardware queue
+        self.streams = B.StreamPair()
+        self.copy_stream = self.streams.copy
         self.stage = None
         if isinstance(pool, FilePool):   # two pinned staging buffers, alternating by layer
             self.stage = [torch.empty(self.per_layer, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
@@ -424,7 +433,15 @@ class WholeLayerPrefill:
         spec = self.spec
         T, d = xi.shape
         K, n = spec.top_k, spec.top_k + spec.n_shared
-        cur = torch.cuda.current_stream()
+        caller = torch.cuda.current_stream()
+        cur = self.streams.compute
+        cur.wait_stream(caller)
+        with torch.cuda.stream(cur):
+            out = self._run(xi, record, spec, T, d, K, n, cur)
+        caller.wait_stream(cur)
+        return out
+
+    def _run(self, xi, record, spec, T, d, K, n, cur):
         r = xi.clone()
         x = torch.empty(T, d, dtype=torch.float16, device="cuda")
         idx = torch.empty(T, K, dtype=torch.int32, device="cuda")
@@ -465,3 +482,4 @@ class WholeLayerPrefill:
     def close(self):
         torch.cuda.synchronize()
         self.table.close()
+        self.streams.close()

@@ -744,6 +744,31 @@ def prefill_whole_layer(torch, tier, spec, routers, pool, wl, T=512):
     return out
 
 
+def tier8b_engine_chain(B, torch, spec, table, layers, wl, L, T=64):
+    """The 8B tier's layers with every expert resident, decoded by the two-half
+    engine (one cooperative launch of T tokens x L layers, prediction-as-routing):
+    the compute the host tier's per-layer launches stand in for."""
+    import synth
+    if not B.engine_chain_supported(spec):
+        return None
+    arr = B.engine_layer_array(layers)
+    ws = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+    r_state = torch.zeros(wl.d, dtype=torch.float32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    tok = torch.from_numpy(synth.token_draws(wl, 0, T + 16, stream=5)).cuda()
+    chain_launch(B, spec, table, arr, L, tok[T:], r_state, ws, status)
+    ms = time_launch(torch, lambda: chain_launch(B, spec, table, arr, L, tok[:T], r_state, ws, status))
+    assert int(status.item()) == 0, "engine status %d" % int(status.item())
+    nbytes = chain_bytes(wl, L, T)
+    out = {"tokens": T, "layers": L, "tokens_per_s": round(T / (ms * 1e-3), 1),
+           "us_per_layer_step": round(ms * 1e3 / (T * L), 3),
+           "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+           "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    log("8B tier, all experts resident, two-half engine chain: %.1f tok/s, %.2f us per layer step, "
+        "%.1f GB/s" % (out["tokens_per_s"], out["us_per_layer_step"], out["GB_s"]))
+    return out
+
+
 def tier_path(B, torch, T=64, L=24, rho=0.5):
     """The 8B tier with host-tier staging: 24 layers whose 64 experts per
     layer live in pinned host memory, 3 x top-4 device slots per layer; the
@@ -794,6 +819,7 @@ def tier_path(B, torch, T=64, L=24, rho=0.5):
             dc.replay_token(t)
 
     compute_s = time_launch(torch, replay_all) * 1e-3
+    engine_res = tier8b_engine_chain(B, torch, spec, table, layers, wl, L)
     table.close()
     del keep
     tok_bytes = L * (nb["ffn"] + nb["route"] // 2)
@@ -817,6 +843,7 @@ def tier_path(B, torch, T=64, L=24, rho=0.5):
         "adjacent_set_overlap": round(tier.set_overlap(ch.log, L), 3),
     }
     res["file_tier"] = file_res
+    res["resident_engine_chain"] = engine_res
     res["prefill_whole_layer"] = prefill_whole_layer(torch, tier, spec, [l["router"] for l in layers],
                                                      pool, wl)
     # slot capacity: the slots of a layer are an LRU cache of its experts (the

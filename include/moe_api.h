@@ -396,14 +396,19 @@ int moe_engine_tokens(const moe_layer_spec* spec, const moe_slot_table* table,
  * y_rec fp32 [.][d] (the layer output).
  * Schedule: on a 256-CU device, for the layer shapes the two-half schedule
  * is compiled for (d 2048 / I 512 / r 16 with K + S <= 9 and E <= 256;
- * d 512 / I 256 / r 8 with K + S <= 2 and E <= 16; the K + S experts' rows
+ * d 512 / I 256 / r 8 with K + S <= 2 and E <= 16; d 4096 / I 1024 / r 16
+ * with K + S <= 4 and E <= 64, the 8B tier's layer; the K + S experts' rows
  * splitting evenly over its 128 workgroups), layer steps alternate between
  * two halves of the chip (even and odd XCDs): one half computes a layer
  * while the other loads the experts of its next layer, known a token ahead
  * from the prediction. There h = silu(g) u is rounded once to fp16 (valid while
  * |h| < 65504) for the down projection and the down adapter's A product.
- * Other shapes run the whole-chip engine of moe_engine_layers (h in fp32).
+ * Other shapes run the whole-chip engine of moe_engine_layers (h in fp32);
+ * moe_engine_chain_supported says whether either takes a shape.
  */
+/* MOE_OK if moe_engine_chain runs this layer shape on this device (on the
+ * two-half schedule or on the whole-chip engine), else MOE_EINVAL. */
+int moe_engine_chain_supported(const moe_layer_spec* spec);
 int moe_engine_chain(const moe_layer_spec* spec, const moe_slot_table* table,
                      const moe_engine_layer* layers, int n_layers, int first_token, int n_tokens,
                      const float* xi, float* r_state, void* x_rec, float* r_rec, int32_t* idx_rec,

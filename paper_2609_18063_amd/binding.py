@@ -136,6 +136,7 @@ SIGNATURES = {
     "moe_engine_tokens": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_void_p, c_int,
                                   c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                   c_void_p, c_void_p, c_size_t, c_void_p]),
+    "moe_engine_chain_supported": (c_int, [ctypes.POINTER(MoeLayerSpec)]),
     "moe_engine_chain": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_int,
                                  c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
@@ -539,6 +540,10 @@ MOE_STATUS_ENGINE_ABORT = 4
 
 def engine_supported(spec):
     return lib().moe_engine_supported(ctypes.byref(spec)) == MOE_OK
+
+
+def engine_chain_supported(spec):
+    return lib().moe_engine_chain_supported(ctypes.byref(spec)) == MOE_OK
 
 
 def engine_workspace_bytes(spec, n_layers):

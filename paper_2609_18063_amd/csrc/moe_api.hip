@@ -682,6 +682,11 @@ int moe_engine_tokens(const moe_layer_spec* s, const moe_slot_table* t,
                       status, ws, ws_bytes, stream);
 }
 
+int moe_engine_chain_supported(const moe_layer_spec* s) {
+  const int rc = engine_pipe_supported(s);
+  return rc == MOE_OK ? MOE_OK : moe_engine_supported(s);
+}
+
 int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,
                      const moe_engine_layer* layers, int n_layers, int first_token, int n_tokens,
                      const float* xi, float* r_state, void* x_rec, float* r_rec, int32_t* idx_rec,

@@ -1131,6 +1131,9 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
 
 using PShapeMoe35b = PShape<2048, 512, 16, 9, 256, 3>;
 using PShapeTiny = PShape<512, 256, 8, 2, 16, 2>;
+// the 8B-tier layer: d 4096, 64 experts top-4, I 1024; each XCD of a half
+// owns one whole expert
+using PShape8b = PShape<4096, 1024, 16, 4, 64, 1>;
 
 template <class SH>
 static int lds_bytes() {
@@ -1183,6 +1186,7 @@ bool engine_pipe_supported(int d, int I, int r, int K, int S, int E) {
   const int n = K + S;
   if (d == 2048 && I == 512 && r == 16) return pipe::fits<pipe::PShapeMoe35b>(n, I, E, K);
   if (d == 512 && I == 256 && r == 8) return pipe::fits<pipe::PShapeTiny>(n, I, E, K);
+  if (d == 4096 && I == 1024 && r == 16) return pipe::fits<pipe::PShape8b>(n, I, E, K);
   return false;
 }
 
@@ -1214,6 +1218,7 @@ size_t engine_pipe_workspace_words(int E, int d, int I, int r, int n_list, int L
 hipError_t launch_engine_pipe(EngineArgs& a, int d, int I, int r, hipStream_t st) {
   if (d == 2048 && I == 512 && r == 16) return pipe::launch<pipe::PShapeMoe35b>(a, st);
   if (d == 512 && I == 256 && r == 8) return pipe::launch<pipe::PShapeTiny>(a, st);
+  if (d == 4096 && I == 1024 && r == 16) return pipe::launch<pipe::PShape8b>(a, st);
   return hipErrorInvalidValue;
 }
 

@@ -186,3 +186,21 @@ def test_engine_rejects_unsupported_shape(torch_cuda):
     assert not B.engine_supported(B.make_spec(512, 16, 16, 0, 256, 8, 2.0))   # 16*256/8 rows
     assert not B.engine_supported(B.spec_from_workload(synth.WORKLOADS["tier8b"]))
     assert B.engine_supported(B.spec_from_workload(synth.WORKLOADS["moe35b"]))
+
+
+def test_engine_chain_8b_tier_shape(torch_cuda):
+    """The 8B-tier layer (d 4096, 64 experts top-4, I 1024, r 16) through the
+    two-half chain: 4 layers x 4 tokens in one launch, teacher-forced at every
+    (token, layer); expert outputs at every layer of the first token and one
+    seeded layer of each later token."""
+    wl = synth.WORKLOADS["tier8b"]
+    L, T = 4, 4
+    chain, np_layers = build_chain(wl, L, torch_cuda)
+    xi = synth.token_draws(wl, 0, T)
+    rec, _, _ = _engine_chain(chain, xi, L, torch_cuda)
+    rec = {k: v.cpu().numpy() for k, v in rec.items()}
+    stats = teacher_forced_chain(rec, xi, np_layers, wl, L,
+                                 y_at=sample_layers(T, L, full_tokens=1, per_token=1),
+                                 what="engine 8B tier")
+    print("engine 8B-tier chain:", stats)
+    assert stats["steps"] == L * T and stats["pred_routing"] == (T - 1) * (L - 1)

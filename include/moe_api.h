@@ -57,8 +57,10 @@ extern "C" {
 /* ---- layer description (the MoESpec of Sec. 3) --------------------------- */
 #define MOE_ROUTING_SOFTMAX_TOPK 0   /* App. A, Softmax-topk                    */
 #define MOE_ROUTING_SIGMOID_GROUP 1  /* App. A, Sigmoid-group (moe_topk, moe_route,
-                                        moe_preroute, moe_preroute_mlp; the
-                                        decode engines take softmax-topk only)  */
+                                        moe_preroute, moe_preroute_mlp, and the
+                                        two-half schedule of moe_engine_chain;
+                                        the whole-chip engines take softmax-topk
+                                        only)                                   */
 
 typedef struct moe_layer_spec {
   int32_t d_model;     /* hidden size d; multiple of 64, <= 8192             */
@@ -402,9 +404,11 @@ int moe_engine_tokens(const moe_layer_spec* spec, const moe_slot_table* table,
  * two halves of the chip (even and odd XCDs): one half computes a layer
  * while the other loads the experts of its next layer, known a token ahead
  * from the prediction. There h = silu(g) u is rounded once to fp16 (valid while
- * |h| < 65504) for the down projection and the down adapter's A product.
- * Other shapes run the whole-chip engine of moe_engine_layers (h in fp32);
- * moe_engine_chain_supported says whether either takes a shape.
+ * |h| < 65504) for the down projection and the down adapter's A product, and
+ * both the own router and the head select by spec->routing (softmax-topk or
+ * sigmoid-group). Other shapes run the whole-chip engine of moe_engine_layers
+ * (h in fp32; softmax-topk only); moe_engine_chain_supported says whether
+ * either takes a spec.
  */
 /* MOE_OK if moe_engine_chain runs this layer shape on this device (on the
  * two-half schedule or on the whole-chip engine), else MOE_EINVAL. */

@@ -556,9 +556,11 @@ int moe_engine_supported(const moe_layer_spec* s) {
 
 static constexpr size_t kEngineCtlBytes = 256;
 
-// the chain on two alternating halves of the chip (same device rule as moe_engine_supported)
+// the chain on two alternating halves of the chip (same device rule as
+// moe_engine_supported); softmax-top-k or sigmoid-group routing
 static int engine_pipe_supported(const moe_layer_spec* s) {
-  if (moe_spec_check(s) != MOE_OK || s->routing != MOE_ROUTING_SOFTMAX_TOPK) return MOE_EINVAL;
+  if (moe_spec_check(s) != MOE_OK) return MOE_EINVAL;
+  if (s->routing != MOE_ROUTING_SOFTMAX_TOPK && s->routing != MOE_ROUTING_SIGMOID_GROUP) return MOE_EINVAL;
   if (!moe::engine_pipe_supported(s->d_model, s->d_expert, s->lora_rank, s->top_k, s->n_shared,
                                   s->n_experts))
     return MOE_EINVAL;
@@ -625,6 +627,9 @@ static int engine_common(const moe_layer_spec* s, const moe_slot_table* t, int n
   a.S = s->n_shared;
   a.r = s->lora_rank;
   a.lora_scale = s->lora_scale;
+  a.n_groups = s->routing == MOE_ROUTING_SIGMOID_GROUP ? s->n_groups : 0;
+  a.top_groups = s->top_groups;
+  a.route_scale = s->route_scale;
   a.n_ids = t->n_ids;
   a.n_slots = t->n_slots;
   a.n_table_layers = t->n_layers;

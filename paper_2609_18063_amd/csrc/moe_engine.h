@@ -15,6 +15,8 @@ struct EngineArgs {
   int consumer_lo, consumer_hi;  // chain: layers that route by the prediction (after token 0)
   int E, K, S, r;
   float lora_scale;
+  int n_groups, top_groups;  // sigmoid-group selection (App. A) when n_groups > 0, else softmax-top-k
+  float route_scale;
   int n_ids, n_slots, n_table_layers;
   const int32_t* slot_of;        // slot-table device copy
   const moe_bundle* bundles;

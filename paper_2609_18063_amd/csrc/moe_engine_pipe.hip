@@ -187,7 +187,8 @@ struct PShape {
   static constexpr int O_YL = O_DP + NLX * RR * 4;             // [NLX][R] fp32 A_down h per expert
   static constexpr int O_LG = O_YL + NLX * R * 4;              // [256] fp32 logits
   static constexpr int O_TK = O_LG + 256 * 4;                  // top-k scratch
-  static constexpr int TK_BYTES = 256 * 8 + 256 * 4 + 128 * 8 + 32 * 8;
+  static constexpr int TK_BYTES = 256 * 8 + 256 * 4 + 128 * 8 + 32 * 8 +
+                                  (int)sizeof(eng::SigmoidScratch);  // + sigmoid-group scratch
   static constexpr int O_GR = O_TK + TK_BYTES;                 // [NWV][NGW][64] fp32 gate/up lane partials
   static constexpr int O_RED = O_GR + (LPR == 64 ? NWV * NGW * 64 * 4 : 0);  // [NWV] f64
   static constexpr int O_MISC = (O_RED + NWV * 8 + 1023) / 1024 * 1024;
@@ -247,7 +248,10 @@ struct StepInfo {
   bool own, head, ok;
 };
 
-template <class SH>
+// SIG: the layers route by sigmoid-group selection (App. A) instead of
+// softmax-top-k; a separate instantiation so that the softmax path carries none
+// of its code
+template <class SH, bool SIG>
 __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   // The arguments are read through a pointer into the kernel-argument segment
@@ -291,6 +295,16 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   int* tk_part = reinterpret_cast<int*>(smem + SH::O_TK + 256 * 8);
   uint64_t* tk_cand = reinterpret_cast<uint64_t*>(smem + SH::O_TK + 256 * 12);
   uint64_t* tk_sorted = tk_cand + 128;
+  eng::SigmoidScratch& tk_sig = *reinterpret_cast<eng::SigmoidScratch*>(smem + SH::O_TK + 256 * 12 + 160 * 8);
+  // the layer's selection on its logits (router or head): softmax-top-k, or
+  // sigmoid-group selection where the spec asks for it
+  auto select = [&](const float* l, int32_t* idx_out, float* w_out) {
+    if constexpr (SIG)
+      eng::block_topk_sigmoid_group(l, nullptr, apx->E, apx->K, apx->n_groups, apx->top_groups, apx->route_scale,
+                                    idx_out, w_out, tk_sig, tk_keys, tk_part, tk_cand, tk_sorted);
+    else
+      block_topk(l, apx->E, apx->K, idx_out, w_out, tk_keys, tk_part, tk_cand, tk_sorted);
+  };
   double* red = reinterpret_cast<double*>(smem + SH::O_RED);
   float* grp_part = reinterpret_cast<float*>(smem + SH::O_GR);
   Misc* mi = reinterpret_cast<Misc*>(smem + SH::O_MISC);
@@ -602,7 +616,7 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
                               [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); }, apx->ctl, apx->status,
                               &mi->abort))
       return false;
-    block_topk(lg, E, K, mi->pidx, mi->pw, tk_keys, tk_part, tk_cand, tk_sorted);
+    select(lg, mi->pidx, mi->pw);
     if ((int)tx < K) {
       const int i = tx;
       uint64_t* pw = pred_of(f.t + 1, f.N + 1);
@@ -747,7 +761,7 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
                                 [&](int i, uint32_t v) { lg[i] = __uint_as_float(v); }, apx->ctl, apx->status,
                                 &mi->abort))
         break;
-      block_topk(lg, E, K, Rt.idx, Rt.w, tk_keys, tk_part, tk_cand, tk_sorted);
+      select(lg, Rt.idx, Rt.w);
       __syncthreads();
       resolve_route(Rt, lay, s);
       staged = false;
@@ -1140,19 +1154,25 @@ static int lds_bytes() {
   return SH::O_SRC + (int)sizeof(Src<SH>);
 }
 
-template <class SH>
-static hipError_t launch(EngineArgs& a, hipStream_t st) {
+template <class SH, bool SIG>
+static hipError_t launch_as(EngineArgs& a, hipStream_t st) {
   const int lds = lds_bytes<SH>();
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)pipe_kernel<SH>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       lds);
+    hipError_t e = hipFuncSetAttribute((const void*)pipe_kernel<SH, SIG>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   void* args[] = {&a};
-  return hipLaunchCooperativeKernel((const void*)pipe_kernel<SH>, dim3(NWG), dim3(NT), args, (size_t)lds, st);
+  return hipLaunchCooperativeKernel((const void*)pipe_kernel<SH, SIG>, dim3(NWG), dim3(NT), args, (size_t)lds,
+                                    st);
+}
+
+template <class SH>
+static hipError_t launch(EngineArgs& a, hipStream_t st) {
+  return a.n_groups > 0 ? launch_as<SH, true>(a, st) : launch_as<SH, false>(a, st);
 }
 
 // most expert segments over the four XCDs of a half

@@ -124,55 +124,17 @@ __global__ void __launch_bounds__(512) topk_sigmoid_group_kernel(const float* __
                                                                  int K, int n_groups, int top_groups,
                                                                  float scale, int32_t* __restrict__ idx,
                                                                  float* __restrict__ w) {
-  __shared__ float sig[256], sel[256], masked[256], gsc[256];
-  __shared__ int keep[256];
-  __shared__ int32_t tidx[32];
-  __shared__ float tw[32];
+  __shared__ float lg[256];
+  __shared__ eng::SigmoidScratch sc;
   __shared__ uint64_t keys[256];
   __shared__ int part[256];
   __shared__ uint64_t cand[128];
   __shared__ uint64_t sorted[32];
-  const int t = blockIdx.x, tid = threadIdx.x;
-  if (tid < E) {
-    const float s = 1.0f / (1.0f + expf(-logits[(size_t)t * E + tid]));
-    sig[tid] = s;
-    sel[tid] = bias ? s + bias[tid] : s;
-  }
+  const int t = blockIdx.x;
+  if ((int)threadIdx.x < E) lg[threadIdx.x] = logits[(size_t)t * E + threadIdx.x];
   __syncthreads();
-  const int per = E / n_groups;
-  if (tid < n_groups) {
-    float m1 = -INFINITY, m2 = -INFINITY;
-    for (int j = 0; j < per; ++j) {
-      const float v = sel[tid * per + j];
-      if (v > m1) {
-        m2 = m1;
-        m1 = v;
-      } else if (v > m2) {
-        m2 = v;
-      }
-    }
-    gsc[tid] = per >= 2 ? m1 + m2 : m1;
-  }
-  __syncthreads();
-  if (tid < n_groups) {
-    const float me = gsc[tid];
-    int rank = 0;
-    for (int g = 0; g < n_groups; ++g) rank += (gsc[g] > me) || (gsc[g] == me && g < tid);
-    keep[tid] = rank < top_groups;
-  }
-  __syncthreads();
-  if (tid < E) masked[tid] = keep[tid / per] ? sel[tid] : -INFINITY;
-  __syncthreads();
-  eng::block_topk(masked, E, K, tidx, tw, keys, part, cand, sorted);
-  __syncthreads();
-  if (tid < 64) {
-    const float s = tid < K ? sig[tidx[tid]] : 0.f;
-    const float sum = wave_sum(s);
-    if (tid < K) {
-      idx[(size_t)t * K + tid] = tidx[tid];
-      w[(size_t)t * K + tid] = scale * s / (sum + 1e-20f);
-    }
-  }
+  eng::block_topk_sigmoid_group(lg, bias, E, K, n_groups, top_groups, scale, idx + (size_t)t * K,
+                                w + (size_t)t * K, sc, keys, part, cand, sorted);
 }
 
 __global__ void __launch_bounds__(64) topk_kernel(const float* __restrict__ logits, int E, int K,

@@ -208,5 +208,70 @@ __device__ void block_topk(const float* l, int E, int K, int32_t* idx_out, float
   }
 }
 
+// Sigmoid-group selection (App. A) of one token's logits by a 512-thread
+// block (E <= 256, K <= 32): sigma = sigmoid(l) in fp32, selection score
+// sigma + bias (bias may be null: zero); a group's score is the sum of its two
+// largest selection scores (its one score if it has one member); the
+// top_groups best groups survive (ties to the lower group); the K largest
+// surviving scores are selected with block_topk (descending, ties to the lower
+// id); the weights use the raw sigma: w = scale sigma / (sum of the selected
+// sigma + 1e-20). Every thread of the block calls it. Scratch (LDS): sig,
+// masked, gsc [256] fp32, keep [256] int, tidx [32], tw [32], and
+// block_topk's. idx_out / w_out: K entries (LDS or global).
+struct SigmoidScratch {
+  float sig[256], masked[256], gsc[256];
+  int keep[256];
+  int32_t tidx[32];
+  float tw[32];
+};
+
+__device__ inline void block_topk_sigmoid_group(const float* l, const float* bias, int E, int K, int n_groups,
+                                                int top_groups, float scale, int32_t* idx_out, float* w_out,
+                                                SigmoidScratch& sc, uint64_t* keys, int* part, uint64_t* cand,
+                                                uint64_t* sorted) {
+  const int tid = threadIdx.x;
+  if (tid < E) {
+    const float s = 1.0f / (1.0f + expf(-l[tid]));
+    sc.sig[tid] = s;
+    sc.masked[tid] = bias ? s + bias[tid] : s;   // the selection score, masked below
+  }
+  __syncthreads();
+  const int per = E / n_groups;
+  if (tid < n_groups) {
+    float m1 = -INFINITY, m2 = -INFINITY;
+    for (int j = 0; j < per; ++j) {
+      const float v = sc.masked[tid * per + j];
+      if (v > m1) {
+        m2 = m1;
+        m1 = v;
+      } else if (v > m2) {
+        m2 = v;
+      }
+    }
+    sc.gsc[tid] = per >= 2 ? m1 + m2 : m1;
+  }
+  __syncthreads();
+  if (tid < n_groups) {
+    const float me = sc.gsc[tid];
+    int rank = 0;
+    for (int g = 0; g < n_groups; ++g) rank += (sc.gsc[g] > me) || (sc.gsc[g] == me && g < tid);
+    sc.keep[tid] = rank < top_groups;
+  }
+  __syncthreads();
+  if (tid < E && !sc.keep[tid / per]) sc.masked[tid] = -INFINITY;
+  __syncthreads();
+  block_topk(sc.masked, E, K, sc.tidx, sc.tw, keys, part, cand, sorted);
+  __syncthreads();
+  if (tid < 64) {
+    const float s = tid < K ? sc.sig[sc.tidx[tid]] : 0.f;
+    const float sum = wave_sum(s);
+    if (tid < K) {
+      idx_out[tid] = sc.tidx[tid];
+      w_out[tid] = scale * s / (sum + 1e-20f);
+    }
+  }
+  __syncthreads();
+}
+
 }  // namespace eng
 }  // namespace moe

@@ -12,7 +12,7 @@ import pytest
 
 import synth
 from tests.gpu_harness import (TOL_REL_INF, DeviceLayer, build_chain, check_routing,
-                               free_running_divergence, oracle_token, rel_inf, sample_layers,
+                               check_sigmoid_routing, free_running_divergence, oracle_token, rel_inf, sample_layers,
                                teacher_forced_chain)
 
 pytestmark = pytest.mark.gpu
@@ -204,3 +204,36 @@ def test_engine_chain_8b_tier_shape(torch_cuda):
                                  what="engine 8B tier")
     print("engine 8B-tier chain:", stats)
     assert stats["steps"] == L * T and stats["pred_routing"] == (T - 1) * (L - 1)
+
+
+@pytest.mark.parametrize("name,L,T,groups", [
+    ("tiny", 8, 24, (4, 2, 1.0)),
+    ("tier8b", 4, 4, (8, 4, 2.5)),
+])
+def test_engine_chain_sigmoid_group(torch_cuda, name, L, T, groups):
+    """The two-half chain with sigmoid-group selection (App. A) for both the
+    own router and the head's predictions: teacher-forced at every (token,
+    layer) against the oracle's sigmoid_group_topk, near-ties within SG_TIE
+    counted; expert outputs at every layer of the first token and one seeded
+    layer of each later token."""
+    from paper_2609_18063_amd import binding as B
+    wl = synth.WORKLOADS[name]
+    n, G, s = groups
+    spec = B.make_spec(wl.d, wl.E, wl.K, wl.S, wl.I, wl.r, wl.lora_scale, sigmoid_group=groups)
+    assert B.engine_chain_supported(spec)
+    chain, np_layers = build_chain(wl, L, torch_cuda, spec=spec)
+    xi = synth.token_draws(wl, 0, T)
+    rec, _, _ = _engine_chain(chain, xi, L, torch_cuda)
+    rec = {k: v.cpu().numpy() for k, v in rec.items()}
+
+    def route_check(idx, w, logits, tag, st):
+        return check_sigmoid_routing(idx, w, logits, wl.K, n, G, s, None, st, tag)
+
+    stats = teacher_forced_chain(rec, xi, np_layers, wl, L,
+                                 y_at=sample_layers(T, L, full_tokens=1, per_token=1),
+                                 what="engine sigmoid-group " + name, route_check=route_check)
+    print("engine sigmoid-group chain %s:" % name, stats)
+    assert stats["steps"] == L * T and stats["pred_routing"] == (T - 1) * (L - 1)
+    assert stats["predictions"] == T * (L - 1)
+    ties = stats["routing_near_ties"].get("near_tie", 0) + stats["prediction_near_ties"].get("near_tie", 0)
+    assert ties <= 2, stats

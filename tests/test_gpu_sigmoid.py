@@ -15,10 +15,10 @@ import pytest
 
 import synth
 from oracle import routing as o_routing
+from tests.gpu_harness import check_sigmoid_routing
 
 pytestmark = pytest.mark.gpu
 
-SG_TIE = 1e-6
 SHAPES = [  # d, E, K, n_groups, top_groups, scale
     (4096, 128, 8, 8, 4, 2.5),
     (4096, 64, 4, 8, 4, 2.5),
@@ -41,28 +41,8 @@ def _spec(B, d, E, K, n, G, s):
                        sigmoid_group=(n, G, s))
 
 
-def _decisions(l, k, n, g, bias):
-    sig = 1.0 / (1.0 + np.exp(-np.asarray(l, dtype=np.float64)))
-    sel = sig + (0.0 if bias is None else np.asarray(bias, dtype=np.float64))
-    per = sel.size // n
-    gs = np.sort(np.array([np.sum(np.sort(r)[::-1][:2]) for r in sel.reshape(n, per)]))[::-1]
-    return sel, gs, per
-
-
 def _check(got_idx, got_w, l, k, n, g, s, bias, stats, what):
-    ref_idx, ref_w = o_routing.sigmoid_group_topk(l, k, n, g, s, bias)
-    if np.asarray(got_idx).tolist() == ref_idx.tolist():
-        assert np.allclose(got_w, ref_w, rtol=2e-6, atol=1e-7), (what, got_w, ref_w)
-        stats["exact"] = stats.get("exact", 0) + 1
-        return
-    sel, gs, per = _decisions(l, k, n, g, bias)
-    group_tie = g < n and gs[g - 1] - gs[g] <= SG_TIE
-    got = np.asarray(got_idx)
-    assert len(set(got.tolist())) == k, (what, got)
-    # every difference must come from near-equal oracle scores
-    member_ok = all(abs(sel[a] - sel[b]) <= SG_TIE for a, b in zip(got.tolist(), ref_idx.tolist()) if a != b)
-    assert group_tie or member_ok, (what, got, ref_idx)
-    stats["near_tie"] = stats.get("near_tie", 0) + 1
+    check_sigmoid_routing(got_idx, got_w, l, k, n, g, s, bias, stats, what)
 
 
 @pytest.mark.parametrize("shape", SHAPES)
@@ -123,7 +103,9 @@ def test_sigmoid_group_route(torch_cuda):
     assert stats.get("near_tie", 0) <= 1
 
 
-def test_engines_take_softmax_only(torch_cuda):
+def test_engine_support_by_routing(torch_cuda):
+    """The whole-chip engines route by softmax-top-k only; the two-half decode
+    chain takes sigmoid-group specs of its shapes too."""
     from paper_2609_18063_amd import binding as B
     spec = B.spec_from_workload(synth.WORKLOADS["moe35b"])
     assert B.engine_supported(spec)
@@ -131,3 +113,6 @@ def test_engines_take_softmax_only(torch_cuda):
     assert B.spec_check(sg) == 0
     assert not B.engine_supported(sg)
     assert not B.engine_tokens_supported(sg)
+    assert B.engine_chain_supported(sg)
+    sg8 = B.make_spec(4096, 64, 4, 0, 1024, 16, 2.0, sigmoid_group=(8, 4, 2.5))
+    assert B.engine_chain_supported(sg8)

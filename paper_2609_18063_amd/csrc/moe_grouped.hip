@@ -466,14 +466,19 @@ __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
   }
   __syncthreads();
 
-  // weight row w_row (0 .. 127): projection w_row / 64, column c0 + w_row % 64
+  // weight row w_row (0 .. 127): projection w_row / 64, column c0 + w_row % 64. The
+  // projection pointers are read here, once, into registers: a pointer read from
+  // the bundle inside the copy loop would be a vector load issued behind the
+  // chunks in flight, and waiting for it would drain them all.
+  const uint8_t* const gq = static_cast<const uint8_t*>(bd->gate.q);
+  const uint8_t* const uq = static_cast<const uint8_t*>(bd->up.q);
+  const uint8_t* const gs = static_cast<const uint8_t*>(bd->gate.sz);
+  const uint8_t* const us = static_cast<const uint8_t*>(bd->up.sz);
   auto wrow = [&](int w_row) -> const uint8_t* {
-    const moe_proj& pj = w_row < kGateCols ? bd->gate : bd->up;
-    return static_cast<const uint8_t*>(pj.q) + (size_t)(c0 + (w_row % kGateCols)) * (d / 2);
+    return (w_row < kGateCols ? gq : uq) + (size_t)(c0 + (w_row % kGateCols)) * (d / 2);
   };
   auto srow = [&](int w_row) -> const uint8_t* {
-    const moe_proj& pj = w_row < kGateCols ? bd->gate : bd->up;
-    return static_cast<const uint8_t*>(pj.sz) + (size_t)(c0 + (w_row % kGateCols)) * (d / 16);
+    return (w_row < kGateCols ? gs : us) + (size_t)(c0 + (w_row % kGateCols)) * (d / 16);
   };
   const char* xbase = reinterpret_cast<const char*>(a.xp);
   auto xsrc = [&](int row, int k) -> const void* {
@@ -590,14 +595,13 @@ __global__ void __launch_bounds__(kGT, 4) grouped_down_kernel(GroupedArgs a) {
     }
     la[row][k] = (_Float16)v;
   }
-  // weight row w_row (0 .. 255): output column by * 256 + w_row
+  // weight row w_row (0 .. 127): output column by * 128 + w_row (the pointers
+  // read once, into registers, as in gate/up)
   const size_t nbase = (size_t)by * kDownCols;
-  auto wrow = [&](int w_row) -> const uint8_t* {
-    return static_cast<const uint8_t*>(bd->down.q) + (nbase + w_row) * (I / 2);
-  };
-  auto srow = [&](int w_row) -> const uint8_t* {
-    return static_cast<const uint8_t*>(bd->down.sz) + (nbase + w_row) * (I / 16);
-  };
+  const uint8_t* const dq = static_cast<const uint8_t*>(bd->down.q);
+  const uint8_t* const dsz = static_cast<const uint8_t*>(bd->down.sz);
+  auto wrow = [&](int w_row) -> const uint8_t* { return dq + (nbase + w_row) * (I / 2); };
+  auto srow = [&](int w_row) -> const uint8_t* { return dsz + (nbase + w_row) * (I / 16); };
   const char* hbase = reinterpret_cast<const char*>(a.h);
   auto xsrc = [&](int row, int k) -> const void* {
     return hbase + ((size_t)(tl.row0 + (row < tl.nrows ? row : 0)) * I + k) * 2;

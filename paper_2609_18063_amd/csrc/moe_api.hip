@@ -29,7 +29,7 @@ bool pow2_dim(int v) {
 
 struct WsLayout {
   size_t counters, logits, gx, ux, h, ag, au, adpart;
-  size_t g_perm, g_tiles, g_ntiles, g_h, g_xp, g_ax, g_adp;  // grouped (batched) path
+  size_t g_perm, g_tiles, g_tok, g_ntiles, g_h, g_xp, g_ax, g_adp;  // grouped (batched) path
   int g_max_tiles;
   size_t total;
 };
@@ -55,10 +55,11 @@ WsLayout ws_layout(const moe_layer_spec* s, int T) {
   w.g_max_tiles = moe::grouped_max_tiles(T, (int)n, s->n_experts + s->n_shared);
   w.g_perm = take((size_t)T * n * sizeof(int32_t));
   w.g_tiles = take((size_t)w.g_max_tiles * sizeof(moe::GroupTile));
+  w.g_tok = take((size_t)w.g_max_tiles * moe::kGroupRows * sizeof(int32_t));
   w.g_ntiles = take(sizeof(int32_t));
   w.g_h = take((size_t)T * n * s->d_expert * sizeof(__half));
   w.g_xp = take((size_t)T * s->d_model * sizeof(__half));
-  w.g_ax = take((size_t)T * n * 2 * 16 * sizeof(float));
+  w.g_ax = take((size_t)T * n * 4 * 2 * 16 * sizeof(float));
   w.g_adp = take((size_t)T * n * (s->d_expert / moe::kGroupSlab > 0 ? s->d_expert / moe::kGroupSlab : 1) * 16 * sizeof(float));
   w.total = off;
   return w;
@@ -444,6 +445,7 @@ int moe_expert_ffn_grouped_int4_lora(const moe_layer_spec* s, const moe_slot_tab
   a.status = status_dev;
   a.perm = at<int32_t>(ws, L.g_perm);
   a.tiles = at<moe::GroupTile>(ws, L.g_tiles);
+  a.tile_tok = at<int32_t>(ws, L.g_tok);
   a.n_tiles = at<int32_t>(ws, L.g_ntiles);
   a.max_tiles = L.g_max_tiles;
   a.h = at<__half>(ws, L.g_h);

@@ -14,9 +14,12 @@ constexpr int kGroupSlab = 64;   // columns of one partial A_d h (one gate/up wo
 
 // One tile of the grouped GEMMs: rows [row0, row0 + nrows) of the permuted
 // list, all routed to group g (expert id g < E, shared expert E + s), whose
-// bundle sits in slot `slot` (-1: not resident).
+// bundle sits in slot `slot` (-1: not resident). The bundle's pointers are
+// copied into the record (zero when not resident), so that a GEMM workgroup
+// can start its weight copies as soon as it has read its record.
 struct GroupTile {
   int32_t g, row0, nrows, slot;
+  moe_bundle b;
 };
 
 struct GroupedArgs {
@@ -30,11 +33,14 @@ struct GroupedArgs {
   // workspace
   int32_t* perm;                // [T * n_list]: y_experts row (t * n_list + k) of each position
   GroupTile* tiles;             // [max_tiles]
+  int32_t* tile_tok;            // [max_tiles][kGroupRows]: token of each tile row (unset
+                                // past nrows)
   int32_t* n_tiles;             // [1]
   int max_tiles;
   __half* h;                    // [T * n_list][I], by permuted position, pair order
   __half* xp;                   // [T][d]: x in pair order
-  float* ax;                    // [T * n_list][2][16]: A_g x, A_u x by permuted position
+  float* ax;                    // [T * n_list][4][2][16]: A_g x, A_u x by permuted position,
+                                // per quarter of d
   float* adp;                   // [T * n_list][I / kGroupSlab][16]: A_d h over column slabs
   float* y_experts;             // [T][n_list][d]
 };

@@ -24,8 +24,11 @@
 //             fp32 rows go straight to y_experts.
 //
 // A GEMM workgroup uses under half of the CU's LDS, so two share a CU: the
-// loads that start and end a tile (tile record, bundle, LoRA rows) of one
-// overlap the streaming of the other.
+// loads that start and end a tile of one overlap the streaming of the other.
+// A workgroup's first copies depend only on its tile record (which carries the
+// bundle's pointers) and on the tile's token list, both written by the
+// permutation; the operands of the epilogue (LoRA rows, A x, the output rows)
+// are requested before the copies and consumed after the k loop.
 //
 // Pair order: inside each 8-element piece the elements run [0,4,1,5,2,6,3,7],
 // the order in which the packed nibbles of one code dword come out of a
@@ -60,8 +63,8 @@ static_assert(kGateRows == 16 * kGW && kDownCols == 16 * kGW, "one row block per
 // bytes per row
 inline int gate_sz_bytes(int d) { return kGateRows * (d / 16); }
 inline int down_sz_bytes(int I) { return kDownCols * (I / 16); }
-constexpr int kGateStatic = 2 * kGroupRows * 16 * 2 + kGroupRows * 4;  // la, rsrc
-constexpr int kDownStatic = kGroupRows * 16 * 2 + kGroupRows * 4;      // la, ydst
+constexpr int kGateStatic = 0;   // static LDS of the GEMM kernels (their epilogues reuse the ring)
+constexpr int kDownStatic = 0;
 constexpr int kLdsMax = 160 * 1024;             // LDS of a CU: the most one workgroup may take
 // (a launch asks only for what its shape needs: up to 80 KB, two workgroups
 // share a CU; the d 4096 gate/up rows need more, and run one per CU)
@@ -107,9 +110,9 @@ __device__ __forceinline__ h8 lora_b_operand(const __half* b, int row, int r, in
   h8 v = {};
   if (kq < 2) {
     const _Float16* p = reinterpret_cast<const _Float16*>(b) + (size_t)row * r + kq * 8;
-    if (r == 16) {
+    if (r == 16 || (r == 8 && kq == 0)) {
       v = as_h8(ld16(p));
-    } else {
+    } else if (r != 8) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         if (kq * 8 + e < r) v[e] = p[e];
@@ -121,7 +124,7 @@ __device__ __forceinline__ h8 lora_b_operand(const __half* b, int row, int r, in
 // ---- copies into LDS --------------------------------------------------------
 // global_load_lds: each lane of the wave moves 16 (or 4) bytes from its own
 // address to lds + 16 * lane (4 * lane). The compiler does not see these as
-// memory instructions; vm_wait / vm_drain order them.
+// memory instructions; vm_wait orders them.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
 }
@@ -148,13 +151,6 @@ __device__ __forceinline__ void dma4(const void* g, const void* lds) {
       : "=&s"(saved)
       : "s"(lds_addr(lds)), "v"(g)
       : "memory");
-}
-// Nothing of the compiler's own outstanding (a wait it would place for one of
-// its loads inside a copy loop would drain the copies too). simm16 0x0F70:
-// vmcnt 0, expcnt and lgkmcnt unconstrained.
-__device__ __forceinline__ void vm_drain() {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 // wait until at most n of this wave's copies are outstanding (n <= 27)
 __device__ __forceinline__ void vm_wait(int n) {
@@ -221,7 +217,8 @@ __device__ __forceinline__ void tile_gemm_mb(char* ring, char* szl, int Kdim, WR
       dma16(xsrc(row, c * kGK + piece * 8), sl + CODE_B + b * 1024);
     }
   };
-  vm_drain();
+  // (loads of the caller still outstanding here are older than every copy:
+  // they complete before the chunks in whose wait they are counted)
   for (int b = wave; b * 1024 < NROWS * szr; b += kGW) {  // (s, z) rows, natural layout
     const int o = b * 1024 + lane * 16;
     dma16(srow(o / szr) + o % szr, szl + b * 1024);
@@ -273,6 +270,8 @@ __device__ __forceinline__ void tile_gemm(char* ring, char* szl, int Kdim, int m
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(1024) grouped_permute_kernel(GroupedArgs a) {
   __shared__ int cnt[kGroupMaxG];
+  __shared__ int goff[kGroupMaxG];   // first permuted row and first tile of each group
+  __shared__ int gtoff[kGroupMaxG];
   __shared__ int scr[2][1024];
   __shared__ int sct[2][1024];
   const int tid = threadIdx.x;
@@ -307,15 +306,42 @@ __global__ void __launch_bounds__(1024) grouped_permute_kernel(GroupedArgs a) {
   }
   const int off0 = scr[pb][tid] - vr, toff0 = sct[pb][tid] - vt;
   const int total_tiles = sct[pb][1023];
-  auto emit = [&](int g, int c, int off, int toff) {
-    if (g >= G || c == 0) return;
-    const int slot = a.slot_of[g];
+  // the slots and bundles of both groups requested together (one dependent
+  // pair of loads for the thread); a group that is not resident copies slot 0's
+  // bundle (a table has at least one slot), which no kernel reads. The bundle
+  // moves as 12 pointer words (held in registers).
+  constexpr int kBW = (int)(sizeof(moe_bundle) / 8);
+  static_assert(sizeof(moe_bundle) == 8 * kBW && sizeof(GroupTile) == 16 + sizeof(moe_bundle), "record layout");
+  const int s0 = g0 < G && c0 ? a.slot_of[g0] : -1, s1 = g1 < G && c1 ? a.slot_of[g1] : -1;
+  uint64_t w0[kBW], w1[kBW];
+  {
+    const uint64_t* p0 = reinterpret_cast<const uint64_t*>(a.bundles + (s0 > 0 ? s0 : 0));
+    const uint64_t* p1 = reinterpret_cast<const uint64_t*>(a.bundles + (s1 > 0 ? s1 : 0));
+#pragma unroll
+    for (int q = 0; q < kBW; ++q) {
+      w0[q] = p0[q];
+      w1[q] = p1[q];
+    }
+  }
+  auto emit = [&](int g, int c, int off, int toff, int slot, const uint64_t (&w)[kBW]) {
+    if (g >= G) return;
+    goff[g] = off;
+    gtoff[g] = toff;
+    if (c == 0) return;
     if (slot < 0 && a.status) atomicOr(a.status, MOE_STATUS_SLOT_MISS);
-    for (int j = 0; j * kGroupRows < c; ++j)
-      a.tiles[toff + j] = GroupTile{g, off + kGroupRows * j, min(kGroupRows, c - kGroupRows * j), slot};
+    for (int j = 0; j * kGroupRows < c; ++j) {
+      GroupTile* o = a.tiles + toff + j;
+      o->g = g;
+      o->row0 = off + kGroupRows * j;
+      o->nrows = min(kGroupRows, c - kGroupRows * j);
+      o->slot = slot;
+      uint64_t* ob = reinterpret_cast<uint64_t*>(&o->b);
+#pragma unroll
+      for (int q = 0; q < kBW; ++q) ob[q] = w[q];
+    }
   };
-  emit(g0, c0, off0, toff0);
-  emit(g1, c1, off0 + c0, toff0 + t0);
+  emit(g0, c0, off0, toff0, s0, w0);
+  emit(g1, c1, off0 + c0, toff0 + t0, s1, w1);
   __syncthreads();  // every count is read: the array becomes the insertion cursors
   if (g0 < G) cnt[g0] = off0;
   if (g1 < G) cnt[g1] = off0 + c0;
@@ -326,7 +352,9 @@ __global__ void __launch_bounds__(1024) grouped_permute_kernel(GroupedArgs a) {
     const int t = i / a.K, k = i - t * a.K;
     const int row = t * a.n_list + k;
     if (e >= 0 && e < a.E) {
-      a.perm[atomicAdd(&cnt[e], 1)] = row;
+      const int pos = atomicAdd(&cnt[e], 1), rel = pos - goff[e];
+      a.perm[pos] = row;
+      a.tile_tok[(size_t)(gtoff[e] + rel / kGroupRows) * kGroupRows + rel % kGroupRows] = t;
     } else {  // an id outside [0, E) contributes zeros and is reported
       if (a.status) atomicOr(a.status, MOE_STATUS_BAD_INDEX);
       float* y = a.y_experts + (size_t)row * a.d;
@@ -334,16 +362,19 @@ __global__ void __launch_bounds__(1024) grouped_permute_kernel(GroupedArgs a) {
     }
   }
   for (int i = tid; i < a.T * a.S; i += 1024) {
-    const int s = i / a.T, t = i - s * a.T;
-    a.perm[cnt[a.E + s] + t] = t * a.n_list + a.K + s;
+    const int s = i / a.T, t = i - s * a.T, g = a.E + s;
+    a.perm[cnt[g] + t] = t * a.n_list + a.K + s;
+    a.tile_tok[(size_t)(gtoff[g] + t / kGroupRows) * kGroupRows + t % kGroupRows] = t;
   }
 }
 
 // ---------------------------------------------------------------------------
-// prep: blocks [0, xb) write x in pair order; blocks [xb, xb + max_tiles) form
-// A_g x and A_u x of one tile: waves 4c .. 4c+3 take projection c, each over a
-// quarter of d, with MFMA (ranks as the 16 columns), then the quarters add up.
-__global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb) {
+// prep: blocks [0, xb) write x in pair order; blocks [xb, xb + 4 max_tiles)
+// form A_g x and A_u x of one tile over one quarter of d (four workgroups per
+// tile): waves 4c .. 4c+3 take projection c, each over a sixteenth of d, with
+// MFMA (ranks as the 16 columns); the waves' sums add up in the workgroup as
+// (w0 + w1) + (w2 + w3), the quarters' in gate/up the same way.
+__global__ void __launch_bounds__(kGT, 6) grouped_prep_kernel(GroupedArgs a, int xb) {
   __shared__ float part[2][4][kGroupRows][16];
   const int tid = threadIdx.x;
   if ((int)blockIdx.x < xb) {
@@ -355,7 +386,7 @@ __global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb
     }
     return;
   }
-  const int ti = blockIdx.x - xb;
+  const int ti = (blockIdx.x - xb) >> 2, Q = (blockIdx.x - xb) & 3;
   if (ti >= *a.n_tiles) return;
   const GroupTile tl = a.tiles[ti];
   if (tl.slot < 0 || a.r <= 0) return;
@@ -379,11 +410,12 @@ __global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb
       const int t = row < tl.nrows ? a.perm[tl.row0 + row] / a.n_list : -1;
       xrow[m] = t >= 0 ? reinterpret_cast<const _Float16*>(a.x) + (size_t)t * d : nullptr;
     }
-    const int kbeg = quarter * (d / 4), kend = kbeg + d / 4;
-    for (int k0 = kbeg + kq * 8; k0 < kend; k0 += 128) {  // four k steps: all loads, then the MFMAs
-      h8 b[4], av[4][4];
+    const int kbeg = Q * (d / 4) + quarter * (d / 16), kend = kbeg + d / 16;
+#pragma unroll 1
+    for (int k0 = kbeg + kq * 8; k0 < kend; k0 += 64) {  // two k steps: all loads, then the MFMAs
+      h8 b[2], av[2][4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 2; ++u) {
         const int k = k0 + 32 * u;
         const bool in = k < kend;
         b[u] = arow && in ? as_h8(ld16(arow + k)) : h8{};
@@ -391,7 +423,7 @@ __global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb
         for (int m = 0; m < 4; ++m) av[u][m] = m < mb && xrow[m] && in ? as_h8(ld16(xrow[m] + k)) : h8{};
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int m = 0; m < 4; ++m)
           if (m < mb) acc[m] = mfma(av[u][m], b[u], acc[m]);
@@ -406,7 +438,7 @@ __global__ void __launch_bounds__(kGT) grouped_prep_kernel(GroupedArgs a, int xb
   for (int p = tid; p < 2 * tl.nrows * 16; p += kGT) {
     const int cc = p / (tl.nrows * 16), rem = p % (tl.nrows * 16), row = rem >> 4, k = rem & 15;
     const float v = (part[cc][0][row][k] + part[cc][1][row][k]) + (part[cc][2][row][k] + part[cc][3][row][k]);
-    a.ax[((size_t)(tl.row0 + row) * 2 + cc) * 16 + k] = v;
+    a.ax[(((size_t)(tl.row0 + row) * 4 + Q) * 2 + cc) * 16 + k] = v;
   }
 }
 
@@ -428,67 +460,58 @@ __device__ __forceinline__ void tile_of_block(int b, int ny, int& x, int& y) {
 
 __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
   extern __shared__ __attribute__((aligned(16))) char ring[];
-  __shared__ __attribute__((aligned(16))) _Float16 la[2][kGroupRows][16];
-  __shared__ int rsrc[kGroupRows];
   char* const szl = ring + kRingBytes;
-  // after the k loop the ring holds the up accumulators, h of the tile and
-  // the A_d rows
+  // after the k loop the ring holds the up accumulators, h of the tile, the
+  // A_d rows and lora_scale * (A x) of the tile's rows
   float* const uacc = reinterpret_cast<float*>(ring);  // [4 waves][4 m][4 e][64 lanes]
   _Float16(*hs)[kGateCols] = reinterpret_cast<_Float16(*)[kGateCols]>(ring + 16384);
   _Float16(*ads)[kGateCols] = reinterpret_cast<_Float16(*)[kGateCols]>(ring + 16384 + kGroupRows * kGateCols * 2);
-  static_assert(16384 + (kGroupRows + 16) * kGateCols * 2 <= kRingBytes, "epilogue fits in the ring");
-  // (the record is read beside the count; one past the count is never used)
+  constexpr int kLaOff = 16384 + (kGroupRows + 16) * kGateCols * 2;
+  _Float16(*la)[kGroupRows][16] = reinterpret_cast<_Float16(*)[kGroupRows][16]>(ring + kLaOff);
+  static_assert(kLaOff + 2 * kGroupRows * 16 * 2 <= kRingBytes, "epilogue fits in the ring");
   int bx, by;
   tile_of_block(blockIdx.x, a.I / kGateCols, bx, by);
-  const GroupTile tl = a.tiles[bx < a.max_tiles ? bx : 0];
-  if (bx >= *a.n_tiles) return;
-  if (tl.slot < 0) return;  // not resident: the down kernel writes zero rows
-  const moe_bundle* bd = a.bundles + tl.slot;
+  const int tix = bx < a.max_tiles ? bx : 0;
+  // (the record and the token list are read beside the count; one past the
+  // count is never used)
+  const GroupTile tl = a.tiles[tix];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  // tokens of this wave's activation copies: rows 4 b .. 4 b + 3 for b = wave
+  // and wave + 8 (uniform per wave)
+  const int32_t* tt = a.tile_tok + (size_t)tix * kGroupRows;
+  const int tr0 = tt[0];
+  const int t0 = tt[4 * wave], t1 = tt[4 * wave + 1], t2 = tt[4 * wave + 2], t3 = tt[4 * wave + 3];
+  const int t4 = tt[4 * (wave + kGW)], t5 = tt[4 * (wave + kGW) + 1], t6 = tt[4 * (wave + kGW) + 2],
+            t7 = tt[4 * (wave + kGW) + 3];
+  if (bx >= *a.n_tiles) return;
+  if (tl.slot < 0) return;  // not resident: the down kernel writes zero rows
+  const moe_bundle& bd = tl.b;
   const int col = lane & 15, kq = lane >> 4;
   const int d = a.d, I = a.I, r = a.r;
   const int mb = (tl.nrows + 15) >> 4;
   const int c0 = by * kGateCols;                // first column of this workgroup
   const int cc = wave >> 2, wb = wave & 3;      // projection (0 gate, 1 up), column block
   const int i = c0 + wb * 16 + col;             // this lane's gate/up column
-  if (tid < kGroupRows) rsrc[tid] = tid < tl.nrows ? a.perm[tl.row0 + tid] / a.n_list : -1;
-  const bool lg = r > 0 && bd->gate.lora_a && bd->gate.lora_b;
-  const bool lu = r > 0 && bd->up.lora_a && bd->up.lora_b;
-  const bool ld = r > 0 && bd->down.lora_a && bd->down.lora_b;
-  // lora_scale * (A x) of the tile's rows, fp16 (rank past r: zero)
-  for (int p = tid; p < 2 * kGroupRows * 16; p += kGT) {
-    const int pc = p / (kGroupRows * 16), row = (p >> 4) % kGroupRows, k = p & 15;
-    float v = 0.f;
-    if (row < tl.nrows && k < r && (pc == 0 ? lg : lu))
-      v = a.lora_scale * a.ax[((size_t)(tl.row0 + row) * 2 + pc) * 16 + k];
-    la[pc][row][k] = (_Float16)v;
+  const bool lg = r > 0 && bd.gate.lora_a && bd.gate.lora_b;
+  const bool lu = r > 0 && bd.up.lora_a && bd.up.lora_b;
+  const bool ld = r > 0 && bd.down.lora_a && bd.down.lora_b;
+
+  // The epilogue's operands, requested now and consumed after the k loop:
+  // A x of the tile's rows (4 values per thread), the LoRA-B operand and the
+  // A_d rows of this workgroup's columns.
+  static_assert(2 * kGroupRows * 16 == 4 * kGT, "four A x values per thread");
+  float axv[4][4];  // [value][quarter of d]
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int p = tid + q * kGT, pc = p / (kGroupRows * 16), row = (p >> 4) % kGroupRows, k = p & 15;
+    const bool on = row < tl.nrows && k < r && (pc == 0 ? lg : lu);
+    const float* src = a.ax + ((size_t)(tl.row0 + row) * 4 * 2 + pc) * 16 + k;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) axv[q][h] = on ? src[h * 32] : 0.f;
   }
-  __syncthreads();
-
-  // weight row w_row (0 .. 127): projection w_row / 64, column c0 + w_row % 64. The
-  // projection pointers are read here, once, into registers: a pointer read from
-  // the bundle inside the copy loop would be a vector load issued behind the
-  // chunks in flight, and waiting for it would drain them all.
-  const uint8_t* const gq = static_cast<const uint8_t*>(bd->gate.q);
-  const uint8_t* const uq = static_cast<const uint8_t*>(bd->up.q);
-  const uint8_t* const gs = static_cast<const uint8_t*>(bd->gate.sz);
-  const uint8_t* const us = static_cast<const uint8_t*>(bd->up.sz);
-  auto wrow = [&](int w_row) -> const uint8_t* {
-    return (w_row < kGateCols ? gq : uq) + (size_t)(c0 + (w_row % kGateCols)) * (d / 2);
-  };
-  auto srow = [&](int w_row) -> const uint8_t* {
-    return (w_row < kGateCols ? gs : us) + (size_t)(c0 + (w_row % kGateCols)) * (d / 16);
-  };
-  const char* xbase = reinterpret_cast<const char*>(a.xp);
-  auto xsrc = [&](int row, int k) -> const void* {
-    const int t = rsrc[row < tl.nrows ? row : 0];
-    return xbase + ((size_t)t * d + k) * 2;
-  };
-
-  // the epilogue's LoRA-B operand and A_d rows, requested before the k loop
   const bool lw = cc == 0 ? lg : lu;
-  const h8 bop = lw ? lora_b_operand(static_cast<const __half*>(cc == 0 ? bd->gate.lora_b : bd->up.lora_b), i,
+  const h8 bop = lw ? lora_b_operand(static_cast<const __half*>(cc == 0 ? bd.gate.lora_b : bd.up.lora_b), i,
                                      r, kq)
                     : h8{};
   static_assert(16 * kGateCols == 2 * kGT, "two A_d values per thread");
@@ -496,14 +519,52 @@ __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int p = tid + q * kGT, k = p / kGateCols, c = p % kGateCols;
-    adv[q] = (ld && k < r) ? reinterpret_cast<const _Float16*>(bd->down.lora_a)[(size_t)k * I + c0 + c]
+    adv[q] = (ld && k < r) ? reinterpret_cast<const _Float16*>(bd.down.lora_a)[(size_t)k * I + c0 + c]
                            : (_Float16)0.f;
   }
+
+  // weight row w_row (0 .. 127): projection w_row / 64, column c0 + w_row % 64
+  // (the projection pointers are in registers: a pointer loaded inside the
+  // copy loop would be a vector load behind the chunks in flight, and its wait
+  // would drain them)
+  const uint8_t* const gq = static_cast<const uint8_t*>(bd.gate.q);
+  const uint8_t* const uq = static_cast<const uint8_t*>(bd.up.q);
+  const uint8_t* const gs = static_cast<const uint8_t*>(bd.gate.sz);
+  const uint8_t* const us = static_cast<const uint8_t*>(bd.up.sz);
+  auto wrow = [&](int w_row) -> const uint8_t* {
+    return (w_row < kGateCols ? gq : uq) + (size_t)(c0 + (w_row % kGateCols)) * (d / 2);
+  };
+  auto srow = [&](int w_row) -> const uint8_t* {
+    return (w_row < kGateCols ? gs : us) + (size_t)(c0 + (w_row % kGateCols)) * (d / 16);
+  };
+  // The activation copies of this wave are b = wave and wave + 8, lane rows
+  // 4 b + (lane >> 4): each lane's two source rows are fixed for the tile. They
+  // are resolved here from plain values (a token array indexed inside the copy
+  // loop would live in scratch memory, and each read's wait would drain the
+  // copies in flight).
+  static_assert(kActRow == 256, "four activation rows per copy");
+  // (rows past nrows hold no token: they take row 0's, and are never stored)
+  const int q4 = lane >> 4;
+  const int tlo = 4 * wave + q4 >= tl.nrows ? tr0 : q4 == 0 ? t0 : q4 == 1 ? t1 : q4 == 2 ? t2 : t3;
+  const int thi = 4 * (wave + kGW) + q4 >= tl.nrows ? tr0 : q4 == 0 ? t4 : q4 == 1 ? t5 : q4 == 2 ? t6 : t7;
+  const char* const xlo = reinterpret_cast<const char*>(a.xp) + (size_t)tlo * d * 2;
+  const long long xdelta = ((long long)thi - tlo) * d * 2;
+  auto xsrc = [=](int row, int k) -> const void* {
+    return xlo + ((row >> 2) >= kGW ? xdelta : 0LL) + (size_t)k * 2;
+  };
+
   f4 acc[1][4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) acc[0][m] = f4{0.f, 0.f, 0.f, 0.f};
   tile_gemm<kGateRows>(ring, szl, d, mb, wrow, srow, xsrc, acc);
 
+  // lora_scale * (A x) of the tile's rows, fp16 (rank past r: zero)
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int p = tid + q * kGT, pc = p / (kGroupRows * 16), row = (p >> 4) % kGroupRows, k = p & 15;
+    la[pc][row][k] = (_Float16)(a.lora_scale * ((axv[q][0] + axv[q][1]) + (axv[q][2] + axv[q][3])));
+  }
+  __syncthreads();
   // LoRA delta of this wave's projection: one MFMA step of K = rank against
   // lora_scale * (A x)
   if (lw) {
@@ -561,8 +622,10 @@ __global__ void __launch_bounds__(kGT, 4) grouped_gateup_kernel(GroupedArgs a) {
 
 __global__ void __launch_bounds__(kGT, 4) grouped_down_kernel(GroupedArgs a) {
   extern __shared__ __attribute__((aligned(16))) char ring[];
-  __shared__ __attribute__((aligned(16))) _Float16 la[kGroupRows][16];
-  __shared__ int ydst[kGroupRows];
+  // after the k loop the ring holds lora_scale * (A_d h) of the tile's rows and
+  // their y_experts rows
+  _Float16(*la)[16] = reinterpret_cast<_Float16(*)[16]>(ring);
+  int* ydst = reinterpret_cast<int*>(ring + kGroupRows * 16 * 2);
   int bx, by;
   tile_of_block(blockIdx.x, a.d / kDownCols, bx, by);
   const GroupTile tl = a.tiles[bx < a.max_tiles ? bx : 0];  // (read beside the count, as in gate/up)
@@ -573,33 +636,38 @@ __global__ void __launch_bounds__(kGT, 4) grouped_down_kernel(GroupedArgs a) {
   const int d = a.d, I = a.I, r = a.r;
   const int mb = (tl.nrows + 15) >> 4;
   const int n0 = by * kDownCols + wave * 16 + col;  // this lane's output column
-  if (tid < kGroupRows) ydst[tid] = tid < tl.nrows ? a.perm[tl.row0 + tid] : -1;
-  __syncthreads();
   if (tl.slot < 0) {  // not resident: the pair contributes zeros (the miss is reported)
     for (int p = tid; p < tl.nrows * kDownCols; p += kGT) {
       const int row = p / kDownCols, c = p % kDownCols;
-      a.y_experts[(size_t)ydst[row] * d + by * kDownCols + c] = 0.f;
+      a.y_experts[(size_t)a.perm[tl.row0 + row] * d + by * kDownCols + c] = 0.f;
     }
     return;
   }
-  const moe_bundle* bd = a.bundles + tl.slot;
-  const bool ld = r > 0 && bd->down.lora_a && bd->down.lora_b;
-  // lora_scale * (A_d h) of the tile's rows: the slab partials in slab order
-  for (int p = tid; p < kGroupRows * 16; p += kGT) {
-    const int row = p >> 4, k = p & 15;
-    float v = 0.f;
-    if (ld && row < tl.nrows && k < r) {
-      const float* q = a.adp + (size_t)(tl.row0 + row) * (I / kGroupSlab) * 16 + k;
-      for (int sl = 0; sl < I / kGroupSlab; ++sl) v += q[sl * 16];
-      v *= a.lora_scale;
-    }
-    la[row][k] = (_Float16)v;
+  const moe_bundle& bd = tl.b;
+  const bool ld = r > 0 && bd.down.lora_a && bd.down.lora_b;
+  // The epilogue's operands, requested now and consumed after the k loop: the
+  // output rows, the LoRA-B operand, and the slab partials of A_d h (thread p
+  // holds (row, rank) = (p / 16, p % 16) and (p + 512) / 16; the first 16 slabs
+  // here, any further ones after the loop).
+  const int nsl = I / kGroupSlab;
+  constexpr int kPreSl = 16;
+  const int ydv = tid < tl.nrows ? a.perm[tl.row0 + tid] : -1;
+  const h8 bop = ld ? lora_b_operand(static_cast<const __half*>(bd.down.lora_b), n0, r, kq) : h8{};
+  static_assert(kGroupRows * 16 == 2 * kGT, "two A_d h sums per thread");
+  float adv[2][kPreSl];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int p = tid + q * kGT, row = p >> 4, k = p & 15;
+    const bool on = ld && row < tl.nrows && k < r;
+    const float* src = a.adp + (size_t)(tl.row0 + row) * nsl * 16 + k;
+#pragma unroll
+    for (int sl = 0; sl < kPreSl; ++sl) adv[q][sl] = on && sl < nsl ? src[sl * 16] : 0.f;
   }
   // weight row w_row (0 .. 127): output column by * 128 + w_row (the pointers
-  // read once, into registers, as in gate/up)
+  // in registers, as in gate/up)
   const size_t nbase = (size_t)by * kDownCols;
-  const uint8_t* const dq = static_cast<const uint8_t*>(bd->down.q);
-  const uint8_t* const dsz = static_cast<const uint8_t*>(bd->down.sz);
+  const uint8_t* const dq = static_cast<const uint8_t*>(bd.down.q);
+  const uint8_t* const dsz = static_cast<const uint8_t*>(bd.down.sz);
   auto wrow = [&](int w_row) -> const uint8_t* { return dq + (nbase + w_row) * (I / 2); };
   auto srow = [&](int w_row) -> const uint8_t* { return dsz + (nbase + w_row) * (I / 16); };
   const char* hbase = reinterpret_cast<const char*>(a.h);
@@ -607,13 +675,26 @@ __global__ void __launch_bounds__(kGT, 4) grouped_down_kernel(GroupedArgs a) {
     return hbase + ((size_t)(tl.row0 + (row < tl.nrows ? row : 0)) * I + k) * 2;
   };
 
-  // the epilogue's LoRA-B operand, requested before the k loop
-  const h8 bop = ld ? lora_b_operand(static_cast<const __half*>(bd->down.lora_b), n0, r, kq) : h8{};
   f4 acc[1][4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) acc[0][m] = f4{0.f, 0.f, 0.f, 0.f};
-  tile_gemm<kDownCols>(ring, ring + kRingBytes, I, mb, wrow, srow, xsrc, acc);  // its barriers also publish la
+  tile_gemm<kDownCols>(ring, ring + kRingBytes, I, mb, wrow, srow, xsrc, acc);
 
+  // lora_scale * (A_d h): the slab partials summed in slab order
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int p = tid + q * kGT, row = p >> 4, k = p & 15;
+    float v = 0.f;
+#pragma unroll
+    for (int sl = 0; sl < kPreSl; ++sl) v += adv[q][sl];
+    if (ld && row < tl.nrows && k < r) {
+      const float* src = a.adp + (size_t)(tl.row0 + row) * nsl * 16 + k;
+      for (int sl = kPreSl; sl < nsl; ++sl) v += src[sl * 16];
+    }
+    la[row][k] = (_Float16)(v * a.lora_scale);
+  }
+  if (tid < kGroupRows) ydst[tid] = ydv;
+  __syncthreads();
   if (ld) {
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
@@ -662,7 +743,7 @@ hipError_t launch_grouped_ffn(const GroupedArgs& a, hipStream_t st) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int xb = (int)(((size_t)a.T * a.d / 8 + kGT - 1) / kGT);
-  hipLaunchKernelGGL(grouped_prep_kernel, dim3(xb + a.max_tiles), dim3(kGT), 0, st, a, xb);
+  hipLaunchKernelGGL(grouped_prep_kernel, dim3(xb + 4 * a.max_tiles), dim3(kGT), 0, st, a, xb);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int tiles8 = (a.max_tiles + 7) / 8 * 8;

@@ -85,14 +85,22 @@ __device__ __forceinline__ U4 perm8(U4 w) {
 __device__ __forceinline__ int pair_slot(int e) { return e < 4 ? 2 * e : 2 * (e - 4) + 1; }
 
 // Eight int4 codes of one dword (nibble m = input m) -> fp16 weights
-// s q + z in pair order. 0x6400 | q is the fp16 value 1024 + q, so
-// subtracting 1024 gives q exactly; the fma rounds once.
+// s q + z in pair order. A nibble masked into the mantissa of the fp16 1024
+// (0x6400) gives 1024 + q from bits 0-3 and 1024 + 16 q from bits 4-7, so
+// nibbles 0, 4 and 1, 5 of v and 2, 6 and 3, 7 of v >> 8 come out with one
+// shift and four three-input bit operations ((x & mask) | 0x6400, truth table
+// 0xEA); q = (1024 + q) - 1024 or (1024 + 16 q) / 16 - 64, both exact, then the
+// fma rounds once.
 __device__ __forceinline__ h8 dequant8(uint32_t v, h2v s, h2v z) {
+  const uint32_t v8 = v >> 8;
   const h2v off = {(_Float16)1024.0f, (_Float16)1024.0f};
-  const h2v q0 = as_h2((v & 0x000F000Fu) | 0x64006400u) - off;
-  const h2v q1 = as_h2(((v >> 4) & 0x000F000Fu) | 0x64006400u) - off;
-  const h2v q2 = as_h2(((v >> 8) & 0x000F000Fu) | 0x64006400u) - off;
-  const h2v q3 = as_h2(((v >> 12) & 0x000F000Fu) | 0x64006400u) - off;
+  const h2v sixteenth = {(_Float16)0.0625f, (_Float16)0.0625f}, m64 = {(_Float16)-64.0f, (_Float16)-64.0f};
+  const h2v q0 = as_h2(__builtin_amdgcn_bitop3_b32(v, 0x000F000Fu, 0x64006400u, 0xEA)) - off;
+  const h2v q1 = __builtin_elementwise_fma(as_h2(__builtin_amdgcn_bitop3_b32(v, 0x00F000F0u, 0x64006400u, 0xEA)),
+                                           sixteenth, m64);
+  const h2v q2 = as_h2(__builtin_amdgcn_bitop3_b32(v8, 0x000F000Fu, 0x64006400u, 0xEA)) - off;
+  const h2v q3 = __builtin_elementwise_fma(as_h2(__builtin_amdgcn_bitop3_b32(v8, 0x00F000F0u, 0x64006400u, 0xEA)),
+                                           sixteenth, m64);
   const h2v w0 = __builtin_elementwise_fma(q0, s, z);
   const h2v w1 = __builtin_elementwise_fma(q1, s, z);
   const h2v w2 = __builtin_elementwise_fma(q2, s, z);
@@ -134,7 +142,7 @@ __device__ __forceinline__ void dma16(const void* g, const void* lds) {
       "s_mov_b32 %0, m0\n\t"
       "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, off nt\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
       : "s"(lds_addr(lds)), "v"(g)
@@ -152,20 +160,27 @@ __device__ __forceinline__ void dma4(const void* g, const void* lds) {
       : "s"(lds_addr(lds)), "v"(g)
       : "memory");
 }
-// wait until at most n of this wave's copies are outstanding (n <= 27)
-__device__ __forceinline__ void vm_wait(int n) {
-  switch (n) {
-#define MOE_VMW(N) \
-  case N:          \
-    asm volatile("s_waitcnt vmcnt(" #N ")" ::: "memory"); \
-    break;
-    MOE_VMW(0) MOE_VMW(1) MOE_VMW(2) MOE_VMW(3) MOE_VMW(4) MOE_VMW(5) MOE_VMW(6) MOE_VMW(7)
-    MOE_VMW(8) MOE_VMW(9) MOE_VMW(10) MOE_VMW(11) MOE_VMW(12) MOE_VMW(13) MOE_VMW(14)
-    MOE_VMW(15) MOE_VMW(16) MOE_VMW(17) MOE_VMW(18) MOE_VMW(19) MOE_VMW(20) MOE_VMW(21)
-    MOE_VMW(22) MOE_VMW(23) MOE_VMW(24) MOE_VMW(25) MOE_VMW(26) MOE_VMW(27)
-#undef MOE_VMW
-    default:
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+// wait until at most N of this wave's copies are outstanding (N an immediate)
+template <int N>
+__device__ __forceinline__ void vm_wait_n() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// the same for N = A * (hi ? PH : PL) with A = ahead in [0, 6): a short chain of
+// scalar compares on uniform values instead of one case per count
+template <int PH, int PL, int A = 0>
+__device__ __forceinline__ void vm_wait_ahead(int ahead, bool hi) {
+  if constexpr (A < 6) {
+    if (ahead == A) {
+      if (hi)
+        vm_wait_n<A * PH>();
+      else
+        vm_wait_n<A * PL>();
+      return;
+    }
+    vm_wait_ahead<PH, PL, A + 1>(ahead, hi);
+  } else {
+    vm_wait_n<0>();
   }
 }
 
@@ -197,8 +212,9 @@ __device__ __forceinline__ void tile_gemm_mb(char* ring, char* szl, int Kdim, WR
   constexpr int XI = MB * 16 * kActRow / 1024;                 // activation copies per chunk
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int col = lane & 15, kq = lane >> 4;
-  const int my_x = (XI - wave + kGW - 1) / kGW;                // this wave's activation copies
-  const int per = CODE_I + my_x;                               // this wave's copies per chunk
+  // this wave's copies per chunk: CODE_I codes and XHI or XLO activation copies
+  constexpr int XLO = XI / kGW, XHI = (XI + kGW - 1) / kGW;
+  const bool xhi = wave < XI % kGW;
   const int nch = Kdim / kGK;
   const int szr = Kdim / 16;                                   // (s, z) bytes per row
   auto slot = [&](int c) { return ring + (c % NBUF) * SLOT; };
@@ -211,10 +227,14 @@ __device__ __forceinline__ void tile_gemm_mb(char* ring, char* szl, int Kdim, WR
       const int piece = phys ^ ((row >> 2) & 3);
       dma16(wrow(row) + c * kCodeRow + piece * 16, sl + b * 1024);
     }
-    for (int b = wave; b < XI; b += kGW) {  // activation rows 4b .. 4b+3, 256 bytes each
-      const int row = 4 * b + (lane >> 4), phys = lane & 15;
-      const int piece = phys ^ (row & 15);
-      dma16(xsrc(row, c * kGK + piece * 8), sl + CODE_B + b * 1024);
+#pragma unroll
+    for (int j = 0; j < XHI; ++j) {  // activation rows 4b .. 4b+3, 256 bytes each
+      const int b = wave + j * kGW;
+      if (b < XI) {
+        const int row = 4 * b + (lane >> 4), phys = lane & 15;
+        const int piece = phys ^ (row & 15);
+        dma16(xsrc(row, c * kGK + piece * 8), sl + CODE_B + b * 1024);
+      }
     }
   };
   // (loads of the caller still outstanding here are older than every copy:
@@ -231,7 +251,7 @@ __device__ __forceinline__ void tile_gemm_mb(char* ring, char* szl, int Kdim, WR
     // chunks issued after chunk c: all of the first NBUF at c = 0, then one
     // per chunk (into the slot of chunk c - 1)
     const int ahead = c == 0 ? pre - 1 : min(nch - 1 - c, NBUF - 2);
-    vm_wait(ahead * per);
+    vm_wait_ahead<CODE_I + XHI, CODE_I + XLO>(ahead, xhi);
     __syncthreads();  // chunk c is in LDS for every wave; chunk c - 1 is consumed
     if (c > 0 && c + NBUF - 1 < nch) issue(c + NBUF - 1);
     const char* sl = slot(c);

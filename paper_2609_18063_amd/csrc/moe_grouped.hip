@@ -299,8 +299,21 @@ __global__ void __launch_bounds__(1024) grouped_permute_kernel(GroupedArgs a) {
   for (int g = tid; g < G; g += 1024) cnt[g] = g >= a.E ? a.T : 0;
   __syncthreads();
   const int TK = a.T * a.K;
-  for (int i = tid; i < TK; i += 1024) {
-    const int e = a.idx[i];
+  // the thread's first kIdxReg routing ids are read once, into registers, for
+  // both passes over them (each pass would otherwise wait on its loads in turn)
+  constexpr int kIdxReg = 8;
+  int ev[kIdxReg];
+#pragma unroll
+  for (int j = 0; j < kIdxReg; ++j) ev[j] = tid + 1024 * j < TK ? a.idx[tid + 1024 * j] : -1;
+  auto id_at = [&](int j, int i) {  // routing id i = tid + 1024 j
+    int e = -1;
+#pragma unroll
+    for (int q = 0; q < kIdxReg; ++q)
+      if (j == q) e = ev[q];
+    return j < kIdxReg ? e : a.idx[i];
+  };
+  for (int i = tid, j = 0; i < TK; i += 1024, ++j) {
+    const int e = id_at(j, i);
     if (e >= 0 && e < a.E) atomicAdd(&cnt[e], 1);
   }
   __syncthreads();
@@ -367,8 +380,8 @@ __global__ void __launch_bounds__(1024) grouped_permute_kernel(GroupedArgs a) {
   if (g1 < G) cnt[g1] = off0 + c0;
   if (tid == 0) *a.n_tiles = total_tiles;
   __syncthreads();
-  for (int i = tid; i < TK; i += 1024) {
-    const int e = a.idx[i];
+  for (int i = tid, j = 0; i < TK; i += 1024, ++j) {
+    const int e = id_at(j, i);
     const int t = i / a.K, k = i - t * a.K;
     const int row = t * a.n_list + k;
     if (e >= 0 && e < a.E) {
@@ -409,14 +422,18 @@ __global__ void __launch_bounds__(kGT, 6) grouped_prep_kernel(GroupedArgs a, int
   const int ti = (blockIdx.x - xb) >> 2, Q = (blockIdx.x - xb) & 3;
   if (ti >= *a.n_tiles) return;
   const GroupTile tl = a.tiles[ti];
-  if (tl.slot < 0 || a.r <= 0) return;
-  const moe_bundle* bd = a.bundles + tl.slot;
   const int wave = tid >> 6, lane = tid & 63, col = lane & 15, kq = lane >> 4;
+  // the tokens of this lane's rows (the tile's token list, read beside the record)
+  int tok[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) tok[m] = a.tile_tok[(size_t)ti * kGroupRows + 16 * m + col];
+  if (tl.slot < 0 || a.r <= 0) return;
+  const moe_bundle& bd = tl.b;
   const int c = wave >> 2, quarter = wave & 3;
   const int d = a.d, r = a.r;
   const int mb = (tl.nrows + 15) >> 4;
-  const void* A = c == 0 ? bd->gate.lora_a : bd->up.lora_a;
-  const void* Bm = c == 0 ? bd->gate.lora_b : bd->up.lora_b;
+  const void* A = c == 0 ? bd.gate.lora_a : bd.up.lora_a;
+  const void* Bm = c == 0 ? bd.gate.lora_b : bd.up.lora_b;
   const bool on = A && Bm;
   f4 acc[4];
 #pragma unroll
@@ -427,8 +444,7 @@ __global__ void __launch_bounds__(kGT, 6) grouped_prep_kernel(GroupedArgs a, int
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       const int row = 16 * m + col;
-      const int t = row < tl.nrows ? a.perm[tl.row0 + row] / a.n_list : -1;
-      xrow[m] = t >= 0 ? reinterpret_cast<const _Float16*>(a.x) + (size_t)t * d : nullptr;
+      xrow[m] = row < tl.nrows ? reinterpret_cast<const _Float16*>(a.x) + (size_t)tok[m] * d : nullptr;
     }
     const int kbeg = Q * (d / 4) + quarter * (d / 16), kend = kbeg + d / 16;
 #pragma unroll 1

@@ -15,8 +15,6 @@ struct EngineArgs {
   int consumer_lo, consumer_hi;  // chain: layers that route by the prediction (after token 0)
   int E, K, S, r;
   float lora_scale;
-  int n_groups, top_groups;  // sigmoid-group selection (App. A) when n_groups > 0, else softmax-top-k
-  float route_scale;
   int n_ids, n_slots, n_table_layers;
   const int32_t* slot_of;        // slot-table device copy
   const moe_bundle* bundles;
@@ -38,6 +36,8 @@ struct EngineArgs {
   // exchange-area offsets and per-parity strides (in 64-bit words)
   size_t xo_logr, xs_logr, xo_loghm, xo_av, xs_av, xo_hv, xs_hv, xo_adp, xs_adp, xo_part, xs_part,
       xo_rv, xs_rv, xo_logh, xs_logh_layer, xo_pred, xs_pred;
+  int n_groups, top_groups;  // sigmoid-group selection (App. A) when n_groups > 0, else softmax-top-k
+  float route_scale;
 };
 
 bool engine_shape_supported(int d, int I, int r, int K, int S, int E);

@@ -187,8 +187,7 @@ struct PShape {
   static constexpr int O_YL = O_DP + NLX * RR * 4;             // [NLX][R] fp32 A_down h per expert
   static constexpr int O_LG = O_YL + NLX * R * 4;              // [256] fp32 logits
   static constexpr int O_TK = O_LG + 256 * 4;                  // top-k scratch
-  static constexpr int TK_BYTES = 256 * 8 + 256 * 4 + 128 * 8 + 32 * 8 +
-                                  (int)sizeof(eng::SigmoidScratch);  // + sigmoid-group scratch
+  static constexpr int TK_BYTES = 256 * 8 + 256 * 4 + 128 * 8 + 32 * 8;
   static constexpr int O_GR = O_TK + TK_BYTES;                 // [NWV][NGW][64] fp32 gate/up lane partials
   static constexpr int O_RED = O_GR + (LPR == 64 ? NWV * NGW * 64 * 4 : 0);  // [NWV] f64
   static constexpr int O_MISC = (O_RED + NWV * 8 + 1023) / 1024 * 1024;
@@ -240,6 +239,13 @@ struct Src {
   const uint8_t* bd[SH::NLX];       // B_down of list position k at the first output row
   const uint8_t* ad[SH::NAP];       // A_down rank rows of the workgroup's (expert, rank) pairs
 };
+
+// LDS offset of the sigmoid-group selection scratch: after the whole layout
+// (16-byte aligned)
+template <class SH>
+__host__ __device__ constexpr int sig_scratch_off() {
+  return (SH::O_SRC + (int)sizeof(Src<SH>) + 15) / 16 * 16;
+}
 
 constexpr int kProfMarks = 24;
 
@@ -295,16 +301,9 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   int* tk_part = reinterpret_cast<int*>(smem + SH::O_TK + 256 * 8);
   uint64_t* tk_cand = reinterpret_cast<uint64_t*>(smem + SH::O_TK + 256 * 12);
   uint64_t* tk_sorted = tk_cand + 128;
-  eng::SigmoidScratch& tk_sig = *reinterpret_cast<eng::SigmoidScratch*>(smem + SH::O_TK + 256 * 12 + 160 * 8);
-  // the layer's selection on its logits (router or head): softmax-top-k, or
-  // sigmoid-group selection where the spec asks for it
-  auto select = [&](const float* l, int32_t* idx_out, float* w_out) {
-    if constexpr (SIG)
-      eng::block_topk_sigmoid_group(l, nullptr, apx->E, apx->K, apx->n_groups, apx->top_groups, apx->route_scale,
-                                    idx_out, w_out, tk_sig, tk_keys, tk_part, tk_cand, tk_sorted);
-    else
-      block_topk(l, apx->E, apx->K, idx_out, w_out, tk_keys, tk_part, tk_cand, tk_sorted);
-  };
+  // (sigmoid-group scratch past the end of the softmax layout, in the SIG
+  // instantiation only)
+  eng::SigmoidScratch& tk_sig = *reinterpret_cast<eng::SigmoidScratch*>(smem + sig_scratch_off<SH>());
   double* red = reinterpret_cast<double*>(smem + SH::O_RED);
   float* grp_part = reinterpret_cast<float*>(smem + SH::O_GR);
   Misc* mi = reinterpret_cast<Misc*>(smem + SH::O_MISC);
@@ -332,6 +331,15 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   const int gw = xg + NXG * m;  // workgroup index in the half
   int wave = __builtin_amdgcn_readfirstlane(tx >> 6), lane = tx & 63;
   const int K = apx->K, E = apx->E;
+  // the layer's selection on its logits (router or head): softmax-top-k, or
+  // sigmoid-group selection where the spec asks for it
+  auto select = [&](const float* l, int32_t* idx_out, float* w_out) {
+    if constexpr (SIG)
+      eng::block_topk_sigmoid_group(l, nullptr, E, K, apx->n_groups, apx->top_groups, apx->route_scale, idx_out, w_out,
+                                    tk_sig, tk_keys, tk_part, tk_cand, tk_sorted);
+    else
+      block_topk(l, E, K, idx_out, w_out, tk_keys, tk_part, tk_cand, tk_sorted);
+  };
   const int n_list = K + apx->S;
   const int GX = n_list * IE / NXG;
   const int RM = GX / NM;
@@ -1149,14 +1157,14 @@ using PShapeTiny = PShape<512, 256, 8, 2, 16, 2>;
 // owns one whole expert
 using PShape8b = PShape<4096, 1024, 16, 4, 64, 1>;
 
-template <class SH>
+template <class SH, bool SIG>
 static int lds_bytes() {
-  return SH::O_SRC + (int)sizeof(Src<SH>);
+  return SIG ? sig_scratch_off<SH>() + (int)sizeof(eng::SigmoidScratch) : SH::O_SRC + (int)sizeof(Src<SH>);
 }
 
 template <class SH, bool SIG>
 static hipError_t launch_as(EngineArgs& a, hipStream_t st) {
-  const int lds = lds_bytes<SH>();
+  const int lds = lds_bytes<SH, SIG>();
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   static bool attr_set = false;
   if (!attr_set) {

@@ -419,6 +419,32 @@ int moe_engine_chain(const moe_layer_spec* spec, const moe_slot_table* table,
                      float* w_rec, int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * The decode chain of moe_engine_chain with the full prerouter head (Sec. 3.2,
+ * Head, Feature drift) as every layer's head: head n (n < n_layers - 1) is
+ * heads[n], a DEVICE array of n_layers moe_head_mlp (entry n_layers - 1 is not
+ * read; layers[n].head is not read), every one with this hidden size. Its
+ * features are x of layer n, the routing layer n used at this token and the
+ * routing it used at the last token (none at token 0; from the previous call
+ * at first_token > 0, so every call of one chain must use this entry): the
+ * same as moe_preroute_mlp's, here fed the chain's own routing (which is the
+ * head's earlier prediction from layer 1 on: the feature drift the paper
+ * describes). fc1 is computed in fp32 from x and the gathered one-hot columns,
+ * erf-GELU, rounded once to fp16; fc2, its bias and the linear path add up in
+ * fp32. Runs on the two-half schedule only: softmax-topk routing, d <= 2048
+ * (the 35B-class and tiny shapes; the fc1 and fc2 rows of a workgroup are held
+ * in LDS), hidden a multiple of 64 in [64, 512]; MOE_EINVAL otherwise
+ * (moe_engine_chain_mlp_supported). heads must be 16-byte aligned (MOE_EALIGN).
+ * The workspace is moe_engine_workspace_bytes(spec, n_layers); the prediction
+ * and routing words persist in it between the calls of a chain.
+ */
+int moe_engine_chain_mlp_supported(const moe_layer_spec* spec, int hidden);
+int moe_engine_chain_mlp(const moe_layer_spec* spec, const moe_slot_table* table,
+                         const moe_engine_layer* layers, const moe_head_mlp* heads, int hidden, int n_layers,
+                         int first_token, int n_tokens, const float* xi, float* r_state, void* x_rec,
+                         float* r_rec, int32_t* idx_rec, float* w_rec, int32_t* pidx_rec, float* pw_rec,
+                         float* y_rec, uint32_t* status, void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- host-tier staging -----------------------------------------------------
  * The staged executor keeps a fixed set of device slots per layer and rewrites
  * only the slots whose expert changed (Sec. 3.1, Executor paths); head N's

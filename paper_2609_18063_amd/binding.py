@@ -137,6 +137,11 @@ SIGNATURES = {
                                   c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                   c_void_p, c_void_p, c_size_t, c_void_p]),
     "moe_engine_chain_supported": (c_int, [ctypes.POINTER(MoeLayerSpec)]),
+    "moe_engine_chain_mlp_supported": (c_int, [ctypes.POINTER(MoeLayerSpec), c_int]),
+    "moe_engine_chain_mlp": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_void_p, c_int, c_int,
+                                     c_int, c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, ctypes.c_size_t,
+                                     c_void_p]),
     "moe_engine_chain": (c_int, [ctypes.POINTER(MoeLayerSpec), c_void_p, c_void_p, c_int, c_int,
                                  c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
@@ -550,6 +555,21 @@ def engine_workspace_bytes(spec, n_layers):
     return int(lib().moe_engine_workspace_bytes(ctypes.byref(spec), int(n_layers)))
 
 
+def engine_chain_mlp_supported(spec, hidden):
+    return lib().moe_engine_chain_mlp_supported(ctypes.byref(spec), int(hidden)) == MOE_OK
+
+
+def head_mlp_array(heads, device="cuda"):
+    """Device array of moe_head_mlp (one per layer; None entries -> all NULL)."""
+    import torch
+    arr = (MoeHeadMlp * len(heads))()
+    for i, h in enumerate(heads):
+        if h is not None:
+            arr[i] = h
+    raw = np.frombuffer(bytes(arr), dtype=np.uint8).copy()
+    return torch.from_numpy(raw).to(device)
+
+
 def engine_layer_array(layers, device="cuda"):
     """Device array of moe_engine_layer from dicts of device tensors
     (router, head, mix_d, mix_perm; missing or None -> NULL)."""
@@ -600,3 +620,17 @@ def engine_chain(spec, table, layer_arr, n_layers, first_token, xi, r_state, wor
                                   _ptr(status), _ptr(workspace),
                                   workspace.numel() * workspace.element_size(), _stream(stream)),
            "moe_engine_chain")
+
+
+def engine_chain_mlp(spec, table, layer_arr, head_arr, hidden, n_layers, first_token, xi, r_state, workspace,
+                     x_rec=None, idx=None, w=None, pidx=None, pw=None, y_rec=None, status=None,
+                     stream=None, r_rec=None):
+    """moe_engine_chain_mlp: the chain with the full prerouter head of every
+    layer (head_arr from head_mlp_array)."""
+    n_tokens = xi.shape[0]
+    _check(lib().moe_engine_chain_mlp(ctypes.byref(spec), table.handle, _ptr(layer_arr), _ptr(head_arr),
+                                      int(hidden), n_layers, first_token, n_tokens, _ptr(xi), _ptr(r_state),
+                                      _ptr(x_rec), _ptr(r_rec), _ptr(idx), _ptr(w), _ptr(pidx), _ptr(pw),
+                                      _ptr(y_rec), _ptr(status), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)),
+           "moe_engine_chain_mlp")

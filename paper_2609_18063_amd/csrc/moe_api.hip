@@ -724,6 +724,48 @@ int moe_engine_chain(const moe_layer_spec* s, const moe_slot_table* t,
   return engine_common(s, t, n_layers, a, ws, ws_bytes, stream);
 }
 
+int moe_engine_chain_mlp_supported(const moe_layer_spec* s, int hidden) {
+  const int rc = engine_pipe_supported(s);
+  if (rc != MOE_OK) return rc;
+  if (s->routing != MOE_ROUTING_SOFTMAX_TOPK || s->d_model > 2048) return MOE_EINVAL;
+  if (hidden < 64 || hidden > moe::kHidMax || hidden % 64) return MOE_EINVAL;
+  return MOE_OK;
+}
+
+int moe_engine_chain_mlp(const moe_layer_spec* s, const moe_slot_table* t, const moe_engine_layer* layers,
+                         const moe_head_mlp* heads, int hidden, int n_layers, int first_token, int n_tokens,
+                         const float* xi, float* r_state, void* x_rec, float* r_rec, int32_t* idx_rec,
+                         float* w_rec, int32_t* pidx_rec, float* pw_rec, float* y_rec, uint32_t* status,
+                         void* ws, size_t ws_bytes, void* stream) {
+  int rc = moe_engine_chain_mlp_supported(s, hidden);
+  if (rc != MOE_OK) return rc;
+  if (!heads || !aligned16(heads)) return heads ? MOE_EALIGN : MOE_EINVAL;
+  if (n_layers < 1 || n_tokens < 0 || first_token < 0 || !r_state) return MOE_EINVAL;
+  if ((long long)n_tokens * n_layers > (1LL << 30)) return MOE_EINVAL;
+  if (n_tokens == 0) return MOE_OK;
+  moe::EngineArgs a{};
+  a.mode = 3;
+  a.n_steps = n_tokens * n_layers;
+  a.L = n_layers;
+  a.first_token = first_token;
+  a.consumer_lo = 1;
+  a.consumer_hi = n_layers - 1;
+  a.layers = layers;
+  a.heads = heads;
+  a.hidden = hidden;
+  a.xi = xi;
+  a.r_state = r_state;
+  a.x_rec = static_cast<__half*>(x_rec);
+  a.r_rec = r_rec;
+  a.idx_rec = idx_rec;
+  a.w_rec = w_rec;
+  a.pidx_rec = pidx_rec;
+  a.pw_rec = pw_rec;
+  a.y = y_rec;
+  a.status = status;
+  return engine_common(s, t, n_layers, a, ws, ws_bytes, stream);
+}
+
 int moe_profile_arm(int which, void* start_event, void* stop_event) {
   if (which == MOE_PROF_ENGINE_PHASES) {
     if (!start_event || !aligned16(start_event)) return MOE_EINVAL;

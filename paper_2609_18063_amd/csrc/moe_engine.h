@@ -38,7 +38,14 @@ struct EngineArgs {
       xo_rv, xs_rv, xo_logh, xs_logh_layer, xo_pred, xs_pred;
   int n_groups, top_groups;  // sigmoid-group selection (App. A) when n_groups > 0, else softmax-top-k
   float route_scale;
+  // two-half chain with the full prerouter head: heads[n] of every layer n < L - 1
+  // (device array), hidden size `hidden`; null: the linear head of layers[n]
+  const moe_head_mlp* heads;
+  int hidden;
+  size_t xo_hid, xo_rtm1;    // hidden words [2 halves][4][kHidMax], routing words [2][L][32]
 };
+
+constexpr int kHidMax = 512;  // largest hidden size of the full head in the two-half chain
 
 bool engine_shape_supported(int d, int I, int r, int K, int S, int E);
 // Fills the exchange offsets of `a`; returns the exchange area size in words.

@@ -247,6 +247,21 @@ __host__ __device__ constexpr int sig_scratch_off() {
   return (SH::O_SRC + (int)sizeof(Src<SH>) + 15) / 16 * 16;
 }
 
+// LDS of the full prerouter head (HM instantiations, after the whole layout):
+// the workgroup's fc1 rows (x part) and fc2 rows, the step's hidden values,
+// its linear-path logits and the layer's routing at the previous token
+template <class SH>
+struct HmLayout {
+  static constexpr int HPWX = kHidMax / NWGG;                   // hidden rows per workgroup
+  static constexpr int O_W1 = 0;                                // [HPWX][D] fp16
+  static constexpr int O_W2 = O_W1 + HPWX * SH::D * 2;          // [HRX][kHidMax] fp16
+  static constexpr int O_HID = O_W2 + SH::HRX * kHidMax * 2;    // [kHidMax] fp32
+  static constexpr int O_HL = O_HID + kHidMax * 4;              // [HRX] fp32 (padded)
+  static constexpr int O_TM1 = O_HL + 16;                       // [32] int
+  static constexpr int BYTES = O_TM1 + 32 * 4;
+  static_assert(kHidMax % NWGG == 0 && HPWX <= NWV && (HPWX * (SH::D / 8)) % 64 == 0, "head rows");
+};
+
 constexpr int kProfMarks = 24;
 
 struct StepInfo {
@@ -257,7 +272,10 @@ struct StepInfo {
 // SIG: the layers route by sigmoid-group selection (App. A) instead of
 // softmax-top-k; a separate instantiation so that the softmax path carries none
 // of its code
-template <class SH, bool SIG>
+// HM: the head of every layer is the full prerouter head (fc1 -> erf-GELU ->
+// fc2 plus the linear path, Sec. 3.2 Head), its one-hot features the routing
+// this layer used at this token and the last; a separate instantiation too
+template <class SH, bool SIG, bool HM>
 __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   // The arguments are read through a pointer into the kernel-argument segment
@@ -274,7 +292,10 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
     f.N = s % apx->L;
     f.own = f.t == 0 || f.N < apx->consumer_lo || f.N > apx->consumer_hi;
     f.ok = f.N < apx->n_table_layers;
-    f.head = f.ok && apx->layers[f.N].head != nullptr && f.N + 1 < apx->L;
+    if constexpr (HM)  // the full head of the layer (its fc1 and fc2 given)
+      f.head = f.ok && f.N + 1 < apx->L && apx->heads[f.N].w1_x != nullptr && apx->heads[f.N].w2 != nullptr;
+    else
+      f.head = f.ok && apx->layers[f.N].head != nullptr && f.N + 1 < apx->L;
     return f;
   };
   constexpr int D = SH::D, IE = SH::IE, R = SH::R;
@@ -304,6 +325,14 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
   // (sigmoid-group scratch past the end of the softmax layout, in the SIG
   // instantiation only)
   eng::SigmoidScratch& tk_sig = *reinterpret_cast<eng::SigmoidScratch*>(smem + sig_scratch_off<SH>());
+  using HL = HmLayout<SH>;
+  char* const hmb = smem + sig_scratch_off<SH>();  // (HM instantiations only; never with SIG)
+  __half* const hw1 = reinterpret_cast<__half*>(hmb + HL::O_W1);
+  __half* const hw2 = reinterpret_cast<__half*>(hmb + HL::O_W2);
+  float* const hhid = reinterpret_cast<float*>(hmb + HL::O_HID);
+  float* const hlin = reinterpret_cast<float*>(hmb + HL::O_HL);
+  int* const htm1 = reinterpret_cast<int*>(hmb + HL::O_TM1);
+  static_assert(!(HM && SIG), "the full head runs with softmax-top-k routing");
   double* red = reinterpret_cast<double*>(smem + SH::O_RED);
   float* grp_part = reinterpret_cast<float*>(smem + SH::O_GR);
   Misc* mi = reinterpret_cast<Misc*>(smem + SH::O_MISC);
@@ -612,7 +641,27 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
       mixp[q] = mp[j];
     }
     if (f.own) stage_rows(rtrow, apx->layers[f.N].router);
-    if (f.head) stage_rows(hdrow, apx->layers[f.N].head);
+    if (f.head) {
+      if constexpr (HM) {
+        const moe_head_mlp* hm = apx->heads + f.N;
+        const int H = apx->hidden;
+        if (hm->w_l) stage_rows(hdrow, hm->w_l);  // the linear path, as head rows
+        // fc1 rows h = gw + NWGG j (x part; row 0 stands in past H, never read)
+        const __half* W1 = static_cast<const __half*>(hm->w1_x);
+        for (int b = wave; b * 64 < HL::HPWX * (D / 8); b += NWV) {
+          const int i = b * 64 + lane, j = i / (D / 8), h = gw + NWGG * j;
+          dma16(W1 + (size_t)(h < H ? h : 0) * D + (i % (D / 8)) * 8, hw1 + b * 512);
+        }
+        // fc2 rows e = gw + NWGG q, padded to kHidMax (the pad is never read)
+        const __half* W2 = static_cast<const __half*>(hm->w2);
+        for (int b = wave; b * 64 < SH::HRX * (kHidMax / 8); b += NWV) {
+          const int i = b * 64 + lane, q = i / (kHidMax / 8), c = i % (kHidMax / 8), e = gw + NWGG * q;
+          dma16(W2 + (e < E && c < H / 8 ? (size_t)e * H + c * 8 : 0), hw2 + b * 512);
+        }
+      } else {
+        stage_rows(hdrow, apx->layers[f.N].head);
+      }
+    }
   };
 
   // ---- the head's prediction of a step (one workgroup per step) -------------
@@ -786,6 +835,11 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
     if (gw == 0 && (int)tx < K) {
       if (apx->idx_rec) apx->idx_rec[(size_t)s * K + tx] = Rt.idx[tx];
       if (apx->w_rec) apx->w_rec[(size_t)s * K + tx] = Rt.w[tx];
+      // the full head of this layer at the next token reads this routing
+      if constexpr (HM)
+        if (f.head)
+          st_word(X + apx->xo_rtm1 + ((size_t)(t & 1) * apx->L + N) * 32 + tx, (uint32_t)t + 1u,
+                  (uint32_t)Rt.idx[tx]);
     }
     mark(s, 3);
 
@@ -820,7 +874,11 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
                      *reinterpret_cast<const U4*>(xh + ch * 8), acc);
       }
       acc = wave_sum(acc);
-      if (lane == 0 && e < E) st_word(logh_of(t + 1, N + 1) + e, (uint32_t)t + 2u, __float_as_uint(acc));
+      if constexpr (HM) {  // the linear path of the full head, completed after the step
+        if (lane == 0) hlin[q] = apx->heads[N].w_l ? acc : 0.f;
+      } else {
+        if (lane == 0 && e < E) st_word(logh_of(t + 1, N + 1) + e, (uint32_t)t + 2u, __float_as_uint(acc));
+      }
     }
 
     // ---- S3: gate/up rows from registers ---------------------------------------
@@ -1104,6 +1162,77 @@ __global__ void __launch_bounds__(NT) pipe_kernel(EngineArgs) {
     }
     mark(s, 9);
 
+    // ---- S7b: the full head (HM), after the residual is out ----------------------
+    // fc1 rows of this workgroup on x and the one-hot features (the routing of
+    // this step and of this layer at the last token), erf-GELU, fp16, published;
+    // then every hidden value of the step, fc2 rows plus the linear path and
+    // fc2's bias -> the logits of the next layer's prediction.
+    if constexpr (HM) {
+      if (f.head) {
+        const moe_head_mlp* hm = apx->heads + N;
+        const int H = apx->hidden;
+        if (wave == 0) {
+          int e = -1;
+          if (lane < K && t > 0) {
+            const uint64_t* p = X + apx->xo_rtm1 + ((size_t)((t - 1) & 1) * apx->L + N) * 32 + lane;
+            uint64_t v = ld_tag(p);
+            long spin = 0;
+            while ((uint32_t)(v >> 32) != (uint32_t)t && ++spin < kSpinMax) {
+              if ((spin & 63) == 0 && ld_u32(&apx->ctl[2])) break;
+              __builtin_amdgcn_s_sleep(1);
+              v = ld_tag(p);
+            }
+            if ((uint32_t)(v >> 32) == (uint32_t)t) {
+              e = (int)(uint32_t)v;
+            } else {  // timed out or aborted: leave (reported like every wait)
+              if (apx->status && spin >= kSpinMax) atomicOr(apx->status, MOE_STATUS_ENGINE_ABORT);
+              __hip_atomic_store(&apx->ctl[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              mi->abort = 1;
+            }
+          }
+          if (lane < 32) htm1[lane] = e;
+        }
+        __syncthreads();
+        if (mi->abort) break;
+        uint64_t* const HID = X + apx->xo_hid + ((size_t)(s & 1) * 4 + ((s >> 1) & 3)) * kHidMax;
+        if (wave < HL::HPWX) {
+          const int h = gw + NWGG * wave;
+          if (h < H) {
+            float acc = 0.f;
+#pragma unroll
+            for (int c = 0; c < D / 512; ++c) {
+              const int ch = lane + 64 * c;
+              acc = dot8_h(*reinterpret_cast<const U4*>(hw1 + (size_t)wave * D + ch * 8),
+                           *reinterpret_cast<const U4*>(xh + ch * 8), acc);
+            }
+            if (lane < 2 * K) {  // one-hot features: columns d + e (this step) and d + E + e (last token)
+              const int e = lane < K ? Rt.idx[lane] : htm1[lane - K];
+              if (e >= 0 && e < E)
+                acc += __half2float(static_cast<const __half*>(hm->w1_r)[(size_t)(lane < K ? e : E + e) * H + h]);
+            }
+            acc = wave_sum(acc);
+            if (hm->b1) acc += __half2float(static_cast<const __half*>(hm->b1)[h]);
+            const float g = 0.5f * acc * (1.f + erff(acc * 0.70710678118654752f));
+            if (lane == 0) st_word(HID + h, tag, __float_as_uint(__half2float(__float2half(g))));
+          }
+        }
+        if (!poll_all<kHidMax / NPT>(H, tag, [&](int i) { return HID + i; },
+                                     [&](int i, uint32_t v) { hhid[i] = __uint_as_float(v); }, apx->ctl, apx->status,
+                                     &mi->abort))
+          break;
+        if (wave < SH::HRX) {
+          const int q = wave, e = gw + NWGG * q;
+          if (e < E) {
+            float acc = 0.f;
+            for (int i = lane; i < H; i += 64) acc = fmaf(__half2float(hw2[q * kHidMax + i]), hhid[i], acc);
+            acc = wave_sum(acc) + hlin[q];
+            if (hm->b2) acc += __half2float(static_cast<const __half*>(hm->b2)[e]);
+            if (lane == 0) st_word(logh_of(t + 1, N + 1) + e, (uint32_t)t + 2u, __float_as_uint(acc));
+          }
+        }
+      }
+    }
+
     // ---- S8: load the half's next step while the other half computes -----------
     staged = false;
     lstaged = false;
@@ -1157,30 +1286,39 @@ using PShapeTiny = PShape<512, 256, 8, 2, 16, 2>;
 // owns one whole expert
 using PShape8b = PShape<4096, 1024, 16, 4, 64, 1>;
 
-template <class SH, bool SIG>
+template <class SH, bool SIG, bool HM>
 static int lds_bytes() {
+  if (HM) return sig_scratch_off<SH>() + HmLayout<SH>::BYTES;
   return SIG ? sig_scratch_off<SH>() + (int)sizeof(eng::SigmoidScratch) : SH::O_SRC + (int)sizeof(Src<SH>);
 }
 
-template <class SH, bool SIG>
+template <class SH, bool SIG, bool HM>
 static hipError_t launch_as(EngineArgs& a, hipStream_t st) {
-  const int lds = lds_bytes<SH, SIG>();
+  const int lds = lds_bytes<SH, SIG, HM>();
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)pipe_kernel<SH, SIG>,
+    hipError_t e = hipFuncSetAttribute((const void*)pipe_kernel<SH, SIG, HM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   void* args[] = {&a};
-  return hipLaunchCooperativeKernel((const void*)pipe_kernel<SH, SIG>, dim3(NWG), dim3(NT), args, (size_t)lds,
+  return hipLaunchCooperativeKernel((const void*)pipe_kernel<SH, SIG, HM>, dim3(NWG), dim3(NT), args, (size_t)lds,
                                     st);
 }
 
 template <class SH>
 static hipError_t launch(EngineArgs& a, hipStream_t st) {
-  return a.n_groups > 0 ? launch_as<SH, true>(a, st) : launch_as<SH, false>(a, st);
+  if (a.heads) {  // the full head: softmax-top-k routing, shapes whose LDS holds its rows
+    if constexpr (SH::D <= 2048) {
+      if (a.n_groups > 0 || a.hidden < 64 || a.hidden > kHidMax || a.hidden % 64) return hipErrorInvalidValue;
+      return launch_as<SH, false, true>(a, st);
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
+  return a.n_groups > 0 ? launch_as<SH, true, false>(a, st) : launch_as<SH, false, false>(a, st);
 }
 
 // most expert segments over the four XCDs of a half
@@ -1240,6 +1378,8 @@ size_t engine_pipe_workspace_words(int E, int d, int I, int r, int n_list, int L
   a->xo_logh = take(2 * (size_t)(L > 0 ? L : 1) * a->xs_logh_layer);
   a->xs_pred = 64;
   a->xo_pred = take(2 * (size_t)(L > 0 ? L : 1) * a->xs_pred);
+  a->xo_hid = take((size_t)2 * 4 * kHidMax);                  // full head: by half and step
+  a->xo_rtm1 = take((size_t)2 * (L > 0 ? L : 1) * 32);          // by token parity and layer
   return off;
 }
 

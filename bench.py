@@ -430,6 +430,33 @@ def head_chain_path(B, torch, wl, table, layers, hidden=512, T=12):
         del dc
     log("per-call chain, 40 layers: linear head %.3f ms/token, full head %.3f ms/token"
         % (out["linear_head"]["ms_per_token"], out["full_head"]["ms_per_token"]))
+    # the two-half engine chain (one launch) with each kind of head
+    if B.engine_chain_mlp_supported(spec, hidden):
+        arr = B.engine_layer_array(layers)
+        harr = B.head_mlp_array(structs)
+        Te = 64
+        xe = torch.from_numpy(synth.token_draws(wl, 0, Te, stream=1)).cuda()
+        ws = torch.zeros(B.engine_workspace_bytes(spec, L), dtype=torch.uint8, device="cuda")
+        r_state = torch.zeros(wl.d, dtype=torch.float32, device="cuda")
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+        def run(full):
+            r_state.zero_()
+            if full:
+                B.engine_chain_mlp(spec, table, arr, harr, hidden, L, 0, xe, r_state, ws, status=status)
+            else:
+                B.engine_chain(spec, table, arr, L, 0, xe, r_state, ws, status=status)
+
+        for label, full in (("engine_linear_head", False), ("engine_full_head", True)):
+            run(full)
+            ms = min(time_launch(torch, lambda: run(full)) for _ in range(3))
+            assert int(status.item()) == 0, "engine chain status %d" % int(status.item())
+            out[label] = {"tokens": Te, "ms_per_token": round(ms / Te, 4), "tokens_per_s": round(Te / (ms * 1e-3), 1),
+                          "us_per_layer_step": round(ms * 1e3 / (Te * L), 3)}
+        log("engine chain, 40 layers, %d tokens: linear head %.2f us per layer step (%.0f tok/s), full head "
+            "%.2f us per layer step (%.0f tok/s)"
+            % (Te, out["engine_linear_head"]["us_per_layer_step"], out["engine_linear_head"]["tokens_per_s"],
+               out["engine_full_head"]["us_per_layer_step"], out["engine_full_head"]["tokens_per_s"]))
     return out
 
 

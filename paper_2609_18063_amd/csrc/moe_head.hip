@@ -34,23 +34,43 @@ __global__ void __launch_bounds__(128) head_fc1_kernel(const __half* __restrict_
   const __half* xr = x + (size_t)t * d;
   {
     const int row = blockIdx.x * kHeadRows + wave;  // H % 8 == 0: always < H
+    // The set members' fc1 columns, requested before the row's dot product
+    // (lane k < K: member k at t; lane K + k: member k at t - 1), so that
+    // their two dependent loads overlap it; added below in member order.
+    const bool lanes = 2 * K <= kWave;
+    float mv = 0.f;
+    int mok = 0;
+    if (lanes && lane < 2 * K) {
+      const bool prev = lane >= K;
+      const int k = prev ? lane - K : lane;
+      const int e = prev ? (rtm1 ? rtm1[(size_t)t * K + k] : -1) : rt[(size_t)t * K + k];
+      mok = e >= 0 && e < E;
+      if (mok) mv = __half2float(w1r[(size_t)(prev ? E + e : e) * H + row]);
+    }
+    const float bv = b1 ? __half2float(b1[row]) : 0.f;
     const __half* wr = w1x + (size_t)row * d;
     float acc = 0.f;
 #pragma unroll 4
     for (int c = lane; c < d / 8; c += kWave) acc = dot8_h(ld16(wr + (size_t)c * 8), ld16(xr + (size_t)c * 8), acc);
     acc = wave_sum(acc);
+    if (lanes) {
+      for (int k = 0; k < 2 * K; ++k)
+        if (__builtin_amdgcn_readlane(mok, k)) acc += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mv), k));
+    }
     if (lane == 0) {
-      for (int k = 0; k < K; ++k) {
-        const int e = rt[(size_t)t * K + k];
-        if (e >= 0 && e < E) acc += __half2float(w1r[(size_t)e * H + row]);
-      }
-      if (rtm1) {
+      if (!lanes) {
         for (int k = 0; k < K; ++k) {
-          const int e = rtm1[(size_t)t * K + k];
-          if (e >= 0 && e < E) acc += __half2float(w1r[(size_t)(E + e) * H + row]);
+          const int e = rt[(size_t)t * K + k];
+          if (e >= 0 && e < E) acc += __half2float(w1r[(size_t)e * H + row]);
+        }
+        if (rtm1) {
+          for (int k = 0; k < K; ++k) {
+            const int e = rtm1[(size_t)t * K + k];
+            if (e >= 0 && e < E) acc += __half2float(w1r[(size_t)(E + e) * H + row]);
+          }
         }
       }
-      if (b1) acc += __half2float(b1[row]);
+      if (b1) acc += bv;
       const float g = 0.5f * acc * (1.0f + erff(acc * 0.70710678118654752f));
       hid[(size_t)t * H + row] = __float2half(g);
     }

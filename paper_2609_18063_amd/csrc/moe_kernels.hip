@@ -51,19 +51,19 @@ __global__ void __launch_bounds__(256) route_kernel(const __half* __restrict__ x
                                                     int32_t* __restrict__ idx,
                                                     float* __restrict__ wout,
                                                     uint32_t* __restrict__ counters) {
-  extern __shared__ U4 xs[];
   const int t = blockIdx.y;
   const int nch = d >> 3;
+  // x is read by every wave from the cache, in the same loads as the rows (a
+  // copy into LDS first would put a barrier and one more memory round trip
+  // ahead of the row loads)
   const U4* xrow = reinterpret_cast<const U4*>(x + (size_t)t * d);
-  for (int c = threadIdx.x; c < nch; c += blockDim.x) xs[c] = xrow[c];
-  __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row0 = (blockIdx.x * 4 + wave) * RPW;
   float acc[RPW];
 #pragma unroll
   for (int r = 0; r < RPW; ++r) acc[r] = 0.f;
   for (int c = lane; c < nch; c += kWave) {
-    const U4 xv = xs[c];
+    const U4 xv = xrow[c];
     U4 wv[RPW];
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
@@ -501,7 +501,7 @@ hipError_t launch_route(const __half* x, const __half* W, int T, int E, int d, i
   constexpr int RPW = 2;
   const int rows_per_wg = 4 * RPW;
   dim3 grid((E + rows_per_wg - 1) / rows_per_wg, T);
-  hipLaunchKernelGGL(route_kernel<RPW>, grid, dim3(256), (size_t)d * 2, st, x, W, E, d, K, logits,
+  hipLaunchKernelGGL(route_kernel<RPW>, grid, dim3(256), 0, st, x, W, E, d, K, logits,
                      idx, w, counters);
   return hipGetLastError();
 }

@@ -88,6 +88,7 @@ __global__ void __launch_bounds__(128) head_fc2_kernel(const __half* __restrict_
   const __half* xr = x + (size_t)t * d;
   {
     const int e = blockIdx.x * kHeadRows + wave;  // E % 8 == 0: always < E
+    const float b2v = b2 ? __half2float(b2[e]) : 0.f;  // requested with the rows
     float acc = 0.f, res = 0.f;
     const __half* w2r = w2 + (size_t)e * H;
     for (int c = lane; c < H / 8; c += kWave) acc = dot8_h(ld16(w2r + (size_t)c * 8), ld16(hr + (size_t)c * 8), acc);
@@ -98,7 +99,7 @@ __global__ void __launch_bounds__(128) head_fc2_kernel(const __half* __restrict_
     }
     acc = wave_sum(acc);
     res = wave_sum(res);
-    if (lane == 0) logits[(size_t)t * E + e] = acc + (b2 ? __half2float(b2[e]) : 0.f) + res;
+    if (lane == 0) logits[(size_t)t * E + e] = acc + b2v + res;
   }
 }
 
